@@ -1,0 +1,240 @@
+"""Plain CPU oracle for the batch-reduce GEMM TPP, its fused epilogue and the Reduce TPP.
+
+TEST INFRASTRUCTURE ONLY.  The product path (the HIP library and its Python binding) never
+imports, links or calls anything in this package; only ``tests/``, the smoke check and the
+benchmark's CPU-baseline leg do.  The arithmetic lives in ``oracle.c`` (plain C, fp64 loops);
+this module only marshals numpy arrays into it.
+
+Operand conventions (shared with nothing, stated here again): every 2D block is column-major
+with a leading dimension; bf16 tensors are numpy ``uint16`` arrays holding the bit patterns,
+fp32 tensors are ``float32`` arrays; strides and offsets count elements of the operand type.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass, field
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_SRC = os.path.join(_HERE, "oracle.c")
+
+F32, BF16 = 0, 1
+STRIDE, OFFSET, ADDRESS = 0, 1, 2
+EPI_BIAS, EPI_RELU, EPI_GELU_TANH = 1, 2, 4
+RED_SUM, RED_MUL, RED_MIN, RED_MAX = 0, 1, 2, 3
+RED_BY_COLS, RED_BY_ROWS, RED_X, RED_X2 = 1, 2, 4, 8
+
+_DTYPES = {"f32": F32, "bf16": BF16}
+_KINDS = {"stride": STRIDE, "offset": OFFSET, "address": ADDRESS}
+
+
+def build(force: bool = False) -> str:
+    """Compile oracle.c with gcc into liboracle.so next to it."""
+    if force or not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
+        tmp = _LIB_PATH + f".tmp{os.getpid()}"
+        subprocess.run(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11", "-Wall",
+                        "-o", tmp, _SRC, "-lm"], check=True)
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+class _Desc(ctypes.Structure):
+    _fields_ = [("m", ctypes.c_int32), ("n", ctypes.c_int32), ("k", ctypes.c_int32),
+                ("lda", ctypes.c_int64), ("ldb", ctypes.c_int64), ("ldc", ctypes.c_int64),
+                ("ab_type", ctypes.c_int32), ("c_type", ctypes.c_int32), ("beta", ctypes.c_double),
+                ("kind", ctypes.c_int32), ("stride_a", ctypes.c_int64), ("stride_b", ctypes.c_int64),
+                ("flags", ctypes.c_uint32)]
+
+
+class _Grid(ctypes.Structure):
+    _fields_ = [(f, ctypes.c_int64) for f in
+                ("gm", "gn", "a_step_m", "b_step_n", "c_step_m", "c_step_n", "bias_step_m")]
+
+
+_lib = None
+
+
+def lib():
+    """Load the oracle library (built on first use).  ORACLE_LIB_OVERRIDE names another build
+    of it; the mutation tests use that to load copies with planted mistakes."""
+    global _lib
+    if _lib is None:
+        override = os.environ.get("ORACLE_LIB_OVERRIDE")
+        _lib = ctypes.CDLL(override if override else build())
+        vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
+        _lib.oracle_brgemm.restype = ctypes.c_int
+        _lib.oracle_brgemm.argtypes = [ctypes.POINTER(_Desc), vp, vp, vp, vp, i64, vp, vp, vp, vp, vp]
+        _lib.oracle_brgemm_batched.restype = ctypes.c_int
+        _lib.oracle_brgemm_batched.argtypes = [ctypes.POINTER(_Desc), ctypes.POINTER(_Grid), i64,
+                                               vp, vp, vp, vp, vp, vp, vp, vp, i64, vp, vp, vp, vp,
+                                               vp, i64, vp, vp, ctypes.c_int]
+        _lib.oracle_reduce.restype = ctypes.c_int
+        _lib.oracle_reduce.argtypes = [i32, i32, i64, i32, vp, i32, ctypes.c_uint32, vp, vp]
+        _lib.oracle_f32_to_bf16.restype = ctypes.c_uint16
+        _lib.oracle_f32_to_bf16.argtypes = [ctypes.c_float]
+        _lib.oracle_f32_to_bf16_array.restype = None
+        _lib.oracle_f32_to_bf16_array.argtypes = [vp, vp, i64]
+        _lib.oracle_bf16_to_f32.restype = ctypes.c_float
+        _lib.oracle_bf16_to_f32.argtypes = [ctypes.c_uint16]
+        _lib.oracle_gelu_tanh.restype = ctypes.c_double
+        _lib.oracle_gelu_tanh.argtypes = [ctypes.c_double]
+        _lib.oracle_max_threads.restype = ctypes.c_int
+    return _lib
+
+
+@dataclass
+class Desc:
+    """BRGEMM problem description (the dispatch-time fields of the TPP)."""
+    m: int
+    n: int
+    k: int
+    lda: int
+    ldb: int
+    ldc: int
+    ab_type: str = "bf16"
+    c_type: str = "f32"
+    beta: float = 0.0
+    kind: str = "stride"
+    stride_a: int = 0
+    stride_b: int = 0
+    flags: set = field(default_factory=set)   # subset of {"bias", "relu", "gelu_tanh"}
+
+    def _c(self) -> _Desc:
+        fl = (EPI_BIAS if "bias" in self.flags else 0) | (EPI_RELU if "relu" in self.flags else 0) \
+            | (EPI_GELU_TANH if "gelu_tanh" in self.flags else 0)
+        return _Desc(self.m, self.n, self.k, self.lda, self.ldb, self.ldc, _DTYPES[self.ab_type],
+                     _DTYPES[self.c_type], float(self.beta), _KINDS[self.kind], self.stride_a,
+                     self.stride_b, fl)
+
+
+def _ptr(x):
+    return None if x is None else x.ctypes.data
+
+
+def _check_dtype(arr, dt, name):
+    want = np.float32 if dt == "f32" else np.uint16
+    if arr is not None and arr.dtype != want:
+        raise TypeError(f"{name}: expected {np.dtype(want).name}, got {arr.dtype}")
+
+
+def _as_i64(x):
+    return None if x is None else np.ascontiguousarray(x, dtype=np.int64)
+
+
+def _pointer_list(base: np.ndarray, elem_offsets, es: int):
+    """Host addresses base + off*es for each element offset: the address variant's lists."""
+    offs = np.asarray(elem_offsets, dtype=np.int64)
+    if offs.size and (offs.min() < 0 or offs.max() >= base.size):
+        raise ValueError("pointer list leaves the pool")
+    return (np.uint64(base.ctypes.data) + offs.astype(np.uint64) * np.uint64(es)).astype(np.uint64)
+
+
+def brgemm_batched(desc: Desc, a, b, c, bias=None, *, grid=None, G=1, a_off=None, b_off=None,
+                   c_off=None, bias_off=None, count=0, offs_a=None, offs_b=None, begin=None,
+                   idx_a=None, idx_b=None, sel=None, want_ref64=False, nthreads=0):
+    """Run G BRGEMM instances in place on ``c``.
+
+    grid: dict with gm, gn, a_step_m, b_step_n, c_step_m, c_step_n, bias_step_m (strided form),
+    or None for the explicit per-instance offset arrays.  Address variant: ``idx_a``/``idx_b`` are
+    element offsets into the pools ``a``/``b``; they become host addresses here, and ``begin``
+    (G+1 entries) splits them into per-instance lists.  Returns the unrounded fp64 results of the
+    selected instances when ``want_ref64``.
+    """
+    _check_dtype(a, desc.ab_type, "a")
+    _check_dtype(b, desc.ab_type, "b")
+    _check_dtype(c, desc.c_type, "c")
+    if bias is not None and bias.dtype != np.float32:
+        raise TypeError("bias must be float32")
+    for arr in (a, b, c, bias):
+        if arr is not None and not arr.flags.c_contiguous:
+            raise ValueError("arrays must be contiguous")
+    d = desc._c()
+    g = None
+    if grid is not None:
+        g = _Grid(*(int(grid[f]) for f in ("gm", "gn", "a_step_m", "b_step_n", "c_step_m",
+                                           "c_step_n", "bias_step_m")))
+    a_off, b_off, c_off, bias_off = map(_as_i64, (a_off, b_off, c_off, bias_off))
+    offs_a, offs_b, begin = map(_as_i64, (offs_a, offs_b, begin))
+    ptrs_a = ptrs_b = None
+    es = 4 if desc.ab_type == "f32" else 2
+    if desc.kind == "address":
+        ptrs_a = _pointer_list(a, idx_a, es)
+        ptrs_b = _pointer_list(b, idx_b, es)
+        if begin is None:
+            raise ValueError("address variant needs begin[]")
+    sel_arr = None if sel is None else _as_i64(sel)
+    n_sel = G if sel_arr is None else len(sel_arr)
+    ref = np.empty((n_sel, desc.n, desc.m), dtype=np.float64) if want_ref64 else None
+    rc = lib().oracle_brgemm_batched(
+        ctypes.byref(d), ctypes.byref(g) if g is not None else None, G,
+        _ptr(a_off), _ptr(b_off), _ptr(c_off), _ptr(bias_off),
+        _ptr(a) if desc.kind != "address" else None, _ptr(b) if desc.kind != "address" else None,
+        _ptr(c), _ptr(bias), count, _ptr(offs_a), _ptr(offs_b), _ptr(begin), _ptr(ptrs_a),
+        _ptr(ptrs_b), n_sel, _ptr(sel_arr), _ptr(ref), nthreads)
+    if rc != 0:
+        raise ValueError("oracle_brgemm_batched rejected its arguments")
+    return ref
+
+
+def brgemm(desc: Desc, a, b, c, bias=None, *, count=0, offs_a=None, offs_b=None, idx_a=None,
+           idx_b=None, want_ref64=False):
+    """One BRGEMM call (the paper's call API) on host arrays, in place on ``c``."""
+    _check_dtype(a, desc.ab_type, "a")
+    _check_dtype(b, desc.ab_type, "b")
+    _check_dtype(c, desc.c_type, "c")
+    d = desc._c()
+    offs_a, offs_b = map(_as_i64, (offs_a, offs_b))
+    ptrs_a = ptrs_b = None
+    es = 4 if desc.ab_type == "f32" else 2
+    if desc.kind == "address":
+        ptrs_a = _pointer_list(a, idx_a, es)
+        ptrs_b = _pointer_list(b, idx_b, es)
+    ref = np.empty((desc.n, desc.m), dtype=np.float64) if want_ref64 else None
+    rc = lib().oracle_brgemm(ctypes.byref(d), _ptr(a) if desc.kind != "address" else None,
+                             _ptr(b) if desc.kind != "address" else None, _ptr(c), _ptr(bias),
+                             count, _ptr(offs_a), _ptr(offs_b), _ptr(ptrs_a), _ptr(ptrs_b), _ptr(ref))
+    if rc != 0:
+        raise ValueError("oracle_brgemm rejected its arguments")
+    return ref
+
+
+def reduce(x, m: int, n: int, ld: int, in_type: str, op: str, by: str, want=("x",)):
+    """Reduce TPP: op in sum/mul/min/max, by in cols/rows, want subset of {"x", "x2"}."""
+    _check_dtype(x, in_type, "x")
+    ops = {"sum": RED_SUM, "mul": RED_MUL, "min": RED_MIN, "max": RED_MAX}
+    flags = (RED_BY_COLS if by == "cols" else RED_BY_ROWS)
+    flags |= (RED_X if "x" in want else 0) | (RED_X2 if "x2" in want else 0)
+    outn = m if by == "cols" else n
+    ox = np.empty(outn, dtype=np.float64) if "x" in want else None
+    ox2 = np.empty(outn, dtype=np.float64) if "x2" in want else None
+    rc = lib().oracle_reduce(m, n, ld, _DTYPES[in_type], _ptr(x), ops[op], flags, _ptr(ox), _ptr(ox2))
+    if rc != 0:
+        raise ValueError("oracle_reduce rejected its arguments")
+    return ox, ox2
+
+
+def f32_to_bf16(x: float) -> int:
+    return int(lib().oracle_f32_to_bf16(float(x)))
+
+
+def f32_to_bf16_array(x: np.ndarray) -> np.ndarray:
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    out = np.empty(x.shape, dtype=np.uint16)
+    lib().oracle_f32_to_bf16_array(_ptr(x), _ptr(out), x.size)
+    return out
+
+
+def bf16_to_f32(h: int) -> float:
+    return float(lib().oracle_bf16_to_f32(int(h)))
+
+
+def gelu_tanh(x: float) -> float:
+    return float(lib().oracle_gelu_tanh(float(x)))
+
+
+def max_threads() -> int:
+    return int(lib().oracle_max_threads())

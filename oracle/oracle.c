@@ -1,0 +1,291 @@
+/*
+ * oracle.c -- plain, slow CPU reference for the batch-reduce GEMM TPP with its fused epilogue,
+ * and for the Reduce TPP.  TEST INFRASTRUCTURE ONLY: the product library never includes, links
+ * or calls it.  Every loop is the definition written out in fp64, with no blocking, fusion or
+ * reordering beyond what the definition states.  Paper: arXiv 2104.05755 (TPP).
+ */
+#include "oracle.h"
+
+#include <math.h>
+#include <stddef.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+static int elem_size(int32_t dtype) { return dtype == ORACLE_F32 ? 4 : 2; }
+
+/* bf16 is the upper 16 bits of an fp32 (Sec. 3.2.2), so widening is a shift and is exact. */
+float oracle_bf16_to_f32(uint16_t h) {
+  uint32_t u = (uint32_t)h << 16;
+  float f;
+  memcpy(&f, &u, sizeof f);
+  return f;
+}
+
+/* fp32 -> bf16, round to nearest, ties to even, on the bit pattern.  NaN stays a (quiet) NaN;
+ * values past the largest finite bf16 round to infinity through the carry into the exponent. */
+uint16_t oracle_f32_to_bf16(float f) {
+  uint32_t u;
+  memcpy(&u, &f, sizeof u);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x0040u);
+  uint32_t keep = u >> 16;
+  uint32_t rest = u & 0xffffu;
+  if (rest > 0x8000u || (rest == 0x8000u && (keep & 1u))) keep += 1u;
+  return (uint16_t)keep;
+}
+
+void oracle_f32_to_bf16_array(const float* in, uint16_t* out, int64_t n) {
+  for (int64_t i = 0; i < n; ++i) out[i] = oracle_f32_to_bf16(in[i]);
+}
+
+double oracle_widen(const void* base, int64_t idx, int32_t dtype) {
+  if (dtype == ORACLE_F32) return (double)((const float*)base)[idx];
+  return (double)oracle_bf16_to_f32(((const uint16_t*)base)[idx]);
+}
+
+/* Output narrowing: the fp64 value is rounded once to fp32 (the accumulation precision), then,
+ * for a bf16 output, once more to bf16.  Both steps are round-to-nearest-even. */
+static void store_rounded(void* base, int64_t idx, int32_t dtype, double v) {
+  float f = (float)v;
+  if (dtype == ORACLE_F32)
+    ((float*)base)[idx] = f;
+  else
+    ((uint16_t*)base)[idx] = oracle_f32_to_bf16(f);
+}
+
+/* GELU in its tanh form: 0.5 x (1 + tanh(sqrt(2/pi) (x + 0.044715 x^3))), libm tanh in fp64. */
+double oracle_gelu_tanh(double x) {
+  const double c = sqrt(2.0 / 3.14159265358979323846);
+  return 0.5 * x * (1.0 + tanh(c * (x + 0.044715 * x * x * x)));
+}
+
+int oracle_max_threads(void) {
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
+}
+
+/* Addresses of the i-th pair of blocks, following the three variants of Sec. 2.3:
+ *   address-based: the user gives the block addresses;
+ *   offset-based:  address_A_i = address_A + offset_A_i;
+ *   stride-based:  address_A_i = address_A_{i-1} + stride_A, starting from address_A.
+ * The stride variant is written as the recurrence the paper states (a running address). */
+static void pair_addresses(const oracle_desc* d, const void* a, const void* b, int64_t count,
+                           const int64_t* offs_a, const int64_t* offs_b,
+                           const void* const* ptrs_a, const void* const* ptrs_b,
+                           const char** out_a, const char** out_b) {
+  const int es = elem_size(d->ab_type);
+  if (d->kind == ORACLE_ADDRESS) {
+    for (int64_t i = 0; i < count; ++i) {
+      out_a[i] = (const char*)ptrs_a[i];
+      out_b[i] = (const char*)ptrs_b[i];
+    }
+  } else if (d->kind == ORACLE_OFFSET) {
+    for (int64_t i = 0; i < count; ++i) {
+      out_a[i] = (const char*)a + offs_a[i] * es;
+      out_b[i] = (const char*)b + offs_b[i] * es;
+    }
+  } else {
+    const char* pa = (const char*)a;
+    const char* pb = (const char*)b;
+    for (int64_t i = 0; i < count; ++i) {
+      if (i > 0) {
+        pa += d->stride_a * es;
+        pb += d->stride_b * es;
+      }
+      out_a[i] = pa;
+      out_b[i] = pb;
+    }
+  }
+}
+
+static int check_desc(const oracle_desc* d) {
+  if (!d || d->m <= 0 || d->n <= 0 || d->k <= 0) return -1;
+  if (d->lda < d->m || d->ldb < d->k || d->ldc < d->m) return -1;
+  if (d->ab_type != ORACLE_F32 && d->ab_type != ORACLE_BF16) return -1;
+  if (d->c_type != ORACLE_F32 && d->c_type != ORACLE_BF16) return -1;
+  if ((d->flags & ORACLE_EPI_RELU) && (d->flags & ORACLE_EPI_GELU_TANH)) return -1;
+  if (d->kind < ORACLE_STRIDE || d->kind > ORACLE_ADDRESS) return -1;
+  return 0;
+}
+
+/* The BRGEMM TPP on already-resolved block addresses, then the fused epilogue, per output
+ * element (r, c):
+ *   s   = sum_i sum_p A_i(r, p) * B_i(p, c)          (Table 3, Sec. 2.3)
+ *   v   = beta * C(r, c) + s                         (C read only when beta != 0)
+ *   v  += bias[r]                                    (Add with a column broadcast over n)
+ *   v   = relu(v) or gelu_tanh(v)                    (unary TPP on the finished block, Alg. 6)
+ *   C(r, c) = round(v)                               (Identity with conversion)            */
+static void brgemm_resolved(const oracle_desc* d, const char* const* pa, const char* const* pb,
+                            int64_t count, void* c, const float* bias, double* ref64) {
+  for (int32_t col = 0; col < d->n; ++col) {
+    for (int32_t row = 0; row < d->m; ++row) {
+      double s = 0.0;
+      for (int64_t i = 0; i < count; ++i) {
+        for (int32_t p = 0; p < d->k; ++p) {
+          double x = oracle_widen(pa[i], (int64_t)row + (int64_t)p * d->lda, d->ab_type);
+          double y = oracle_widen(pb[i], (int64_t)p + (int64_t)col * d->ldb, d->ab_type);
+          s += x * y;
+        }
+      }
+      const int64_t ci = (int64_t)row + (int64_t)col * d->ldc;
+      double v = s;
+      if (d->beta != 0.0) v = d->beta * oracle_widen(c, ci, d->c_type) + s;
+      if (d->flags & ORACLE_EPI_BIAS) v += (double)bias[row];
+      if (d->flags & ORACLE_EPI_RELU) v = v > 0.0 ? v : 0.0;
+      if (d->flags & ORACLE_EPI_GELU_TANH) v = oracle_gelu_tanh(v);
+      if (ref64) ref64[(int64_t)row + (int64_t)col * d->m] = v;
+      store_rounded(c, ci, d->c_type, v);
+    }
+  }
+}
+
+static int check_pairs(const oracle_desc* d, const void* a, const void* b, int64_t count,
+                       const int64_t* offs_a, const int64_t* offs_b,
+                       const void* const* ptrs_a, const void* const* ptrs_b) {
+  if (count < 0) return -1;
+  if (count == 0) return 0;
+  if (d->kind == ORACLE_ADDRESS) return (ptrs_a && ptrs_b) ? 0 : -1;
+  if (d->kind == ORACLE_OFFSET) return (a && b && offs_a && offs_b) ? 0 : -1;
+  return (a && b) ? 0 : -1;
+}
+
+/* One call: resolve the count block addresses, then run the definition. */
+static int brgemm_one(const oracle_desc* d, const void* a, const void* b, void* c,
+                      const float* bias, int64_t count, const int64_t* offs_a,
+                      const int64_t* offs_b, const void* const* ptrs_a,
+                      const void* const* ptrs_b, double* ref64) {
+  if (check_pairs(d, a, b, count, offs_a, offs_b, ptrs_a, ptrs_b) != 0) return -1;
+  const char** pa = (const char**)malloc(sizeof(char*) * (size_t)(count > 0 ? count : 1));
+  const char** pb = (const char**)malloc(sizeof(char*) * (size_t)(count > 0 ? count : 1));
+  if (!pa || !pb) {
+    free(pa);
+    free(pb);
+    return -1;
+  }
+  pair_addresses(d, a, b, count, offs_a, offs_b, ptrs_a, ptrs_b, pa, pb);
+  brgemm_resolved(d, pa, pb, count, c, bias, ref64);
+  free(pa);
+  free(pb);
+  return 0;
+}
+
+int oracle_brgemm(const oracle_desc* d, const void* a, const void* b, void* c, const float* bias,
+                  int64_t count, const int64_t* offs_a, const int64_t* offs_b,
+                  const void* const* ptrs_a, const void* const* ptrs_b, double* ref64) {
+  if (check_desc(d) != 0 || !c) return -1;
+  if ((d->flags & ORACLE_EPI_BIAS) && !bias) return -1;
+  return brgemm_one(d, a, b, c, bias, count, offs_a, offs_b, ptrs_a, ptrs_b, ref64);
+}
+
+/* The loops around the BRGEMM call that Alg. 6 (FC layer: ib_n, ib_m over output blocks) and
+ * Alg. 7 (dilated convolution: pos) write out: G independent calls, each with its own bases.
+ * Strided form: instance g = gi_m + gm * gi_n, with
+ *   A base  = a + gi_m * a_step_m           B base = b + gi_n * b_step_n
+ *   C base  = c + gi_m * c_step_m + gi_n * c_step_n     bias base = bias + gi_m * bias_step_m
+ * Explicit form: element offsets a_off[g], b_off[g], c_off[g], bias_off[g].
+ * Address variant: instance g reduces pairs begin[g] .. begin[g+1]-1 of the pointer lists. */
+int oracle_brgemm_batched(const oracle_desc* d, const oracle_grid* grid, int64_t G,
+                          const int64_t* a_off, const int64_t* b_off, const int64_t* c_off,
+                          const int64_t* bias_off,
+                          const void* a, const void* b, void* c, const float* bias,
+                          int64_t count, const int64_t* offs_a, const int64_t* offs_b,
+                          const int64_t* begin, const void* const* ptrs_a, const void* const* ptrs_b,
+                          int64_t n_sel, const int64_t* sel, double* ref64, int nthreads) {
+  if (check_desc(d) != 0 || G < 0 || !c) return -1;
+  if ((d->flags & ORACLE_EPI_BIAS) && !bias) return -1;
+  if (grid && (grid->gm <= 0 || grid->gn <= 0 || grid->gm * grid->gn != G)) return -1;
+  if (d->kind == ORACLE_ADDRESS && G > 0 && !begin) return -1;
+  if (!sel) n_sel = G;
+  for (int64_t s = 0; s < n_sel; ++s) {
+    int64_t g = sel ? sel[s] : s;
+    if (g < 0 || g >= G) return -1;
+  }
+  const int es_ab = elem_size(d->ab_type);
+  const int es_c = elem_size(d->c_type);
+  int failed = 0;
+#ifdef _OPENMP
+  if (nthreads <= 0) nthreads = omp_get_max_threads();
+#pragma omp parallel for schedule(dynamic, 1) num_threads(nthreads) reduction(| : failed)
+#endif
+  for (int64_t s = 0; s < n_sel; ++s) {
+    const int64_t g = sel ? sel[s] : s;
+    int64_t ao, bo, co, zo;
+    if (grid) {
+      const int64_t gi_m = g % grid->gm, gi_n = g / grid->gm;
+      ao = gi_m * grid->a_step_m;
+      bo = gi_n * grid->b_step_n;
+      co = gi_m * grid->c_step_m + gi_n * grid->c_step_n;
+      zo = gi_m * grid->bias_step_m;
+    } else {
+      ao = a_off ? a_off[g] : 0;
+      bo = b_off ? b_off[g] : 0;
+      co = c_off ? c_off[g] : 0;
+      zo = bias_off ? bias_off[g] : 0;
+    }
+    void* cg = (char*)c + co * es_c;
+    const float* zg = bias ? bias + zo : NULL;
+    double* rg = ref64 ? ref64 + s * (int64_t)d->m * d->n : NULL;
+    int rc;
+    if (d->kind == ORACLE_ADDRESS) {
+      const int64_t lo = begin[g], hi = begin[g + 1];
+      rc = (hi < lo) ? -1
+                     : brgemm_one(d, NULL, NULL, cg, zg, hi - lo, NULL, NULL,
+                                  ptrs_a ? ptrs_a + lo : NULL, ptrs_b ? ptrs_b + lo : NULL, rg);
+    } else {
+      const void* ag = a ? (const char*)a + ao * es_ab : NULL;
+      const void* bg = b ? (const char*)b + bo * es_ab : NULL;
+      rc = brgemm_one(d, ag, bg, cg, zg, count, offs_a, offs_b, NULL, NULL, rg);
+    }
+    if (rc != 0) failed |= 1;
+  }
+  return failed ? -1 : 0;
+}
+
+/* Reduce TPP (Table 1): fold rows or columns with SUM / MUL / MIN / MAX, of x or of x*x.
+ * SUM starts at 0, MUL at 1; MIN and MAX start from the first element. */
+static double fold(int32_t op, double acc, double v) {
+  switch (op) {
+    case ORACLE_RED_SUM: return acc + v;
+    case ORACLE_RED_MUL: return acc * v;
+    case ORACLE_RED_MIN: return v < acc ? v : acc;
+    default: return v > acc ? v : acc;
+  }
+}
+
+int oracle_reduce(int32_t m, int32_t n, int64_t ld, int32_t in_type, const void* in,
+                  int32_t op, uint32_t flags, double* out_x, double* out_x2) {
+  if (m <= 0 || n <= 0 || ld < m || !in) return -1;
+  if (in_type != ORACLE_F32 && in_type != ORACLE_BF16) return -1;
+  if (op < ORACLE_RED_SUM || op > ORACLE_RED_MAX) return -1;
+  const int by_cols = (flags & ORACLE_RED_BY_COLS) != 0;
+  const int by_rows = (flags & ORACLE_RED_BY_ROWS) != 0;
+  if (by_cols == by_rows) return -1;
+  if (!(flags & (ORACLE_RED_X | ORACLE_RED_X2))) return -1;
+  if ((flags & ORACLE_RED_X) && !out_x) return -1;
+  if ((flags & ORACLE_RED_X2) && !out_x2) return -1;
+  const int32_t outer = by_cols ? m : n;
+  const int32_t inner = by_cols ? n : m;
+  for (int32_t o = 0; o < outer; ++o) {
+    double ax = 0.0, ax2 = 0.0;
+    for (int32_t t = 0; t < inner; ++t) {
+      const int32_t row = by_cols ? o : t;
+      const int32_t col = by_cols ? t : o;
+      const double x = oracle_widen(in, (int64_t)row + (int64_t)col * ld, in_type);
+      if (t == 0) {
+        ax = (op == ORACLE_RED_MUL) ? 1.0 : (op == ORACLE_RED_SUM ? 0.0 : x);
+        ax2 = (op == ORACLE_RED_MUL) ? 1.0 : (op == ORACLE_RED_SUM ? 0.0 : x * x);
+        if (op == ORACLE_RED_MIN || op == ORACLE_RED_MAX) continue;
+      }
+      ax = fold(op, ax, x);
+      ax2 = fold(op, ax2, x * x);
+    }
+    if (flags & ORACLE_RED_X) out_x[o] = ax;
+    if (flags & ORACLE_RED_X2) out_x2[o] = ax2;
+  }
+  return 0;
+}

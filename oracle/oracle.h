@@ -1,0 +1,88 @@
+/*
+ * oracle.h -- plain CPU reference for the batch-reduce GEMM TPP and the Reduce TPP.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing on the product path may include, link or call this code;
+ * only the test suite, the smoke check and the benchmark's CPU-baseline leg use it.  It shares
+ * no header, helper, table or constant with the HIP library: every definition below is its own.
+ *
+ * What it computes (Tensor Processing Primitives, arXiv 2104.05755):
+ *   - Ternary BRGEMM TPP, Table 3 and Sec. 2.3: C = beta*C + sum_{i<n} A_i x B_i, with the three
+ *     block-addressing variants of Sec. 2.3 (address-, offset- and stride-based).
+ *   - The unary/binary TPPs fused after it (Sec. 2.1 principle 5; Table 1 Identity-with-conversion,
+ *     RELU, GELU; Table 2 Add with column broadcast, Sec. 2.2), applied as Alg. 6 applies its UNARY
+ *     to the finished C block.
+ *   - Unary Reduce TPP, Table 1 and Sec. 3.1 (reduction-by-columns turns M x N into M x 1).
+ *
+ * Storage reading: every 2D block is column-major with a leading dimension (element (r, c) of an
+ * m x n block sits at base + r + c*ld), which is how Alg. 6 lays out its blocked tensors (the
+ * b_m / b_k index innermost).  Strides and offsets count elements of the operand's own type.
+ * Arithmetic is fp64; bf16 values widen exactly (bf16 is the top half of an fp32, Sec. 3.2.2).
+ */
+#ifndef TPP_ORACLE_H
+#define TPP_ORACLE_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum { ORACLE_F32 = 0, ORACLE_BF16 = 1 };
+enum { ORACLE_STRIDE = 0, ORACLE_OFFSET = 1, ORACLE_ADDRESS = 2 };
+enum { ORACLE_EPI_BIAS = 1u, ORACLE_EPI_RELU = 2u, ORACLE_EPI_GELU_TANH = 4u };
+enum { ORACLE_RED_SUM = 0, ORACLE_RED_MUL = 1, ORACLE_RED_MIN = 2, ORACLE_RED_MAX = 3 };
+enum { ORACLE_RED_BY_COLS = 1u, ORACLE_RED_BY_ROWS = 2u, ORACLE_RED_X = 4u, ORACLE_RED_X2 = 8u };
+
+typedef struct {
+  int32_t m, n, k;           /* C is m x n, A_i is m x k, B_i is k x n                        */
+  int64_t lda, ldb, ldc;     /* leading dimensions, elements                                    */
+  int32_t ab_type;           /* ORACLE_F32 or ORACLE_BF16 (A and B share it)                   */
+  int32_t c_type;            /* ORACLE_F32 or ORACLE_BF16                                       */
+  double  beta;              /* 0 => C is not read                                              */
+  int32_t kind;              /* ORACLE_STRIDE / ORACLE_OFFSET / ORACLE_ADDRESS                  */
+  int64_t stride_a, stride_b;/* elements, stride variant                                        */
+  uint32_t flags;            /* ORACLE_EPI_* bits                                               */
+} oracle_desc;
+
+typedef struct { int64_t gm, gn, a_step_m, b_step_n, c_step_m, c_step_n, bias_step_m; } oracle_grid;
+
+/* One BRGEMM call (the paper's call API).  a/b: base addresses (stride, offset variants);
+ * offs_a/offs_b: count element offsets (offset variant); ptrs_a/ptrs_b: count block addresses
+ * (address variant).  bias: m floats (ORACLE_EPI_BIAS).  ref64 (optional): m*n doubles,
+ * column-major with ld m, receiving the unrounded result.  Returns 0, or -1 on bad arguments. */
+int oracle_brgemm(const oracle_desc* d, const void* a, const void* b, void* c, const float* bias,
+                  int64_t count, const int64_t* offs_a, const int64_t* offs_b,
+                  const void* const* ptrs_a, const void* const* ptrs_b, double* ref64);
+
+/* G independent calls (the outer loops of Alg. 6 / Alg. 7 around the BRGEMM).  Instance g's
+ * bases: strided form when grid != NULL (gi_m = g % gm, gi_n = g / gm), else the explicit
+ * per-instance offset arrays (any may be NULL = zeros).  Address variant: instance g reduces the
+ * pairs [begin[g], begin[g+1]) of ptrs_a/ptrs_b.  sel (optional, n_sel entries) restricts the
+ * work to those instances; ref64 then holds n_sel blocks of m*n doubles.  nthreads <= 0 uses
+ * the OpenMP default. */
+int oracle_brgemm_batched(const oracle_desc* d, const oracle_grid* grid, int64_t G,
+                          const int64_t* a_off, const int64_t* b_off, const int64_t* c_off,
+                          const int64_t* bias_off,
+                          const void* a, const void* b, void* c, const float* bias,
+                          int64_t count, const int64_t* offs_a, const int64_t* offs_b,
+                          const int64_t* begin, const void* const* ptrs_a, const void* const* ptrs_b,
+                          int64_t n_sel, const int64_t* sel, double* ref64, int nthreads);
+
+/* Reduce TPP on an m x n column-major tensor.  BY_COLS folds across the n columns (m outputs),
+ * BY_ROWS folds across the m rows (n outputs).  X / X2 select the input x or its square x*x;
+ * both may be set.  Outputs are unrounded doubles. */
+int oracle_reduce(int32_t m, int32_t n, int64_t ld, int32_t in_type, const void* in,
+                  int32_t op, uint32_t flags, double* out_x, double* out_x2);
+
+/* Helpers the tests pin on their own: exact widening and the round-to-nearest-even narrowing
+ * used for every output element. */
+double   oracle_widen(const void* base, int64_t idx, int32_t dtype);
+uint16_t oracle_f32_to_bf16(float f);
+void     oracle_f32_to_bf16_array(const float* in, uint16_t* out, int64_t n);
+float    oracle_bf16_to_f32(uint16_t h);
+double   oracle_gelu_tanh(double x);
+int      oracle_max_threads(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

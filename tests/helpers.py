@@ -1,0 +1,45 @@
+"""Shared test helpers: run a workload call through the oracle, compare results."""
+from __future__ import annotations
+
+import numpy as np
+
+import oracle
+from workloads import Call, Workload, bf16_values
+
+
+def oracle_desc(call: Call) -> oracle.Desc:
+    return oracle.Desc(call.m, call.n, call.k, call.lda, call.ldb, call.ldc, call.ab_type,
+                       call.c_type, call.beta, call.kind, call.stride_a, call.stride_b,
+                       set(call.flags))
+
+
+def run_oracle(wl: Workload, ci: int = 0, c_init=None, sel=None, want_ref64=False, nthreads=0):
+    """Run call ``ci`` of ``wl`` through the oracle on a copy of its C array.
+
+    Returns (c_out, ref64).  ``c_init`` overrides the C array (e.g. the output of an earlier
+    call for chained workloads)."""
+    call = wl.calls[ci]
+    arrs = wl.arrays
+    c = np.array(arrs[call.c] if c_init is None else c_init, copy=True)
+    bias = arrs[call.bias] if call.bias else None
+    ref = oracle.brgemm_batched(
+        oracle_desc(call), arrs[call.a], arrs[call.b], c, bias, grid=call.grid, G=call.G,
+        a_off=call.a_off, b_off=call.b_off, c_off=call.c_off, bias_off=call.bias_off,
+        count=call.count, offs_a=call.offs_a, offs_b=call.offs_b, begin=call.begin,
+        idx_a=call.idx_a, idx_b=call.idx_b, sel=sel, want_ref64=want_ref64, nthreads=nthreads)
+    return c, ref
+
+
+def values(arr: np.ndarray, dtype: str) -> np.ndarray:
+    """Numeric values of an operand array (bf16 bit patterns or fp32) as float64."""
+    if dtype == "bf16":
+        return bf16_values(arr).astype(np.float64)
+    return arr.astype(np.float64)
+
+
+def rel_fro(got: np.ndarray, ref: np.ndarray) -> float:
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    den = np.linalg.norm(ref)
+    num = np.linalg.norm(got - ref)
+    return float(num / den) if den > 0 else float(num)

@@ -1,0 +1,65 @@
+"""Plant plausible mistakes in copies of the oracle (on the CPU) and check that the pins catch
+every one: a dropped term, a wrong sign or index, a transposed operand, a wrong unit."""
+from __future__ import annotations
+
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "oracle.c")
+
+MUTANTS = {
+    "wrong_operand": ("s += x * y;", "s += x * x;"),
+    "transposed_a": ("(int64_t)row + (int64_t)p * d->lda", "(int64_t)p + (int64_t)row * d->lda"),
+    "transposed_b": ("(int64_t)p + (int64_t)col * d->ldb", "(int64_t)col + (int64_t)p * d->ldb"),
+    "dropped_k_term": ("for (int32_t p = 0; p < d->k; ++p)", "for (int32_t p = 1; p < d->k; ++p)"),
+    "dropped_pair": ("for (int64_t i = 0; i < count; ++i) {\n        for (int32_t p",
+                     "for (int64_t i = 1; i < count; ++i) {\n        for (int32_t p"),
+    "stride_recurrence": ("if (i > 0) {", "if (i > 1) {"),
+    "offset_in_bytes": ("out_a[i] = (const char*)a + offs_a[i] * es;",
+                        "out_a[i] = (const char*)a + offs_a[i];"),
+    "beta_dropped": ("v = d->beta * oracle_widen(c, ci, d->c_type) + s;",
+                     "v = oracle_widen(c, ci, d->c_type) + s;"),
+    "beta_zero_reads_c": ("if (d->beta != 0.0) v =", "if (1) v ="),
+    "bias_by_column": ("v += (double)bias[row];", "v += (double)bias[col % d->m];"),
+    "relu_sign": ("v = v > 0.0 ? v : 0.0;", "v = v < 0.0 ? v : 0.0;"),
+    "gelu_sign": ("(1.0 + tanh(", "(1.0 - tanh("),
+    "gelu_cubic": ("0.044715 * x * x * x", "0.044715 * x * x"),
+    "rne_ties_up": ("rest > 0x8000u ||", "rest >= 0x8000u ||"),
+    "grid_swapped": ("co = gi_m * grid->c_step_m + gi_n * grid->c_step_n;",
+                     "co = gi_n * grid->c_step_m + gi_m * grid->c_step_n;"),
+    "explicit_b_offset": ("bo = b_off ? b_off[g] : 0;", "bo = a_off ? a_off[g] : 0;"),
+    "csr_bounds": ("const int64_t lo = begin[g], hi = begin[g + 1];",
+                   "const int64_t lo = begin[g], hi = begin[g + 1] - (g > 0);"),
+    "reduce_square_dropped": ("ax2 = fold(op, ax2, x * x);", "ax2 = fold(op, ax2, x);"),
+    "reduce_direction": ("const int32_t row = by_cols ? o : t;", "const int32_t row = by_cols ? t : o;"),
+    "reduce_min_init": ("ax = (op == ORACLE_RED_MUL) ? 1.0 : (op == ORACLE_RED_SUM ? 0.0 : x);",
+                        "ax = (op == ORACLE_RED_MUL) ? 1.0 : 0.0;"),
+}
+
+
+@pytest.fixture(scope="module")
+def source():
+    with open(SRC) as f:
+        return f.read()
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_catch_planted_mistake(name, source, tmp_path):
+    old, new = MUTANTS[name]
+    assert source.count(old) == 1, f"mutation site for {name} not unique"
+    mutated = source.replace(old, new)
+    src = tmp_path / "oracle.c"
+    src.write_text(mutated)
+    (tmp_path / "oracle.h").write_text(open(os.path.join(ROOT, "oracle", "oracle.h")).read())
+    so = tmp_path / "liboracle_mutant.so"
+    subprocess.run(["gcc", "-O1", "-fopenmp", "-fPIC", "-shared", "-std=c11", "-o", str(so),
+                    str(src), "-lm"], check=True)
+    env = dict(os.environ, ORACLE_LIB_OVERRIDE=str(so), OMP_NUM_THREADS="2")
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                        os.path.join(ROOT, "tests", "test_oracle_pins.py")],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    assert r.returncode != 0, f"no pin caught mutant {name}:\n{r.stdout[-2000:]}"

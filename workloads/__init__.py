@@ -1,0 +1,267 @@
+"""Seeded synthetic inputs for the batch-reduce GEMM TPP workloads.
+
+This module is the one piece shared by the oracle side (tests, CPU baseline) and the HIP side
+(tests, benchmark): it draws random numbers and lays them out, and holds none of the method's
+arithmetic.  bf16 inputs are fp32 samples rounded by torch's CPU conversion (a library routine),
+stored as ``uint16`` bit patterns; fp32 inputs are ``float32``.
+
+Workloads (all blocks column-major with a leading dimension, i.e. element (r, c) of a block at
+base + r + c*ld, the way Alg. 6 lays out its blocked tensors with the b_m / b_k index innermost):
+
+  fp32_single   one stride-based fp32 BRGEMM, m = n = k = 64, 16 pairs, beta = 0
+  mlp_fc        fully-connected forward on the blocked layout of Alg. 6, bias + ReLU, bf16 out
+  conv3x3       3x3 convolution (stride 1, pad 1) on NCHWc with c = 64 as an offset-based BRGEMM
+                per output row (Sec. 5.1.4), ReLU, bf16 out
+  mlp_block     transformer MLP: 1024 -> 4096 (bias + GELU-tanh) -> 1024 (bias), bf16 blocked
+  gathered      address-based BRGEMM over seeded random block lists (8..64 pairs per output
+                block) drawn from pools of blocks, beta = 1, fp32 out
+  reduce_bn     the Reduce TPP on a conv output: per-channel sum and sum of squares (the
+                statistics step of batchnorm, Sec. 5.1.2)
+
+The default sizes are the full sizes; every generator takes smaller sizes for oracle-speed tests.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import Optional
+
+import numpy as np
+import torch
+
+BLK = 64
+
+
+def bf16_bits(x: np.ndarray) -> np.ndarray:
+    """fp32 samples -> bf16 bit patterns (uint16), rounded by torch's CPU conversion."""
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32))
+    return t.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16).copy()
+
+
+def bf16_values(bits: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns -> the fp32 values they denote (a reinterpretation, no rounding)."""
+    return (bits.astype(np.uint32) << 16).view(np.float32)
+
+
+@dataclass
+class Call:
+    """One batched BRGEMM call: descriptor fields + instance grid + operand arrays (host)."""
+    m: int
+    n: int
+    k: int
+    lda: int
+    ldb: int
+    ldc: int
+    ab_type: str
+    c_type: str
+    beta: float
+    kind: str
+    stride_a: int = 0
+    stride_b: int = 0
+    flags: set = field(default_factory=set)
+    G: int = 1
+    grid: Optional[dict] = None            # strided form
+    a_off: Optional[np.ndarray] = None     # explicit form (element offsets per instance)
+    b_off: Optional[np.ndarray] = None
+    c_off: Optional[np.ndarray] = None
+    bias_off: Optional[np.ndarray] = None
+    count: int = 0
+    offs_a: Optional[np.ndarray] = None    # offset variant
+    offs_b: Optional[np.ndarray] = None
+    begin: Optional[np.ndarray] = None     # address variant: CSR over pairs
+    idx_a: Optional[np.ndarray] = None     # address variant: element offsets into the pools
+    idx_b: Optional[np.ndarray] = None
+    a: Optional[str] = None                # names of the arrays in Workload.arrays
+    b: Optional[str] = None
+    c: Optional[str] = None
+    bias: Optional[str] = None
+
+    @property
+    def pairs(self) -> int:
+        if self.kind == "address":
+            return int(self.begin[-1] - self.begin[0])
+        return self.G * self.count
+
+    @property
+    def flops(self) -> int:
+        """Algorithmic FLOPs: 2*m*n*k per multiplied pair of blocks."""
+        return 2 * self.m * self.n * self.k * self.pairs
+
+
+@dataclass
+class Workload:
+    name: str
+    arrays: dict
+    calls: list
+    reduce: Optional[dict] = None
+    notes: str = ""
+
+    @property
+    def flops(self) -> int:
+        return sum(c.flops for c in self.calls)
+
+
+def _uniform(rng, shape):
+    return rng.uniform(-1.0, 1.0, size=shape).astype(np.float32)
+
+
+def _normal(rng, shape, std):
+    return (rng.standard_normal(size=shape) * std).astype(np.float32)
+
+
+def fp32_single(seed: int = 1, m: int = 64, n: int = 64, k: int = 64, count: int = 16) -> Workload:
+    rng = np.random.default_rng(seed)
+    a = _uniform(rng, (count, k, m))          # block i: m x k, column-major, lda = m
+    b = _uniform(rng, (count, n, k))          # block i: k x n, column-major, ldb = k
+    c = np.full((n, m), np.nan, dtype=np.float32)
+    call = Call(m, n, k, m, k, m, "f32", "f32", 0.0, "stride", m * k, k * n, set(), G=1,
+                grid=dict(gm=1, gn=1, a_step_m=0, b_step_n=0, c_step_m=0, c_step_n=0, bias_step_m=0),
+                count=count, a="a", b="b", c="c")
+    return Workload("fp32_single", dict(a=a, b=b, c=c), [call])
+
+
+def mlp_fc(seed: int = 2, minibatch: int = 2048, c_in: int = 1024, k_out: int = 1024) -> Workload:
+    """Alg. 6: A = W[Kb][Cb][b_c][b_k] (A role, m = output feature), B = X[Nb][Cb][b_n][b_c]."""
+    rng = np.random.default_rng(seed)
+    nb, cb, kb = minibatch // BLK, c_in // BLK, k_out // BLK
+    x = bf16_bits(_uniform(rng, (nb, cb, BLK, BLK)))
+    w = bf16_bits(_uniform(rng, (kb, cb, BLK, BLK)))
+    bias = _uniform(rng, (k_out,))
+    out = np.full((nb, kb, BLK, BLK), 0x7FC0, dtype=np.uint16)   # NaN-filled, beta = 0
+    blk = BLK * BLK
+    call = Call(BLK, BLK, BLK, BLK, BLK, BLK, "bf16", "bf16", 0.0, "stride", blk, blk,
+                {"bias", "relu"}, G=kb * nb,
+                grid=dict(gm=kb, gn=nb, a_step_m=cb * blk, b_step_n=cb * blk, c_step_m=blk,
+                          c_step_n=kb * blk, bias_step_m=BLK),
+                count=cb, a="w", b="x", c="out", bias="bias")
+    return Workload("mlp_fc", dict(x=x, w=w, bias=bias, out=out), [call])
+
+
+def conv3x3(seed: int = 3, images: int = 28, h: int = 56, w: int = 56, c: int = 64,
+            k: int = 64) -> Workload:
+    """3x3 convolution, stride 1, pad 1, as an offset-based BRGEMM per output row.
+
+    Input I[img][H][W][c] (NCHWc with one channel block), zero-padded by a setup copy to
+    [img][H+2][W+2][c].  Weights Wt[r][s][c][k] (k innermost): the A block for tap (r, s) is the
+    k x c matrix at Wt[r][s], column-major with lda = k.  Instance (img, oj) computes output row
+    oj: C = out[img][oj] (k x W, ldc = k), pairs (r, s) with B block = the c x W slab of the padded
+    input starting at [img][oj + r][s], ldb = c.
+    """
+    rng = np.random.default_rng(seed)
+    x = bf16_bits(_normal(rng, (images, h, w, c), 0.1))
+    wt = bf16_bits(_normal(rng, (3, 3, c, k), 0.1))
+    xp = np.zeros((images, h + 2, w + 2, c), dtype=np.uint16)
+    xp[:, 1:h + 1, 1:w + 1, :] = x
+    out = np.full((images, h, w, k), 0x7FC0, dtype=np.uint16)
+    taps = [(r, s) for r in range(3) for s in range(3)]
+    offs_a = np.array([(r * 3 + s) * c * k for r, s in taps], dtype=np.int64)
+    offs_b = np.array([(r * (w + 2) + s) * c for r, s in taps], dtype=np.int64)
+    img, oj = np.meshgrid(np.arange(images), np.arange(h), indexing="ij")
+    b_off = ((img * (h + 2) * (w + 2) + oj * (w + 2)) * c).reshape(-1).astype(np.int64)
+    c_off = ((img * h * w + oj * w) * k).reshape(-1).astype(np.int64)
+    call = Call(k, w, c, k, c, k, "bf16", "bf16", 0.0, "offset", 0, 0, {"relu"}, G=images * h,
+                a_off=np.zeros(images * h, dtype=np.int64), b_off=b_off, c_off=c_off,
+                count=9, offs_a=offs_a, offs_b=offs_b, a="wt", b="xp", c="out")
+    return Workload("conv3x3", dict(x=x, wt=wt, xp=xp, out=out), [call],
+                    reduce=dict(src="out", m=k, n=images * h * w, ld=k, in_type="bf16", op="sum",
+                                by="cols", want=("x", "x2")))
+
+
+def mlp_block(seed: int = 4, tokens: int = 8192, hidden: int = 1024, inter: int = 4096) -> Workload:
+    """Transformer MLP as two blocked stride-based BRGEMM calls (Alg. 6 twice)."""
+    rng = np.random.default_rng(seed)
+    nb, hb, ib = tokens // BLK, hidden // BLK, inter // BLK
+    blk = BLK * BLK
+    x = bf16_bits(_normal(rng, (nb, hb, BLK, BLK), 1.0))
+    w1 = bf16_bits(_normal(rng, (ib, hb, BLK, BLK), 0.02))
+    b1 = _normal(rng, (inter,), 0.02)
+    w2 = bf16_bits(_normal(rng, (hb, ib, BLK, BLK), 0.02))
+    b2 = _normal(rng, (hidden,), 0.02)
+    hmid = np.full((nb, ib, BLK, BLK), 0x7FC0, dtype=np.uint16)
+    y = np.full((nb, hb, BLK, BLK), 0x7FC0, dtype=np.uint16)
+    g1 = Call(BLK, BLK, BLK, BLK, BLK, BLK, "bf16", "bf16", 0.0, "stride", blk, blk,
+              {"bias", "gelu_tanh"}, G=ib * nb,
+              grid=dict(gm=ib, gn=nb, a_step_m=hb * blk, b_step_n=hb * blk, c_step_m=blk,
+                        c_step_n=ib * blk, bias_step_m=BLK),
+              count=hb, a="w1", b="x", c="h", bias="b1")
+    g2 = Call(BLK, BLK, BLK, BLK, BLK, BLK, "bf16", "bf16", 0.0, "stride", blk, blk,
+              {"bias"}, G=hb * nb,
+              grid=dict(gm=hb, gn=nb, a_step_m=ib * blk, b_step_n=ib * blk, c_step_m=blk,
+                        c_step_n=hb * blk, bias_step_m=BLK),
+              count=ib, a="w2", b="h", c="y", bias="b2")
+    return Workload("mlp_block", dict(x=x, w1=w1, b1=b1, w2=w2, b2=b2, h=hmid, y=y), [g1, g2])
+
+
+def gathered(seed: int = 5, n_out: int = 4096, pool: int = 8192, m: int = 128, n: int = 128,
+             k: int = 64, min_len: int = 8, max_len: int = 64) -> Workload:
+    """Address-based BRGEMM: each output block reduces a random list of (A, B) pool blocks.
+
+    List lengths are uniform on {min_len..max_len}; A and B indices are independent, uniform on
+    the pool, with replacement.  A pool block is m x k (lda = m), a B pool block k x n (ldb = k).
+    """
+    rng = np.random.default_rng(seed)
+    apool = bf16_bits(_uniform(rng, (pool, k, m)))
+    bpool = bf16_bits(_uniform(rng, (pool, n, k)))
+    c = _uniform(rng, (n_out, n, m))
+    lens = rng.integers(min_len, max_len + 1, size=n_out)
+    begin = np.zeros(n_out + 1, dtype=np.int64)
+    begin[1:] = np.cumsum(lens)
+    ia = rng.integers(0, pool, size=int(begin[-1]))
+    ib = rng.integers(0, pool, size=int(begin[-1]))
+    call = Call(m, n, k, m, k, m, "bf16", "f32", 1.0, "address", 0, 0, set(), G=n_out,
+                c_off=(np.arange(n_out, dtype=np.int64) * m * n), begin=begin,
+                idx_a=(ia * m * k).astype(np.int64), idx_b=(ib * k * n).astype(np.int64),
+                a="apool", b="bpool", c="c")
+    return Workload("gathered", dict(apool=apool, bpool=bpool, c=c), [call])
+
+
+CONFIGS = {
+    1: fp32_single,
+    2: mlp_fc,
+    3: conv3x3,
+    4: mlp_block,
+    5: gathered,
+}
+
+
+def small_case(rng: np.random.Generator, m: int, n: int, k: int, count: int, kind: str,
+               ab_type: str, c_type: str, beta: float, flags: set, pad: int = 0,
+               integer: bool = False) -> Workload:
+    """One random BRGEMM call of arbitrary shape for sweeps.
+
+    Operands live in one pool per side; the pairs are laid out per ``kind`` (stride: blocks
+    ``stride`` apart; offset: a shuffled list of block offsets; address: a shuffled list of
+    block addresses, with repeats).  ``pad`` widens every leading dimension.  ``integer`` draws
+    small integers (exact in bf16 and in fp32 sums) for bit-exact checks.
+    """
+    lda, ldb, ldc = m + pad, k + pad, m + pad
+    a_blk, b_blk = lda * k, ldb * n
+    nblk = max(count, 1) + 2
+    draw = (lambda shape: rng.integers(-4, 5, size=shape).astype(np.float32)) if integer \
+        else (lambda shape: _uniform(rng, shape))
+    conv = (lambda v: v) if ab_type == "f32" else bf16_bits
+    a = conv(draw((nblk * a_blk,)))
+    b = conv(draw((nblk * b_blk,)))
+    cval = draw((n * ldc,))
+    c = cval if c_type == "f32" else bf16_bits(cval)
+    if beta == 0.0:
+        c = np.full_like(c, np.nan) if c_type == "f32" else np.full_like(c, 0x7FC0)
+    bias = draw((m,)) if "bias" in flags else None
+    call = Call(m, n, k, lda, ldb, ldc, ab_type, c_type, beta, kind, flags=set(flags), G=1,
+                a="a", b="b", c="c", bias="bias" if bias is not None else None)
+    if kind == "stride":
+        call.stride_a, call.stride_b = a_blk, b_blk
+        call.count = count
+        call.grid = dict(gm=1, gn=1, a_step_m=0, b_step_n=0, c_step_m=0, c_step_n=0,
+                         bias_step_m=0)
+    elif kind == "offset":
+        call.count = count
+        call.offs_a = (rng.permutation(nblk)[:count] * a_blk).astype(np.int64)
+        call.offs_b = (rng.permutation(nblk)[:count] * b_blk).astype(np.int64)
+    else:
+        call.begin = np.array([0, count], dtype=np.int64)
+        call.idx_a = (rng.integers(0, nblk, size=count) * a_blk).astype(np.int64)
+        call.idx_b = (rng.integers(0, nblk, size=count) * b_blk).astype(np.int64)
+    arrays = dict(a=a, b=b, c=c)
+    if bias is not None:
+        arrays["bias"] = bias
+    return Workload("small", arrays, [call])
