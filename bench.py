@@ -1,0 +1,214 @@
+#!/usr/bin/env python3
+"""Benchmark of the MI355X batch-reduce GEMM TPP path.
+
+Headline step: the transformer-encoder MLP block (8192 tokens, 1024 -> 4096 with fused bias +
+GELU-tanh, then 4096 -> 1024 with fused bias), bf16 blocked 64x64 tiles, fp32 accumulation:
+two batched BRGEMM launches (8192 instances x 16 pairs, then 2048 instances x 64 pairs).
+``value`` is BRGEMM TFLOP/s over K timed steps (inputs resident in HBM).  The same run also
+times the other workloads (fp32 single BRGEMM, MLP fully-connected layer, 3x3 convolution with
+batchnorm statistics via the Reduce TPP, gathered address-based BRGEMM) under ``per_config``,
+and the CPU oracle on a bounded sample of the headline workload under ``cpu_baseline``.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
+Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+# MI355X published peaks (dense): bf16 MFMA, fp32 MFMA, HBM3E.
+PEAK_BF16_TFLOPS = 2516.6
+PEAK_F32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="target wall time of the oracle CPU baseline sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-per-config", action="store_true")
+    return ap.parse_args()
+
+
+def array_bytes(a) -> int:
+    return int(a.nbytes)
+
+
+def alg_bytes(wl, call) -> int:
+    """Compulsory HBM bytes of one call: its operand arrays once, C written (and read when
+    beta != 0), bias, offset / pointer lists."""
+    arrs = wl.arrays
+    n = array_bytes(arrs[call.a]) + array_bytes(arrs[call.b])
+    c_elems = call.G * call.m * call.n
+    es_c = 4 if call.c_type == "f32" else 2
+    n += c_elems * es_c * (2 if call.beta != 0.0 else 1)
+    if call.bias:
+        n += array_bytes(arrs[call.bias])
+    if call.kind == "address":
+        n += 16 * call.pairs + 8 * (call.G + 1)
+    return n
+
+
+def time_launches(fns, steps, warmup, torch):
+    """Run each fn in order per step; returns (elapsed_s, per-fn mean ms from HIP events)."""
+    for _ in range(warmup):
+        for f in fns:
+            f()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(fns) + 1)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(steps):
+        for i, f in enumerate(fns):
+            evs[s][i].record()
+            f()
+        evs[s][-1].record()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    per = [sum(evs[s][i].elapsed_time(evs[s][i + 1]) for s in range(steps)) / steps
+           for i in range(len(fns))]
+    return elapsed, per
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no "
+              "multi-GPU path", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import paper_2104_05755_amd as tpp
+    from paper_2104_05755_amd import torch_io
+    import workloads as wk
+
+    torch.cuda.init()
+    dev_name = torch.cuda.get_device_name(0)
+    stream = tpp.current_stream()
+
+    # ---------------- headline: transformer MLP block ----------------
+    wl = wk.mlp_block()
+    dev = torch_io.upload(wl)
+    dcs = [torch_io.prepare(c, dev) for c in wl.calls]
+    fns = [lambda dc=dc: torch_io.launch(dc, stream) for dc in dcs]
+    elapsed, per = time_launches(fns, args.steps, args.warmup, torch)
+    flops_step = wl.flops
+    value = flops_step * args.steps / elapsed / 1e12
+    kernel_names = [tpp.tpp_brgemm_describe(dc.handle) for dc in dcs]
+    # dominant kernel = the launch with the largest mean duration
+    dom = int(np.argmax(per))
+    dom_flops = wl.calls[dom].flops
+    achieved = dom_flops / (per[dom] * 1e-3) / 1e12
+    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "kernel": f"call {dom} ({'GEMM1 1024->4096 bias+GELU' if dom == 0 else 'GEMM2 4096->1024 bias'})",
+                "launch_ms": round(per[dom], 4), "flops_per_launch": dom_flops}
+    result = {
+        "metric": "BRGEMM TFLOP/s (bf16, fp32 acc) and % of MFMA peak per config",
+        "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(elapsed / args.steps * 1e3, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded numpy draws, bf16-rounded; no dataset, random-init weights)",
+        "config": {"workload": "transformer MLP block as blocked BRGEMM: 8192 tokens, "
+                               "1024->4096 (bias+GELU-tanh) -> 1024 (bias), bf16 64x64 blocks",
+                   "tokens": 8192, "hidden": 1024, "intermediate": 4096,
+                   "instances": [c.G for c in wl.calls], "pairs_per_instance": [c.count for c in wl.calls],
+                   "flops_per_step": flops_step, "kernels": kernel_names,
+                   "launch_ms": [round(x, 4) for x in per], "device": dev_name},
+        "roofline": roofline,
+    }
+    del dev, dcs, fns
+    torch.cuda.empty_cache()
+
+    if not args.no_per_config:
+        result["per_config"] = per_config(args, torch, tpp, torch_io, wk, np, stream)
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = run_cpu_baseline(args.cpu_seconds, wl)
+    print(json.dumps(result), flush=True)
+
+
+def per_config(args, torch, tpp, torch_io, wk, np, stream):
+    """Each of the other workloads: one launch per call (plus the reduce for the convolution),
+    timed with HIP events over max(steps, 50) launches after the warmup."""
+    out = {}
+    steps = max(args.steps, 50)
+    for cfg in (1, 2, 3, 5):
+        wl = wk.CONFIGS[cfg]()
+        dev = torch_io.upload(wl)
+        dcs = [torch_io.prepare(c, dev) for c in wl.calls]
+        fns = [lambda dc=dc: torch_io.launch(dc, stream) for dc in dcs]
+        red = None
+        if wl.reduce is not None:
+            r = wl.reduce
+            ox = torch.empty(r["m"], device="cuda")
+            ox2 = torch.empty(r["m"], device="cuda")
+            src = dev[r["src"]]
+            flags = tpp.TPP_RED_BY_COLS | tpp.TPP_RED_X | tpp.TPP_RED_X2
+
+            def red_fn(src=src, r=r, ox=ox, ox2=ox2, flags=flags):
+                tpp.tpp_reduce(r["m"], r["n"], r["ld"], tpp.TPP_DT_BF16, src, tpp.TPP_RED_SUM,
+                               flags, ox, ox2, stream)
+            red = red_fn
+            fns.append(red)
+        elapsed, per = time_launches(fns, steps, args.warmup, torch)
+        call = wl.calls[0]
+        ms = per[0]
+        flops = call.flops
+        tfl = flops / (ms * 1e-3) / 1e12
+        byts = alg_bytes(wl, call)
+        gbs = byts / (ms * 1e-3) / 1e9
+        peak = PEAK_F32_TFLOPS if call.ab_type == "f32" else PEAK_BF16_TFLOPS
+        entry = {"workload": wl.name, "kernel": tpp.tpp_brgemm_describe(dcs[0].handle),
+                 "instances": call.G, "pairs": call.pairs, "launch_us": round(ms * 1e3, 2),
+                 "tflops": round(tfl, 2), "mfma_frac": round(tfl / peak, 4),
+                 "alg_bytes": byts, "hbm_gbs": round(gbs, 1),
+                 "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)}
+        if red is not None:
+            rb = wl.reduce["m"] * wl.reduce["n"] * 2 + 8 * wl.reduce["m"]
+            entry["reduce"] = {"what": "per-channel sum and sum of squares of the conv output "
+                                       "(Reduce TPP, by columns, bf16 in)",
+                               "launch_us": round(per[1] * 1e3, 2), "alg_bytes": rb,
+                               "hbm_gbs": round(rb / (per[1] * 1e-3) / 1e9, 1),
+                               "hbm_frac": round(rb / (per[1] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+        out[str(cfg)] = entry
+        del dev, dcs, fns
+        torch.cuda.empty_cache()
+    return out
+
+
+def run_cpu_baseline(seconds: float, wl):
+    """Time the oracle (as it is) on growing samples of GEMM1 instances of the headline workload
+    until the sample takes about `seconds`; report TFLOP/s on the threads it used."""
+    import numpy as np
+    import oracle
+    sys.path.insert(0, os.path.join(os.path.dirname(os.path.abspath(__file__)), "tests"))
+    from helpers import run_oracle
+    call = wl.calls[0]
+    rng = np.random.default_rng(0)
+    n = 16
+    while True:
+        sel = np.sort(rng.choice(call.G, size=min(n, call.G), replace=False))
+        t0 = time.perf_counter()
+        run_oracle(wl, 0, sel=sel)
+        dt = time.perf_counter() - t0
+        if dt >= seconds * 0.5 or n >= call.G:
+            break
+        n = min(call.G, max(2 * n, int(n * seconds / max(dt, 1e-3))))
+    flops = 2 * call.m * call.n * call.k * call.count * len(sel)
+    return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": oracle.max_threads(),
+            "kind": "oracle",
+            "sample": f"{len(sel)} of {call.G} GEMM1 instances (64x64 output block, 16 pairs of "
+                      f"64x64x64) of the headline workload, fp64 loops, {dt:.1f} s"}
+
+
+if __name__ == "__main__":
+    main()

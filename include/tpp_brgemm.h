@@ -1,0 +1,175 @@
+/*
+ * tpp_brgemm.h -- C ABI of the MI355X (gfx950) batch-reduce GEMM TPP library.
+ *
+ * Tensor Processing Primitives (arXiv 2104.05755).  The library exposes the paper's two-step
+ * usage (Sec. 3: a dispatch call that prepares a kernel for a problem description and returns a
+ * handle, and a call that runs it) for two TPPs:
+ *
+ *   - the ternary batch-reduce GEMM, Table 3 and Sec. 2.3:
+ *         C = beta * C + sum_{i=0}^{count-1} A_i x B_i
+ *     with the blocks A_i (m x k) and B_i (k x n) named by one of the three variants of Sec. 2.3
+ *     (stride-, offset- or address-based), followed by the unary/binary TPPs fused as its
+ *     epilogue (Sec. 2.1 principle 5; Table 2 Add with a column broadcast, Sec. 2.2; Table 1 RELU,
+ *     GELU and Identity-with-conversion), applied to the finished C block as Alg. 6 applies its
+ *     UNARY:  C = cvt( act( beta * C + sum_i A_i B_i + bias[row] ) );
+ *   - the unary Reduce TPP, Table 1 (rows or columns, SUM / MUL / MIN / MAX, of x or x*x).
+ *
+ * Conventions for every entry point
+ *   - 2D blocks are column-major with a leading dimension: element (r, c) of an m x n block lives
+ *     at base + r + c * ld (the storage of Alg. 6's blocked tensors, whose b_m / b_k index is
+ *     innermost).  Leading dimensions, strides and offsets count ELEMENTS of the operand's type.
+ *   - Tensors, offset arrays, pointer arrays and CSR arrays are caller-owned DEVICE memory
+ *     (Sec. 2.1 principle 3: memory-to-memory operations on user memory).  The library never
+ *     frees or retains them past the call.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).  Execute calls are
+ *     asynchronous on it and never synchronise; device faults surface at the caller's next sync.
+ *   - Every call returns a tpp_status; nothing throws or aborts across the ABI.  On error,
+ *     tpp_last_error_message() (per thread) says what was wrong.
+ *   - Two instances of one call writing overlapping C, or C overlapping an A_i / B_i, is
+ *     undefined.  A and B may alias each other (Sec. 2.3).
+ */
+#ifndef TPP_BRGEMM_H
+#define TPP_BRGEMM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  TPP_OK = 0,
+  TPP_ERR_INVALID_ARG = -1,   /* a size, pointer, flag or handle is not acceptable            */
+  TPP_ERR_UNSUPPORTED = -2,   /* well-formed, but a type combination this build does not do  */
+  TPP_ERR_HIP = -4,           /* a HIP runtime call failed (launch, device query, memory)    */
+  TPP_ERR_NO_MEMORY = -5      /* a host or device allocation failed                         */
+} tpp_status;
+
+typedef enum { TPP_DT_F32 = 0, TPP_DT_BF16 = 1 } tpp_datatype;
+
+/* The three block-addressing variants of Sec. 2.3. */
+typedef enum {
+  TPP_BR_STRIDE = 0,   /* address_A_i = address_A_{i-1} + stride_a (elements), A_0 = a        */
+  TPP_BR_OFFSET = 1,   /* address_A_i = a + offs_a[i]                                          */
+  TPP_BR_ADDRESS = 2   /* address_A_i = ptrs_a[i]                                               */
+} tpp_br_kind;
+
+/* Epilogue bits.  RELU and GELU_TANH exclude each other. */
+enum {
+  TPP_EPI_BIAS = 1u << 0,      /* + bias[row]: fp32 column vector of length m, broadcast over n  */
+  TPP_EPI_RELU = 1u << 1,      /* x > 0 ? x : +0                                                 */
+  TPP_EPI_GELU_TANH = 1u << 2  /* 0.5 x (1 + tanh(sqrt(2/pi) (x + 0.044715 x^3)))                */
+};
+
+/* Problem description: the dispatch-time fields of the TPP (Sec. 2.2: rows, columns, leading
+ * dimension and datatype of every 2D operand, plus flags; Sec. 2.3: the batch variant). */
+typedef struct {
+  int32_t m, n, k;          /* C: m x n, A_i: m x k, B_i: k x n; all > 0                     */
+  int64_t lda, ldb, ldc;    /* lda >= m, ldb >= k, ldc >= m                                    */
+  int32_t a_type, b_type;   /* tpp_datatype: {F32, F32} or {BF16, BF16}                        */
+  int32_t c_type;           /* F32 or BF16: type of C, read when beta != 0 and written        */
+  int32_t comp_type;        /* accumulation type: F32 (the only one)                           */
+  float beta;               /* 0 => C is not read (NaN in C does not propagate)                */
+  int32_t kind;             /* tpp_br_kind                                                     */
+  int64_t stride_a;         /* TPP_BR_STRIDE: element stride between consecutive A_i           */
+  int64_t stride_b;         /* TPP_BR_STRIDE: element stride between consecutive B_i           */
+  uint32_t flags;           /* TPP_EPI_* bits                                                  */
+} tpp_brgemm_desc;
+
+/* Opaque kernel handle, owned by the library's process-wide cache (never freed by the caller). */
+typedef struct tpp_brgemm_kernel_s* tpp_brgemm_handle;
+
+/* Dispatch (Sec. 3): validate the description and return the cached handle for it; equal
+ * descriptions return the same handle.  Host-only: no device work, safe without a GPU.
+ * Errors: INVALID_ARG for sizes <= 0, ld too small, RELU together with GELU_TANH, unknown kind
+ * or flag bits, NULL desc/out; UNSUPPORTED for other type combinations. */
+tpp_status tpp_brgemm_dispatch(const tpp_brgemm_desc* desc, tpp_brgemm_handle* out);
+
+/* The call API for one BRGEMM (Sec. 2.3 / Alg. 2): C = epi(beta C + sum_{i<count} A_i B_i).
+ * count == 0 is valid and gives epi(beta C).  bias (device, m floats) is required iff the
+ * handle has TPP_EPI_BIAS.  The kind-specific calls reject a handle of another kind.
+ *   stride:  A_i = a + i * stride_a, B_i = b + i * stride_b
+ *   offset:  A_i = a + offs_a[i],    B_i = b + offs_b[i]      (device int64 arrays, elements)
+ *   address: A_i = ptrs_a[i],        B_i = ptrs_b[i]          (device arrays of device pointers)
+ * Errors: INVALID_ARG for a NULL handle, count < 0, or a NULL pointer the call needs. */
+tpp_status tpp_brgemm_execute_stride(tpp_brgemm_handle h, const void* a, const void* b, void* c,
+                                     const float* bias, int64_t count, void* stream);
+tpp_status tpp_brgemm_execute_offset(tpp_brgemm_handle h, const void* a, const void* b,
+                                     const int64_t* offs_a, const int64_t* offs_b, void* c,
+                                     const float* bias, int64_t count, void* stream);
+tpp_status tpp_brgemm_execute_address(tpp_brgemm_handle h, const void* const* ptrs_a,
+                                      const void* const* ptrs_b, void* c, const float* bias,
+                                      int64_t count, void* stream);
+
+/* Strided instance grid: G = gm * gn instances, instance g = gi_m + gm * gi_n, with
+ *   A base = a + gi_m * a_step_m       B base = b + gi_n * b_step_n
+ *   C base = c + gi_m * c_step_m + gi_n * c_step_n       bias base = bias + gi_m * bias_step_m
+ * This is the ib_m / ib_n loop nest of Alg. 6 around its BRGEMM call (all steps in elements). */
+typedef struct {
+  int64_t gm, gn;
+  int64_t a_step_m, b_step_n;
+  int64_t c_step_m, c_step_n;
+  int64_t bias_step_m;
+} tpp_grid_strided;
+
+/* G independent BRGEMMs in one launch: the loops of Alg. 6 (ib_n, ib_m), Alg. 7 (pos) or a
+ * convolution's output rows (Sec. 5.1.4) around the call, handed to the GPU as its grid.
+ * Instance g computes exactly what one single call computes with its bases moved:
+ *   - grid != NULL: the strided form above (gm * gn must equal G); the four offset arrays must
+ *     be NULL.
+ *   - grid == NULL: the explicit form; d_a_off, d_b_off, d_c_off, d_bias_off are device int64
+ *     arrays of G element offsets (any may be NULL, meaning all zeros).
+ * Stride and offset kinds: every instance reduces the same `count` pairs relative to its bases
+ * (offset kind: d_offs_a / d_offs_b, count entries each).
+ * Address kind: instance g reduces pairs d_begin[g] .. d_begin[g+1]-1 of d_ptrs_a / d_ptrs_b
+ * (CSR; d_begin has G+1 non-decreasing entries); a, b, d_a_off, d_b_off and count are unused,
+ * and the grid moves only C and bias.
+ * G == 0 is a no-op.  Errors: INVALID_ARG as for the single calls, plus gm*gn != G, a negative
+ * grid field, offset arrays given together with a grid, or a NULL d_begin for the address kind. */
+tpp_status tpp_brgemm_execute_batched(tpp_brgemm_handle h, const tpp_grid_strided* grid,
+                                      int64_t G, const int64_t* d_a_off, const int64_t* d_b_off,
+                                      const int64_t* d_c_off, const int64_t* d_bias_off,
+                                      const void* a, const void* b, void* c, const float* bias,
+                                      int64_t count, const int64_t* d_offs_a,
+                                      const int64_t* d_offs_b, const int64_t* d_begin,
+                                      const void* const* d_ptrs_a, const void* const* d_ptrs_b,
+                                      void* stream);
+
+/* Handles live in the cache until the process ends; release is a no-op kept for symmetry with
+ * dispatch, and is safe on NULL. */
+void tpp_brgemm_release(tpp_brgemm_handle h);
+
+/* Human-readable description of the kernel instance a handle selected (tile shape, load path).
+ * Writes at most len bytes including the terminating NUL.  Host-only. */
+tpp_status tpp_brgemm_describe(tpp_brgemm_handle h, char* buf, size_t len);
+
+/* Reduce TPP (Table 1; Sec. 3.1: reduction-by-columns turns an M x N input into M x 1).
+ *   in: device, m x n column-major with leading dimension ld >= m, type in_type (F32 or BF16).
+ *   TPP_RED_BY_COLS: out[r] = fold_{c<n} f(in(r, c))   (m outputs)
+ *   TPP_RED_BY_ROWS: out[c] = fold_{r<m} f(in(r, c))   (n outputs)
+ *   f(x) = x into out_x when TPP_RED_X is set, f(x) = x*x into out_x2 when TPP_RED_X2 is set
+ *   (both may be set: one pass, two outputs).  fold: SUM (from 0), MUL (from 1), MIN, MAX.
+ *   Outputs are device fp32 arrays.  Arithmetic is fp32; the summation order is unspecified.
+ * The library keeps a small device work buffer per GPU for partial results (allocated on first
+ * use and kept until the process ends).  Exactly one of BY_COLS / BY_ROWS, and at least one of
+ * X / X2, must be set.  Errors: INVALID_ARG for m, n <= 0, ld < m, bad flags, NULL pointers;
+ * NO_MEMORY if the work buffer cannot be allocated. */
+typedef enum { TPP_RED_SUM = 0, TPP_RED_MUL = 1, TPP_RED_MIN = 2, TPP_RED_MAX = 3 } tpp_reduce_op;
+enum {
+  TPP_RED_BY_COLS = 1u << 0,
+  TPP_RED_BY_ROWS = 1u << 1,
+  TPP_RED_X = 1u << 2,
+  TPP_RED_X2 = 1u << 3
+};
+tpp_status tpp_reduce(int32_t m, int32_t n, int64_t ld, int32_t in_type, const void* in,
+                      int32_t op, uint32_t flags, float* out_x, float* out_x2, void* stream);
+
+/* Static text for a status code, and the last error's detail for the calling thread. */
+const char* tpp_status_string(tpp_status s);
+const char* tpp_last_error_message(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TPP_BRGEMM_H */

@@ -1,0 +1,171 @@
+"""MI355X (gfx950) batch-reduce GEMM TPP: thin Python binding of the C ABI in include/tpp_brgemm.h.
+
+Argument marshalling only: every step of the computation runs in the HIP kernels of
+``libtpp_mi355x.so``.  The functions keep the C names; pointers are plain integers (device
+addresses) or objects with ``data_ptr()`` (torch tensors), streams are integers (a hipStream_t)
+or None for the default stream.  A non-OK status raises :class:`TppError`.
+
+The library must have been built (``__graft_entry__.build()`` or
+``python paper_2104_05755_amd/build.py``); importing this package without it raises ImportError.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libtpp_mi355x.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build the HIP library first "
+                      "(python paper_2104_05755_amd/build.py)")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+# ---- constants (mirroring include/tpp_brgemm.h) ---------------------------------------------
+TPP_OK, TPP_ERR_INVALID_ARG, TPP_ERR_UNSUPPORTED, TPP_ERR_HIP, TPP_ERR_NO_MEMORY = 0, -1, -2, -4, -5
+TPP_DT_F32, TPP_DT_BF16 = 0, 1
+TPP_BR_STRIDE, TPP_BR_OFFSET, TPP_BR_ADDRESS = 0, 1, 2
+TPP_EPI_BIAS, TPP_EPI_RELU, TPP_EPI_GELU_TANH = 1, 2, 4
+TPP_RED_SUM, TPP_RED_MUL, TPP_RED_MIN, TPP_RED_MAX = 0, 1, 2, 3
+TPP_RED_BY_COLS, TPP_RED_BY_ROWS, TPP_RED_X, TPP_RED_X2 = 1, 2, 4, 8
+
+_c_void_p, _i64, _i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
+
+
+class tpp_brgemm_desc(ctypes.Structure):
+    _fields_ = [("m", _i32), ("n", _i32), ("k", _i32),
+                ("lda", _i64), ("ldb", _i64), ("ldc", _i64),
+                ("a_type", _i32), ("b_type", _i32), ("c_type", _i32), ("comp_type", _i32),
+                ("beta", ctypes.c_float), ("kind", _i32),
+                ("stride_a", _i64), ("stride_b", _i64), ("flags", ctypes.c_uint32)]
+
+
+class tpp_grid_strided(ctypes.Structure):
+    _fields_ = [(f, _i64) for f in ("gm", "gn", "a_step_m", "b_step_n", "c_step_m", "c_step_n",
+                                    "bias_step_m")]
+
+
+class TppError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        msg = _lib.tpp_last_error_message().decode()
+        super().__init__(f"{where}: {_lib.tpp_status_string(status).decode()} ({msg})")
+        self.status = status
+
+
+def _sig(name, restype, *argtypes):
+    f = getattr(_lib, name)
+    f.restype = restype
+    f.argtypes = list(argtypes)
+    return f
+
+
+_sig("tpp_status_string", ctypes.c_char_p, _i32)
+_sig("tpp_last_error_message", ctypes.c_char_p)
+_sig("tpp_brgemm_dispatch", _i32, ctypes.POINTER(tpp_brgemm_desc), ctypes.POINTER(_c_void_p))
+_sig("tpp_brgemm_execute_stride", _i32, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p,
+     _i64, _c_void_p)
+_sig("tpp_brgemm_execute_offset", _i32, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p,
+     _c_void_p, _c_void_p, _i64, _c_void_p)
+_sig("tpp_brgemm_execute_address", _i32, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p,
+     _i64, _c_void_p)
+_sig("tpp_brgemm_execute_batched", _i32, _c_void_p, ctypes.POINTER(tpp_grid_strided), _i64,
+     _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p,
+     _i64, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p)
+_sig("tpp_brgemm_release", None, _c_void_p)
+_sig("tpp_brgemm_describe", _i32, _c_void_p, ctypes.c_char_p, ctypes.c_size_t)
+_sig("tpp_reduce", _i32, _i32, _i32, _i64, _i32, _c_void_p, _i32, ctypes.c_uint32, _c_void_p,
+     _c_void_p, _c_void_p)
+
+
+def _p(x):
+    """Device address of x: None, an int, or an object with data_ptr()."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _check(status: int, where: str):
+    if status != TPP_OK:
+        raise TppError(status, where)
+
+
+def current_stream() -> int:
+    """hipStream_t of torch's current stream on the current device (torch is the memory and
+    stream provider; the library itself does not depend on it)."""
+    import torch
+    return torch.cuda.current_stream().cuda_stream
+
+
+def tpp_brgemm_dispatch(desc: tpp_brgemm_desc) -> int:
+    h = _c_void_p()
+    _check(_lib.tpp_brgemm_dispatch(ctypes.byref(desc), ctypes.byref(h)), "tpp_brgemm_dispatch")
+    return h.value
+
+
+def tpp_brgemm_execute_stride(h, a, b, c, bias, count, stream=None):
+    _check(_lib.tpp_brgemm_execute_stride(h, _p(a), _p(b), _p(c), _p(bias), count, stream),
+           "tpp_brgemm_execute_stride")
+
+
+def tpp_brgemm_execute_offset(h, a, b, offs_a, offs_b, c, bias, count, stream=None):
+    _check(_lib.tpp_brgemm_execute_offset(h, _p(a), _p(b), _p(offs_a), _p(offs_b), _p(c),
+                                          _p(bias), count, stream), "tpp_brgemm_execute_offset")
+
+
+def tpp_brgemm_execute_address(h, ptrs_a, ptrs_b, c, bias, count, stream=None):
+    _check(_lib.tpp_brgemm_execute_address(h, _p(ptrs_a), _p(ptrs_b), _p(c), _p(bias), count,
+                                           stream), "tpp_brgemm_execute_address")
+
+
+def tpp_brgemm_execute_batched(h, grid, G, a_off, b_off, c_off, bias_off, a, b, c, bias, count,
+                               offs_a, offs_b, begin, ptrs_a, ptrs_b, stream=None):
+    """grid: tpp_grid_strided, a dict with its fields, or None (explicit offset arrays)."""
+    g = None
+    if grid is not None:
+        g = grid if isinstance(grid, tpp_grid_strided) else tpp_grid_strided(
+            *(int(grid[f]) for f in ("gm", "gn", "a_step_m", "b_step_n", "c_step_m",
+                                     "c_step_n", "bias_step_m")))
+    _check(_lib.tpp_brgemm_execute_batched(
+        h, ctypes.byref(g) if g is not None else None, G, _p(a_off), _p(b_off), _p(c_off),
+        _p(bias_off), _p(a), _p(b), _p(c), _p(bias), count, _p(offs_a), _p(offs_b), _p(begin),
+        _p(ptrs_a), _p(ptrs_b), stream), "tpp_brgemm_execute_batched")
+
+
+def tpp_brgemm_release(h):
+    _lib.tpp_brgemm_release(h)
+
+
+def tpp_brgemm_describe(h) -> str:
+    buf = ctypes.create_string_buffer(256)
+    _check(_lib.tpp_brgemm_describe(h, buf, 256), "tpp_brgemm_describe")
+    return buf.value.decode()
+
+
+def tpp_reduce(m, n, ld, in_type, x, op, flags, out_x, out_x2, stream=None):
+    _check(_lib.tpp_reduce(m, n, ld, in_type, _p(x), op, flags, _p(out_x), _p(out_x2), stream),
+           "tpp_reduce")
+
+
+def tpp_status_string(s: int) -> str:
+    return _lib.tpp_status_string(s).decode()
+
+
+def tpp_last_error_message() -> str:
+    return _lib.tpp_last_error_message().decode()
+
+
+def make_desc(m, n, k, lda, ldb, ldc, ab_type="bf16", c_type="f32", beta=0.0, kind="stride",
+              stride_a=0, stride_b=0, flags=()) -> tpp_brgemm_desc:
+    """Convenience: a descriptor from readable names (dtype "f32"/"bf16", kind
+    "stride"/"offset"/"address", flags from {"bias", "relu", "gelu_tanh"})."""
+    dt = {"f32": TPP_DT_F32, "bf16": TPP_DT_BF16}
+    kd = {"stride": TPP_BR_STRIDE, "offset": TPP_BR_OFFSET, "address": TPP_BR_ADDRESS}
+    fl = {"bias": TPP_EPI_BIAS, "relu": TPP_EPI_RELU, "gelu_tanh": TPP_EPI_GELU_TANH}
+    bits = 0
+    for f in flags:
+        bits |= fl[f]
+    return tpp_brgemm_desc(m, n, k, lda, ldb, ldc, dt[ab_type], dt[ab_type], dt[c_type],
+                           TPP_DT_F32, float(beta), kd[kind], stride_a, stride_b, bits)

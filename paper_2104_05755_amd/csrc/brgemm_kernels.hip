@@ -1,0 +1,597 @@
+// brgemm_kernels.hip -- the batch-reduce GEMM TPP kernel family for gfx950 (CDNA4).
+//
+// Computes, for every instance g of a launch and every (r, c) of its m x n output block,
+//     C(r, c) = cvt( act( beta * C(r, c) + sum_i sum_p A_i(r, p) B_i(p, c) + bias[r] ) )
+// (Table 3 BRGEMM; Sec. 2.3 variants; the epilogue TPPs of Table 1 / Table 2 fused before the
+// single store as Sec. 2.1 principle 5 allows).
+//
+// Structure, following Alg. 2 re-tiled for the GPU:
+//   - a workgroup owns one BM x BN tile of the "virtual C" of its tile group.  For a strided
+//     instance grid the virtual C is the (gm*m) x (gn*n) matrix formed by the instances' output
+//     blocks side by side, so a tile may fuse several neighbouring instances (they share their
+//     A_i rows and B_i columns, as the ib_m / ib_n loops of Alg. 6 do); for an explicit grid the
+//     virtual C is one instance's m x n block;
+//   - Alg. 2 lines 4-7: the loop over pairs i and over k in steps of BK=64 is one flat loop over
+//     stages; each stage copies an A_i panel (BM x 64) and a B_i panel (64 x BN) from HBM into
+//     one of two LDS buffers with 16-byte loads, while the MFMAs consume the other buffer;
+//   - A is M-contiguous in memory but the MFMA wants 8 consecutive k per lane, so every thread
+//     loads an 8x8 bf16 sub-block (8 columns of 8 rows) and transposes it in registers before
+//     its LDS store; B is already K-contiguous and is copied as is;
+//   - fp32 accumulators stay in registers for the whole reduction (v_mfma_f32_32x32x16_bf16);
+//   - the epilogue (beta*C, bias, ReLU / GELU-tanh, fp32 -> bf16) runs on the accumulators and
+//     each output element is stored once.
+#include <hip/hip_runtime.h>
+
+#include "internal.h"
+
+namespace tpp {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int NT = 256;            // threads per workgroup: 4 wavefronts of 64
+constexpr int BK = 64;             // k extent of one stage (bf16)
+constexpr int LDS_ROW = BK + 8;    // bf16 per LDS row: 128 B of data + 16 B against bank conflicts
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
+
+__device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
+  // Lowers to v_cvt_pk_bf16_f32 on gfx950: round to nearest even, NaN stays NaN.
+  return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
+}
+
+// GELU in its tanh form, 0.5 x (1 + tanh(sqrt(2/pi) (x + 0.044715 x^3))), with the device math
+// library's tanhf.
+__device__ __forceinline__ float gelu_tanh(float x) {
+  const float kSqrt2OverPi = 0.7978845608028654f;
+  return 0.5f * x * (1.0f + tanhf(kSqrt2OverPi * (x + 0.044715f * x * x * x)));
+}
+
+__device__ __forceinline__ float activate(float v, uint32_t flags) {
+  if (flags & TPP_EPI_RELU) return v > 0.0f ? v : 0.0f;
+  if (flags & TPP_EPI_GELU_TANH) return gelu_tanh(v);
+  return v;
+}
+
+// XCD-aware tile order: workgroups are handed to the 8 XCDs round-robin, so consecutive block
+// ids land on different L2s.  Remapping gives each XCD a contiguous run of tiles (neighbouring
+// tiles share A rows or B columns and so share that XCD's L2).
+__device__ __forceinline__ int64_t xcd_tile(int64_t bid, int64_t total) {
+  if ((total & 7) != 0) return bid;
+  return (bid & 7) * (total >> 3) + (bid >> 3);
+}
+
+struct TileCoord {
+  int64_t g;        // instance (explicit form) or 0 (strided form)
+  int32_t row0;     // first virtual row of the tile
+  int32_t col0;     // first virtual column of the tile
+};
+
+__device__ __forceinline__ TileCoord decode_tile(const BrgemmParams& p, int bm, int bn) {
+  const int64_t t = xcd_tile(blockIdx.x, p.total_tiles);
+  const int64_t per_group = (int64_t)p.tiles_m * p.tiles_n;
+  TileCoord tc;
+  tc.g = t / per_group;
+  const int64_t tin = t - tc.g * per_group;
+  tc.row0 = (int32_t)(tin % p.tiles_m) * bm;   // tiles of one column run consecutively
+  tc.col0 = (int32_t)(tin / p.tiles_m) * bn;
+  return tc;
+}
+
+// Virtual row R -> element offset of that row inside A (relative to the instance's A base) and
+// whether it exists.  Fused strided grid: R = gi_m * m + r.  One instance per group: R = r.
+__device__ __forceinline__ bool row_in_a(const BrgemmParams& p, int32_t R, int64_t& off) {
+  if (p.fused) {
+    if (R >= p.vrows) return false;
+    const int32_t gi = R / p.m, r = R - gi * p.m;
+    off = (int64_t)gi * p.a_step_m + r;
+    return true;
+  }
+  off = R;
+  return R < p.m;
+}
+
+// Virtual column C -> element offset of that column inside B (relative to the instance base).
+__device__ __forceinline__ bool col_in_b(const BrgemmParams& p, int32_t C, int64_t& off) {
+  if (p.fused) {
+    if (C >= p.vcols) return false;
+    const int32_t gi = C / p.n, c = C - gi * p.n;
+    off = (int64_t)gi * p.b_step_n + (int64_t)c * p.ldb;
+    return true;
+  }
+  off = (int64_t)C * p.ldb;
+  return C < p.n;
+}
+
+// Per-launch instance data for tile group g: bases added to every A_i / B_i / C / bias address,
+// and the pair list.
+struct Instance {
+  int64_t a, b, c, bias;   // element offsets
+  int64_t pair0, npairs;
+};
+
+__device__ __forceinline__ Instance instance_of(const BrgemmParams& p, int64_t g) {
+  Instance in;
+  in.a = in.b = in.c = in.bias = 0;
+  if (!p.fused && p.grid_form) {
+    const int64_t gi_m = g % p.gm, gi_n = g / p.gm;
+    in.a = gi_m * p.a_step_m;
+    in.b = gi_n * p.b_step_n;
+    in.c = gi_m * p.c_step_m + gi_n * p.c_step_n;
+    in.bias = gi_m * p.bias_step_m;
+  } else if (!p.fused) {
+    in.a = p.a_off ? p.a_off[g] : 0;
+    in.b = p.b_off ? p.b_off[g] : 0;
+    in.c = p.c_off ? p.c_off[g] : 0;
+    in.bias = p.bias_off ? p.bias_off[g] : 0;
+  }
+  in.pair0 = 0;
+  in.npairs = p.count;
+  if (p.kind == TPP_BR_ADDRESS && p.begin) {   // a single address call has no begin[]
+    in.pair0 = p.begin[g];
+    in.npairs = p.begin[g + 1] - in.pair0;
+  }
+  return in;
+}
+
+// Addresses of pair i (Sec. 2.3): stride A + i*stride, offset A + offs[i], address ptrs[i].
+template <typename T>
+__device__ __forceinline__ void pair_bases(const BrgemmParams& p, const Instance& in, int64_t i,
+                                           const T*& pa, const T*& pb) {
+  if (p.kind == TPP_BR_STRIDE) {
+    pa = static_cast<const T*>(p.a) + in.a + i * p.stride_a;
+    pb = static_cast<const T*>(p.b) + in.b + i * p.stride_b;
+  } else if (p.kind == TPP_BR_OFFSET) {
+    pa = static_cast<const T*>(p.a) + in.a + p.offs_a[i];
+    pb = static_cast<const T*>(p.b) + in.b + p.offs_b[i];
+  } else {
+    pa = static_cast<const T*>(p.ptrs_a[in.pair0 + i]);
+    pb = static_cast<const T*>(p.ptrs_b[in.pair0 + i]);
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// Epilogue shared by all kernels.  The accumulator layout of a 32x32 MFMA tile: lane l holds
+// column l%32, and in register v the row 8*(v/4) + 4*(l/32) + v%4.
+// ---------------------------------------------------------------------------------------------
+template <bool GENERIC>
+__device__ __forceinline__ void store_group(const BrgemmParams& p, const Instance& in, int32_t R0,
+                                            int32_t C, const float v_in[4]) {
+  // Column C of the virtual C -> element offset in C (relative to the instance base).
+  int64_t col_off;
+  if (p.fused) {
+    if (C >= p.vcols) return;
+    const int32_t gi = C / p.n, c = C - gi * p.n;
+    col_off = (int64_t)gi * p.c_step_n + (int64_t)c * p.ldc;
+  } else {
+    if (C >= p.n) return;
+    col_off = (int64_t)C * p.ldc;
+  }
+  const float* bias = p.bias;
+  const bool has_bias = (p.flags & TPP_EPI_BIAS) != 0;
+  if (!GENERIC) {
+    // m % 8 == 0: the four rows R0..R0+3 are valid together and belong to one instance.
+    int64_t row_off, bias_idx;
+    if (p.fused) {
+      if (R0 >= p.vrows) return;
+      const int32_t gi = R0 / p.m, r = R0 - gi * p.m;
+      row_off = (int64_t)gi * p.c_step_m + r;
+      bias_idx = (int64_t)gi * p.bias_step_m + r;
+    } else {
+      if (R0 >= p.m) return;
+      row_off = R0;
+      bias_idx = in.bias + R0;
+    }
+    const int64_t e0 = in.c + row_off + col_off;
+    float v[4] = {v_in[0], v_in[1], v_in[2], v_in[3]};
+    if (p.c_bf16) {
+      uint16_t* cp = static_cast<uint16_t*>(p.c) + e0;
+      const bool vec = (reinterpret_cast<uintptr_t>(cp) & 7) == 0;
+      if (p.beta != 0.0f) {
+        uint32_t h[4];
+        if (vec) {
+          const uint2 w = *reinterpret_cast<const uint2*>(cp);
+          h[0] = w.x & 0xffff; h[1] = w.x >> 16; h[2] = w.y & 0xffff; h[3] = w.y >> 16;
+        } else {
+          for (int e = 0; e < 4; ++e) h[e] = cp[e];
+        }
+        for (int e = 0; e < 4; ++e) v[e] = p.beta * bf16_bits_to_f32(h[e]) + v[e];
+      }
+      if (has_bias)
+        for (int e = 0; e < 4; ++e) v[e] += bias[bias_idx + e];
+      uint32_t o[4];
+      for (int e = 0; e < 4; ++e) o[e] = f32_to_bf16_bits(activate(v[e], p.flags));
+      if (vec) {
+        *reinterpret_cast<uint2*>(cp) = make_uint2(o[0] | (o[1] << 16), o[2] | (o[3] << 16));
+      } else {
+        for (int e = 0; e < 4; ++e) cp[e] = (uint16_t)o[e];
+      }
+    } else {
+      float* cp = static_cast<float*>(p.c) + e0;
+      const bool vec = (reinterpret_cast<uintptr_t>(cp) & 15) == 0;
+      if (p.beta != 0.0f) {
+        if (vec) {
+          const float4 w = *reinterpret_cast<const float4*>(cp);
+          v[0] = p.beta * w.x + v[0]; v[1] = p.beta * w.y + v[1];
+          v[2] = p.beta * w.z + v[2]; v[3] = p.beta * w.w + v[3];
+        } else {
+          for (int e = 0; e < 4; ++e) v[e] = p.beta * cp[e] + v[e];
+        }
+      }
+      if (has_bias)
+        for (int e = 0; e < 4; ++e) v[e] += bias[bias_idx + e];
+      for (int e = 0; e < 4; ++e) v[e] = activate(v[e], p.flags);
+      if (vec) {
+        *reinterpret_cast<float4*>(cp) = make_float4(v[0], v[1], v[2], v[3]);
+      } else {
+        for (int e = 0; e < 4; ++e) cp[e] = v[e];
+      }
+    }
+  } else {
+    for (int e = 0; e < 4; ++e) {
+      const int32_t R = R0 + e;
+      int64_t row_off, bias_idx;
+      if (p.fused) {
+        if (R >= p.vrows) continue;
+        const int32_t gi = R / p.m, r = R - gi * p.m;
+        row_off = (int64_t)gi * p.c_step_m + r;
+        bias_idx = (int64_t)gi * p.bias_step_m + r;
+      } else {
+        if (R >= p.m) continue;
+        row_off = R;
+        bias_idx = in.bias + R;
+      }
+      const int64_t ei = in.c + row_off + col_off;
+      float v = v_in[e];
+      if (p.c_bf16) {
+        uint16_t* cp = static_cast<uint16_t*>(p.c) + ei;
+        if (p.beta != 0.0f) v = p.beta * bf16_bits_to_f32(*cp) + v;
+        if (has_bias) v += bias[bias_idx];
+        *cp = f32_to_bf16_bits(activate(v, p.flags));
+      } else {
+        float* cp = static_cast<float*>(p.c) + ei;
+        if (p.beta != 0.0f) v = p.beta * *cp + v;
+        if (has_bias) v += bias[bias_idx];
+        *cp = activate(v, p.flags);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// bf16 kernel family
+// ---------------------------------------------------------------------------------------------
+// 16 bytes = 8 bf16 of one column, zero when `ok` is false; element loads if the address is not
+// 16-byte aligned.
+__device__ __forceinline__ uint4 load8(const uint16_t* ptr, bool ok, bool aligned) {
+  uint4 v = make_uint4(0u, 0u, 0u, 0u);
+  if (ok) {
+    if (aligned) {
+      v = *reinterpret_cast<const uint4*>(ptr);
+    } else {
+      v.x = (uint32_t)ptr[0] | ((uint32_t)ptr[1] << 16);
+      v.y = (uint32_t)ptr[2] | ((uint32_t)ptr[3] << 16);
+      v.z = (uint32_t)ptr[4] | ((uint32_t)ptr[5] << 16);
+      v.w = (uint32_t)ptr[6] | ((uint32_t)ptr[7] << 16);
+    }
+  }
+  return v;
+}
+
+__device__ __forceinline__ uint32_t word(const uint4& v, int d) {
+  return d == 0 ? v.x : d == 1 ? v.y : d == 2 ? v.z : v.w;
+}
+
+// Transpose an 8x8 bf16 sub-block held as 8 k-columns of 8 rows into 8 rows of 8 k, and store
+// the rows (16 B each) into the K-contiguous LDS panel.
+__device__ __forceinline__ void store_a_transposed(uint16_t* dst_row0, const uint4 col[8]) {
+#pragma unroll
+  for (int mi = 0; mi < 8; ++mi) {
+    const int d = mi >> 1;
+    uint32_t w[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const uint32_t lo = word(col[2 * e], d), hi = word(col[2 * e + 1], d);
+      w[e] = (mi & 1) ? ((lo >> 16) | (hi & 0xffff0000u)) : ((lo & 0xffffu) | (hi << 16));
+    }
+    *reinterpret_cast<uint4*>(dst_row0 + mi * LDS_ROW) = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+}
+
+template <int BM, int BN, int WAVES_M, int WAVES_N, bool GENERIC>
+__global__ __launch_bounds__(NT) void brgemm_bf16_kernel(BrgemmParams p) {
+  constexpr int WTM = BM / WAVES_M, WTN = BN / WAVES_N;
+  constexpr int TM = WTM / 32, TN = WTN / 32;
+  constexpr int KCH = BK / 8;                        // 8-element k chunks per stage
+  constexpr int A_SUB = (BM / 8) * KCH;              // 8x8 sub-blocks of the A panel
+  constexpr int A_REP = (A_SUB + NT - 1) / NT;
+  constexpr int B_CH = BN * KCH;                     // 16-byte chunks of the B panel
+  constexpr int B_REP = (B_CH + NT - 1) / NT;
+  constexpr int STAGE = (BM + BN) * LDS_ROW;
+  static_assert(WAVES_M * WAVES_N * 64 == NT, "4 waves");
+  static_assert(TM >= 1 && TN >= 1, "wave tile at least 32x32");
+
+  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * STAGE];
+
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int wm = wave % WAVES_M, wn = wave / WAVES_M;
+  const TileCoord tc = decode_tile(p, BM, BN);
+  const Instance in = instance_of(p, tc.g);
+  const int32_t ksteps = (p.k + BK - 1) / BK;
+  const int64_t stages = in.npairs * ksteps;
+
+  // Staging assignments, fixed for the whole reduction.
+  int64_t a_off[A_REP][GENERIC ? 8 : 1];
+  bool a_ok[A_REP][GENERIC ? 8 : 1];
+  int a_kc[A_REP], a_row[A_REP];
+#pragma unroll
+  for (int rep = 0; rep < A_REP; ++rep) {
+    const int q = t + NT * rep;
+    a_kc[rep] = q % KCH;
+    a_row[rep] = (q / KCH) * 8;
+#pragma unroll
+    for (int e = 0; e < (GENERIC ? 8 : 1); ++e) {
+      a_off[rep][e] = 0;
+      a_ok[rep][e] = (q < A_SUB) && row_in_a(p, tc.row0 + a_row[rep] + e, a_off[rep][e]);
+    }
+  }
+  int64_t b_off[B_REP];
+  bool b_ok[B_REP];
+  int b_kc[B_REP], b_col[B_REP];
+#pragma unroll
+  for (int rep = 0; rep < B_REP; ++rep) {
+    const int q = t + NT * rep;
+    b_kc[rep] = q % KCH;
+    b_col[rep] = q / KCH;
+    b_off[rep] = 0;
+    b_ok[rep] = (q < B_CH) && col_in_b(p, tc.col0 + b_col[rep], b_off[rep]);
+  }
+
+  uint4 a_reg[A_REP][8];
+  uint4 b_reg[B_REP];
+
+  auto load_stage = [&](int64_t s) {
+    const int64_t i = s / ksteps;
+    const int32_t kk = (int32_t)(s - i * ksteps) * BK;
+    const uint16_t* pa;
+    const uint16_t* pb;
+    pair_bases<uint16_t>(p, in, i, pa, pb);
+    const bool aligned =
+        !GENERIC && ((reinterpret_cast<uintptr_t>(pa) | reinterpret_cast<uintptr_t>(pb)) & 15) == 0;
+#pragma unroll
+    for (int rep = 0; rep < A_REP; ++rep) {
+      const int32_t k0 = kk + a_kc[rep] * 8;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        if (!GENERIC) {
+          const bool ok = a_ok[rep][0] && k0 < p.k;
+          a_reg[rep][j] = load8(pa + a_off[rep][0] + (int64_t)(k0 + j) * p.lda, ok, aligned);
+        } else {
+          // element loads: each of the 8 rows and the k index checked on its own
+          uint32_t h[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const bool ok = a_ok[rep][e] && (k0 + j) < p.k;
+            h[e] = ok ? pa[a_off[rep][e] + (int64_t)(k0 + j) * p.lda] : 0u;
+          }
+          a_reg[rep][j] = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16),
+                                     h[4] | (h[5] << 16), h[6] | (h[7] << 16));
+        }
+      }
+    }
+#pragma unroll
+    for (int rep = 0; rep < B_REP; ++rep) {
+      const int32_t k0 = kk + b_kc[rep] * 8;
+      if (!GENERIC) {
+        b_reg[rep] = load8(pb + b_off[rep] + k0, b_ok[rep] && k0 < p.k, aligned);
+      } else {
+        uint32_t h[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const bool ok = b_ok[rep] && (k0 + e) < p.k;
+          h[e] = ok ? pb[b_off[rep] + k0 + e] : 0u;
+        }
+        b_reg[rep] = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
+                                h[6] | (h[7] << 16));
+      }
+    }
+  };
+
+  auto store_stage = [&](int buf) {
+    uint16_t* As = lds + buf * STAGE;
+    uint16_t* Bs = As + BM * LDS_ROW;
+#pragma unroll
+    for (int rep = 0; rep < A_REP; ++rep) {
+      if (t + NT * rep < A_SUB)
+        store_a_transposed(As + a_row[rep] * LDS_ROW + a_kc[rep] * 8, a_reg[rep]);
+    }
+#pragma unroll
+    for (int rep = 0; rep < B_REP; ++rep) {
+      if (t + NT * rep < B_CH)
+        *reinterpret_cast<uint4*>(Bs + b_col[rep] * LDS_ROW + b_kc[rep] * 8) = b_reg[rep];
+    }
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[tm][tn][v] = 0.0f;
+
+  const int frag_row = lane & 31;
+  const int frag_k = (lane >> 5) * 8;
+
+  if (stages > 0) {
+    load_stage(0);
+    store_stage(0);
+    __syncthreads();
+    for (int64_t s = 0; s < stages; ++s) {
+      const int buf = (int)(s & 1);
+      if (s + 1 < stages) load_stage(s + 1);   // global loads in flight during the MFMAs
+      const uint16_t* As = lds + buf * STAGE;
+      const uint16_t* Bs = As + BM * LDS_ROW;
+#pragma unroll
+      for (int kq = 0; kq < BK / 16; ++kq) {
+        bf16x8 af[TM], bfr[TN];
+#pragma unroll
+        for (int tm = 0; tm < TM; ++tm)
+          af[tm] = *reinterpret_cast<const bf16x8*>(
+              As + (wm * WTM + tm * 32 + frag_row) * LDS_ROW + kq * 16 + frag_k);
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn)
+          bfr[tn] = *reinterpret_cast<const bf16x8*>(
+              Bs + (wn * WTN + tn * 32 + frag_row) * LDS_ROW + kq * 16 + frag_k);
+#pragma unroll
+        for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+          for (int tn = 0; tn < TN; ++tn)
+            acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[tm], bfr[tn], acc[tm][tn],
+                                                                  0, 0, 0);
+      }
+      if (s + 1 < stages) store_stage(buf ^ 1);
+      __syncthreads();
+    }
+  }
+
+  // Epilogue on the accumulators, one store per output element.
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) {
+      const int32_t C = tc.col0 + wn * WTN + tn * 32 + (lane & 31);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int32_t R0 = tc.row0 + wm * WTM + tm * 32 + q * 8 + (lane >> 5) * 4;
+        const float v[4] = {acc[tm][tn][q * 4 + 0], acc[tm][tn][q * 4 + 1],
+                            acc[tm][tn][q * 4 + 2], acc[tm][tn][q * 4 + 3]};
+        store_group<GENERIC>(p, in, R0, C, v);
+      }
+    }
+}
+
+// ---------------------------------------------------------------------------------------------
+// fp32 kernel: 64x64 tile, 4 waves of 32x32, v_mfma_f32_32x32x2f32, element loads with full
+// bounds checks (any shape, leading dimension or alignment).
+// ---------------------------------------------------------------------------------------------
+constexpr int F_BM = 64, F_BN = 64, F_BK = 32;
+constexpr int F_AROW = F_BM + 4;   // A panel stored k-major: As[k][m]
+constexpr int F_BROW = F_BK + 1;   // B panel stored n-major: Bs[n][k], odd stride
+
+__global__ __launch_bounds__(NT) void brgemm_f32_kernel(BrgemmParams p) {
+  __shared__ float As[F_BK * F_AROW];
+  __shared__ float Bs[F_BN * F_BROW];
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int wm = wave & 1, wn = wave >> 1;
+  const TileCoord tc = decode_tile(p, F_BM, F_BN);
+  const Instance in = instance_of(p, tc.g);
+  const int32_t ksteps = (p.k + F_BK - 1) / F_BK;
+  const int64_t stages = in.npairs * ksteps;
+
+  // A element e = t + 256*j: row t%64 (fixed), k = t/64 + 4*j.
+  const int a_r = t & 63, a_k0 = t >> 6;
+  int64_t a_off = 0;
+  const bool a_ok = row_in_a(p, tc.row0 + a_r, a_off);
+  // B element e = t + 256*j: k = t%32 (fixed), column t/32 + 8*j.
+  const int b_k = t & 31, b_c0 = t >> 5;
+  int64_t b_off[8];
+  bool b_ok[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    b_off[j] = 0;
+    b_ok[j] = col_in_b(p, tc.col0 + b_c0 + 8 * j, b_off[j]);
+  }
+
+  f32x16 acc;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
+  float ar[8], br[8];
+  auto load = [&](int64_t s) {
+    const int64_t i = s / ksteps;
+    const int32_t kk = (int32_t)(s - i * ksteps) * F_BK;
+    const float* pa;
+    const float* pb;
+    pair_bases<float>(p, in, i, pa, pb);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int32_t ka = kk + a_k0 + 4 * j;
+      ar[j] = (a_ok && ka < p.k) ? pa[a_off + (int64_t)ka * p.lda] : 0.0f;
+      const int32_t kb = kk + b_k;
+      br[j] = (b_ok[j] && kb < p.k) ? pb[b_off[j] + kb] : 0.0f;
+    }
+  };
+  if (stages > 0) load(0);
+  for (int64_t s = 0; s < stages; ++s) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      As[(a_k0 + 4 * j) * F_AROW + a_r] = ar[j];
+      Bs[(b_c0 + 8 * j) * F_BROW + b_k] = br[j];
+    }
+    __syncthreads();
+    if (s + 1 < stages) load(s + 1);
+#pragma unroll
+    for (int kq = 0; kq < F_BK / 2; ++kq) {
+      const float a = As[(kq * 2 + (lane >> 5)) * F_AROW + wm * 32 + (lane & 31)];
+      const float b = Bs[(wn * 32 + (lane & 31)) * F_BROW + kq * 2 + (lane >> 5)];
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, acc, 0, 0, 0);
+    }
+    __syncthreads();
+  }
+  const int32_t C = tc.col0 + wn * 32 + (lane & 31);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int32_t R0 = tc.row0 + wm * 32 + q * 8 + (lane >> 5) * 4;
+    const float v[4] = {acc[q * 4 + 0], acc[q * 4 + 1], acc[q * 4 + 2], acc[q * 4 + 3]};
+    store_group<true>(p, in, R0, C, v);
+  }
+}
+
+struct KernelInfo {
+  const char* name;
+  int bm, bn;
+};
+
+constexpr KernelInfo kInfo[K_COUNT] = {
+    {"bf16_256x256_vec", 256, 256}, {"bf16_256x128_vec", 256, 128},
+    {"bf16_128x128_vec", 128, 128}, {"bf16_64x64_vec", 64, 64},
+    {"bf16_64x64_generic", 64, 64}, {"f32_64x64_generic", 64, 64},
+};
+
+}  // namespace
+
+const char* kernel_name(int32_t id) { return (id >= 0 && id < K_COUNT) ? kInfo[id].name : "?"; }
+
+hipError_t launch_brgemm(BrgemmParams& p, int32_t id, hipStream_t stream) {
+  if (id < 0 || id >= K_COUNT) return hipErrorInvalidValue;
+  const int bm = kInfo[id].bm, bn = kInfo[id].bn;
+  p.tiles_m = (p.vrows + bm - 1) / bm;
+  p.tiles_n = (p.vcols + bn - 1) / bn;
+  p.total_tiles = p.groups * p.tiles_m * p.tiles_n;
+  if (p.total_tiles <= 0) return hipSuccess;
+  const dim3 grid((unsigned)p.total_tiles), block(NT);
+  switch (id) {
+    case K_BF16_256x256:
+      hipLaunchKernelGGL((brgemm_bf16_kernel<256, 256, 2, 2, false>), grid, block, 0, stream, p);
+      break;
+    case K_BF16_256x128:
+      hipLaunchKernelGGL((brgemm_bf16_kernel<256, 128, 2, 2, false>), grid, block, 0, stream, p);
+      break;
+    case K_BF16_128x128:
+      hipLaunchKernelGGL((brgemm_bf16_kernel<128, 128, 2, 2, false>), grid, block, 0, stream, p);
+      break;
+    case K_BF16_64x64:
+      hipLaunchKernelGGL((brgemm_bf16_kernel<64, 64, 2, 2, false>), grid, block, 0, stream, p);
+      break;
+    case K_BF16_GENERIC:
+      hipLaunchKernelGGL((brgemm_bf16_kernel<64, 64, 2, 2, true>), grid, block, 0, stream, p);
+      break;
+    default:
+      hipLaunchKernelGGL(brgemm_f32_kernel, grid, block, 0, stream, p);
+      break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace tpp

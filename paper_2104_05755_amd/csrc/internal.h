@@ -1,0 +1,80 @@
+// internal.h -- structures shared by the C-ABI front end and the HIP kernels (not installed).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "tpp_brgemm.h"
+
+namespace tpp {
+
+// Everything one batched BRGEMM launch needs, resolved on the host and passed by value.
+struct BrgemmParams {
+  const void* a;
+  const void* b;
+  void* c;
+  const float* bias;
+  int32_t m, n, k;
+  int64_t lda, ldb, ldc;
+  float beta;
+  uint32_t flags;
+  int32_t c_bf16;  // 1: C is bf16, 0: C is fp32
+  int32_t kind;    // tpp_br_kind
+  int64_t count;
+  int64_t stride_a, stride_b;
+  const int64_t* offs_a;
+  const int64_t* offs_b;
+  const int64_t* begin;
+  const void* const* ptrs_a;
+  const void* const* ptrs_b;
+  // Instance grid.  fused = 1: the gm x gn instances of a strided grid are laid side by side
+  // into one virtual (gm*m) x (gn*n) C, tiled as one group (tiles may span instances).
+  // fused = 0: G separate instances, each its own m x n virtual C and tile group; their bases
+  // come from the strided formula (grid_form = 1) or from the offset arrays (grid_form = 0).
+  int32_t fused;
+  int32_t grid_form;
+  int64_t gm, gn;
+  int64_t a_step_m, b_step_n, c_step_m, c_step_n, bias_step_m;
+  const int64_t* a_off;
+  const int64_t* b_off;
+  const int64_t* c_off;
+  const int64_t* bias_off;
+  // Tiling, filled by the launcher.
+  int32_t vrows, vcols;      // virtual C extent of one tile group
+  int32_t tiles_m, tiles_n;  // tiles per group
+  int64_t groups;            // 1 (strided) or G (explicit)
+  int64_t total_tiles;
+};
+
+// Kernel instances of the bf16 family (tile shape + load path) and the fp32 kernel.
+enum KernelId : int32_t {
+  K_BF16_256x256 = 0,   // 4 waves, 128x128 per wave, vector loads
+  K_BF16_256x128 = 1,   // 4 waves, 128x64 per wave, vector loads
+  K_BF16_128x128 = 2,   // 4 waves, 64x64 per wave, vector loads
+  K_BF16_64x64 = 3,     // 4 waves, 32x32 per wave, vector loads
+  K_BF16_GENERIC = 4,   // 64x64, element loads with full bounds checks (any shape / alignment)
+  K_F32_GENERIC = 5,    // 64x64 fp32 MFMA, element loads with full bounds checks
+  K_COUNT = 6
+};
+
+const char* kernel_name(int32_t id);
+
+// Fill the tiling fields of p for kernel `id` and launch on `stream`.
+hipError_t launch_brgemm(BrgemmParams& p, int32_t id, hipStream_t stream);
+
+// Reduce TPP launcher; `work` is a device buffer of `work_floats` floats for partial results.
+struct ReduceParams {
+  const void* in;
+  int32_t m, n;
+  int64_t ld;
+  int32_t in_bf16;
+  int32_t op;
+  uint32_t flags;
+  float* out_x;
+  float* out_x2;
+};
+// Number of floats of work space a reduce of this shape needs (0 if none).
+int64_t reduce_work_floats(const ReduceParams& p);
+hipError_t launch_reduce(const ReduceParams& p, float* work, hipStream_t stream);
+
+}  // namespace tpp

@@ -1,0 +1,284 @@
+// reduce_kernels.hip -- the Reduce TPP (Table 1) for gfx950.
+//
+// Folds an m x n column-major tensor (leading dimension ld, fp32 or bf16) along its rows or its
+// columns with SUM / MUL / MIN / MAX, of x and/or of x*x, into fp32 outputs.  Reduction by
+// columns turns m x n into m x 1 (Sec. 3.1); reduction by rows gives 1 x n.
+//
+//   BY_ROWS (out[c] = fold over r): each column is contiguous, so one wavefront folds one
+//     column (or one row segment of it) with 16-byte loads per lane, then across its 64 lanes
+//     with cross-lane shuffles.
+//   BY_COLS (out[r] = fold over c): a thread owns 16 bytes of consecutive rows and walks the
+//     columns of its workgroup's column range; the column lanes of a workgroup then meet in
+//     LDS.  Column ranges of different workgroups meet in a second, tiny pass.
+// Arithmetic is fp32.  When a shape needs several partial results per output (row segments or
+// column ranges), they go to a device work buffer and a second kernel folds them in a fixed
+// order, so results do not depend on scheduling.
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+
+#include "internal.h"
+
+namespace tpp {
+namespace {
+
+constexpr int RT = 256;   // threads per workgroup
+
+template <int OP>
+__device__ __forceinline__ float fold(float acc, float v) {
+  if (OP == TPP_RED_SUM) return acc + v;
+  if (OP == TPP_RED_MUL) return acc * v;
+  if (OP == TPP_RED_MIN) return v < acc ? v : acc;
+  return v > acc ? v : acc;
+}
+
+template <int OP>
+__device__ __forceinline__ float fold_identity() {
+  if (OP == TPP_RED_SUM) return 0.0f;
+  if (OP == TPP_RED_MUL) return 1.0f;
+  if (OP == TPP_RED_MIN) return INFINITY;
+  return -INFINITY;
+}
+
+template <int OP>
+__device__ __forceinline__ float wave_fold(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v = fold<OP>(v, __shfl_xor(v, off, 64));
+  return v;
+}
+
+template <bool BF16>
+__device__ __forceinline__ float load1(const void* base, int64_t idx) {
+  if (BF16) return __uint_as_float((uint32_t) static_cast<const uint16_t*>(base)[idx] << 16);
+  return static_cast<const float*>(base)[idx];
+}
+
+// V consecutive elements starting at idx (16 bytes, aligned): V = 8 for bf16, 4 for fp32.
+template <bool BF16, int V>
+__device__ __forceinline__ void loadv(const void* base, int64_t idx, float out[V]) {
+  if (BF16) {
+    const uint4 w = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(base) + idx);
+    const uint32_t d[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      out[2 * e] = __uint_as_float(d[e] << 16);
+      out[2 * e + 1] = __uint_as_float(d[e] & 0xffff0000u);
+    }
+  } else {
+    const float4 w = *reinterpret_cast<const float4*>(static_cast<const float*>(base) + idx);
+    out[0] = w.x; out[1] = w.y; out[2] = w.z; out[3] = w.w;
+  }
+}
+
+// BY_ROWS: wavefront wid folds rows [s*seg_rows, min(m, (s+1)*seg_rows)) of column c, where
+// c = wid % n, s = wid / n.  V == 1 means element loads.
+template <int OP, bool BF16, int V>
+__global__ __launch_bounds__(RT) void reduce_rows_kernel(ReduceParams p, int32_t seg_rows,
+                                                         int32_t nseg, float* work) {
+  const int lane = threadIdx.x & 63;
+  const int64_t wid = (int64_t)blockIdx.x * (RT / 64) + (threadIdx.x >> 6);
+  if (wid >= (int64_t)p.n * nseg) return;
+  const int32_t c = (int32_t)(wid % p.n), s = (int32_t)(wid / p.n);
+  const int32_t r_lo = s * seg_rows;
+  const int32_t r_hi = min(p.m, r_lo + seg_rows);
+  const int64_t col = (int64_t)c * p.ld;
+  const bool want_x = (p.flags & TPP_RED_X) != 0, want_x2 = (p.flags & TPP_RED_X2) != 0;
+  float ax = fold_identity<OP>(), ax2 = fold_identity<OP>();
+  const int32_t nv = (r_hi - r_lo) / V;   // full V-chunks
+  for (int32_t j = lane; j < nv; j += 64) {
+    float x[V];
+    if (V == 1) {
+      x[0] = load1<BF16>(p.in, col + r_lo + j);
+    } else {
+      loadv<BF16, V>(p.in, col + r_lo + (int64_t)j * V, x);
+    }
+#pragma unroll
+    for (int e = 0; e < V; ++e) {
+      ax = fold<OP>(ax, x[e]);
+      ax2 = fold<OP>(ax2, x[e] * x[e]);
+    }
+  }
+  for (int32_t r = r_lo + nv * V + lane; r < r_hi; r += 64) {
+    const float x = load1<BF16>(p.in, col + r);
+    ax = fold<OP>(ax, x);
+    ax2 = fold<OP>(ax2, x * x);
+  }
+  ax = wave_fold<OP>(ax);
+  ax2 = wave_fold<OP>(ax2);
+  if (lane == 0) {
+    if (nseg == 1) {
+      if (want_x) p.out_x[c] = ax;
+      if (want_x2) p.out_x2[c] = ax2;
+    } else {
+      work[(int64_t)s * p.n + c] = ax;
+      work[(int64_t)nseg * p.n + (int64_t)s * p.n + c] = ax2;
+    }
+  }
+}
+
+// BY_COLS: workgroup (rb, s) folds columns [s*col_seg, min(n, (s+1)*col_seg)) for rows
+// [rb*TR*V, (rb+1)*TR*V).  Thread t: row vector tr = t % TR, column lane tc = t / TR.
+template <int OP, bool BF16, int V>
+__global__ __launch_bounds__(RT) void reduce_cols_kernel(ReduceParams p, int32_t TR,
+                                                         int32_t col_seg, int32_t nseg,
+                                                         int32_t nrb, float* work) {
+  __shared__ float sx[RT * V];
+  __shared__ float sx2[RT * V];
+  const int t = threadIdx.x;
+  const int TC = RT / TR;
+  const int tr = t % TR, tc = t / TR;
+  const int32_t rb = (int32_t)(blockIdx.x % nrb), s = (int32_t)(blockIdx.x / nrb);
+  const int32_t r0 = rb * TR * V + tr * V;
+  const int32_t c_lo = s * col_seg, c_hi = min(p.n, c_lo + col_seg);
+  float ax[V], ax2[V];
+#pragma unroll
+  for (int e = 0; e < V; ++e) ax[e] = ax2[e] = fold_identity<OP>();
+  const bool full = r0 + V <= p.m;
+  for (int32_t c = c_lo + tc; c < c_hi; c += TC) {
+    const int64_t base = (int64_t)c * p.ld + r0;
+    float x[V];
+    if (V > 1 && full) {
+      loadv<BF16, V>(p.in, base, x);
+    } else {
+#pragma unroll
+      for (int e = 0; e < V; ++e) x[e] = (r0 + e < p.m) ? load1<BF16>(p.in, base + e) : 0.0f;
+    }
+#pragma unroll
+    for (int e = 0; e < V; ++e) {
+      ax[e] = fold<OP>(ax[e], x[e]);
+      ax2[e] = fold<OP>(ax2[e], x[e] * x[e]);
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < V; ++e) {
+    sx[tc * TR * V + tr * V + e] = ax[e];
+    sx2[tc * TR * V + tr * V + e] = ax2[e];
+  }
+  __syncthreads();
+  // Fold the TC column lanes; thread t handles row slot t (and t + RT, ... when TR*V > RT).
+  const bool want_x = (p.flags & TPP_RED_X) != 0, want_x2 = (p.flags & TPP_RED_X2) != 0;
+  for (int slot = t; slot < TR * V; slot += RT) {
+    float fx = sx[slot], fx2 = sx2[slot];
+    for (int l = 1; l < TC; ++l) {
+      fx = fold<OP>(fx, sx[l * TR * V + slot]);
+      fx2 = fold<OP>(fx2, sx2[l * TR * V + slot]);
+    }
+    const int32_t r = rb * TR * V + slot;
+    if (r >= p.m) continue;
+    if (nseg == 1) {
+      if (want_x) p.out_x[r] = fx;
+      if (want_x2) p.out_x2[r] = fx2;
+    } else {
+      work[(int64_t)s * p.m + r] = fx;
+      work[(int64_t)nseg * p.m + (int64_t)s * p.m + r] = fx2;
+    }
+  }
+}
+
+// Second pass: out[o] = fold over s < nseg of work[s * n_out + o] (x part, then x2 part).
+template <int OP>
+__global__ __launch_bounds__(RT) void reduce_combine_kernel(const float* work, int32_t n_out,
+                                                            int32_t nseg, uint32_t flags,
+                                                            float* out_x, float* out_x2) {
+  const int64_t o = (int64_t)blockIdx.x * RT + threadIdx.x;
+  if (o >= n_out) return;
+  float fx = fold_identity<OP>(), fx2 = fold_identity<OP>();
+  for (int32_t s = 0; s < nseg; ++s) {
+    fx = fold<OP>(fx, work[(int64_t)s * n_out + o]);
+    fx2 = fold<OP>(fx2, work[(int64_t)nseg * n_out + (int64_t)s * n_out + o]);
+  }
+  if (flags & TPP_RED_X) out_x[o] = fx;
+  if (flags & TPP_RED_X2) out_x2[o] = fx2;
+}
+
+struct Plan {
+  bool by_cols;
+  int v;          // elements per load (1, 4 or 8)
+  int32_t nseg;   // partial results per output
+  int32_t seg;    // rows per segment (BY_ROWS) or columns per range (BY_COLS)
+  int32_t tr;     // BY_COLS: row vectors per workgroup
+  int32_t nrb;    // BY_COLS: row blocks
+  int64_t blocks; // first-pass workgroups
+};
+
+Plan make_plan(const ReduceParams& p) {
+  Plan pl{};
+  pl.by_cols = (p.flags & TPP_RED_BY_COLS) != 0;
+  const int es = p.in_bf16 ? 2 : 4;
+  const bool aligned = (reinterpret_cast<uintptr_t>(p.in) & 15) == 0 && ((p.ld * es) % 16) == 0;
+  pl.v = aligned ? 16 / es : 1;
+  if (!pl.by_cols) {
+    const int64_t rows_per_pass = 64LL * pl.v;
+    const int64_t max_seg = (p.m + rows_per_pass - 1) / rows_per_pass;
+    int64_t nseg = (4096 + p.n - 1) / p.n;   // aim for >= 4096 wavefronts
+    nseg = nseg < 1 ? 1 : (nseg > max_seg ? max_seg : nseg);
+    if (nseg > 256) nseg = 256;
+    const int64_t per = (p.m + nseg - 1) / nseg;
+    pl.seg = (int32_t)(((per + rows_per_pass - 1) / rows_per_pass) * rows_per_pass);
+    pl.nseg = (int32_t)((p.m + pl.seg - 1) / pl.seg);
+    pl.blocks = ((int64_t)p.n * pl.nseg + (RT / 64) - 1) / (RT / 64);
+  } else {
+    const int64_t vecs = (p.m + pl.v - 1) / pl.v;
+    int32_t tr = 1;
+    while (tr < vecs && tr < RT) tr <<= 1;
+    pl.tr = tr;
+    pl.nrb = (int32_t)((p.m + (int64_t)tr * pl.v - 1) / ((int64_t)tr * pl.v));
+    const int32_t tc = RT / tr;
+    // aim for ~512 workgroups, each walking at least 4 columns per column lane
+    int64_t nseg = (512 + pl.nrb - 1) / pl.nrb;
+    const int64_t max_seg = (p.n + 4LL * tc - 1) / (4LL * tc);
+    nseg = nseg < 1 ? 1 : (nseg > max_seg ? max_seg : nseg);
+    if (nseg > 256) nseg = 256;
+    pl.seg = (int32_t)((p.n + nseg - 1) / nseg);
+    pl.nseg = (int32_t)((p.n + pl.seg - 1) / pl.seg);
+    pl.blocks = (int64_t)pl.nrb * pl.nseg;
+  }
+  return pl;
+}
+
+template <int OP, bool BF16, int V>
+void launch_first(const ReduceParams& p, const Plan& pl, float* work, hipStream_t stream) {
+  if (!pl.by_cols)
+    hipLaunchKernelGGL((reduce_rows_kernel<OP, BF16, V>), dim3((unsigned)pl.blocks), dim3(RT), 0,
+                       stream, p, pl.seg, pl.nseg, work);
+  else
+    hipLaunchKernelGGL((reduce_cols_kernel<OP, BF16, V>), dim3((unsigned)pl.blocks), dim3(RT), 0,
+                       stream, p, pl.tr, pl.seg, pl.nseg, pl.nrb, work);
+}
+
+template <int OP>
+void launch_op(const ReduceParams& p, const Plan& pl, float* work, hipStream_t stream) {
+  if (p.in_bf16) {
+    if (pl.v == 8) launch_first<OP, true, 8>(p, pl, work, stream);
+    else launch_first<OP, true, 1>(p, pl, work, stream);
+  } else {
+    if (pl.v == 4) launch_first<OP, false, 4>(p, pl, work, stream);
+    else launch_first<OP, false, 1>(p, pl, work, stream);
+  }
+  if (pl.nseg > 1) {
+    const int32_t n_out = pl.by_cols ? p.m : p.n;
+    hipLaunchKernelGGL(reduce_combine_kernel<OP>, dim3((unsigned)((n_out + RT - 1) / RT)),
+                       dim3(RT), 0, stream, work, n_out, pl.nseg, p.flags, p.out_x, p.out_x2);
+  }
+}
+
+}  // namespace
+
+int64_t reduce_work_floats(const ReduceParams& p) {
+  const Plan pl = make_plan(p);
+  if (pl.nseg <= 1) return 0;
+  return 2LL * pl.nseg * (pl.by_cols ? p.m : p.n);
+}
+
+hipError_t launch_reduce(const ReduceParams& p, float* work, hipStream_t stream) {
+  const Plan pl = make_plan(p);
+  switch (p.op) {
+    case TPP_RED_SUM: launch_op<TPP_RED_SUM>(p, pl, work, stream); break;
+    case TPP_RED_MUL: launch_op<TPP_RED_MUL>(p, pl, work, stream); break;
+    case TPP_RED_MIN: launch_op<TPP_RED_MIN>(p, pl, work, stream); break;
+    default: launch_op<TPP_RED_MAX>(p, pl, work, stream); break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace tpp

@@ -1,0 +1,376 @@
+// tpp_api.hip -- the C ABI of include/tpp_brgemm.h: argument checks, the dispatch cache, kernel
+// selection and launches.  Host code only; the kernels live in brgemm_kernels.hip and
+// reduce_kernels.hip.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdlib>
+#include <cstdio>
+#include <cstring>
+#include <memory>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "internal.h"
+
+struct tpp_brgemm_kernel_s {
+  tpp_brgemm_desc desc;
+  bool bf16;         // A/B are bf16 (else fp32)
+  bool vec_ok;       // descriptor allows the 16-byte load path
+  char name[96];
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+tpp_status fail(tpp_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+tpp_status fail(tpp_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+tpp_status ok() {
+  g_last_error.clear();
+  return TPP_OK;
+}
+
+bool same_desc(const tpp_brgemm_desc& x, const tpp_brgemm_desc& y) {
+  return x.m == y.m && x.n == y.n && x.k == y.k && x.lda == y.lda && x.ldb == y.ldb &&
+         x.ldc == y.ldc && x.a_type == y.a_type && x.b_type == y.b_type && x.c_type == y.c_type &&
+         x.comp_type == y.comp_type && std::memcmp(&x.beta, &y.beta, sizeof(float)) == 0 &&
+         x.kind == y.kind && x.stride_a == y.stride_a && x.stride_b == y.stride_b &&
+         x.flags == y.flags;
+}
+
+std::mutex g_cache_mu;
+std::vector<std::unique_ptr<tpp_brgemm_kernel_s>>& cache() {
+  static std::vector<std::unique_ptr<tpp_brgemm_kernel_s>> c;
+  return c;
+}
+
+bool valid_dtype(int32_t t) { return t == TPP_DT_F32 || t == TPP_DT_BF16; }
+
+// Kernel choice for one launch.  bf16 inputs take a 16-byte-load instance when the descriptor
+// and the grid keep every 8-element chunk contiguous and aligned (m, k, lda, ldb and all element
+// steps multiples of 8); the tile shape is the largest whose tile count still fills the 256
+// compute units.  Anything else takes the element-load instance.
+int32_t choose_kernel(const tpp_brgemm_kernel_s& h, const tpp::BrgemmParams& p) {
+  if (!h.bf16) return tpp::K_F32_GENERIC;
+  bool vec = h.vec_ok;
+  if (p.fused) vec = vec && (p.a_step_m % 8 == 0) && (p.b_step_n % 8 == 0);
+  if (!vec) return tpp::K_BF16_GENERIC;
+  if (const char* env = std::getenv("TPP_FORCE_KERNEL")) {
+    const int id = std::atoi(env);
+    if (id >= tpp::K_BF16_256x256 && id <= tpp::K_BF16_64x64) return id;
+  }
+  struct Cand { int32_t id; int bm, bn; };
+  const Cand cands[] = {{tpp::K_BF16_256x256, 256, 256},
+                        {tpp::K_BF16_256x128, 256, 128},
+                        {tpp::K_BF16_128x128, 128, 128},
+                        {tpp::K_BF16_64x64, 64, 64}};
+  for (const Cand& c : cands) {
+    const int64_t tiles = p.groups * ((p.vrows + c.bm - 1) / c.bm) * ((p.vcols + c.bn - 1) / c.bn);
+    // do not pad a small instance out to a much larger tile
+    const bool fits = (int64_t)c.bm <= 2LL * p.vrows && (int64_t)c.bn <= 2LL * p.vcols;
+    if (fits && tiles >= 256) return c.id;
+  }
+  return tpp::K_BF16_64x64;
+}
+
+tpp_status launch(const tpp_brgemm_kernel_s* h, tpp::BrgemmParams& p, void* stream) {
+  const int32_t id = choose_kernel(*h, p);
+  if (std::getenv("TPP_LOG"))
+    std::fprintf(stderr, "[tpp] %s: G=%lld vrows=%d vcols=%d fused=%d -> %s\n", h->name,
+                 (long long)p.groups, p.vrows, p.vcols, p.fused, tpp::kernel_name(id));
+  const hipError_t e = tpp::launch_brgemm(p, id, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess)
+    return fail(TPP_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+void fill_common(const tpp_brgemm_kernel_s* h, tpp::BrgemmParams& p) {
+  std::memset(&p, 0, sizeof p);
+  const tpp_brgemm_desc& d = h->desc;
+  p.m = d.m; p.n = d.n; p.k = d.k;
+  p.lda = d.lda; p.ldb = d.ldb; p.ldc = d.ldc;
+  p.beta = d.beta;
+  p.flags = d.flags;
+  p.c_bf16 = d.c_type == TPP_DT_BF16;
+  p.kind = d.kind;
+  p.stride_a = d.stride_a;
+  p.stride_b = d.stride_b;
+}
+
+tpp_status check_handle(tpp_brgemm_handle h) {
+  if (!h) return fail(TPP_ERR_INVALID_ARG, "NULL handle");
+  return TPP_OK;
+}
+
+tpp_status check_bias(const tpp_brgemm_kernel_s* h, const float* bias) {
+  if ((h->desc.flags & TPP_EPI_BIAS) && !bias)
+    return fail(TPP_ERR_INVALID_ARG, "TPP_EPI_BIAS set but bias is NULL");
+  return TPP_OK;
+}
+
+// Single call = a batched call with one instance of a 1x1 strided grid.
+tpp_status run_single(const tpp_brgemm_kernel_s* h, tpp::BrgemmParams& p, void* stream) {
+  p.fused = 1;
+  p.gm = p.gn = 1;
+  p.groups = 1;
+  p.vrows = p.m;
+  p.vcols = p.n;
+  return launch(h, p, stream);
+}
+
+struct WorkBuffer {
+  float* ptr = nullptr;
+  int64_t floats = 0;
+};
+std::mutex g_work_mu;
+std::vector<WorkBuffer> g_work;   // one per device
+
+}  // namespace
+
+extern "C" {
+
+const char* tpp_status_string(tpp_status s) {
+  switch (s) {
+    case TPP_OK: return "TPP_OK";
+    case TPP_ERR_INVALID_ARG: return "TPP_ERR_INVALID_ARG";
+    case TPP_ERR_UNSUPPORTED: return "TPP_ERR_UNSUPPORTED";
+    case TPP_ERR_HIP: return "TPP_ERR_HIP";
+    case TPP_ERR_NO_MEMORY: return "TPP_ERR_NO_MEMORY";
+  }
+  return "TPP_ERR_UNKNOWN";
+}
+
+const char* tpp_last_error_message(void) { return g_last_error.c_str(); }
+
+tpp_status tpp_brgemm_dispatch(const tpp_brgemm_desc* desc, tpp_brgemm_handle* out) {
+  if (!desc || !out) return fail(TPP_ERR_INVALID_ARG, "NULL desc or out");
+  *out = nullptr;
+  const tpp_brgemm_desc& d = *desc;
+  if (d.m <= 0 || d.n <= 0 || d.k <= 0)
+    return fail(TPP_ERR_INVALID_ARG, "m, n, k must be > 0 (got %d, %d, %d)", d.m, d.n, d.k);
+  if (d.lda < d.m || d.ldb < d.k || d.ldc < d.m)
+    return fail(TPP_ERR_INVALID_ARG, "leading dimension too small (lda %lld < m, ldb %lld < k or ldc %lld < m)",
+                (long long)d.lda, (long long)d.ldb, (long long)d.ldc);
+  if (!valid_dtype(d.a_type) || !valid_dtype(d.b_type) || !valid_dtype(d.c_type) ||
+      !valid_dtype(d.comp_type))
+    return fail(TPP_ERR_INVALID_ARG, "unknown datatype code");
+  if (d.a_type != d.b_type)
+    return fail(TPP_ERR_UNSUPPORTED, "A and B must share a datatype");
+  if (d.comp_type != TPP_DT_F32)
+    return fail(TPP_ERR_UNSUPPORTED, "accumulation is fp32 only");
+  if (d.kind != TPP_BR_STRIDE && d.kind != TPP_BR_OFFSET && d.kind != TPP_BR_ADDRESS)
+    return fail(TPP_ERR_INVALID_ARG, "unknown batch kind %d", d.kind);
+  if (d.flags & ~(uint32_t)(TPP_EPI_BIAS | TPP_EPI_RELU | TPP_EPI_GELU_TANH))
+    return fail(TPP_ERR_INVALID_ARG, "unknown epilogue flag bits 0x%x", d.flags);
+  if ((d.flags & TPP_EPI_RELU) && (d.flags & TPP_EPI_GELU_TANH))
+    return fail(TPP_ERR_INVALID_ARG, "RELU and GELU_TANH exclude each other");
+  if (!std::isfinite(d.beta)) return fail(TPP_ERR_INVALID_ARG, "beta must be finite");
+
+  std::lock_guard<std::mutex> lock(g_cache_mu);
+  for (auto& h : cache()) {
+    if (same_desc(h->desc, d)) {
+      *out = h.get();
+      return ok();
+    }
+  }
+  auto h = std::make_unique<tpp_brgemm_kernel_s>();
+  h->desc = d;
+  h->bf16 = d.a_type == TPP_DT_BF16;
+  h->vec_ok = h->bf16 && d.m % 8 == 0 && d.k % 8 == 0 && d.lda % 8 == 0 && d.ldb % 8 == 0 &&
+              (d.kind != TPP_BR_STRIDE || (d.stride_a % 8 == 0 && d.stride_b % 8 == 0));
+  static const char* kinds[] = {"stride", "offset", "address"};
+  std::snprintf(h->name, sizeof h->name, "brgemm_%s_%s_m%d_n%d_k%d_%s%s", h->bf16 ? "bf16" : "f32",
+                d.c_type == TPP_DT_BF16 ? "bf16out" : "f32out", d.m, d.n, d.k, kinds[d.kind],
+                h->vec_ok ? "_vec" : "_generic");
+  *out = h.get();
+  cache().push_back(std::move(h));
+  return ok();
+}
+
+void tpp_brgemm_release(tpp_brgemm_handle) {}
+
+tpp_status tpp_brgemm_describe(tpp_brgemm_handle h, char* buf, size_t len) {
+  if (tpp_status s = check_handle(h)) return s;
+  if (!buf || len == 0) return fail(TPP_ERR_INVALID_ARG, "NULL buffer");
+  std::snprintf(buf, len, "%s", h->name);
+  return ok();
+}
+
+tpp_status tpp_brgemm_execute_stride(tpp_brgemm_handle h, const void* a, const void* b, void* c,
+                                     const float* bias, int64_t count, void* stream) {
+  if (tpp_status s = check_handle(h)) return s;
+  if (h->desc.kind != TPP_BR_STRIDE)
+    return fail(TPP_ERR_INVALID_ARG, "handle is not a stride-based BRGEMM");
+  if (count < 0) return fail(TPP_ERR_INVALID_ARG, "count < 0");
+  if (!c) return fail(TPP_ERR_INVALID_ARG, "NULL c");
+  if (count > 0 && (!a || !b)) return fail(TPP_ERR_INVALID_ARG, "NULL a or b");
+  if (tpp_status s = check_bias(h, bias)) return s;
+  tpp::BrgemmParams p;
+  fill_common(h, p);
+  p.a = a; p.b = b; p.c = c; p.bias = bias;
+  p.count = count;
+  return run_single(h, p, stream);
+}
+
+tpp_status tpp_brgemm_execute_offset(tpp_brgemm_handle h, const void* a, const void* b,
+                                     const int64_t* offs_a, const int64_t* offs_b, void* c,
+                                     const float* bias, int64_t count, void* stream) {
+  if (tpp_status s = check_handle(h)) return s;
+  if (h->desc.kind != TPP_BR_OFFSET)
+    return fail(TPP_ERR_INVALID_ARG, "handle is not an offset-based BRGEMM");
+  if (count < 0) return fail(TPP_ERR_INVALID_ARG, "count < 0");
+  if (!c) return fail(TPP_ERR_INVALID_ARG, "NULL c");
+  if (count > 0 && (!a || !b || !offs_a || !offs_b))
+    return fail(TPP_ERR_INVALID_ARG, "NULL a, b or offset array");
+  if (tpp_status s = check_bias(h, bias)) return s;
+  tpp::BrgemmParams p;
+  fill_common(h, p);
+  p.a = a; p.b = b; p.c = c; p.bias = bias;
+  p.offs_a = offs_a; p.offs_b = offs_b;
+  p.count = count;
+  return run_single(h, p, stream);
+}
+
+tpp_status tpp_brgemm_execute_address(tpp_brgemm_handle h, const void* const* ptrs_a,
+                                      const void* const* ptrs_b, void* c, const float* bias,
+                                      int64_t count, void* stream) {
+  if (tpp_status s = check_handle(h)) return s;
+  if (h->desc.kind != TPP_BR_ADDRESS)
+    return fail(TPP_ERR_INVALID_ARG, "handle is not an address-based BRGEMM");
+  if (count < 0) return fail(TPP_ERR_INVALID_ARG, "count < 0");
+  if (!c) return fail(TPP_ERR_INVALID_ARG, "NULL c");
+  if (count > 0 && (!ptrs_a || !ptrs_b)) return fail(TPP_ERR_INVALID_ARG, "NULL pointer list");
+  if (tpp_status s = check_bias(h, bias)) return s;
+  tpp::BrgemmParams p;
+  fill_common(h, p);
+  p.c = c; p.bias = bias;
+  p.ptrs_a = ptrs_a; p.ptrs_b = ptrs_b;
+  // The kernel reads an address-kind pair list through begin[]; a single call is the list
+  // [0, count), kept in the kernel arguments (no device array needed).
+  p.kind = TPP_BR_ADDRESS;
+  p.count = count;
+  p.begin = nullptr;
+  return run_single(h, p, stream);
+}
+
+tpp_status tpp_brgemm_execute_batched(tpp_brgemm_handle h, const tpp_grid_strided* grid,
+                                      int64_t G, const int64_t* d_a_off, const int64_t* d_b_off,
+                                      const int64_t* d_c_off, const int64_t* d_bias_off,
+                                      const void* a, const void* b, void* c, const float* bias,
+                                      int64_t count, const int64_t* d_offs_a,
+                                      const int64_t* d_offs_b, const int64_t* d_begin,
+                                      const void* const* d_ptrs_a, const void* const* d_ptrs_b,
+                                      void* stream) {
+  if (tpp_status s = check_handle(h)) return s;
+  const tpp_brgemm_desc& d = h->desc;
+  if (G < 0) return fail(TPP_ERR_INVALID_ARG, "G < 0");
+  if (grid) {
+    if (grid->gm <= 0 || grid->gn <= 0) return fail(TPP_ERR_INVALID_ARG, "grid gm, gn must be > 0");
+    if (grid->gm * grid->gn != G)
+      return fail(TPP_ERR_INVALID_ARG, "grid gm*gn (%lld) != G (%lld)",
+                  (long long)(grid->gm * grid->gn), (long long)G);
+    if (d_a_off || d_b_off || d_c_off || d_bias_off)
+      return fail(TPP_ERR_INVALID_ARG, "offset arrays given together with a strided grid");
+  }
+  if (G == 0) return ok();
+  if (!c) return fail(TPP_ERR_INVALID_ARG, "NULL c");
+  if (tpp_status s = check_bias(h, bias)) return s;
+  if (d.kind == TPP_BR_ADDRESS) {
+    if (!d_begin) return fail(TPP_ERR_INVALID_ARG, "address kind needs d_begin");
+    if (!d_ptrs_a || !d_ptrs_b) return fail(TPP_ERR_INVALID_ARG, "NULL pointer list");
+  } else {
+    if (count < 0) return fail(TPP_ERR_INVALID_ARG, "count < 0");
+    if (count > 0 && (!a || !b)) return fail(TPP_ERR_INVALID_ARG, "NULL a or b");
+    if (d.kind == TPP_BR_OFFSET && count > 0 && (!d_offs_a || !d_offs_b))
+      return fail(TPP_ERR_INVALID_ARG, "NULL offset array");
+  }
+  tpp::BrgemmParams p;
+  fill_common(h, p);
+  p.a = a; p.b = b; p.c = c; p.bias = bias;
+  p.count = count;
+  p.offs_a = d_offs_a; p.offs_b = d_offs_b;
+  p.begin = d_begin; p.ptrs_a = d_ptrs_a; p.ptrs_b = d_ptrs_b;
+  p.a_off = d_a_off; p.b_off = d_b_off; p.c_off = d_c_off; p.bias_off = d_bias_off;
+  if (grid) {
+    p.gm = grid->gm; p.gn = grid->gn;
+    p.a_step_m = grid->a_step_m; p.b_step_n = grid->b_step_n;
+    p.c_step_m = grid->c_step_m; p.c_step_n = grid->c_step_n;
+    p.bias_step_m = grid->bias_step_m;
+  }
+  // A strided grid of stride/offset kind is fused into one virtual C when that C fits int32
+  // indexing; address kind (one pair list per instance) and explicit grids tile per instance.
+  const int64_t vr = grid ? grid->gm * (int64_t)d.m : d.m;
+  const int64_t vc = grid ? grid->gn * (int64_t)d.n : d.n;
+  const int64_t lim = (1LL << 31) - 512;
+  if (grid && d.kind != TPP_BR_ADDRESS && vr < lim && vc < lim) {
+    p.fused = 1;
+    p.groups = 1;
+    p.vrows = (int32_t)vr;
+    p.vcols = (int32_t)vc;
+  } else {
+    p.fused = 0;
+    p.grid_form = grid ? 1 : 0;
+    p.groups = G;
+    p.vrows = d.m;
+    p.vcols = d.n;
+  }
+  return launch(h, p, stream);
+}
+
+tpp_status tpp_reduce(int32_t m, int32_t n, int64_t ld, int32_t in_type, const void* in,
+                      int32_t op, uint32_t flags, float* out_x, float* out_x2, void* stream) {
+  if (m <= 0 || n <= 0) return fail(TPP_ERR_INVALID_ARG, "m, n must be > 0");
+  if (ld < m) return fail(TPP_ERR_INVALID_ARG, "ld < m");
+  if (!valid_dtype(in_type)) return fail(TPP_ERR_INVALID_ARG, "unknown datatype code");
+  if (!in) return fail(TPP_ERR_INVALID_ARG, "NULL input");
+  if (op < TPP_RED_SUM || op > TPP_RED_MAX) return fail(TPP_ERR_INVALID_ARG, "unknown op %d", op);
+  if (flags & ~(uint32_t)(TPP_RED_BY_COLS | TPP_RED_BY_ROWS | TPP_RED_X | TPP_RED_X2))
+    return fail(TPP_ERR_INVALID_ARG, "unknown reduce flag bits");
+  const bool by_cols = flags & TPP_RED_BY_COLS, by_rows = flags & TPP_RED_BY_ROWS;
+  if (by_cols == by_rows) return fail(TPP_ERR_INVALID_ARG, "set exactly one of BY_COLS, BY_ROWS");
+  if (!(flags & (TPP_RED_X | TPP_RED_X2))) return fail(TPP_ERR_INVALID_ARG, "set X and/or X2");
+  if ((flags & TPP_RED_X) && !out_x) return fail(TPP_ERR_INVALID_ARG, "NULL out_x");
+  if ((flags & TPP_RED_X2) && !out_x2) return fail(TPP_ERR_INVALID_ARG, "NULL out_x2");
+  tpp::ReduceParams p{in, m, n, ld, in_type == TPP_DT_BF16, op, flags, out_x, out_x2};
+  const int64_t need = tpp::reduce_work_floats(p);
+  float* work = nullptr;
+  if (need > 0) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return fail(TPP_ERR_HIP, "hipGetDevice failed");
+    std::lock_guard<std::mutex> lock(g_work_mu);
+    if ((int)g_work.size() <= dev) g_work.resize(dev + 1);
+    WorkBuffer& wb = g_work[dev];
+    if (wb.floats < need) {
+      // Growing waits for the device: the old buffer may still be read by queued reductions.
+      if (wb.ptr) {
+        if (hipDeviceSynchronize() != hipSuccess || hipFree(wb.ptr) != hipSuccess)
+          return fail(TPP_ERR_HIP, "could not release the old work buffer");
+        wb.ptr = nullptr;
+        wb.floats = 0;
+      }
+      void* ptr = nullptr;
+      if (hipMalloc(&ptr, (size_t)need * sizeof(float)) != hipSuccess)
+        return fail(TPP_ERR_NO_MEMORY, "work buffer of %lld floats", (long long)need);
+      wb.ptr = static_cast<float*>(ptr);
+      wb.floats = need;
+    }
+    work = wb.ptr;
+  }
+  const hipError_t e = tpp::launch_reduce(p, work, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(TPP_ERR_HIP, "reduce launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+}  // extern "C"

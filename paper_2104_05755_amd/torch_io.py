@@ -1,0 +1,98 @@
+"""torch glue for the binding: device copies of host operands and one batched call per workload.
+
+torch supplies device memory and the stream; every computation happens in the HIP library.
+A workload call (see ``workloads.Call``) names its operand arrays, its instance grid and its pair
+list; :func:`prepare` uploads what the call needs once, and :func:`launch` issues the batched
+BRGEMM on the current stream.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import Optional
+
+import numpy as np
+import torch
+
+import paper_2104_05755_amd as tpp
+
+
+def to_device(arr: np.ndarray, device="cuda") -> torch.Tensor:
+    """Copy a host array to the device; bf16 bit patterns (uint16) travel as int16."""
+    if arr.dtype == np.uint16:
+        return torch.from_numpy(arr.view(np.int16)).to(device)
+    return torch.from_numpy(np.ascontiguousarray(arr)).to(device)
+
+
+def to_host(t: torch.Tensor, like: np.ndarray) -> np.ndarray:
+    out = t.cpu().numpy()
+    return out.view(np.uint16) if like.dtype == np.uint16 else out
+
+
+@dataclass
+class DeviceCall:
+    handle: int
+    call: object
+    a: Optional[torch.Tensor]
+    b: Optional[torch.Tensor]
+    c: torch.Tensor
+    bias: Optional[torch.Tensor]
+    a_off: Optional[torch.Tensor] = None
+    b_off: Optional[torch.Tensor] = None
+    c_off: Optional[torch.Tensor] = None
+    bias_off: Optional[torch.Tensor] = None
+    offs_a: Optional[torch.Tensor] = None
+    offs_b: Optional[torch.Tensor] = None
+    begin: Optional[torch.Tensor] = None
+    ptrs_a: Optional[torch.Tensor] = None
+    ptrs_b: Optional[torch.Tensor] = None
+
+
+def descriptor(call) -> tpp.tpp_brgemm_desc:
+    return tpp.make_desc(call.m, call.n, call.k, call.lda, call.ldb, call.ldc, call.ab_type,
+                         call.c_type, call.beta, call.kind, call.stride_a, call.stride_b,
+                         sorted(call.flags))
+
+
+def _i64(x, device):
+    """int64 device array; an empty list still gets one (unused) element so that its address is
+    not NULL."""
+    if x is None:
+        return None
+    arr = np.ascontiguousarray(x, dtype=np.int64)
+    if arr.size == 0:
+        arr = np.zeros(1, dtype=np.int64)
+    return torch.from_numpy(arr).to(device)
+
+
+def prepare(call, dev: dict, device="cuda") -> DeviceCall:
+    """Dispatch the call's descriptor and upload its offset / pointer / CSR arrays.  ``dev`` maps
+    array names to device tensors (the operands, already resident)."""
+    h = tpp.tpp_brgemm_dispatch(descriptor(call))
+    a = dev[call.a] if call.a else None
+    b = dev[call.b] if call.b else None
+    dc = DeviceCall(h, call, a, b, dev[call.c], dev[call.bias] if call.bias else None)
+    if call.grid is None:
+        dc.a_off, dc.b_off = _i64(call.a_off, device), _i64(call.b_off, device)
+        dc.c_off, dc.bias_off = _i64(call.c_off, device), _i64(call.bias_off, device)
+    dc.offs_a, dc.offs_b = _i64(call.offs_a, device), _i64(call.offs_b, device)
+    if call.kind == "address":
+        es = 4 if call.ab_type == "f32" else 2
+        dc.begin = _i64(call.begin, device)
+        dc.ptrs_a = _i64(a.data_ptr() + np.asarray(call.idx_a, dtype=np.int64) * es, device)
+        dc.ptrs_b = _i64(b.data_ptr() + np.asarray(call.idx_b, dtype=np.int64) * es, device)
+    return dc
+
+
+def launch(dc: DeviceCall, stream: Optional[int] = None):
+    """One batched BRGEMM launch for the whole call (all G instances)."""
+    call = dc.call
+    if stream is None:
+        stream = tpp.current_stream()
+    tpp.tpp_brgemm_execute_batched(
+        dc.handle, call.grid, call.G, dc.a_off, dc.b_off, dc.c_off, dc.bias_off,
+        dc.a if call.kind != "address" else None, dc.b if call.kind != "address" else None,
+        dc.c, dc.bias, call.count, dc.offs_a, dc.offs_b, dc.begin, dc.ptrs_a, dc.ptrs_b, stream)
+
+
+def upload(wl, device="cuda") -> dict:
+    return {name: to_device(arr, device) for name, arr in wl.arrays.items()}

@@ -1,0 +1,144 @@
+"""The C-ABI library on the host: it loads, exports every declared symbol, and its host-only
+paths (dispatch validation, the handle cache, argument checks that precede any launch) behave
+as include/tpp_brgemm.h states.  No device work happens here."""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tpp_brgemm.h")
+
+
+@pytest.fixture(scope="module")
+def tpp():
+    import paper_2104_05755_amd as tpp
+    return tpp
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(tpp_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function(tpp):
+    names = declared_functions()
+    assert "tpp_brgemm_dispatch" in names and "tpp_reduce" in names
+    lib = ctypes.CDLL(tpp.LIB_PATH)
+    missing = [n for n in names if not hasattr(lib, n)]
+    assert not missing, f"not exported: {missing}"
+
+
+def test_library_is_built_for_gfx950_only(tpp):
+    """The offload bundle of our own build names its target; gfx950 must be the only one."""
+    blob = open(tpp.LIB_PATH, "rb").read()
+    targets = set(re.findall(rb"amdgcn-amd-amdhsa-+(gfx[0-9a-f]+)", blob))
+    assert targets == {b"gfx950"}, targets
+
+
+def test_struct_layout_matches_header(tpp):
+    # int32 m,n,k | pad | int64 lda,ldb,ldc | int32 x4 | float | int32 | int64 x2 | uint32
+    assert ctypes.sizeof(tpp.tpp_brgemm_desc) == 88
+    assert tpp.tpp_brgemm_desc.lda.offset == 16
+    assert tpp.tpp_brgemm_desc.beta.offset == 56
+    assert tpp.tpp_brgemm_desc.stride_a.offset == 64
+    assert tpp.tpp_brgemm_desc.flags.offset == 80
+    assert ctypes.sizeof(tpp.tpp_grid_strided) == 56
+
+
+def test_dispatch_caches_equal_descriptors(tpp):
+    d1 = tpp.make_desc(64, 64, 64, 64, 64, 64, "bf16", "bf16", 0.0, "stride", 4096, 4096, ["bias", "relu"])
+    d2 = tpp.make_desc(64, 64, 64, 64, 64, 64, "bf16", "bf16", 0.0, "stride", 4096, 4096, ["bias", "relu"])
+    d3 = tpp.make_desc(64, 64, 64, 64, 64, 64, "bf16", "bf16", 0.0, "stride", 4096, 4096, ["bias"])
+    h1, h2, h3 = (tpp.tpp_brgemm_dispatch(d) for d in (d1, d2, d3))
+    assert h1 == h2 and h1 != h3
+    assert "bf16" in tpp.tpp_brgemm_describe(h1) and "vec" in tpp.tpp_brgemm_describe(h1)
+    odd = tpp.make_desc(17, 5, 3, 17, 3, 17, "bf16", "f32")
+    assert "generic" in tpp.tpp_brgemm_describe(tpp.tpp_brgemm_dispatch(odd))
+    tpp.tpp_brgemm_release(h1)
+    tpp.tpp_brgemm_release(None)
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("m", 0, -1), ("n", -3, -1), ("k", 0, -1),
+    ("lda", 10, -1), ("ldb", 5, -1), ("ldc", 1, -1),
+    ("a_type", 7, -1), ("comp_type", 1, -2), ("kind", 3, -1), ("flags", 8, -1),
+    ("flags", 2 | 4, -1), ("beta", float("nan"), -1),
+])
+def test_dispatch_rejects(tpp, field, value, status):
+    d = tpp.make_desc(16, 16, 16, 16, 16, 16, "bf16", "f32")
+    setattr(d, field, value)
+    with pytest.raises(tpp.TppError) as e:
+        tpp.tpp_brgemm_dispatch(d)
+    assert e.value.status == status
+    assert tpp.tpp_last_error_message()
+
+
+def test_dispatch_rejects_mixed_input_types(tpp):
+    d = tpp.make_desc(16, 16, 16, 16, 16, 16, "bf16", "f32")
+    d.b_type = tpp.TPP_DT_F32
+    with pytest.raises(tpp.TppError) as e:
+        tpp.tpp_brgemm_dispatch(d)
+    assert e.value.status == tpp.TPP_ERR_UNSUPPORTED
+
+
+def test_execute_argument_checks_precede_any_launch(tpp):
+    hs = tpp.tpp_brgemm_dispatch(tpp.make_desc(16, 16, 16, 16, 16, 16, "bf16", "f32", kind="stride"))
+    ho = tpp.tpp_brgemm_dispatch(tpp.make_desc(16, 16, 16, 16, 16, 16, "bf16", "f32", kind="offset"))
+    hb = tpp.tpp_brgemm_dispatch(tpp.make_desc(16, 16, 16, 16, 16, 16, "bf16", "f32", flags=["bias"]))
+    ha = tpp.tpp_brgemm_dispatch(tpp.make_desc(16, 16, 16, 16, 16, 16, "bf16", "f32", kind="address"))
+    fake = 1 << 40   # never dereferenced: every call below fails its checks first
+    bad = [
+        lambda: tpp.tpp_brgemm_execute_stride(None, fake, fake, fake, None, 1),
+        lambda: tpp.tpp_brgemm_execute_stride(hs, fake, fake, fake, None, -1),
+        lambda: tpp.tpp_brgemm_execute_stride(hs, None, fake, fake, None, 2),
+        lambda: tpp.tpp_brgemm_execute_stride(hs, fake, fake, None, None, 0),
+        lambda: tpp.tpp_brgemm_execute_stride(ho, fake, fake, fake, None, 1),      # wrong kind
+        lambda: tpp.tpp_brgemm_execute_offset(ho, fake, fake, None, fake, fake, None, 1),
+        lambda: tpp.tpp_brgemm_execute_stride(hb, fake, fake, fake, None, 1),      # bias missing
+        lambda: tpp.tpp_brgemm_execute_address(ha, None, fake, fake, None, 1),
+        lambda: tpp.tpp_brgemm_execute_batched(hs, dict(gm=2, gn=2, a_step_m=0, b_step_n=0,
+                                                        c_step_m=0, c_step_n=0, bias_step_m=0),
+                                               3, None, None, None, None, fake, fake, fake, None,
+                                               1, None, None, None, None, None),    # gm*gn != G
+        lambda: tpp.tpp_brgemm_execute_batched(hs, dict(gm=1, gn=1, a_step_m=0, b_step_n=0,
+                                                        c_step_m=0, c_step_n=0, bias_step_m=0),
+                                               1, fake, None, None, None, fake, fake, fake, None,
+                                               1, None, None, None, None, None),    # grid + arrays
+        lambda: tpp.tpp_brgemm_execute_batched(ha, None, 4, None, None, fake, None, None, None,
+                                               fake, None, 0, None, None, None, fake, fake),
+        lambda: tpp.tpp_brgemm_execute_batched(hs, None, -1, None, None, None, None, fake, fake,
+                                               fake, None, 1, None, None, None, None, None),
+    ]
+    for i, f in enumerate(bad):
+        with pytest.raises(tpp.TppError) as e:
+            f()
+        assert e.value.status == tpp.TPP_ERR_INVALID_ARG, i
+
+
+def test_zero_instances_is_a_no_op(tpp):
+    hs = tpp.tpp_brgemm_dispatch(tpp.make_desc(16, 16, 16, 16, 16, 16, "bf16", "f32"))
+    tpp.tpp_brgemm_execute_batched(hs, None, 0, None, None, None, None, None, None, None, None,
+                                   0, None, None, None, None, None)
+
+
+@pytest.mark.parametrize("args", [
+    (0, 4, 4, 0, 1, 0, 1 | 4),           # m = 0
+    (4, 4, 3, 0, 1, 0, 1 | 4),           # ld < m
+    (4, 4, 4, 9, 1, 0, 1 | 4),           # bad dtype
+    (4, 4, 4, 0, 1, 7, 1 | 4),           # bad op
+    (4, 4, 4, 0, 1, 0, 1 | 2 | 4),       # both directions
+    (4, 4, 4, 0, 1, 0, 1),               # no output selected
+    (4, 4, 4, 0, 1, 0, 1 | 8),           # X2 without out_x2
+    (4, 4, 4, 0, None, 0, 1 | 4),        # NULL input
+])
+def test_reduce_argument_checks(tpp, args):
+    m, n, ld, dt, x, op, flags = args
+    fake = 1 << 40
+    with pytest.raises(tpp.TppError) as e:
+        tpp.tpp_reduce(m, n, ld, dt, fake if x else None, op, flags, fake, None)
+    assert e.value.status == tpp.TPP_ERR_INVALID_ARG

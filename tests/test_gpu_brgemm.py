@@ -1,0 +1,252 @@
+"""GPU parity: the HIP BRGEMM path (through the C ABI) against the CPU oracle.
+
+Bars: relative Frobenius error <= 1e-5 for fp32 inputs and <= 5e-3 for bf16 inputs with fp32
+accumulation, against the oracle's output rounded to the GPU's output type; bit-exact equality
+where the arithmetic is exact (small-integer data: every product and partial sum is an integer
+below 2^24, so any summation order gives the same fp32 value, and the fp32 -> bf16 narrowing is
+then the same decision on both sides).  No oracle input comes from the GPU."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as wk
+from helpers import rel_fro, run_oracle, values
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    import paper_2104_05755_amd  # noqa: F401  (fails loudly if the HIP library is missing)
+    return torch.device("cuda:0")
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def run_gpu(wl, calls=None, dev=None):
+    """Run the workload's calls in order on the GPU; returns host copies of every array."""
+    from paper_2104_05755_amd import torch_io
+    dev = dev if dev is not None else torch_io.upload(wl)
+    for ci in (calls if calls is not None else range(len(wl.calls))):
+        dc = torch_io.prepare(wl.calls[ci], dev)
+        torch_io.launch(dc)
+    torch.cuda.synchronize()
+    return {k: torch_io.to_host(v, wl.arrays[k]) for k, v in dev.items()}
+
+
+def tol(call):
+    return 1e-5 if call.ab_type == "f32" else 5e-3
+
+
+def blocks(flat, call, insts):
+    """The m x n output blocks of the given instances (as [n][m] arrays) from a flat C."""
+    out = []
+    for g in insts:
+        if call.grid is not None:
+            gi_m, gi_n = g % call.grid["gm"], g // call.grid["gm"]
+            off = gi_m * call.grid["c_step_m"] + gi_n * call.grid["c_step_n"]
+        else:
+            off = int(call.c_off[g]) if call.c_off is not None else 0
+        idx = off + np.arange(call.n)[:, None] * call.ldc + np.arange(call.m)[None, :]
+        out.append(flat.reshape(-1)[idx])
+    return np.stack(out)
+
+
+def check_close(got, ref, call, what):
+    g = values(got, call.c_type)
+    r = values(ref, call.c_type)
+    assert not np.isnan(g).any(), f"{what}: NaN in GPU output"
+    err = rel_fro(g, r)
+    assert err <= tol(call), f"{what}: rel Frobenius error {err:.3e} > {tol(call)}"
+    return err
+
+
+# ----------------------------------------------------------------------------------------------
+# Small shapes: every kind, dtype combination, epilogue, beta, ragged sizes, padding
+# ----------------------------------------------------------------------------------------------
+SHAPES = [(1, 1, 1, 1), (5, 3, 7, 2), (16, 16, 16, 3), (17, 33, 65, 2), (64, 64, 64, 4),
+          (64, 56, 64, 9), (72, 40, 24, 5), (128, 128, 64, 3), (200, 136, 80, 2), (64, 64, 64, 0),
+          (8, 8, 8, 1), (96, 160, 128, 2), (40, 72, 8, 6)]
+TYPES = [("f32", "f32"), ("bf16", "f32"), ("bf16", "bf16"), ("f32", "bf16")]
+EPIS = [set(), {"bias"}, {"relu"}, {"bias", "relu"}, {"bias", "gelu_tanh"}]
+
+
+def _cases():
+    rng = np.random.default_rng(7)
+    cases = []
+    for si, (m, n, k, cnt) in enumerate(SHAPES):
+        for ti, (ab, ct) in enumerate(TYPES):
+            kind = ("stride", "offset", "address")[(si + ti) % 3]
+            beta = (0.0, 1.0, 0.5)[(si * 3 + ti) % 3]
+            epi = EPIS[(si + 2 * ti) % len(EPIS)]
+            pad = (0, 8, 3)[(si + ti) % 3]
+            cases.append((m, n, k, cnt, kind, ab, ct, beta, tuple(sorted(epi)), pad))
+    return cases
+
+
+@pytest.mark.parametrize("m,n,k,count,kind,ab,ct,beta,epi,pad", _cases())
+def test_small_shapes_match_oracle(m, n, k, count, kind, ab, ct, beta, epi, pad):
+    rng = np.random.default_rng(hash((m, n, k, count, kind, ab, ct, beta, epi, pad)) % 2**32)
+    wl = wk.small_case(rng, m, n, k, count, kind, ab, ct, beta, set(epi), pad=pad)
+    say(f"case m={m} n={n} k={k} count={count} {kind} {ab}->{ct} beta={beta} {epi} pad={pad}")
+    ref, _ = run_oracle(wl)
+    got = run_gpu(wl)["c"]
+    call = wl.calls[0]
+    live = blocks(got, call, [0]), blocks(ref, call, [0])
+    check_close(live[0], live[1], call, "small")
+    if beta == 0.0:   # C was NaN-filled: the padding of C (ldc > m) must be untouched
+        pad_g = got.reshape(n, call.ldc)[:, m:]
+        assert np.array_equal(pad_g.view(np.uint8), wl.arrays["c"].reshape(n, call.ldc)[:, m:].view(np.uint8))
+
+
+@pytest.mark.parametrize("kind", ["stride", "offset", "address"])
+@pytest.mark.parametrize("ab,ct", [("bf16", "bf16"), ("bf16", "f32"), ("f32", "f32")])
+@pytest.mark.parametrize("m,n,k,count", [(64, 64, 64, 16), (128, 128, 64, 8), (24, 17, 40, 3),
+                                         (64, 56, 64, 9)])
+def test_integer_data_bit_exact(kind, ab, ct, m, n, k, count):
+    rng = np.random.default_rng(m * 1000 + n * 10 + count)
+    wl = wk.small_case(rng, m, n, k, count, kind, ab, ct, 1.0, {"bias", "relu"}, integer=True)
+    say(f"integer case {m}x{n}x{k} count={count} {kind} {ab}->{ct}")
+    ref, _ = run_oracle(wl)
+    got = run_gpu(wl)["c"]
+    assert np.array_equal(got, ref)
+
+
+def test_three_variants_bit_identical_on_gpu():
+    rng = np.random.default_rng(99)
+    base = wk.small_case(rng, 128, 96, 64, 7, "stride", "bf16", "bf16", 0.0, {"bias", "gelu_tanh"})
+    call = base.calls[0]
+    outs = [run_gpu(base)["c"]]
+    for kind in ("offset", "address"):
+        kw = dict(call.__dict__, kind=kind, grid=None)
+        if kind == "offset":
+            kw.update(offs_a=np.arange(7) * call.stride_a, offs_b=np.arange(7) * call.stride_b)
+        else:
+            kw.update(begin=np.array([0, 7]), idx_a=np.arange(7) * call.stride_a,
+                      idx_b=np.arange(7) * call.stride_b)
+        outs.append(run_gpu(wk.Workload(kind, base.arrays, [wk.Call(**kw)]))["c"])
+    assert np.array_equal(outs[0], outs[1]) and np.array_equal(outs[0], outs[2])
+
+
+def test_single_call_entry_points_match_batched():
+    """The paper-shaped single calls (stride / offset / address) equal one-instance batches."""
+    import paper_2104_05755_amd as tpp
+    from paper_2104_05755_amd import torch_io
+    rng = np.random.default_rng(5)
+    wl = wk.small_case(rng, 64, 48, 64, 5, "stride", "bf16", "f32", 0.5, {"bias"})
+    call = wl.calls[0]
+    ref, _ = run_oracle(wl)
+    dev = torch_io.upload(wl)
+    h = tpp.tpp_brgemm_dispatch(torch_io.descriptor(call))
+    tpp.tpp_brgemm_execute_stride(h, dev["a"], dev["b"], dev["c"], dev["bias"], 5,
+                                  tpp.current_stream())
+    got_s = torch_io.to_host(dev["c"], wl.arrays["c"])
+    dev = torch_io.upload(wl)
+    ho = tpp.tpp_brgemm_dispatch(torch_io.descriptor(wk.Call(**dict(call.__dict__, kind="offset"))))
+    offs_a = torch.arange(5, device="cuda", dtype=torch.int64) * call.stride_a
+    offs_b = torch.arange(5, device="cuda", dtype=torch.int64) * call.stride_b
+    tpp.tpp_brgemm_execute_offset(ho, dev["a"], dev["b"], offs_a, offs_b, dev["c"], dev["bias"], 5,
+                                  tpp.current_stream())
+    got_o = torch_io.to_host(dev["c"], wl.arrays["c"])
+    dev = torch_io.upload(wl)
+    ha = tpp.tpp_brgemm_dispatch(torch_io.descriptor(wk.Call(**dict(call.__dict__, kind="address"))))
+    pa = dev["a"].data_ptr() + offs_a * 2
+    pb = dev["b"].data_ptr() + offs_b * 2
+    tpp.tpp_brgemm_execute_address(ha, pa, pb, dev["c"], dev["bias"], 5, tpp.current_stream())
+    got_a = torch_io.to_host(dev["c"], wl.arrays["c"])
+    torch.cuda.synchronize()
+    assert np.array_equal(got_s, got_o) and np.array_equal(got_s, got_a)
+    check_close(got_s, ref, call, "single stride")
+
+
+# ----------------------------------------------------------------------------------------------
+# The five workloads: reduced sizes (whole output vs oracle), then full sizes (sampled)
+# ----------------------------------------------------------------------------------------------
+REDUCED = {
+    1: lambda: wk.fp32_single(),
+    2: lambda: wk.mlp_fc(minibatch=320, c_in=256, k_out=448),
+    3: lambda: wk.conv3x3(images=2, h=9, w=56, c=64, k=64),
+    4: lambda: wk.mlp_block(tokens=576, hidden=320, inter=512),
+    5: lambda: wk.gathered(n_out=24, pool=64, min_len=0, max_len=12),
+}
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_workload_reduced_size_whole_output(cfg):
+    wl = REDUCED[cfg]()
+    say(f"workload {wl.name} reduced")
+    got = run_gpu(wl)
+    if wl.name == "mlp_block":
+        h_ref, _ = run_oracle(wl, 0)
+        check_close(got["h"], h_ref, wl.calls[0], "mlp_block h")
+        wl2 = wk.Workload(wl.name, dict(wl.arrays, h=h_ref), wl.calls)
+        y_ref, _ = run_oracle(wl2, 1)
+        check_close(got["y"], y_ref, wl.calls[1], "mlp_block y")
+    else:
+        call = wl.calls[0]
+        ref, _ = run_oracle(wl)
+        check_close(got[call.c], ref, call, wl.name)
+
+
+def _sample(G, k, seed):
+    rng = np.random.default_rng(seed)
+    s = set(rng.choice(G, size=min(k, G), replace=False).tolist()) | {0, G - 1}
+    return sorted(s)
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 5])
+def test_workload_full_size_sampled(cfg):
+    wl = wk.CONFIGS[cfg]()
+    call = wl.calls[0]
+    say(f"workload {wl.name} full size, G={call.G}")
+    got = run_gpu(wl)[call.c]
+    sel = _sample(call.G, 48, cfg)
+    ref, _ = run_oracle(wl, sel=sel)
+    check_close(blocks(got, call, sel), blocks(ref, call, sel), call, wl.name)
+
+
+def test_mlp_block_full_size_sampled():
+    wl = wk.mlp_block()
+    g1, g2 = wl.calls
+    say("workload mlp_block full size")
+    got = run_gpu(wl)
+    nbs = [0, 77, 127]
+    # GEMM2 instances of token blocks nbs need every GEMM1 instance of those token blocks.
+    sel1 = [ib + g1.grid["gm"] * nb for nb in nbs for ib in range(g1.grid["gm"])]
+    h_ref, _ = run_oracle(wl, 0, sel=sel1)
+    check_close(blocks(got["h"], g1, sel1), blocks(h_ref, g1, sel1), g1, "mlp_block h")
+    sel2 = [hb + g2.grid["gm"] * nb for nb in nbs for hb in range(g2.grid["gm"])]
+    wl2 = wk.Workload(wl.name, dict(wl.arrays, h=h_ref), wl.calls)
+    y_ref, _ = run_oracle(wl2, 1, sel=sel2)
+    check_close(blocks(got["y"], g2, sel2), blocks(y_ref, g2, sel2), g2, "mlp_block y")
+
+
+# ----------------------------------------------------------------------------------------------
+# The device downconvert: fp32 -> bf16 round to nearest even, against the oracle's bit-level one
+# ----------------------------------------------------------------------------------------------
+def test_device_bf16_narrowing_is_rne():
+    rng = np.random.default_rng(3)
+    hi = np.arange(0, 1 << 16, dtype=np.uint32)
+    bits = np.concatenate([hi << 16 | 0x8000, hi << 16 | 0x7FFF, hi << 16 | 0x8001,
+                           rng.integers(0, 1 << 32, size=1 << 21, dtype=np.uint64).astype(np.uint32)])
+    x = bits.view(np.float32)
+    keep = np.isfinite(x) & (np.abs(x) >= np.float32(1.1754944e-38))   # no zeros, denormals
+    x = np.ascontiguousarray(x[keep])
+    m = x.size
+    call = wk.Call(m, 1, 1, m, 1, m, "f32", "bf16", 0.0, "stride", 0, 0, set(), G=1,
+                   grid=dict(gm=1, gn=1, a_step_m=0, b_step_n=0, c_step_m=0, c_step_n=0,
+                             bias_step_m=0), count=1, a="a", b="b", c="c")
+    wl = wk.Workload("cvt", dict(a=x, b=np.ones(1, np.float32),
+                                 c=np.full(m, 0x7FC0, np.uint16)), [call])
+    got = run_gpu(wl)["c"]
+    want = oracle.f32_to_bf16_array(x)
+    assert np.array_equal(got, want)

@@ -1,0 +1,90 @@
+"""GPU parity of the Reduce TPP (through the C ABI) against the CPU oracle.
+
+SUM and MUL are fp32 folds in an unspecified order: |gpu - ref| <= 1e-5 * (sum of |terms|)
+(SUM) or (4 sqrt(count) 2^-24 + 1e-6) * |ref| (MUL, factors near 1).  MIN and MAX decide nothing but comparisons, and
+fp32 rounding is monotone, so they are bit-exact against the oracle's value rounded to fp32 (also
+for x*x: min of rounded squares = rounded min of squares)."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as wk
+from helpers import values
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+
+
+def gpu_reduce(x_host, m, n, ld, in_type, op, by, want):
+    import paper_2104_05755_amd as tpp
+    from paper_2104_05755_amd import torch_io
+    x = torch_io.to_device(x_host)
+    nout = m if by == "cols" else n
+    ox = torch.full((nout,), float("nan"), device="cuda") if "x" in want else None
+    ox2 = torch.full((nout,), float("nan"), device="cuda") if "x2" in want else None
+    ops = dict(sum=tpp.TPP_RED_SUM, mul=tpp.TPP_RED_MUL, min=tpp.TPP_RED_MIN, max=tpp.TPP_RED_MAX)
+    flags = (tpp.TPP_RED_BY_COLS if by == "cols" else tpp.TPP_RED_BY_ROWS)
+    flags |= (tpp.TPP_RED_X if "x" in want else 0) | (tpp.TPP_RED_X2 if "x2" in want else 0)
+    dt = tpp.TPP_DT_BF16 if in_type == "bf16" else tpp.TPP_DT_F32
+    tpp.tpp_reduce(m, n, ld, dt, x, ops[op], flags, ox, ox2, tpp.current_stream())
+    torch.cuda.synchronize()
+    return (None if ox is None else ox.cpu().numpy(), None if ox2 is None else ox2.cpu().numpy())
+
+
+def check(got, ref, absdata, op, by, what):
+    count = absdata.shape[1] if by == "cols" else absdata.shape[0]
+    assert got is not None and not np.isnan(got).any(), what
+    if op in ("min", "max"):
+        assert np.array_equal(got, ref.astype(np.float32)), what
+    elif op == "sum":
+        scale = absdata.sum(axis=1 if by == "cols" else 0)
+        assert np.all(np.abs(got - ref) <= 1e-5 * scale + 1e-30), what
+    else:
+        # each of the count-1 products rounds once: a random walk of fp32 rounding errors
+        rtol = 4.0 * np.sqrt(count) * 2.0 ** -24 + 1e-6
+        assert np.all(np.abs(got - ref) <= rtol * np.abs(ref) + 1e-30), what
+
+
+SHAPES = [(1, 1, 1), (3, 5, 3), (64, 100, 64), (64, 100, 67), (37, 513, 40), (1000, 7, 1000),
+          (100000, 3, 100003), (8, 200000, 8), (257, 1031, 264), (4096, 64, 4096)]
+
+
+@pytest.mark.parametrize("m,n,ld", SHAPES)
+@pytest.mark.parametrize("in_type", ["f32", "bf16"])
+@pytest.mark.parametrize("by", ["cols", "rows"])
+def test_reduce_matches_oracle(m, n, ld, in_type, by):
+    rng = np.random.default_rng(m * 7 + n * 13 + ld)
+    for op in ("sum", "max", "min", "mul"):
+        lo, hi = (0.97, 1.03) if op == "mul" else (-2.0, 2.0)
+        raw = rng.uniform(lo, hi, size=n * ld).astype(np.float32)
+        x = raw if in_type == "f32" else wk.bf16_bits(raw)
+        print(f"reduce {op} by {by} m={m} n={n} ld={ld} {in_type}", flush=True)
+        sys.stdout.flush()
+        want = ("x",) if op == "mul" else ("x", "x2")
+        rx, rx2 = oracle.reduce(x, m, n, ld, in_type, op, by, want)
+        gx, gx2 = gpu_reduce(x, m, n, ld, in_type, op, by, want)
+        X = np.abs(values(x, in_type).reshape(n, ld)[:, :m].T)          # m x n
+        check(gx, rx, X, op, by, f"{op} x")
+        if "x2" in want:
+            check(gx2, rx2, X * X, op, by, f"{op} x2")
+
+
+def test_reduce_batchnorm_statistics_shape():
+    """The per-channel statistics of a conv output: NHWc bf16 with c = 64, reduced by columns."""
+    rng = np.random.default_rng(17)
+    t = wk.bf16_bits(rng.standard_normal((28, 56, 56, 64)).astype(np.float32) * 0.5)
+    m, n = 64, 28 * 56 * 56
+    rx, rx2 = oracle.reduce(t.reshape(-1), m, n, m, "bf16", "sum", "cols", ("x", "x2"))
+    gx, gx2 = gpu_reduce(t.reshape(-1), m, n, m, "bf16", "sum", "cols", ("x", "x2"))
+    X = np.abs(values(t.reshape(-1), "bf16").reshape(n, m).T)
+    check(gx, rx, X, "sum", "cols", "bn sum")
+    check(gx2, rx2, X * X, "sum", "cols", "bn sumsq")
