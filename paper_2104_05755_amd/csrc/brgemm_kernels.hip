@@ -29,6 +29,27 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Global-memory accesses through address-space-1 pointers, so that they compile to global_*
+// instructions.  (Through generic pointers they become flat_* instructions, which also count
+// against the LDS wait counter: every wait for an LDS operand would then wait for the global
+// prefetch as well.)
+#define GLOBAL_AS __attribute__((address_space(1)))
+template <typename T>
+__device__ __forceinline__ T gld(const void* p) {
+  return *(const GLOBAL_AS T*)p;
+}
+template <typename T>
+__device__ __forceinline__ void gst(void* p, T v) {
+  *(GLOBAL_AS T*)p = v;
+}
+
+template <int V>
+struct IntC {
+  static constexpr int value = V;
+};
 
 constexpr int NT = 256;            // threads per workgroup: 4 wavefronts of 64
 constexpr int BK = 64;             // k extent of one stage (bf16)
@@ -41,11 +62,15 @@ __device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
   return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
 }
 
-// GELU in its tanh form, 0.5 x (1 + tanh(sqrt(2/pi) (x + 0.044715 x^3))), with the device math
-// library's tanhf.
+// GELU in its tanh form, 0.5 x (1 + tanh(u)) with u = sqrt(2/pi) (x + 0.044715 x^3).
+// Since 0.5 (1 + tanh(u)) = 1 / (1 + e^(-2u)), this is x / (1 + 2^(-2u log2(e))): one hardware
+// exp2 (v_exp_f32) and one hardware reciprocal (v_rcp_f32), a few ulp of fp32 in all, and no
+// cancellation anywhere (for u -> -inf the denominator goes to +inf and the result to -0).
 __device__ __forceinline__ float gelu_tanh(float x) {
   const float kSqrt2OverPi = 0.7978845608028654f;
-  return 0.5f * x * (1.0f + tanhf(kSqrt2OverPi * (x + 0.044715f * x * x * x)));
+  const float kMinus2Log2e = -2.8853900817779268f;   // -2 / ln(2)
+  const float u = kSqrt2OverPi * (x + 0.044715f * x * x * x);
+  return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(kMinus2Log2e * u));
 }
 
 __device__ __forceinline__ float activate(float v, uint32_t flags) {
@@ -473,6 +498,355 @@ __global__ __launch_bounds__(NT) void brgemm_bf16_kernel(BrgemmParams p) {
 }
 
 // ---------------------------------------------------------------------------------------------
+// bf16 16-byte-load kernel.  Preconditions (checked on the host): m, k, lda, ldb and every
+// element step of the grid are multiples of 8, so each 8-element chunk a thread moves is
+// contiguous and, when the pair's block bases are 16-byte aligned (checked per stage, uniform
+// over the workgroup), aligned.  FULL: every tile is complete (no row, column or k tail), so
+// the loads carry no bounds logic at all; otherwise out-of-range chunks read a clamped,
+// in-range address and are replaced by zeros without branching.
+// ---------------------------------------------------------------------------------------------
+__device__ __forceinline__ u32x4 ld16(const uint16_t* ptr) { return gld<u32x4>(ptr); }
+
+__device__ __forceinline__ u32x4 ld16_unaligned(const uint16_t* ptr) {
+  uint32_t h[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) h[e] = gld<uint16_t>(ptr + e);
+  return (u32x4){h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
+                 h[6] | (h[7] << 16)};
+}
+
+__device__ __forceinline__ u32x4 keep_if(u32x4 v, bool ok) {
+  return (u32x4){ok ? v.x : 0u, ok ? v.y : 0u, ok ? v.z : 0u, ok ? v.w : 0u};
+}
+
+// Transpose an 8 x SK bf16 sub-block held as SK k-columns of 8 rows into 8 rows of SK k, and
+// store the rows (2*SK bytes each) into the K-contiguous LDS panel.
+template <int SK>
+__device__ __forceinline__ void store_a_transposed_v(uint16_t* dst_row0, const u32x4 col[SK]) {
+#pragma unroll
+  for (int mi = 0; mi < 8; ++mi) {
+    const int d = mi >> 1;
+    uint32_t w[SK / 2];
+#pragma unroll
+    for (int e = 0; e < SK / 2; ++e) {
+      const uint32_t lo = col[2 * e][d], hi = col[2 * e + 1][d];
+      w[e] = (mi & 1) ? ((lo >> 16) | (hi & 0xffff0000u)) : ((lo & 0xffffu) | (hi << 16));
+    }
+    if constexpr (SK == 8)
+      *reinterpret_cast<u32x4*>(dst_row0 + mi * LDS_ROW) = (u32x4){w[0], w[1], w[2], w[3]};
+    else
+      *reinterpret_cast<uint2*>(dst_row0 + mi * LDS_ROW) = make_uint2(w[0], w[1]);
+  }
+}
+
+template <int BM, int BN, int WAVES_M, int WAVES_N, bool FULL>
+__global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void brgemm_bf16_vec_kernel(BrgemmParams p) {
+  constexpr int NTH = 64 * WAVES_M * WAVES_N;        // threads per workgroup
+  constexpr int WTM = BM / WAVES_M, WTN = BN / WAVES_N;
+  constexpr int TM = WTM / 32, TN = WTN / 32;
+  constexpr int KCH = BK / 8;                        // 8-element k chunks per stage
+  // A moves in 8-row x SK-k sub-blocks; SK = 4 when 8x8 sub-blocks would leave threads idle.
+  constexpr int SK = ((BM / 8) * (BK / 8) >= NTH) ? 8 : 4;
+  constexpr int KCA = BK / SK;
+  constexpr int A_SUB = (BM / 8) * KCA;
+  constexpr int A_REP = (A_SUB + NTH - 1) / NTH;
+  constexpr int B_CH = BN * KCH;                     // 16-byte chunks of the B panel
+  constexpr int B_REP = (B_CH + NTH - 1) / NTH;
+  constexpr int STAGE = (BM + BN) * LDS_ROW;
+  constexpr int EP_ROW = WTM + 4;                    // epilogue slab: 32 columns x WTM rows fp32
+  constexpr int CPC = WTM / 8;                       // 8-row chunks per slab column
+  constexpr int EP_ITERS = 32 * CPC / 64;
+  static_assert(TM >= 1 && TN >= 1, "wave tile at least 32x32");
+  static_assert(WAVES_M * WAVES_N * 32 * EP_ROW * 4 <= 2 * STAGE * 2,
+                "epilogue slabs fit in the stage buffers");
+  static_assert(64 % CPC == 0, "row chunks per column divide the wavefront");
+
+  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * STAGE];
+
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int wm = wave % WAVES_M, wn = wave / WAVES_M;
+  const TileCoord tc = decode_tile(p, BM, BN);
+  const Instance in = instance_of(p, tc.g);
+  const int32_t ksteps = (p.k + BK - 1) / BK;
+  const int32_t stages = (int32_t)(in.npairs * ksteps);
+
+  // Staging assignments, fixed for the whole reduction.  Out-of-range rows / columns keep
+  // offset 0 (an in-range address) and a false flag.
+  int64_t a_off[A_REP];
+  bool a_ok[A_REP];
+  int a_kc[A_REP], a_row[A_REP];
+#pragma unroll
+  for (int rep = 0; rep < A_REP; ++rep) {
+    const int q = t + NTH * rep;
+    a_kc[rep] = q % KCA;
+    a_row[rep] = (q / KCA) * 8;
+    a_off[rep] = 0;
+    a_ok[rep] = (q < A_SUB) && row_in_a(p, tc.row0 + a_row[rep], a_off[rep]);
+    if (!a_ok[rep]) a_off[rep] = 0;
+  }
+  int64_t b_off[B_REP];
+  bool b_ok[B_REP];
+  int b_kc[B_REP], b_col[B_REP];
+#pragma unroll
+  for (int rep = 0; rep < B_REP; ++rep) {
+    const int q = t + NTH * rep;
+    b_kc[rep] = q % KCH;
+    b_col[rep] = q / KCH;
+    b_off[rep] = 0;
+    b_ok[rep] = (q < B_CH) && col_in_b(p, tc.col0 + b_col[rep], b_off[rep]);
+    if (!b_ok[rep]) b_off[rep] = 0;
+  }
+
+  // Two register sets for staged operands: while the MFMAs consume LDS buffer s&1, set s&1
+  // receives the global loads of stage s+2 and set (s+1)&1 (loaded one stage earlier) is written
+  // to LDS buffer (s+1)&1 in between the MFMAs.
+  struct Staged {
+    u32x4 a[A_REP][SK];
+    u32x4 b[B_REP];
+  };
+  Staged st0, st1;
+
+  auto load_stage = [&](int32_t s, Staged& r) {
+    const int32_t i = s / ksteps;
+    const int32_t kk = (s - i * ksteps) * BK;
+    const uint16_t* pa;
+    const uint16_t* pb;
+    pair_bases<uint16_t>(p, in, i, pa, pb);
+    const bool aligned =
+        ((reinterpret_cast<uintptr_t>(pa) | reinterpret_cast<uintptr_t>(pb)) & 15) == 0;
+    if (aligned) {
+#pragma unroll
+      for (int rep = 0; rep < A_REP; ++rep) {
+        const int32_t k0 = kk + a_kc[rep] * SK;
+        const bool ok = FULL || (a_ok[rep] && k0 < p.k);
+        const int32_t kc = (FULL || k0 < p.k) ? k0 : 0;
+        const uint16_t* base = pa + a_off[rep] + (int64_t)kc * p.lda;
+#pragma unroll
+        for (int j = 0; j < SK; ++j) {
+          const u32x4 v = ld16(base + (int64_t)j * p.lda);
+          r.a[rep][j] = FULL ? v : keep_if(v, ok);
+        }
+      }
+#pragma unroll
+      for (int rep = 0; rep < B_REP; ++rep) {
+        const int32_t k0 = kk + b_kc[rep] * 8;
+        const bool ok = FULL || (b_ok[rep] && k0 < p.k);
+        const int32_t kc = (FULL || k0 < p.k) ? k0 : 0;
+        const u32x4 v = ld16(pb + b_off[rep] + kc);
+        r.b[rep] = FULL ? v : keep_if(v, ok);
+      }
+    } else {
+#pragma unroll
+      for (int rep = 0; rep < A_REP; ++rep) {
+        const int32_t k0 = kk + a_kc[rep] * SK;
+        const bool ok = FULL || (a_ok[rep] && k0 < p.k);
+        const int32_t kc = (FULL || k0 < p.k) ? k0 : 0;
+        const uint16_t* base = pa + a_off[rep] + (int64_t)kc * p.lda;
+#pragma unroll
+        for (int j = 0; j < SK; ++j)
+          r.a[rep][j] = keep_if(ld16_unaligned(base + (int64_t)j * p.lda), ok);
+      }
+#pragma unroll
+      for (int rep = 0; rep < B_REP; ++rep) {
+        const int32_t k0 = kk + b_kc[rep] * 8;
+        const bool ok = FULL || (b_ok[rep] && k0 < p.k);
+        const int32_t kc = (FULL || k0 < p.k) ? k0 : 0;
+        r.b[rep] = keep_if(ld16_unaligned(pb + b_off[rep] + kc), ok);
+      }
+    }
+  };
+
+  auto store_a = [&](int buf, const Staged& r) {
+    uint16_t* As = lds + buf * STAGE;
+#pragma unroll
+    for (int rep = 0; rep < A_REP; ++rep) {
+      if (A_SUB % NTH == 0 || t + NTH * rep < A_SUB)
+        store_a_transposed_v<SK>(As + a_row[rep] * LDS_ROW + a_kc[rep] * SK, r.a[rep]);
+    }
+  };
+  auto store_b = [&](int buf, const Staged& r) {
+    uint16_t* Bs = lds + buf * STAGE + BM * LDS_ROW;
+#pragma unroll
+    for (int rep = 0; rep < B_REP; ++rep) {
+      if (B_CH % NTH == 0 || t + NTH * rep < B_CH)
+        *reinterpret_cast<u32x4*>(Bs + b_col[rep] * LDS_ROW + b_kc[rep] * 8) = r.b[rep];
+    }
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[tm][tn][v] = 0.0f;
+
+  const int frag_row = lane & 31;
+  const int frag_k = (lane >> 5) * 8;
+
+  // MFMAs of one LDS buffer: the fragments of k-step kq+1 are read while the MFMAs of kq run;
+  // hook(kq) runs after the MFMAs of k-step kq are issued.
+  auto compute = [&](int buf, auto&& hook) {
+    const uint16_t* As = lds + buf * STAGE;
+    const uint16_t* Bs = As + BM * LDS_ROW;
+    bf16x8 fa[2][TM], fb[2][TN];
+    auto frags = [&](int kq, bf16x8* a, bf16x8* b) {
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm)
+        a[tm] = *reinterpret_cast<const bf16x8*>(
+            As + (wm * WTM + tm * 32 + frag_row) * LDS_ROW + kq * 16 + frag_k);
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn)
+        b[tn] = *reinterpret_cast<const bf16x8*>(
+            Bs + (wn * WTN + tn * 32 + frag_row) * LDS_ROW + kq * 16 + frag_k);
+    };
+    frags(0, fa[0], fb[0]);
+#pragma unroll
+    for (int kq = 0; kq < BK / 16; ++kq) {
+      if (kq + 1 < BK / 16) frags(kq + 1, fa[(kq + 1) & 1], fb[(kq + 1) & 1]);
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn)
+          acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[kq & 1][tm], fb[kq & 1][tn],
+                                                                acc[tm][tn], 0, 0, 0);
+      hook(kq);
+    }
+  };
+
+  if (stages > 0) {
+    load_stage(0, st0);
+    if (stages > 1) load_stage(1, st1);
+    store_a(0, st0);
+    store_b(0, st0);
+    __syncthreads();
+    int32_t s = 0;
+    // One stage; PAR = s & 1 is a compile-time constant so the register sets are never indexed
+    // at run time.
+    auto step = [&](auto par) {
+      constexpr int PAR = decltype(par)::value;
+      Staged& cur = PAR ? st1 : st0;   // stage s (already in LDS buffer PAR): free for s+2
+      Staged& nxt = PAR ? st0 : st1;   // stage s+1, loaded one stage ago
+      if (s + 2 < stages) load_stage(s + 2, cur);
+      const bool more = s + 1 < stages;
+      compute(PAR, [&](int kq) {
+        if (more && kq == 1) store_a(PAR ^ 1, nxt);
+        if (more && kq == 2) store_b(PAR ^ 1, nxt);
+      });
+      __syncthreads();
+      ++s;
+    };
+    while (s + 1 < stages) {
+      step(IntC<0>());
+      step(IntC<1>());
+    }
+    if (s < stages) step(IntC<0>());
+  }
+
+  // ---- Epilogue through LDS.  Each wave parks one 32-column slab of its accumulators
+  // (WTM rows x 32 columns, fp32) in its own LDS region, then every lane takes 8 consecutive rows
+  // of one column: beta*C, bias, activation and narrowing on 8 values, one 16-byte store.
+  float* slab = reinterpret_cast<float*>(lds) + wave * 32 * EP_ROW;
+  const int my_chunk = lane % CPC;
+  const int32_t R = tc.row0 + wm * WTM + my_chunk * 8;
+  bool row_ok = true;
+  int64_t row_off, bias_idx;
+  if (p.fused) {
+    const int32_t gi = R / p.m, r = R - gi * p.m;
+    row_ok = FULL || R < p.vrows;
+    row_off = (int64_t)gi * p.c_step_m + r;
+    bias_idx = (int64_t)gi * p.bias_step_m + r;
+  } else {
+    row_ok = FULL || R < p.m;
+    row_off = R;
+    bias_idx = in.bias + R;
+  }
+  float bias8[8];
+  const bool has_bias = (p.flags & TPP_EPI_BIAS) != 0;
+#pragma unroll
+  for (int e = 0; e < 8; ++e)
+    bias8[e] = (has_bias && row_ok) ? gld<float>(p.bias + bias_idx + e) : 0.0f;
+
+#pragma unroll
+  for (int tn = 0; tn < TN; ++tn) {
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float4 w = make_float4(acc[tm][tn][q * 4 + 0], acc[tm][tn][q * 4 + 1],
+                               acc[tm][tn][q * 4 + 2], acc[tm][tn][q * 4 + 3]);
+        *reinterpret_cast<float4*>(slab + (lane & 31) * EP_ROW + tm * 32 + q * 8 +
+                                   (lane >> 5) * 4) = w;
+      }
+    __syncthreads();
+    // kept rolled: the accumulators are not indexed here, and unrolling the activation code
+    // would only grow the kernel
+#pragma unroll 1
+    for (int it = 0; it < EP_ITERS; ++it) {
+      const int col_local = it * (64 / CPC) + lane / CPC;
+      const float4 lo = *reinterpret_cast<const float4*>(slab + col_local * EP_ROW + my_chunk * 8);
+      const float4 hi =
+          *reinterpret_cast<const float4*>(slab + col_local * EP_ROW + my_chunk * 8 + 4);
+      const int32_t C = tc.col0 + wn * WTN + tn * 32 + col_local;
+      int64_t col_off;
+      bool col_ok;
+      if (p.fused) {
+        const int32_t gi = C / p.n, c = C - gi * p.n;
+        col_ok = FULL || C < p.vcols;
+        col_off = (int64_t)gi * p.c_step_n + (int64_t)c * p.ldc;
+      } else {
+        col_ok = FULL || C < p.n;
+        col_off = (int64_t)C * p.ldc;
+      }
+      if (row_ok && col_ok) {
+        float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+        const int64_t e0 = in.c + row_off + col_off;
+        if (p.c_bf16) {
+          uint16_t* cp = static_cast<uint16_t*>(p.c) + e0;
+          const bool vec = (reinterpret_cast<uintptr_t>(cp) & 15) == 0;
+          if (p.beta != 0.0f) {
+            const u32x4 w = vec ? ld16(cp) : ld16_unaligned(cp);
+            const uint32_t d[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              v[2 * e] = p.beta * bf16_bits_to_f32(d[e] & 0xffffu) + v[2 * e];
+              v[2 * e + 1] = p.beta * bf16_bits_to_f32(d[e] >> 16) + v[2 * e + 1];
+            }
+          }
+          uint32_t o[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[e] = f32_to_bf16_bits(activate(v[e] + bias8[e], p.flags));
+          if (vec) {
+            gst<u32x4>(cp, (u32x4){o[0] | (o[1] << 16), o[2] | (o[3] << 16),
+                                   o[4] | (o[5] << 16), o[6] | (o[7] << 16)});
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) gst<uint16_t>(cp + e, (uint16_t)o[e]);
+          }
+        } else {
+          float* cp = static_cast<float*>(p.c) + e0;
+          const bool vec = (reinterpret_cast<uintptr_t>(cp) & 15) == 0;
+          if (p.beta != 0.0f) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] = p.beta * gld<float>(cp + e) + v[e];
+          }
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] = activate(v[e] + bias8[e], p.flags);
+          if (vec) {
+            gst<f32x4>(cp, (f32x4){v[0], v[1], v[2], v[3]});
+            gst<f32x4>(cp + 4, (f32x4){v[4], v[5], v[6], v[7]});
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) gst<float>(cp + e, v[e]);
+          }
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
 // fp32 kernel: 64x64 tile, 4 waves of 32x32, v_mfma_f32_32x32x2f32, element loads with full
 // bounds checks (any shape, leading dimension or alignment).
 // ---------------------------------------------------------------------------------------------
@@ -554,14 +928,25 @@ struct KernelInfo {
 };
 
 constexpr KernelInfo kInfo[K_COUNT] = {
-    {"bf16_256x256_vec", 256, 256}, {"bf16_256x128_vec", 256, 128},
-    {"bf16_128x128_vec", 128, 128}, {"bf16_64x64_vec", 64, 64},
-    {"bf16_64x64_generic", 64, 64}, {"f32_64x64_generic", 64, 64},
+    {"bf16_256x256_w8_vec", 256, 256}, {"bf16_256x128_w4_vec", 256, 128},
+    {"bf16_128x128_w4_vec", 128, 128}, {"bf16_64x64_w4_vec", 64, 64},
+    {"bf16_64x64_generic", 64, 64},    {"f32_64x64_generic", 64, 64},
+    {"bf16_256x256_w4_vec", 256, 256}, {"bf16_256x128_w8_vec", 256, 128},
+    {"bf16_128x128_w8_vec", 128, 128},
 };
 
 }  // namespace
 
 const char* kernel_name(int32_t id) { return (id >= 0 && id < K_COUNT) ? kInfo[id].name : "?"; }
+
+template <int BM, int BN, int WM, int WN>
+void launch_vec(const BrgemmParams& p, bool full, dim3 grid, hipStream_t stream) {
+  const dim3 block(64 * WM * WN);
+  if (full)
+    hipLaunchKernelGGL((brgemm_bf16_vec_kernel<BM, BN, WM, WN, true>), grid, block, 0, stream, p);
+  else
+    hipLaunchKernelGGL((brgemm_bf16_vec_kernel<BM, BN, WM, WN, false>), grid, block, 0, stream, p);
+}
 
 hipError_t launch_brgemm(BrgemmParams& p, int32_t id, hipStream_t stream) {
   if (id < 0 || id >= K_COUNT) return hipErrorInvalidValue;
@@ -571,19 +956,15 @@ hipError_t launch_brgemm(BrgemmParams& p, int32_t id, hipStream_t stream) {
   p.total_tiles = p.groups * p.tiles_m * p.tiles_n;
   if (p.total_tiles <= 0) return hipSuccess;
   const dim3 grid((unsigned)p.total_tiles), block(NT);
+  const bool full = (p.k % BK == 0) && (p.vrows % bm == 0) && (p.vcols % bn == 0);
   switch (id) {
-    case K_BF16_256x256:
-      hipLaunchKernelGGL((brgemm_bf16_kernel<256, 256, 2, 2, false>), grid, block, 0, stream, p);
-      break;
-    case K_BF16_256x128:
-      hipLaunchKernelGGL((brgemm_bf16_kernel<256, 128, 2, 2, false>), grid, block, 0, stream, p);
-      break;
-    case K_BF16_128x128:
-      hipLaunchKernelGGL((brgemm_bf16_kernel<128, 128, 2, 2, false>), grid, block, 0, stream, p);
-      break;
-    case K_BF16_64x64:
-      hipLaunchKernelGGL((brgemm_bf16_kernel<64, 64, 2, 2, false>), grid, block, 0, stream, p);
-      break;
+    case K_BF16_256x256: launch_vec<256, 256, 2, 4>(p, full, grid, stream); break;
+    case K_BF16_256x128: launch_vec<256, 128, 2, 2>(p, full, grid, stream); break;
+    case K_BF16_128x128: launch_vec<128, 128, 2, 2>(p, full, grid, stream); break;
+    case K_BF16_64x64: launch_vec<64, 64, 2, 2>(p, full, grid, stream); break;
+    case K_BF16_256x256_W4: launch_vec<256, 256, 2, 2>(p, full, grid, stream); break;
+    case K_BF16_256x128_W8: launch_vec<256, 128, 4, 2>(p, full, grid, stream); break;
+    case K_BF16_128x128_W8: launch_vec<128, 128, 2, 4>(p, full, grid, stream); break;
     case K_BF16_GENERIC:
       hipLaunchKernelGGL((brgemm_bf16_kernel<64, 64, 2, 2, true>), grid, block, 0, stream, p);
       break;

@@ -48,13 +48,16 @@ struct BrgemmParams {
 
 // Kernel instances of the bf16 family (tile shape + load path) and the fp32 kernel.
 enum KernelId : int32_t {
-  K_BF16_256x256 = 0,   // 4 waves, 128x128 per wave, vector loads
+  K_BF16_256x256 = 0,   // 8 waves, 128x64 per wave, vector loads
   K_BF16_256x128 = 1,   // 4 waves, 128x64 per wave, vector loads
   K_BF16_128x128 = 2,   // 4 waves, 64x64 per wave, vector loads
   K_BF16_64x64 = 3,     // 4 waves, 32x32 per wave, vector loads
   K_BF16_GENERIC = 4,   // 64x64, element loads with full bounds checks (any shape / alignment)
   K_F32_GENERIC = 5,    // 64x64 fp32 MFMA, element loads with full bounds checks
-  K_COUNT = 6
+  K_BF16_256x256_W4 = 6,  // 4 waves, 128x128 per wave
+  K_BF16_256x128_W8 = 7,  // 8 waves, 64x64 per wave
+  K_BF16_128x128_W8 = 8,  // 8 waves, 64x32 per wave
+  K_COUNT = 9
 };
 
 const char* kernel_name(int32_t id);

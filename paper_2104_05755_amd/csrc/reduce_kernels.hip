@@ -176,19 +176,25 @@ __global__ __launch_bounds__(RT) void reduce_cols_kernel(ReduceParams p, int32_t
 }
 
 // Second pass: out[o] = fold over s < nseg of work[s * n_out + o] (x part, then x2 part).
+// One wavefront per output: lanes take every 64th partial, then fold across the wavefront.
 template <int OP>
 __global__ __launch_bounds__(RT) void reduce_combine_kernel(const float* work, int32_t n_out,
                                                             int32_t nseg, uint32_t flags,
                                                             float* out_x, float* out_x2) {
-  const int64_t o = (int64_t)blockIdx.x * RT + threadIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int64_t o = (int64_t)blockIdx.x * (RT / 64) + (threadIdx.x >> 6);
   if (o >= n_out) return;
   float fx = fold_identity<OP>(), fx2 = fold_identity<OP>();
-  for (int32_t s = 0; s < nseg; ++s) {
+  for (int32_t s = lane; s < nseg; s += 64) {
     fx = fold<OP>(fx, work[(int64_t)s * n_out + o]);
     fx2 = fold<OP>(fx2, work[(int64_t)nseg * n_out + (int64_t)s * n_out + o]);
   }
-  if (flags & TPP_RED_X) out_x[o] = fx;
-  if (flags & TPP_RED_X2) out_x2[o] = fx2;
+  fx = wave_fold<OP>(fx);
+  fx2 = wave_fold<OP>(fx2);
+  if (lane == 0) {
+    if (flags & TPP_RED_X) out_x[o] = fx;
+    if (flags & TPP_RED_X2) out_x2[o] = fx2;
+  }
 }
 
 struct Plan {
@@ -257,7 +263,7 @@ void launch_op(const ReduceParams& p, const Plan& pl, float* work, hipStream_t s
   }
   if (pl.nseg > 1) {
     const int32_t n_out = pl.by_cols ? p.m : p.n;
-    hipLaunchKernelGGL(reduce_combine_kernel<OP>, dim3((unsigned)((n_out + RT - 1) / RT)),
+    hipLaunchKernelGGL(reduce_combine_kernel<OP>, dim3((unsigned)((n_out + 3) / 4)),
                        dim3(RT), 0, stream, work, n_out, pl.nseg, p.flags, p.out_x, p.out_x2);
   }
 }

@@ -60,8 +60,8 @@ bool valid_dtype(int32_t t) { return t == TPP_DT_F32 || t == TPP_DT_BF16; }
 
 // Kernel choice for one launch.  bf16 inputs take a 16-byte-load instance when the descriptor
 // and the grid keep every 8-element chunk contiguous and aligned (m, k, lda, ldb and all element
-// steps multiples of 8); the tile shape is the largest whose tile count still fills the 256
-// compute units.  Anything else takes the element-load instance.
+// steps multiples of 8); the tile shape is the largest that still gives two tiles per compute
+// unit (512 tiles on the 256 CUs).  Anything else takes the element-load instance.
 int32_t choose_kernel(const tpp_brgemm_kernel_s& h, const tpp::BrgemmParams& p) {
   if (!h.bf16) return tpp::K_F32_GENERIC;
   bool vec = h.vec_ok;
@@ -69,23 +69,28 @@ int32_t choose_kernel(const tpp_brgemm_kernel_s& h, const tpp::BrgemmParams& p) 
   if (!vec) return tpp::K_BF16_GENERIC;
   if (const char* env = std::getenv("TPP_FORCE_KERNEL")) {
     const int id = std::atoi(env);
-    if (id >= tpp::K_BF16_256x256 && id <= tpp::K_BF16_64x64) return id;
+    if (id >= 0 && id < tpp::K_COUNT && id != tpp::K_BF16_GENERIC && id != tpp::K_F32_GENERIC)
+      return id;
   }
   struct Cand { int32_t id; int bm, bn; };
   const Cand cands[] = {{tpp::K_BF16_256x256, 256, 256},
-                        {tpp::K_BF16_256x128, 256, 128},
                         {tpp::K_BF16_128x128, 128, 128},
                         {tpp::K_BF16_64x64, 64, 64}};
   for (const Cand& c : cands) {
+    // never pad a virtual C out to a larger tile (the 64x64 tile is the floor)
+    if ((c.bm > p.vrows && c.bm > 64) || (c.bn > p.vcols && c.bn > 64)) continue;
     const int64_t tiles = p.groups * ((p.vrows + c.bm - 1) / c.bm) * ((p.vcols + c.bn - 1) / c.bn);
-    // do not pad a small instance out to a much larger tile
-    const bool fits = (int64_t)c.bm <= 2LL * p.vrows && (int64_t)c.bn <= 2LL * p.vcols;
-    if (fits && tiles >= 256) return c.id;
+    // two tiles per compute unit: one workgroup's barriers and epilogue overlap the other's MFMAs
+    if (tiles >= 512) return c.id;
   }
   return tpp::K_BF16_64x64;
 }
 
 tpp_status launch(const tpp_brgemm_kernel_s* h, tpp::BrgemmParams& p, void* stream) {
+  // the kernels count stages (pairs x k-steps of 64) and tiles in 32 bits
+  const int64_t ksteps = (h->desc.k + 63) / 64;
+  if (p.kind != TPP_BR_ADDRESS && p.count * ksteps >= (1LL << 31))
+    return fail(TPP_ERR_UNSUPPORTED, "count * ceil(k/64) must be below 2^31");
   const int32_t id = choose_kernel(*h, p);
   if (std::getenv("TPP_LOG"))
     std::fprintf(stderr, "[tpp] %s: G=%lld vrows=%d vcols=%d fused=%d -> %s\n", h->name,

@@ -8,6 +8,7 @@ then the same decision on both sides).  No oracle input comes from the GPU."""
 from __future__ import annotations
 
 import sys
+import zlib
 
 import numpy as np
 import pytest
@@ -44,7 +45,9 @@ def run_gpu(wl, calls=None, dev=None):
 
 
 def tol(call):
-    return 1e-5 if call.ab_type == "f32" else 5e-3
+    """1e-5 when inputs and output are fp32; 5e-3 as soon as bf16 is involved (bf16 inputs, or
+    a bf16 output whose rounding-boundary flips alone move single elements by 2^-8)."""
+    return 1e-5 if (call.ab_type == "f32" and call.c_type == "f32") else 5e-3
 
 
 def blocks(flat, call, insts):
@@ -95,7 +98,7 @@ def _cases():
 
 @pytest.mark.parametrize("m,n,k,count,kind,ab,ct,beta,epi,pad", _cases())
 def test_small_shapes_match_oracle(m, n, k, count, kind, ab, ct, beta, epi, pad):
-    rng = np.random.default_rng(hash((m, n, k, count, kind, ab, ct, beta, epi, pad)) % 2**32)
+    rng = np.random.default_rng(zlib.crc32(repr((m, n, k, count, kind, ab, ct, beta, epi, pad)).encode()))
     wl = wk.small_case(rng, m, n, k, count, kind, ab, ct, beta, set(epi), pad=pad)
     say(f"case m={m} n={n} k={k} count={count} {kind} {ab}->{ct} beta={beta} {epi} pad={pad}")
     ref, _ = run_oracle(wl)
@@ -250,3 +253,29 @@ def test_device_bf16_narrowing_is_rne():
     got = run_gpu(wl)["c"]
     want = oracle.f32_to_bf16_array(x)
     assert np.array_equal(got, want)
+
+
+# ----------------------------------------------------------------------------------------------
+# Every tile instance of the 16-byte-load family, forced one at a time (complete and ragged tiles)
+# ----------------------------------------------------------------------------------------------
+VEC_KERNEL_IDS = [0, 1, 2, 3, 6, 7, 8]
+
+
+@pytest.mark.parametrize("kid", VEC_KERNEL_IDS)
+@pytest.mark.parametrize("shape", ["full", "ragged"])
+def test_every_tile_kernel_matches_oracle(kid, shape, monkeypatch):
+    monkeypatch.setenv("TPP_FORCE_KERNEL", str(kid))
+    if shape == "full":
+        wl = wk.mlp_block(seed=11, tokens=512, hidden=512, inter=512)
+    else:   # 5 x 7 instances of 64 x 64: no tile shape divides the virtual C
+        wl = wk.mlp_fc(seed=12, minibatch=7 * 64, c_in=192, k_out=5 * 64)
+    say(f"kernel {kid} {shape} {wl.name}")
+    got = run_gpu(wl)
+    if wl.name == "mlp_block":
+        h_ref, _ = run_oracle(wl, 0)
+        check_close(got["h"], h_ref, wl.calls[0], f"k{kid} h")
+        y_ref, _ = run_oracle(wk.Workload(wl.name, dict(wl.arrays, h=h_ref), wl.calls), 1)
+        check_close(got["y"], y_ref, wl.calls[1], f"k{kid} y")
+    else:
+        ref, _ = run_oracle(wl)
+        check_close(got["out"], ref, wl.calls[0], f"k{kid} ragged")

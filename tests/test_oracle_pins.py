@@ -8,6 +8,7 @@ from __future__ import annotations
 
 import itertools
 import math
+import zlib
 from fractions import Fraction
 
 import numpy as np
@@ -112,7 +113,7 @@ def _exact_sum(pairs, r, c):
 @pytest.mark.parametrize("kind", ["stride", "offset", "address"])
 @pytest.mark.parametrize("ab_type,c_type", [("f32", "f32"), ("bf16", "f32"), ("bf16", "bf16")])
 def test_brute_force_exact_rational(kind, ab_type, c_type):
-    rng = np.random.default_rng(hash((kind, ab_type, c_type)) % 2**32)
+    rng = np.random.default_rng(zlib.crc32(repr((kind, ab_type, c_type)).encode()))
     for (m, n, k, count) in [(1, 1, 1, 1), (2, 3, 5, 2), (5, 2, 3, 3), (3, 4, 2, 0)]:
         for beta in (0.0, 1.0, -0.5):
             wl = wk.small_case(rng, m, n, k, count, kind, ab_type, c_type, beta, {"bias"}, pad=1)
