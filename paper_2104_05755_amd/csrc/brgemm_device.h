@@ -1,0 +1,310 @@
+// brgemm_device.h -- device-side pieces shared by the BRGEMM kernel files: vector types, global
+// accesses, the epilogue arithmetic, tile / instance decoding, the Sec. 2.3 pair addresses and the
+// LDS-staged epilogue.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "internal.h"
+
+namespace tpp {
+namespace dev {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Global-memory accesses through address-space-1 pointers, so that they compile to global_*
+// instructions.  (Through generic pointers they become flat_* instructions, which also count
+// against the LDS wait counter: every wait for an LDS operand would then wait for the global
+// prefetch as well.)
+#define GLOBAL_AS __attribute__((address_space(1)))
+template <typename T>
+__device__ __forceinline__ T gld(const void* p) {
+  return *(const GLOBAL_AS T*)p;
+}
+template <typename T>
+__device__ __forceinline__ void gst(void* p, T v) {
+  *(GLOBAL_AS T*)p = v;
+}
+
+template <int V>
+struct IntC {
+  static constexpr int value = V;
+};
+
+constexpr int NT = 256;            // threads per workgroup: 4 wavefronts of 64
+constexpr int BK = 64;             // k extent of one stage (bf16)
+constexpr int LDS_ROW = BK + 8;    // bf16 per LDS row: 128 B of data + 16 B against bank conflicts
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
+
+__device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
+  // Lowers to v_cvt_pk_bf16_f32 on gfx950: round to nearest even, NaN stays NaN.
+  return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
+}
+
+// GELU in its tanh form, 0.5 x (1 + tanh(u)) with u = sqrt(2/pi) (x + 0.044715 x^3).
+// Since 0.5 (1 + tanh(u)) = 1 / (1 + e^(-2u)), this is x / (1 + 2^(-2u log2(e))): one hardware
+// exp2 (v_exp_f32) and one hardware reciprocal (v_rcp_f32), a few ulp of fp32 in all, and no
+// cancellation anywhere (for u -> -inf the denominator goes to +inf and the result to -0).
+__device__ __forceinline__ float gelu_tanh(float x) {
+  const float kSqrt2OverPi = 0.7978845608028654f;
+  const float kMinus2Log2e = -2.8853900817779268f;   // -2 / ln(2)
+  const float u = kSqrt2OverPi * (x + 0.044715f * x * x * x);
+  return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(kMinus2Log2e * u));
+}
+
+__device__ __forceinline__ float activate(float v, uint32_t flags) {
+  if (flags & TPP_EPI_RELU) return v > 0.0f ? v : 0.0f;
+  if (flags & TPP_EPI_GELU_TANH) return gelu_tanh(v);
+  return v;
+}
+
+// XCD-aware tile order: workgroups are handed to the 8 XCDs round-robin, so consecutive block
+// ids land on different L2s.  Remapping gives each XCD a contiguous run of tiles (neighbouring
+// tiles share A rows or B columns and so share that XCD's L2).
+__device__ __forceinline__ int64_t xcd_tile(int64_t bid, int64_t total) {
+  if ((total & 7) != 0) return bid;
+  return (bid & 7) * (total >> 3) + (bid >> 3);
+}
+
+struct TileCoord {
+  int64_t g;        // instance (explicit form) or 0 (strided form)
+  int32_t row0;     // first virtual row of the tile
+  int32_t col0;     // first virtual column of the tile
+};
+
+__device__ __forceinline__ TileCoord decode_tile(const BrgemmParams& p, int bm, int bn) {
+  const int64_t t = xcd_tile(blockIdx.x, p.total_tiles);
+  const int64_t per_group = (int64_t)p.tiles_m * p.tiles_n;
+  TileCoord tc;
+  tc.g = t / per_group;
+  const int64_t tin = t - tc.g * per_group;
+  tc.row0 = (int32_t)(tin % p.tiles_m) * bm;   // tiles of one column run consecutively
+  tc.col0 = (int32_t)(tin / p.tiles_m) * bn;
+  return tc;
+}
+
+// Virtual row R -> element offset of that row inside A (relative to the instance's A base) and
+// whether it exists.  Fused strided grid: R = gi_m * m + r.  One instance per group: R = r.
+__device__ __forceinline__ bool row_in_a(const BrgemmParams& p, int32_t R, int64_t& off) {
+  if (p.fused) {
+    if (R >= p.vrows) return false;
+    const int32_t gi = R / p.m, r = R - gi * p.m;
+    off = (int64_t)gi * p.a_step_m + r;
+    return true;
+  }
+  off = R;
+  return R < p.m;
+}
+
+// Virtual column C -> element offset of that column inside B (relative to the instance base).
+__device__ __forceinline__ bool col_in_b(const BrgemmParams& p, int32_t C, int64_t& off) {
+  if (p.fused) {
+    if (C >= p.vcols) return false;
+    const int32_t gi = C / p.n, c = C - gi * p.n;
+    off = (int64_t)gi * p.b_step_n + (int64_t)c * p.ldb;
+    return true;
+  }
+  off = (int64_t)C * p.ldb;
+  return C < p.n;
+}
+
+// Per-launch instance data for tile group g: bases added to every A_i / B_i / C / bias address,
+// and the pair list.
+struct Instance {
+  int64_t a, b, c, bias;   // element offsets
+  int64_t pair0, npairs;
+};
+
+__device__ __forceinline__ Instance instance_of(const BrgemmParams& p, int64_t g) {
+  Instance in;
+  in.a = in.b = in.c = in.bias = 0;
+  if (!p.fused && p.grid_form) {
+    const int64_t gi_m = g % p.gm, gi_n = g / p.gm;
+    in.a = gi_m * p.a_step_m;
+    in.b = gi_n * p.b_step_n;
+    in.c = gi_m * p.c_step_m + gi_n * p.c_step_n;
+    in.bias = gi_m * p.bias_step_m;
+  } else if (!p.fused) {
+    in.a = p.a_off ? p.a_off[g] : 0;
+    in.b = p.b_off ? p.b_off[g] : 0;
+    in.c = p.c_off ? p.c_off[g] : 0;
+    in.bias = p.bias_off ? p.bias_off[g] : 0;
+  }
+  in.pair0 = 0;
+  in.npairs = p.count;
+  if (p.kind == TPP_BR_ADDRESS && p.begin) {   // a single address call has no begin[]
+    in.pair0 = p.begin[g];
+    in.npairs = p.begin[g + 1] - in.pair0;
+  }
+  return in;
+}
+
+// Addresses of pair i (Sec. 2.3): stride A + i*stride, offset A + offs[i], address ptrs[i].
+template <typename T>
+__device__ __forceinline__ void pair_bases(const BrgemmParams& p, const Instance& in, int64_t i,
+                                           const T*& pa, const T*& pb) {
+  if (p.kind == TPP_BR_STRIDE) {
+    pa = static_cast<const T*>(p.a) + in.a + i * p.stride_a;
+    pb = static_cast<const T*>(p.b) + in.b + i * p.stride_b;
+  } else if (p.kind == TPP_BR_OFFSET) {
+    pa = static_cast<const T*>(p.a) + in.a + p.offs_a[i];
+    pb = static_cast<const T*>(p.b) + in.b + p.offs_b[i];
+  } else {
+    pa = static_cast<const T*>(p.ptrs_a[in.pair0 + i]);
+    pb = static_cast<const T*>(p.ptrs_b[in.pair0 + i]);
+  }
+}
+
+// The same, with the variant fixed at compile time (no per-stage branch on the kind).
+template <int KIND, typename T>
+__device__ __forceinline__ void pair_bases_k(const BrgemmParams& p, const Instance& in, int64_t i,
+                                             const T*& pa, const T*& pb) {
+  if constexpr (KIND == TPP_BR_STRIDE) {
+    pa = static_cast<const T*>(p.a) + in.a + i * p.stride_a;
+    pb = static_cast<const T*>(p.b) + in.b + i * p.stride_b;
+  } else if constexpr (KIND == TPP_BR_OFFSET) {
+    pa = static_cast<const T*>(p.a) + in.a + p.offs_a[i];
+    pb = static_cast<const T*>(p.b) + in.b + p.offs_b[i];
+  } else {
+    pa = static_cast<const T*>(p.ptrs_a[in.pair0 + i]);
+    pb = static_cast<const T*>(p.ptrs_b[in.pair0 + i]);
+  }
+}
+
+// 16 bytes of bf16 from global memory, aligned or not; zeroing without branches.
+__device__ __forceinline__ u32x4 ld16(const uint16_t* ptr) { return gld<u32x4>(ptr); }
+
+__device__ __forceinline__ u32x4 ld16_unaligned(const uint16_t* ptr) {
+  uint32_t h[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) h[e] = gld<uint16_t>(ptr + e);
+  return (u32x4){h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
+                 h[6] | (h[7] << 16)};
+}
+
+__device__ __forceinline__ u32x4 keep_if(u32x4 v, bool ok) {
+  return (u32x4){ok ? v.x : 0u, ok ? v.y : 0u, ok ? v.z : 0u, ok ? v.w : 0u};
+}
+
+// ---------------------------------------------------------------------------------------------
+// Epilogue of the 16-byte-load kernels, through LDS.  Each wave parks one 32-column slab of its
+// accumulators (WTM rows x 32 columns, fp32) in its own LDS region, then every lane takes 8
+// consecutive rows of one column: beta*C, bias, activation and narrowing on 8 values, one 16-byte
+// store.  The caller has passed a barrier after the last LDS read of the main loop.
+// The accumulator layout of a 32x32 MFMA tile: lane l holds column l%32, and in register v the
+// row 8*(v/4) + 4*(l/32) + v%4.
+// ---------------------------------------------------------------------------------------------
+template <int WTM, int WTN, int TM, int TN, bool FULL>
+__device__ __forceinline__ void epilogue_via_lds(const BrgemmParams& p, const Instance& in,
+                                                 const TileCoord& tc, int wm, int wn, int lane,
+                                                 int wave, float* lds_f, f32x16 (&acc)[TM][TN]) {
+  constexpr int EP_ROW = WTM + 4;                    // slab: 32 columns x WTM rows fp32
+  constexpr int CPC = WTM / 8;                       // 8-row chunks per slab column
+  constexpr int EP_ITERS = 32 * CPC / 64;
+  static_assert(64 % CPC == 0, "row chunks per column divide the wavefront");
+  float* slab = lds_f + wave * 32 * EP_ROW;
+  const int my_chunk = lane % CPC;
+  const int32_t R = tc.row0 + wm * WTM + my_chunk * 8;
+  bool row_ok = true;
+  int64_t row_off, bias_idx;
+  if (p.fused) {
+    const int32_t gi = R / p.m, r = R - gi * p.m;
+    row_ok = FULL || R < p.vrows;
+    row_off = (int64_t)gi * p.c_step_m + r;
+    bias_idx = (int64_t)gi * p.bias_step_m + r;
+  } else {
+    row_ok = FULL || R < p.m;
+    row_off = R;
+    bias_idx = in.bias + R;
+  }
+  float bias8[8];
+  const bool has_bias = (p.flags & TPP_EPI_BIAS) != 0;
+#pragma unroll
+  for (int e = 0; e < 8; ++e)
+    bias8[e] = (has_bias && row_ok) ? gld<float>(p.bias + bias_idx + e) : 0.0f;
+
+#pragma unroll
+  for (int tn = 0; tn < TN; ++tn) {
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float4 w = make_float4(acc[tm][tn][q * 4 + 0], acc[tm][tn][q * 4 + 1],
+                               acc[tm][tn][q * 4 + 2], acc[tm][tn][q * 4 + 3]);
+        *reinterpret_cast<float4*>(slab + (lane & 31) * EP_ROW + tm * 32 + q * 8 +
+                                   (lane >> 5) * 4) = w;
+      }
+    __syncthreads();
+    // kept rolled: the accumulators are not indexed here, and unrolling the activation code
+    // would only grow the kernel
+#pragma unroll 1
+    for (int it = 0; it < EP_ITERS; ++it) {
+      const int col_local = it * (64 / CPC) + lane / CPC;
+      const float4 lo = *reinterpret_cast<const float4*>(slab + col_local * EP_ROW + my_chunk * 8);
+      const float4 hi =
+          *reinterpret_cast<const float4*>(slab + col_local * EP_ROW + my_chunk * 8 + 4);
+      const int32_t C = tc.col0 + wn * WTN + tn * 32 + col_local;
+      int64_t col_off;
+      bool col_ok;
+      if (p.fused) {
+        const int32_t gi = C / p.n, c = C - gi * p.n;
+        col_ok = FULL || C < p.vcols;
+        col_off = (int64_t)gi * p.c_step_n + (int64_t)c * p.ldc;
+      } else {
+        col_ok = FULL || C < p.n;
+        col_off = (int64_t)C * p.ldc;
+      }
+      if (row_ok && col_ok) {
+        float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+        const int64_t e0 = in.c + row_off + col_off;
+        if (p.c_bf16) {
+          uint16_t* cp = static_cast<uint16_t*>(p.c) + e0;
+          const bool vec = (reinterpret_cast<uintptr_t>(cp) & 15) == 0;
+          if (p.beta != 0.0f) {
+            const u32x4 w = vec ? ld16(cp) : ld16_unaligned(cp);
+            const uint32_t d[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              v[2 * e] = p.beta * bf16_bits_to_f32(d[e] & 0xffffu) + v[2 * e];
+              v[2 * e + 1] = p.beta * bf16_bits_to_f32(d[e] >> 16) + v[2 * e + 1];
+            }
+          }
+          uint32_t o[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[e] = f32_to_bf16_bits(activate(v[e] + bias8[e], p.flags));
+          if (vec) {
+            gst<u32x4>(cp, (u32x4){o[0] | (o[1] << 16), o[2] | (o[3] << 16),
+                                   o[4] | (o[5] << 16), o[6] | (o[7] << 16)});
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) gst<uint16_t>(cp + e, (uint16_t)o[e]);
+          }
+        } else {
+          float* cp = static_cast<float*>(p.c) + e0;
+          const bool vec = (reinterpret_cast<uintptr_t>(cp) & 15) == 0;
+          if (p.beta != 0.0f) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] = p.beta * gld<float>(cp + e) + v[e];
+          }
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] = activate(v[e] + bias8[e], p.flags);
+          if (vec) {
+            gst<f32x4>(cp, (f32x4){v[0], v[1], v[2], v[3]});
+            gst<f32x4>(cp + 4, (f32x4){v[4], v[5], v[6], v[7]});
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) gst<float>(cp + e, v[e]);
+          }
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
+}  // namespace dev
+}  // namespace tpp

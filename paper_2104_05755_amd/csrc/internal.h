@@ -19,6 +19,7 @@ struct BrgemmParams {
   float beta;
   uint32_t flags;
   int32_t c_bf16;  // 1: C is bf16, 0: C is fp32
+  int32_t aligned; // host-verified: every A_i / B_i base is 16-byte aligned (stride kind)
   int32_t kind;    // tpp_br_kind
   int64_t count;
   int64_t stride_a, stride_b;
@@ -48,22 +49,24 @@ struct BrgemmParams {
 
 // Kernel instances of the bf16 family (tile shape + load path) and the fp32 kernel.
 enum KernelId : int32_t {
-  K_BF16_256x256 = 0,   // 8 waves, 128x64 per wave, vector loads
-  K_BF16_256x128 = 1,   // 4 waves, 128x64 per wave, vector loads
-  K_BF16_128x128 = 2,   // 4 waves, 64x64 per wave, vector loads
-  K_BF16_64x64 = 3,     // 4 waves, 32x32 per wave, vector loads
-  K_BF16_GENERIC = 4,   // 64x64, element loads with full bounds checks (any shape / alignment)
-  K_F32_GENERIC = 5,    // 64x64 fp32 MFMA, element loads with full bounds checks
-  K_BF16_256x256_W4 = 6,  // 4 waves, 128x128 per wave
-  K_BF16_256x128_W8 = 7,  // 8 waves, 64x64 per wave
-  K_BF16_128x128_W8 = 8,  // 8 waves, 64x32 per wave
-  K_COUNT = 9
+  K_BF16_256x256 = 0,   // 8 waves, 128x64 per wave, 16-byte loads
+  K_BF16_128x128 = 1,   // 4 waves, 64x64 per wave, 16-byte loads (two workgroups per CU)
+  K_BF16_64x64 = 2,     // 4 waves, 32x32 per wave, 16-byte loads
+  K_BF16_GENERIC = 3,   // 64x64, element loads with full bounds checks (any shape / alignment)
+  K_F32_GENERIC = 4,    // 64x64 fp32 MFMA, element loads with full bounds checks
+  K_BF16_DL_256x256 = 5,  // direct global->LDS staging, 8 waves (k a multiple of 32)
+  K_BF16_DL_128x128 = 6,  // direct global->LDS staging, 4 waves
+  K_BF16_DL_64x64 = 7,    // direct global->LDS staging, 4 waves
+  K_COUNT = 8
 };
 
 const char* kernel_name(int32_t id);
 
 // Fill the tiling fields of p for kernel `id` and launch on `stream`.
 hipError_t launch_brgemm(BrgemmParams& p, int32_t id, hipStream_t stream);
+// The direct-to-LDS instances (brgemm_dl_kernels.hip); p's tiling fields already filled.
+hipError_t launch_brgemm_dl(const BrgemmParams& p, int32_t id, bool full, dim3 grid,
+                            hipStream_t stream);
 
 // Reduce TPP launcher; `work` is a device buffer of `work_floats` floats for partial results.
 struct ReduceParams {

@@ -69,13 +69,17 @@ int32_t choose_kernel(const tpp_brgemm_kernel_s& h, const tpp::BrgemmParams& p) 
   if (!vec) return tpp::K_BF16_GENERIC;
   if (const char* env = std::getenv("TPP_FORCE_KERNEL")) {
     const int id = std::atoi(env);
-    if (id >= 0 && id < tpp::K_COUNT && id != tpp::K_BF16_GENERIC && id != tpp::K_F32_GENERIC)
+    const bool is_dl = id >= tpp::K_BF16_DL_256x256 && id <= tpp::K_BF16_DL_64x64;
+    if (id >= 0 && id < tpp::K_COUNT && id != tpp::K_BF16_GENERIC && id != tpp::K_F32_GENERIC &&
+        (!is_dl || h.desc.k % 32 == 0))
       return id;
   }
   struct Cand { int32_t id; int bm, bn; };
-  const Cand cands[] = {{tpp::K_BF16_256x256, 256, 256},
-                        {tpp::K_BF16_128x128, 128, 128},
-                        {tpp::K_BF16_64x64, 64, 64}};
+  // k a multiple of 32: the direct global->LDS instances; otherwise register staging.
+  const bool dl = h.desc.k % 32 == 0;
+  const Cand cands[] = {{dl ? tpp::K_BF16_DL_256x256 : tpp::K_BF16_256x256, 256, 256},
+                        {dl ? tpp::K_BF16_DL_128x128 : tpp::K_BF16_128x128, 128, 128},
+                        {dl ? tpp::K_BF16_DL_64x64 : tpp::K_BF16_64x64, 64, 64}};
   for (const Cand& c : cands) {
     // never pad a virtual C out to a larger tile (the 64x64 tile is the floor)
     if ((c.bm > p.vrows && c.bm > 64) || (c.bn > p.vcols && c.bn > 64)) continue;
@@ -83,7 +87,7 @@ int32_t choose_kernel(const tpp_brgemm_kernel_s& h, const tpp::BrgemmParams& p) 
     // two tiles per compute unit: one workgroup's barriers and epilogue overlap the other's MFMAs
     if (tiles >= 512) return c.id;
   }
-  return tpp::K_BF16_64x64;
+  return dl ? tpp::K_BF16_DL_64x64 : tpp::K_BF16_64x64;
 }
 
 tpp_status launch(const tpp_brgemm_kernel_s* h, tpp::BrgemmParams& p, void* stream) {
@@ -91,6 +95,14 @@ tpp_status launch(const tpp_brgemm_kernel_s* h, tpp::BrgemmParams& p, void* stre
   const int64_t ksteps = (h->desc.k + 63) / 64;
   if (p.kind != TPP_BR_ADDRESS && p.count * ksteps >= (1LL << 31))
     return fail(TPP_ERR_UNSUPPORTED, "count * ceil(k/64) must be below 2^31");
+  // Stride kind: every pair base is a + i*stride_a (+ an instance step), so 16-byte alignment of
+  // all of them follows from the base pointers and the element steps, checked here once.
+  if (p.kind == TPP_BR_STRIDE) {
+    const auto al = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; };
+    p.aligned = al(p.a) && al(p.b) && p.stride_a % 8 == 0 && p.stride_b % 8 == 0 &&
+                (p.fused || !p.grid_form || (p.a_step_m % 8 == 0 && p.b_step_n % 8 == 0)) &&
+                (p.fused || p.grid_form || (!p.a_off && !p.b_off));
+  }
   const int32_t id = choose_kernel(*h, p);
   if (std::getenv("TPP_LOG"))
     std::fprintf(stderr, "[tpp] %s: G=%lld vrows=%d vcols=%d fused=%d -> %s\n", h->name,
