@@ -82,8 +82,16 @@ __device__ __forceinline__ TileCoord decode_tile(const BrgemmParams& p, int bm, 
   TileCoord tc;
   tc.g = t / per_group;
   const int64_t tin = t - tc.g * per_group;
-  tc.row0 = (int32_t)(tin % p.tiles_m) * bm;   // tiles of one column run consecutively
-  tc.col0 = (int32_t)(tin / p.tiles_m) * bn;
+  // Bands of up to 8 tile rows: consecutive tiles walk down a band, then move one tile column
+  // right, so the 32 tiles an XCD runs at once cover about 8 rows x 4 columns and share both
+  // their A rows and their B columns in that XCD's L2.
+  const int32_t band = p.tiles_m < 8 ? p.tiles_m : 8;
+  const int64_t per_band = (int64_t)band * p.tiles_n;
+  const int32_t b0 = (int32_t)(tin / per_band) * band;
+  const int32_t bh = (p.tiles_m - b0) < band ? (p.tiles_m - b0) : band;
+  const int64_t tb = tin - (int64_t)b0 * p.tiles_n;
+  tc.row0 = (b0 + (int32_t)(tb % bh)) * bm;
+  tc.col0 = (int32_t)(tb / bh) * bn;
   return tc;
 }
 
@@ -173,6 +181,18 @@ __device__ __forceinline__ void pair_bases_k(const BrgemmParams& p, const Instan
     pa = static_cast<const T*>(p.ptrs_a[in.pair0 + i]);
     pb = static_cast<const T*>(p.ptrs_b[in.pair0 + i]);
   }
+}
+
+// Workgroup barrier that first waits for this wave's own LDS operations only.  __syncthreads()
+// also waits for every outstanding global load (vmcnt 0), which would drain direct-to-LDS loads of
+// later pipeline stages at each barrier; kernels that keep such loads in flight wait for the ones
+// they need with an explicit s_waitcnt vmcnt before calling this.  The memory clobber keeps the
+// compiler from moving LDS accesses across the barrier.
+// The scheduling barriers keep register-only work (MFMAs) on its side of it as well.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
 }
 
 // 16 bytes of bf16 from global memory, aligned or not; zeroing without branches.

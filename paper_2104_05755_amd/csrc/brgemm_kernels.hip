@@ -688,6 +688,7 @@ constexpr KernelInfo kInfo[K_COUNT] = {
     {"bf16_256x256_w8_direct_lds", 256, 256},
     {"bf16_128x128_w4_direct_lds", 128, 128},
     {"bf16_64x64_w4_direct_lds", 64, 64},
+    {"bf16_256x256_w8_direct_lds_pingpong", 256, 256},
 };
 
 }  // namespace
@@ -742,6 +743,7 @@ hipError_t launch_brgemm(BrgemmParams& p, int32_t id, hipStream_t stream) {
     case K_BF16_DL_256x256:
     case K_BF16_DL_128x128:
     case K_BF16_DL_64x64:
+    case K_BF16_PP_256x256:
       return launch_brgemm_dl(p, id, full, grid, stream);
     case K_BF16_GENERIC:
       hipLaunchKernelGGL((brgemm_bf16_kernel<64, 64, 2, 2, true>), grid, block, 0, stream, p);

@@ -57,7 +57,8 @@ enum KernelId : int32_t {
   K_BF16_DL_256x256 = 5,  // direct global->LDS staging, 8 waves (k a multiple of 32)
   K_BF16_DL_128x128 = 6,  // direct global->LDS staging, 4 waves
   K_BF16_DL_64x64 = 7,    // direct global->LDS staging, 4 waves
-  K_COUNT = 8
+  K_BF16_PP_256x256 = 8,  // direct global->LDS staging, 8 waves in two alternating groups
+  K_COUNT = 9
 };
 
 const char* kernel_name(int32_t id);

@@ -69,7 +69,7 @@ int32_t choose_kernel(const tpp_brgemm_kernel_s& h, const tpp::BrgemmParams& p) 
   if (!vec) return tpp::K_BF16_GENERIC;
   if (const char* env = std::getenv("TPP_FORCE_KERNEL")) {
     const int id = std::atoi(env);
-    const bool is_dl = id >= tpp::K_BF16_DL_256x256 && id <= tpp::K_BF16_DL_64x64;
+    const bool is_dl = id >= tpp::K_BF16_DL_256x256 && id <= tpp::K_BF16_PP_256x256;
     if (id >= 0 && id < tpp::K_COUNT && id != tpp::K_BF16_GENERIC && id != tpp::K_F32_GENERIC &&
         (!is_dl || h.desc.k % 32 == 0))
       return id;
