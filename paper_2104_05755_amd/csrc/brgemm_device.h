@@ -45,15 +45,24 @@ __device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
   return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
 }
 
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+// Two floats narrowed together (one v_cvt_pk_bf16_f32, round to nearest even): lo in bits 15:0.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){lo, hi}, bf16x2_t));
+}
+
 // GELU in its tanh form, 0.5 x (1 + tanh(u)) with u = sqrt(2/pi) (x + 0.044715 x^3).
 // Since 0.5 (1 + tanh(u)) = 1 / (1 + e^(-2u)), this is x / (1 + 2^(-2u log2(e))): one hardware
 // exp2 (v_exp_f32) and one hardware reciprocal (v_rcp_f32), a few ulp of fp32 in all, and no
 // cancellation anywhere (for u -> -inf the denominator goes to +inf and the result to -0).
+// The exponent -2u log2(e) = x (k1 + k2 x^2) has its constants folded: 5 VALU operations and two
+// transcendental ones per element.
 __device__ __forceinline__ float gelu_tanh(float x) {
-  const float kSqrt2OverPi = 0.7978845608028654f;
-  const float kMinus2Log2e = -2.8853900817779268f;   // -2 / ln(2)
-  const float u = kSqrt2OverPi * (x + 0.044715f * x * x * x);
-  return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(kMinus2Log2e * u));
+  const float k1 = -2.3022082f;    // -2 log2(e) sqrt(2/pi)
+  const float k2 = -0.10294324f;   // k1 * 0.044715
+  const float e = __builtin_amdgcn_exp2f(x * __builtin_fmaf(k2, x * x, k1));
+  return x * __builtin_amdgcn_rcpf(1.0f + e);
 }
 
 __device__ __forceinline__ float activate(float v, uint32_t flags) {
@@ -324,6 +333,137 @@ __device__ __forceinline__ void epilogue_via_lds(const BrgemmParams& p, const In
     }
     __syncthreads();
   }
+}
+
+// ---------------------------------------------------------------------------------------------
+// Epilogue for a bf16 C that is not read (beta = 0).  Bias and activation are applied to the
+// accumulators where they are, each lane narrows its four consecutive rows of a column to bf16
+// and parks them in its own wave's LDS slab (column-major, WTM rows per column, 16-byte row
+// chunks XOR-swizzled by the column), and the wave then stores the slab as 16-byte runs of 8
+// rows, so every global store instruction writes whole 128-byte lines.  A wave touches only its
+// own slab, so no workgroup barrier is involved; the caller has passed one after the last LDS
+// read of the main loop.  ACT: 0 none, 1 ReLU, 2 GELU-tanh.
+// ---------------------------------------------------------------------------------------------
+template <int WTM, int WTN, int TM, int TN, bool FULL, int ACT>
+__device__ __forceinline__ void epilogue_bf16_act(const BrgemmParams& p, const Instance& in,
+                                                  const TileCoord& tc, int wm, int wn, int lane,
+                                                  int wave, char* lds, f32x16 (&acc)[TM][TN]) {
+  constexpr int CPC = WTM / 8;                 // 16-byte row chunks per slab column
+  constexpr int COL_BYTES = WTM * 2;
+  static_assert((CPC & (CPC - 1)) == 0 && CPC <= 64, "power-of-two chunks per column");
+  char* slab = lds + wave * WTN * COL_BYTES;
+  const int32_t row_base = tc.row0 + wm * WTM;
+  const bool has_bias = (p.flags & TPP_EPI_BIAS) != 0;
+  const int half = lane >> 5;                  // rows 4*half.. of each 8-row group
+  // Bias of the lane's rows, all issued before any is used: for group tm and q, the four rows
+  // 32 tm + 8 q + 4 half + e (an 8-row chunk never straddles an instance: m % 8 == 0).
+  f32x4 bias4[TM][4];
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int32_t R = row_base + tm * 32 + 8 * q + 4 * half;
+      int64_t idx;
+      bool ok;
+      if (p.fused) {
+        const int32_t gi = R / p.m, r = R - gi * p.m;
+        idx = (int64_t)gi * p.bias_step_m + r;
+        ok = FULL || R < p.vrows;
+      } else {
+        idx = in.bias + R;
+        ok = FULL || R < p.m;
+      }
+      f32x4 b = {0.0f, 0.0f, 0.0f, 0.0f};
+      if (has_bias && ok) {
+        const float* bp = p.bias + idx;
+        if ((reinterpret_cast<uintptr_t>(bp) & 15) == 0) {
+          b = gld<f32x4>(bp);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) b[e] = gld<float>(bp + e);
+        }
+      }
+      bias4[tm][q] = b;
+    }
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm) {
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) {
+      const int col = tn * 32 + (lane & 31);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          float x = acc[tm][tn][4 * q + e] + bias4[tm][q][e];
+          if constexpr (ACT == 1) x = x > 0.0f ? x : 0.0f;
+          if constexpr (ACT == 2) x = gelu_tanh(x);
+          v[e] = x;
+        }
+        const int ch = tm * 4 + q;             // 16-byte chunk of this lane's 8-row group
+        *reinterpret_cast<uint2*>(slab + col * COL_BYTES + ((ch ^ (col & (CPC - 1))) << 4) +
+                                  half * 8) = make_uint2(pack_bf16x2(v[0], v[1]),
+                                                         pack_bf16x2(v[2], v[3]));
+      }
+    }
+  }
+  // Read back: 64 lanes = 64 / CPC columns x CPC chunks per instruction.  LDS operations of one
+  // wave complete in order, so the reads see this wave's writes.
+  constexpr int COLS_PER_IT = 64 / CPC;
+  const int chunk = lane % CPC, csub = lane / CPC;
+  const int32_t R = row_base + chunk * 8;
+  bool row_ok;
+  int64_t row_off;
+  if (p.fused) {
+    const int32_t gi = R / p.m, r = R - gi * p.m;
+    row_ok = FULL || R < p.vrows;
+    row_off = (int64_t)gi * p.c_step_m + r;
+  } else {
+    row_ok = FULL || R < p.m;
+    row_off = R;
+  }
+#pragma unroll 4
+  for (int it = 0; it < WTN / COLS_PER_IT; ++it) {
+    const int col_local = it * COLS_PER_IT + csub;
+    const u32x4 w = *reinterpret_cast<const u32x4*>(
+        slab + col_local * COL_BYTES + ((chunk ^ (col_local & (CPC - 1))) << 4));
+    const int32_t C = tc.col0 + wn * WTN + col_local;
+    bool col_ok;
+    int64_t col_off;
+    if (p.fused) {
+      const int32_t gi = C / p.n, c = C - gi * p.n;
+      col_ok = FULL || C < p.vcols;
+      col_off = (int64_t)gi * p.c_step_n + (int64_t)c * p.ldc;
+    } else {
+      col_ok = FULL || C < p.n;
+      col_off = (int64_t)C * p.ldc;
+    }
+    if (row_ok && col_ok) {
+      uint16_t* cp = static_cast<uint16_t*>(p.c) + in.c + row_off + col_off;
+      if ((reinterpret_cast<uintptr_t>(cp) & 15) == 0) {
+        gst<u32x4>(cp, w);
+      } else {
+        const uint32_t d[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          gst<uint16_t>(cp + 2 * e, (uint16_t)(d[e] & 0xffffu));
+          gst<uint16_t>(cp + 2 * e + 1, (uint16_t)(d[e] >> 16));
+        }
+      }
+    }
+  }
+}
+
+template <int WTM, int WTN, int TM, int TN, bool FULL>
+__device__ __forceinline__ void epilogue_bf16(const BrgemmParams& p, const Instance& in,
+                                              const TileCoord& tc, int wm, int wn, int lane,
+                                              int wave, char* lds, f32x16 (&acc)[TM][TN]) {
+  if (p.flags & TPP_EPI_GELU_TANH)
+    epilogue_bf16_act<WTM, WTN, TM, TN, FULL, 2>(p, in, tc, wm, wn, lane, wave, lds, acc);
+  else if (p.flags & TPP_EPI_RELU)
+    epilogue_bf16_act<WTM, WTN, TM, TN, FULL, 1>(p, in, tc, wm, wn, lane, wave, lds, acc);
+  else
+    epilogue_bf16_act<WTM, WTN, TM, TN, FULL, 0>(p, in, tc, wm, wn, lane, wave, lds, acc);
 }
 
 }  // namespace dev

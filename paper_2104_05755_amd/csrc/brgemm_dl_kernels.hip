@@ -82,6 +82,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void brgemm_bf16_dl_kernel(
   static_assert(A_BYTES % (1024 * NW) == 0 && B_BYTES % (1024 * NW) == 0, "whole wave-loads");
   static_assert(A_PER_W >= 1 && B_PER_W >= 1, "every wave loads both panels");
   static_assert(TM >= 1 && TN >= 1, "wave tile at least 32x32");
+  static_assert(BM * BN * 2 <= LDS_BYTES, "bf16 epilogue slabs fit in the ring");
 
   __shared__ __attribute__((aligned(1024))) char lds[LDS_BYTES];
 
@@ -279,8 +280,11 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void brgemm_bf16_dl_kernel(
     if (lead) lds_barrier();
   }
   __syncthreads();
-  epilogue_via_lds<WTM, WTN, TM, TN, FULL>(p, in, tc, wm, wn, lane, wave,
-                                          reinterpret_cast<float*>(lds), acc);
+  if (p.c_bf16 && p.beta == 0.0f)
+    epilogue_bf16<WTM, WTN, TM, TN, FULL>(p, in, tc, wm, wn, lane, wave, lds, acc);
+  else
+    epilogue_via_lds<WTM, WTN, TM, TN, FULL>(p, in, tc, wm, wn, lane, wave,
+                                            reinterpret_cast<float*>(lds), acc);
 }
 
 template <int BM, int BN, int WM, int WN, bool FULL, int KIND, bool PP>

@@ -75,9 +75,11 @@ int32_t choose_kernel(const tpp_brgemm_kernel_s& h, const tpp::BrgemmParams& p) 
       return id;
   }
   struct Cand { int32_t id; int bm, bn; };
-  // k a multiple of 32: the direct global->LDS instances; otherwise register staging.
-  const bool dl = h.desc.k % 32 == 0;
-  const Cand cands[] = {{dl ? tpp::K_BF16_DL_256x256 : tpp::K_BF16_256x256, 256, 256},
+  // k a multiple of 32: the direct global->LDS instances (the 256x256 one in its ping-pong
+  // schedule), except for pointer lists, whose scattered pair blocks stream better through
+  // registers; otherwise register staging.
+  const bool dl = h.desc.k % 32 == 0 && h.desc.kind != TPP_BR_ADDRESS;
+  const Cand cands[] = {{dl ? tpp::K_BF16_PP_256x256 : tpp::K_BF16_256x256, 256, 256},
                         {dl ? tpp::K_BF16_DL_128x128 : tpp::K_BF16_128x128, 128, 128},
                         {dl ? tpp::K_BF16_DL_64x64 : tpp::K_BF16_64x64, 64, 64}};
   for (const Cand& c : cands) {
