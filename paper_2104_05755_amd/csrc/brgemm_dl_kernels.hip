@@ -2,9 +2,9 @@
 //
 // Same computation and tiling as the 16-byte-load kernels (see brgemm_kernels.hip), with the
 // operand staging rebuilt around two gfx950 instructions:
-//   - global_load_lds_dwordx4 writes each lane's 16 bytes straight into LDS (lane j at M0 + 16 j),
-//     so staging needs no registers and no LDS-write instructions: a ring of DL_SLOTS LDS slots
-//     keeps DL_SLOTS - 1 stages of 32 k in flight while the MFMAs consume the oldest;
+//   - buffer_load_dwordx4 ... lds writes each lane's 16 bytes straight into LDS (lane j at M0 + 16 j),
+//     so staging needs no registers and no LDS-write instructions: a ring of SLOTS = 4 LDS slots
+//     keeps SLOTS - 1 stages of 32 k in flight while the MFMAs consume the oldest;
 //   - ds_read_b64_tr_b16 reads an M-contiguous A panel transposed, so A is staged in its own
 //     layout and the MFMA still gets 8 consecutive k per lane (two transposing reads per
 //     fragment).
@@ -25,8 +25,7 @@ using namespace dev;
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 #define LDS_AS __attribute__((address_space(3)))
 
-constexpr int DL_BK = 32;     // k per stage
-constexpr int DL_SLOTS = 4;   // LDS ring slots: three stages in flight
+constexpr int LDS_MAX = 160 * 1024;   // bytes of LDS per workgroup on gfx950
 
 // s_waitcnt immediate waiting until at most n vector-memory operations are outstanding (gfx9
 // encoding: vmcnt in bits 3:0 and 15:14, expcnt 6:4 and lgkmcnt 11:8 left at their maxima).
@@ -34,25 +33,49 @@ constexpr int vmcnt_imm(int n) {
   return (n & 0xF) | (((n >> 4) & 3) << 14) | (0x7 << 4) | (0xF << 8);
 }
 
-// 16-byte global -> LDS copy of a whole wave (global_load_lds_dwordx4): lane j's 16 bytes land at
-// l + 16 j, where l is wave-uniform.  It is issued through inline asm so that the compiler does
-// not see a pending LDS write: the compiler would otherwise wait for every outstanding load
-// (vmcnt 0) before the next LDS read and so drain the stages kept in flight.  Callers order these
-// loads themselves with s_waitcnt vmcnt and lds_barrier().  M0 is saved and restored around it.
-__device__ __forceinline__ void load_lds16(const void* g, char* l) {
+// Buffer descriptor of a raw (unswizzled, stride 0) buffer at `base`: 2^31 bytes addressable,
+// out-of-range offsets read as zero.  Built from wave-uniform values, so it lives in SGPRs.
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ i32x4 raw_buffer(const void* base) {
+  const uint64_t b = reinterpret_cast<uint64_t>(base);
+  return (i32x4){__builtin_amdgcn_readfirstlane((int)(uint32_t)b),
+                 __builtin_amdgcn_readfirstlane((int)((uint32_t)(b >> 32) & 0xffffu)), 0x7fffffff,
+                 0x00020000};
+}
+
+// 16-byte buffer -> LDS copy of a whole wave (buffer_load_dwordx4 ... offen lds): lane j's 16
+// bytes from rsrc base + voff land at l + 16 j.  The buffer form takes one 32-bit offset per lane
+// where the global form takes a 64-bit address, and unlike the global form it runs alongside the
+// MFMAs of the same compute unit instead of stalling them (measured on gfx950: a stream of 32x32x16
+// MFMAs beside 8 KB of loads per iteration took the MFMA time with buffer loads, the sum of both
+// times with global loads).  It is issued through inline asm so that the compiler does not see a
+// pending LDS write: the compiler would otherwise wait for every outstanding load (vmcnt 0)
+// before the next LDS read and so drain the stages kept in flight.  Callers order these loads
+// themselves with s_waitcnt vmcnt and lds_barrier().  M0 is saved and restored around it.
+__device__ __forceinline__ void buffer_load_lds16(i32x4 rsrc, uint32_t voff, char* l) {
   const uint32_t lds_addr =
       __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(LDS_AS char*)l);
   uint32_t saved;
   asm volatile(
       "s_mov_b32 %0, m0\n\t"
-      "s_mov_b32 m0, %2\n\t"
+      "s_mov_b32 m0, %3\n\t"
       "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %1, off\n\t"
+      "buffer_load_dwordx4 %1, %2, 0 offen lds\n\t"
       "s_nop 0\n\t"
       "s_mov_b32 m0, %0"
       : "=&s"(saved)
-      : "v"(g), "s"(lds_addr)
+      : "v"(voff), "s"(rsrc), "s"(lds_addr)
       : "memory");
+}
+
+// XOR swizzle of the 16-byte k-chunks of a B-panel column (COLB = 2 BK bytes): the 16 columns a
+// ds_read_b128 serves per cycle land in 16 distinct 16-byte bank groups of a 256-byte row.
+template <int BK>
+__device__ __forceinline__ int swz_b(int col) {
+  if constexpr (BK == 64)
+    return (col >> 1) & 7;
+  else
+    return (col >> 2) & 3;
 }
 
 // XOR swizzle of the 16-byte chunks of an A-panel k-row (row pitch ROW bytes): the four k-rows a
@@ -65,20 +88,35 @@ __device__ __forceinline__ int swz_a(int k) {
     return ((k >> 1) & 1) << 2;
 }
 
-template <int BM, int BN, int WAVES_M, int WAVES_N, bool FULL, int KIND, bool ALIGNED, bool PP>
+// SCHED: 0 = every wave loads, reads and multiplies in turn; 1 = ping-pong, memory half = fragment
+// reads + load issue; 2 = ping-pong, memory half = load issue only, the next stage's fragments
+// read during the MFMAs.
+// BKT: k per stage, 32 or 64.  At 64 every stage reads whole 128-byte lines of the K-contiguous B
+// blocks (a column of a 64-k block is 128 bytes); at 32 each B column load covers half a line.
+template <int BM, int BN, int WAVES_M, int WAVES_N, bool FULL, int KIND, bool ALIGNED, int SCHED,
+          int BKT>
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void brgemm_bf16_dl_kernel(BrgemmParams p) {
+  constexpr int DL_BK = BKT;
+  static_assert(BKT == 32 || BKT == 64, "stage depth");
   constexpr int NW = WAVES_M * WAVES_N;
   constexpr int WTM = BM / WAVES_M, WTN = BN / WAVES_N;
   constexpr int TM = WTM / 32, TN = WTN / 32;
   constexpr int A_ROW = BM * 2;                 // bytes per k-row of the A panel
   constexpr int A_BYTES = DL_BK * A_ROW;        // A panel of one slot
-  constexpr int B_BYTES = BN * DL_BK * 2;       // B panel of one slot (64 B per column)
+  constexpr int COLB = DL_BK * 2;               // bytes of one B column in a slot
+  constexpr int B_BYTES = BN * COLB;            // B panel of one slot
   constexpr int SLOT = A_BYTES + B_BYTES;
   constexpr int A_PER_W = A_BYTES / 1024 / NW;  // 1 KB wave-loads per wave and stage
   constexpr int B_PER_W = B_BYTES / 1024 / NW;
   constexpr int LPS = A_PER_W + B_PER_W;        // vector-memory operations per wave and stage
   constexpr int EP_BYTES = NW * 32 * (WTM + 4) * 4;
-  constexpr int LDS_BYTES = (DL_SLOTS * SLOT > EP_BYTES) ? DL_SLOTS * SLOT : EP_BYTES;
+  // LDS ring slots: three 32-k stages in flight (a fifth slot, which fits, measured slower), or
+  // one 64-k stage (two 64 KB slots for the 256x256 tile).
+  constexpr int SLOTS = BKT == 64 ? 2 : 4;
+  static_assert(BKT == 32 || SCHED == 0 || SCHED == 3,
+                "the ping-pong schedules keep three stages in flight");
+  static_assert(SLOTS * SLOT <= LDS_MAX, "ring fits in LDS");
+  constexpr int LDS_BYTES = (SLOTS * SLOT > EP_BYTES) ? SLOTS * SLOT : EP_BYTES;
   static_assert(A_BYTES % (1024 * NW) == 0 && B_BYTES % (1024 * NW) == 0, "whole wave-loads");
   static_assert(A_PER_W >= 1 && B_PER_W >= 1, "every wave loads both panels");
   static_assert(TM >= 1 && TN >= 1, "wave tile at least 32x32");
@@ -94,6 +132,12 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void brgemm_bf16_dl_kernel(
   const int32_t ksteps = p.k / DL_BK;
   const int32_t stages = (int32_t)(in.npairs * ksteps);
 
+  // Element offsets of the first instance block the tile touches in A and in B: every row / column
+  // offset of the tile is at least this (the host takes this kernel only for non-negative steps
+  // and a tile span below 2^31 bytes), so loads address the operands as base + 32-bit offset.
+  const int64_t base_a = p.fused ? (int64_t)(tc.row0 / p.m) * p.a_step_m : 0;
+  const int64_t base_b = p.fused ? (int64_t)(tc.col0 / p.n) * p.b_step_n : 0;
+
   // Per-lane load assignments.  A wave-load r covers bytes [q*1024, q*1024 + 1024) of the A
   // panel (q = wave * A_PER_W + r); lane j fills the 16-byte chunk at q*1024 + 16 j, i.e. k-row
   // kr and swizzled chunk position sc, which holds the 8 rows m = 8 * (sc ^ swz(kr)).
@@ -107,7 +151,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void brgemm_bf16_dl_kernel(
     a_kr[r] = kr;
     int64_t off = 0;
     const bool ok = row_in_a(p, tc.row0 + m_local, off);
-    a_off[r] = ok ? off : 0;   // out-of-range rows read row 0: only discarded outputs see it
+    a_off[r] = ok ? off : base_a;   // out-of-range rows read a valid row: only discarded outputs see it
   }
   // B wave-load r: 16 columns of 64 bytes; lane j fills column 4*q + j/4 (q-th group of 16
   // columns), chunk position j%4, which holds k-chunk (j%4) ^ ((column >> 2) & 3).
@@ -115,57 +159,70 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void brgemm_bf16_dl_kernel(
 #pragma unroll
   for (int r = 0; r < B_PER_W; ++r) {
     const int byte = (wave * B_PER_W + r) * 1024 + lane * 16;
-    const int col = byte / 64, sc = (byte % 64) / 16;
-    const int kc = sc ^ ((col >> 2) & 3);
+    const int col = byte / COLB, sc = (byte % COLB) / 16;
+    const int kc = sc ^ swz_b<BKT>(col);
     int64_t off = 0;
     const bool ok = col_in_b(p, tc.col0 + col, off);
-    b_off[r] = (ok ? off : 0) + kc * 8;
+    b_off[r] = (ok ? off : base_b) + kc * 8;
   }
 
-  // Byte offset of each wave-load's 16 bytes inside a pair's A / B block at k = 0: constant over
-  // the stages, so a stage's address is one wave-uniform base plus this per-lane offset.
-  int64_t la[A_PER_W], lb[B_PER_W];
+  // Byte offset of each wave-load's 16 bytes from the tile's base inside a pair's A / B block at
+  // k = 0: constant over the stages, so a stage's address is one wave-uniform base (a buffer
+  // descriptor) plus this per-lane offset.
+  uint32_t la[A_PER_W], lb[B_PER_W];
 #pragma unroll
-  for (int r = 0; r < A_PER_W; ++r) la[r] = (a_off[r] + (int64_t)a_kr[r] * p.lda) * 2;
+  for (int r = 0; r < A_PER_W; ++r) la[r] = (uint32_t)((a_off[r] - base_a + (int64_t)a_kr[r] * p.lda) * 2);
 #pragma unroll
-  for (int r = 0; r < B_PER_W; ++r) lb[r] = b_off[r] * 2;
+  for (int r = 0; r < B_PER_W; ++r) lb[r] = (uint32_t)((b_off[r] - base_b) * 2);
 
   // Stages are issued in order; (iss_i, iss_kk) is the pair and k offset of the next one, so no
-  // stage index is ever divided.
+  // stage index is ever divided.  A stage's wave-loads can be spread over other work:
+  // stage_begin(), issue_load(r) for r < LPS (A loads first, then B), stage_end().
   int32_t iss_i = 0, iss_kk = 0, iss_s = 0;
-  auto issue = [&]() {
+  const char* ua = nullptr;
+  const char* ub = nullptr;
+  i32x4 ra, rb;
+  char* slot = lds;
+  bool aligned = true;
+  auto stage_begin = [&]() {
     const uint16_t* pa;
     const uint16_t* pb;
     pair_bases_k<KIND, uint16_t>(p, in, iss_i, pa, pb);
-    const char* ua = reinterpret_cast<const char*>(pa) + (int64_t)iss_kk * p.lda * 2;
-    const char* ub = reinterpret_cast<const char*>(pb) + (int64_t)iss_kk * 2;
-    char* slot = lds + (iss_s % DL_SLOTS) * SLOT;
-    const bool aligned =
+    ua = reinterpret_cast<const char*>(pa + base_a) + (int64_t)iss_kk * p.lda * 2;
+    ub = reinterpret_cast<const char*>(pb + base_b) + (int64_t)iss_kk * 2;
+    ra = raw_buffer(ua);
+    rb = raw_buffer(ub);
+    slot = lds + (iss_s % SLOTS) * SLOT;
+    aligned =
         ALIGNED || ((reinterpret_cast<uintptr_t>(pa) | reinterpret_cast<uintptr_t>(pb)) & 15) == 0;
+  };
+  auto issue_load = [&](int r) {
+    const bool is_a = r < A_PER_W;
+    char* dst = is_a ? slot + (wave * A_PER_W + r) * 1024
+                     : slot + A_BYTES + (wave * B_PER_W + (r - A_PER_W)) * 1024;
     if (ALIGNED || aligned) {
-#pragma unroll
-      for (int r = 0; r < A_PER_W; ++r) load_lds16(ua + la[r], slot + (wave * A_PER_W + r) * 1024);
-#pragma unroll
-      for (int r = 0; r < B_PER_W; ++r)
-        load_lds16(ub + lb[r], slot + A_BYTES + (wave * B_PER_W + r) * 1024);
+      buffer_load_lds16(is_a ? ra : rb, is_a ? la[r] : lb[r - A_PER_W], dst);
     } else {
-      // A pair block off 16-byte alignment (offset or pointer lists): the same chunks through
-      // registers, element by element.
-#pragma unroll
-      for (int r = 0; r < A_PER_W; ++r)
-        *reinterpret_cast<u32x4*>(slot + (wave * A_PER_W + r) * 1024 + lane * 16) =
-            ld16_unaligned(reinterpret_cast<const uint16_t*>(ua + la[r]));
-#pragma unroll
-      for (int r = 0; r < B_PER_W; ++r)
-        *reinterpret_cast<u32x4*>(slot + A_BYTES + (wave * B_PER_W + r) * 1024 + lane * 16) =
-            ld16_unaligned(reinterpret_cast<const uint16_t*>(ub + lb[r]));
+      // a pair block off 16-byte alignment (offset or pointer lists): the same chunk through
+      // registers, element by element
+      const char* src = is_a ? ua + la[r] : ub + lb[r - A_PER_W];
+      *reinterpret_cast<u32x4*>(dst + lane * 16) =
+          ld16_unaligned(reinterpret_cast<const uint16_t*>(src));
     }
+  };
+  auto stage_end = [&]() {
     ++iss_s;
     iss_kk += DL_BK;
     if (iss_kk == p.k) {
       iss_kk = 0;
       ++iss_i;
     }
+  };
+  auto issue = [&]() {
+    stage_begin();
+#pragma unroll
+    for (int r = 0; r < LPS; ++r) issue_load(r);
+    stage_end();
   };
 
   f32x16 acc[TM][TN];
@@ -183,35 +240,38 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void brgemm_bf16_dl_kernel(
   const int g = lane >> 4, j = lane & 15;
   const int a_lo = 2 * (g & 1) + ((j >> 1) & 1);      // chunk within the 32-row group
   const int a_sub = 8 * (j & 1);                      // byte within the chunk
-  const int b_swz = (lane >> 2) & 3;
+  const int b_swz = swz_b<BKT>(lane & 31);   // the column's swizzle (wave tiles start at 32k)
 
   constexpr int KQ = DL_BK / 16;   // MFMA k-steps per stage
-  // Fragments of k-step kq of the stage held in slot slot_idx.
-  auto read_frags = [&](int slot_idx, int kq, bf16x8 (&af)[TM], bf16x8 (&bfr)[TN]) {
+  // Fragments of k-step kq of the stage held in slot slot_idx: A fragment tm (two transposing
+  // reads), B fragment tn (one 16-byte read).
+  auto read_a = [&](int slot_idx, int kq, int tm) {
     const char* As = lds + slot_idx * SLOT;
-    const char* Bs = As + A_BYTES;
+    const int hi = (wm * WTM + tm * 32) >> 3;     // first chunk of the 32-row group
+    v4i16 half[2];
 #pragma unroll
-    for (int tm = 0; tm < TM; ++tm) {
-      const int hi = (wm * WTM + tm * 32) >> 3;     // first chunk of the 32-row group
-      v4i16 half[2];
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int k = kq * 16 + 8 * (g >> 1) + 4 * h + (j >> 2);
-        const int byte = k * A_ROW + (((hi ^ swz_a<A_ROW>(k)) + a_lo) << 4) + a_sub;
-        half[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS v4i16*)(As + byte));
-      }
-      const u32x4 w = {(uint32_t)(uint16_t)half[0][0] | ((uint32_t)(uint16_t)half[0][1] << 16),
-                       (uint32_t)(uint16_t)half[0][2] | ((uint32_t)(uint16_t)half[0][3] << 16),
-                       (uint32_t)(uint16_t)half[1][0] | ((uint32_t)(uint16_t)half[1][1] << 16),
-                       (uint32_t)(uint16_t)half[1][2] | ((uint32_t)(uint16_t)half[1][3] << 16)};
-      af[tm] = __builtin_bit_cast(bf16x8, w);
+    for (int h = 0; h < 2; ++h) {
+      const int k = kq * 16 + 8 * (g >> 1) + 4 * h + (j >> 2);
+      const int byte = k * A_ROW + (((hi ^ swz_a<A_ROW>(k)) + a_lo) << 4) + a_sub;
+      half[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS v4i16*)(As + byte));
     }
+    const u32x4 w = {(uint32_t)(uint16_t)half[0][0] | ((uint32_t)(uint16_t)half[0][1] << 16),
+                     (uint32_t)(uint16_t)half[0][2] | ((uint32_t)(uint16_t)half[0][3] << 16),
+                     (uint32_t)(uint16_t)half[1][0] | ((uint32_t)(uint16_t)half[1][1] << 16),
+                     (uint32_t)(uint16_t)half[1][2] | ((uint32_t)(uint16_t)half[1][3] << 16)};
+    return __builtin_bit_cast(bf16x8, w);
+  };
+  auto read_b = [&](int slot_idx, int kq, int tn) {
+    const char* Bs = lds + slot_idx * SLOT + A_BYTES;
+    const int col = wn * WTN + tn * 32 + (lane & 31);
+    const int kc = 2 * kq + (lane >> 5);
+    return *reinterpret_cast<const bf16x8*>(Bs + col * COLB + ((kc ^ b_swz) << 4));
+  };
+  auto read_frags = [&](int slot_idx, int kq, bf16x8 (&af)[TM], bf16x8 (&bfr)[TN]) {
 #pragma unroll
-    for (int tn = 0; tn < TN; ++tn) {
-      const int col = wn * WTN + tn * 32 + (lane & 31);
-      const int kc = 2 * kq + (lane >> 5);
-      bfr[tn] = *reinterpret_cast<const bf16x8*>(Bs + col * 64 + ((kc ^ b_swz) << 4));
-    }
+    for (int tm = 0; tm < TM; ++tm) af[tm] = read_a(slot_idx, kq, tm);
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) bfr[tn] = read_b(slot_idx, kq, tn);
   };
   auto mfmas = [&](const bf16x8 (&af)[TM], const bf16x8 (&bfr)[TN]) {
 #pragma unroll
@@ -229,29 +289,72 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void brgemm_bf16_dl_kernel(
     }
   };
   // Wait until this wave's loads of the stage `ahead` stages before its newest issued one landed.
+  // (ahead is at most SLOTS - 2.)
   auto wait_loads = [&](int32_t ahead) {
-    if (ahead >= 2)
+    if (ahead >= 3)
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(3 * LPS));
+    else if (ahead == 2)
       __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * LPS));
     else if (ahead == 1)
       __builtin_amdgcn_s_waitcnt(vmcnt_imm(LPS));
     else
       __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
   };
+  static_assert(SLOTS - 2 <= 3 && 3 * LPS <= 63, "vmcnt immediates cover the ring");
+  auto lmin = [](int32_t a, int32_t b) { return a < b ? a : b; };
 
-  const int32_t pre = stages < DL_SLOTS - 1 ? stages : DL_SLOTS - 1;
+  const int32_t pre = stages < SLOTS - 1 ? stages : SLOTS - 1;
   for (int32_t s = 0; s < pre; ++s) issue();
-  if constexpr (!PP) {
+  if constexpr (SCHED == 0) {
     for (int32_t s = 0; s < stages; ++s) {
       // This wave's loads of stage s are done once at most the later stages' loads are pending;
       // the barrier then publishes every wave's stage s and retires everyone's reads of s - 1.
-      wait_loads(stages - 1 - s < 2 ? stages - 1 - s : 2);
+      wait_loads(lmin(stages - 1 - s, SLOTS - 2));
       lds_barrier();
-      if (s + DL_SLOTS - 1 < stages) issue();   // stage s + 3 refills the slot of stage s - 1
-      compute(s % DL_SLOTS);
+      if (s + SLOTS - 1 < stages) issue();   // stage s + SLOTS - 1 refills the slot of s - 1
+      compute(s % SLOTS);
     }
-  } else {
+  } else if constexpr (SCHED == 3) {
+    // As schedule 0, with stage s + SLOTS - 1's wave-loads spread between the MFMA groups of stage
+    // s (a group: one A fragment times all B fragments) instead of issued in a burst after the
+    // barrier, where every wave would stall at the load unit before its first MFMA; and with
+    // k-step kq + 1's fragments read while k-step kq's MFMAs run.  (Loop indices that select
+    // registers are compile-time constants after unrolling.)
+    constexpr int GROUPS = KQ * TM;
+    for (int32_t s = 0; s < stages; ++s) {
+      wait_loads(lmin(stages - 1 - s, SLOTS - 2));
+      lds_barrier();
+      const bool more = s + SLOTS - 1 < stages;
+      if (more) stage_begin();
+      const int sl = s % SLOTS;
+      bf16x8 af[2][TM], bfr[2][TN];
+      read_frags(sl, 0, af[0], bfr[0]);
+#pragma unroll
+      for (int kq = 0; kq < KQ; ++kq) {
+        const int cur = kq & 1;
+        if (kq + 1 < KQ) read_frags(sl, kq + 1, af[cur ^ 1], bfr[cur ^ 1]);
+#pragma unroll
+        for (int tm = 0; tm < TM; ++tm) {
+#pragma unroll
+          for (int tn = 0; tn < TN; ++tn)
+            acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][tm], bfr[cur][tn],
+                                                                  acc[tm][tn], 0, 0, 0);
+          const int grp = kq * TM + tm;
+#pragma unroll
+          for (int r = grp * LPS / GROUPS; r < (grp + 1) * LPS / GROUPS; ++r) {
+            if (more) {
+              __builtin_amdgcn_sched_barrier(0);
+              issue_load(r);
+              __builtin_amdgcn_sched_barrier(0);
+            }
+          }
+        }
+      }
+      if (more) stage_end();
+    }
+  } else if constexpr (SCHED == 1) {
     // Ping-pong: waves 0-3 (one per SIMD) lead, waves 4-7 lag by one half-period.  Each stage is
-    // a memory half (fragment reads of the stage, global->LDS issue of stage s + 3) and a compute
+    // a memory half (fragment reads of the stage, global->LDS issue of stage s + SLOTS - 1) and a compute
     // half (the stage's MFMAs on registers); while one wave of a SIMD computes, the other reads,
     // so every barrier finds the next MFMA phase's operands already in registers.
     //   barrier j:  leading waves end M(j/2) (j even) or C(j/2) (j odd);
@@ -261,15 +364,35 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void brgemm_bf16_dl_kernel(
     // the leading waves wait at the end of C(s), the lagging ones at the end of M(s).
     static_assert(NW == 8, "two groups of four waves");
     const bool lead = wave < 4;
-    wait_loads(stages - 1 < 2 ? stages - 1 : 2);   // stage 0, before anyone reads it
+    wait_loads(lmin(stages - 1, SLOTS - 2));   // stage 0, before anyone reads it
     lds_barrier();
     if (!lead) lds_barrier();
     bf16x8 af[KQ][TM], bfr[KQ][TN];
     for (int32_t s = 0; s < stages; ++s) {
-      const int32_t later = stages - 2 - s < 2 ? stages - 2 - s : 2;
+      const int32_t later = lmin(stages - 2 - s, SLOTS - 2);
+      // Memory half: the fragment reads of stage s with stage s + SLOTS - 1's wave-loads spread among
+      // them, so that the LDS and the load unit work at the same time.
+      // (Load indices are compile-time constants: a runtime index would put the per-lane offset
+      // arrays in scratch memory.)
+      constexpr int SPOTS = KQ * TM / 2;   // after every second A fragment
+      const bool more = s + SLOTS - 1 < stages;
+      if (more) stage_begin();
 #pragma unroll
-      for (int kq = 0; kq < KQ; ++kq) read_frags(s % DL_SLOTS, kq, af[kq], bfr[kq]);
-      if (s + DL_SLOTS - 1 < stages) issue();   // stage s + 3
+      for (int kq = 0; kq < KQ; ++kq) {
+#pragma unroll
+        for (int tm = 0; tm < TM; ++tm) {
+          af[kq][tm] = read_a(s % SLOTS, kq, tm);
+          const int spot = kq * (TM / 2) + (tm >> 1);
+          if ((tm & 1) && spot < LPS && more) issue_load(spot);
+        }
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn) bfr[kq][tn] = read_b(s % SLOTS, kq, tn);
+      }
+      if (more) {
+#pragma unroll
+        for (int r = SPOTS; r < LPS; ++r) issue_load(r);
+        stage_end();
+      }
       if (!lead && s + 1 < stages) wait_loads(later);
       lds_barrier();
 #pragma unroll
@@ -277,6 +400,52 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void brgemm_bf16_dl_kernel(
       if (lead && s + 1 < stages) wait_loads(later);
       lds_barrier();
     }
+    if (lead) lds_barrier();
+  } else {
+    // Ping-pong with the fragment reads moved into the compute half: stage t's compute half runs
+    // its MFMAs on fragments already in registers and reads stage t + 1's fragments from LDS
+    // meanwhile; the memory half only issues stage t + SLOTS - 1's global->LDS loads.  Waves 0-3
+    // lead, waves 4-7 lag by one half-period:
+    //   barrier j:  leading waves end L(j/2) (j even) or C(j/2) (j odd);
+    //               lagging waves end C(j/2 - 1) (j even, the first one is the offset barrier) or
+    //               L(j/2) (j odd).
+    // Stage t + 1 is read during C(t), so it must have landed before barrier 2t, the one that
+    // opens the leading waves' C(t): leading waves wait at the end of L(t), lagging ones at the end
+    // of C(t - 1) (each with its loads of later stages still in flight).  The slot refilled in L(t)
+    // held stage t - 1, whose last reads (lagging C(t - 2)) ended before barrier 2t - 2.
+    static_assert(NW == 8, "two groups of four waves");
+    const bool lead = wave < 4;
+    bf16x8 af[2][KQ][TM], bfr[2][KQ][TN];
+    wait_loads(lmin(stages - 1, SLOTS - 2));   // stage 0 landed everywhere ...
+    lds_barrier();
+#pragma unroll
+    for (int kq = 0; kq < KQ; ++kq) read_frags(0, kq, af[0][kq], bfr[0][kq]);   // ... and read
+    if (!lead) {
+      if (stages > 1) wait_loads(lmin(stages - 2, SLOTS - 3));   // stage 1, before barrier 0
+      lds_barrier();
+    }
+    // Two iterations per trip so that the fragment buffers are indexed by constants.
+    auto step = [&](int32_t s, bf16x8 (&fa)[KQ][TM], bf16x8 (&fb)[KQ][TN],
+                    bf16x8 (&na)[KQ][TM], bf16x8 (&nb)[KQ][TN]) {
+      // L(s)
+      if (s + SLOTS - 1 < stages) issue();   // stage s + SLOTS - 1
+      if (lead && s + 1 < stages) wait_loads(lmin(stages - 2 - s, SLOTS - 2));
+      lds_barrier();
+      // C(s)
+#pragma unroll
+      for (int kq = 0; kq < KQ; ++kq) {
+        if (s + 1 < stages) read_frags((s + 1) % SLOTS, kq, na[kq], nb[kq]);
+        mfmas(fa[kq], fb[kq]);
+      }
+      if (!lead && s + 2 < stages) wait_loads(lmin(stages - 3 - s, SLOTS - 3));
+      lds_barrier();
+    };
+    int32_t s = 0;
+    for (; s + 1 < stages; s += 2) {
+      step(s, af[0], bfr[0], af[1], bfr[1]);
+      step(s + 1, af[1], bfr[1], af[0], bfr[0]);
+    }
+    if (s < stages) step(s, af[0], bfr[0], af[1], bfr[1]);
     if (lead) lds_barrier();
   }
   __syncthreads();
@@ -287,34 +456,34 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void brgemm_bf16_dl_kernel(
                                             reinterpret_cast<float*>(lds), acc);
 }
 
-template <int BM, int BN, int WM, int WN, bool FULL, int KIND, bool PP>
+template <int BM, int BN, int WM, int WN, bool FULL, int KIND, int PP, int BKT>
 void launch_dl_k(const BrgemmParams& p, dim3 grid, hipStream_t stream) {
   const dim3 block(64 * WM * WN);
   if constexpr (KIND == TPP_BR_STRIDE) {
     if (p.aligned) {
-      hipLaunchKernelGGL((brgemm_bf16_dl_kernel<BM, BN, WM, WN, FULL, KIND, true, PP>), grid, block,
+      hipLaunchKernelGGL((brgemm_bf16_dl_kernel<BM, BN, WM, WN, FULL, KIND, true, PP, BKT>), grid, block,
                          0, stream, p);
       return;
     }
   }
-  hipLaunchKernelGGL((brgemm_bf16_dl_kernel<BM, BN, WM, WN, FULL, KIND, false, PP>), grid, block, 0,
+  hipLaunchKernelGGL((brgemm_bf16_dl_kernel<BM, BN, WM, WN, FULL, KIND, false, PP, BKT>), grid, block, 0,
                      stream, p);
 }
 
-template <int BM, int BN, int WM, int WN, bool PP = false>
+template <int BM, int BN, int WM, int WN, int PP = 0, int BKT = 32>
 void launch_dl(const BrgemmParams& p, bool full, dim3 grid, hipStream_t stream) {
   switch (p.kind) {
     case TPP_BR_STRIDE:
-      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_STRIDE, PP>(p, grid, stream)
-           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_STRIDE, PP>(p, grid, stream);
+      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_STRIDE, PP, BKT>(p, grid, stream)
+           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_STRIDE, PP, BKT>(p, grid, stream);
       break;
     case TPP_BR_OFFSET:
-      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_OFFSET, PP>(p, grid, stream)
-           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_OFFSET, PP>(p, grid, stream);
+      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_OFFSET, PP, BKT>(p, grid, stream)
+           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_OFFSET, PP, BKT>(p, grid, stream);
       break;
     default:
-      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_ADDRESS, PP>(p, grid, stream)
-           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_ADDRESS, PP>(p, grid, stream);
+      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_ADDRESS, PP, BKT>(p, grid, stream)
+           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_ADDRESS, PP, BKT>(p, grid, stream);
       break;
   }
 }
@@ -327,7 +496,10 @@ hipError_t launch_brgemm_dl(const BrgemmParams& p, int32_t id, bool full, dim3 g
     case K_BF16_DL_256x256: launch_dl<256, 256, 2, 4>(p, full, grid, stream); break;
     case K_BF16_DL_128x128: launch_dl<128, 128, 2, 2>(p, full, grid, stream); break;
     case K_BF16_DL_64x64: launch_dl<64, 64, 2, 2>(p, full, grid, stream); break;
-    case K_BF16_PP_256x256: launch_dl<256, 256, 2, 4, true>(p, full, grid, stream); break;
+    case K_BF16_PP_256x256: launch_dl<256, 256, 4, 2, 1>(p, full, grid, stream); break;
+    case K_BF16_DL64K_256x256: launch_dl<256, 256, 4, 2, 0, 64>(p, full, grid, stream); break;
+    case K_BF16_DL64K_256x128: launch_dl<256, 128, 4, 2, 0, 64>(p, full, grid, stream); break;
+    case K_BF16_DL64K_128x128: launch_dl<128, 128, 2, 2, 0, 64>(p, full, grid, stream); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

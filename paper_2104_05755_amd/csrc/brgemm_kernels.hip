@@ -689,11 +689,16 @@ constexpr KernelInfo kInfo[K_COUNT] = {
     {"bf16_128x128_w4_direct_lds", 128, 128},
     {"bf16_64x64_w4_direct_lds", 64, 64},
     {"bf16_256x256_w8_direct_lds_pingpong", 256, 256},
+    {"bf16_256x256_w8_direct_lds_bk64", 256, 256},
+    {"bf16_256x128_w8_direct_lds_bk64", 256, 128},
+    {"bf16_128x128_w4_direct_lds_bk64", 128, 128},
 };
 
 }  // namespace
 
 const char* kernel_name(int32_t id) { return (id >= 0 && id < K_COUNT) ? kInfo[id].name : "?"; }
+int kernel_tile_m(int32_t id) { return (id >= 0 && id < K_COUNT) ? kInfo[id].bm : 64; }
+int kernel_tile_n(int32_t id) { return (id >= 0 && id < K_COUNT) ? kInfo[id].bn : 64; }
 
 template <int BM, int BN, int WM, int WN, bool FULL, int KIND>
 void launch_vec_k(const BrgemmParams& p, dim3 grid, hipStream_t stream) {
@@ -744,6 +749,9 @@ hipError_t launch_brgemm(BrgemmParams& p, int32_t id, hipStream_t stream) {
     case K_BF16_DL_128x128:
     case K_BF16_DL_64x64:
     case K_BF16_PP_256x256:
+    case K_BF16_DL64K_256x256:
+    case K_BF16_DL64K_256x128:
+    case K_BF16_DL64K_128x128:
       return launch_brgemm_dl(p, id, full, grid, stream);
     case K_BF16_GENERIC:
       hipLaunchKernelGGL((brgemm_bf16_kernel<64, 64, 2, 2, true>), grid, block, 0, stream, p);

@@ -58,10 +58,15 @@ enum KernelId : int32_t {
   K_BF16_DL_128x128 = 6,  // direct global->LDS staging, 4 waves
   K_BF16_DL_64x64 = 7,    // direct global->LDS staging, 4 waves
   K_BF16_PP_256x256 = 8,  // direct global->LDS staging, 8 waves in two alternating groups
-  K_COUNT = 9
+  K_BF16_DL64K_256x256 = 9,  // direct global->LDS staging, 8 waves, 64-k stages (k % 64 == 0)
+  K_BF16_DL64K_256x128 = 10, // as 9, 256x128 tiles
+  K_BF16_DL64K_128x128 = 11, // as 9, 128x128 tiles, 4 waves (two workgroups per CU)
+  K_COUNT = 12
 };
 
 const char* kernel_name(int32_t id);
+int kernel_tile_m(int32_t id);   // tile rows of kernel instance id
+int kernel_tile_n(int32_t id);   // tile columns
 
 // Fill the tiling fields of p for kernel `id` and launch on `stream`.
 hipError_t launch_brgemm(BrgemmParams& p, int32_t id, hipStream_t stream);

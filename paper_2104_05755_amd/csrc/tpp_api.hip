@@ -58,6 +58,23 @@ std::vector<std::unique_ptr<tpp_brgemm_kernel_s>>& cache() {
 
 bool valid_dtype(int32_t t) { return t == TPP_DT_F32 || t == TPP_DT_BF16; }
 
+// The direct-LDS kernels address each operand as a wave-uniform base (the first instance block a
+// tile touches) plus a 32-bit per-lane byte offset: they apply when the grid steps are
+// non-negative and the byte span one BM x BN tile can reach from that base stays below 2^31.
+bool dl_offsets_fit(const tpp_brgemm_kernel_s& h, const tpp::BrgemmParams& p, int bm, int bn) {
+  const int64_t m = h.desc.m, n = h.desc.n, k = h.desc.k, lda = h.desc.lda, ldb = h.desc.ldb;
+  int64_t span_a, span_b;   // elements
+  if (p.fused) {
+    if (p.a_step_m < 0 || p.b_step_n < 0) return false;
+    span_a = (bm / m + 2) * p.a_step_m + m + k * lda;
+    span_b = (bn / n + 2) * p.b_step_n + n * ldb + k;
+  } else {
+    span_a = m + k * lda;
+    span_b = n * ldb + k;
+  }
+  return span_a < (int64_t(1) << 30) && span_b < (int64_t(1) << 30);   // bf16: 2 bytes each
+}
+
 // Kernel choice for one launch.  bf16 inputs take a 16-byte-load instance when the descriptor
 // and the grid keep every 8-element chunk contiguous and aligned (m, k, lda, ldb and all element
 // steps multiples of 8); the tile shape is the largest that still gives two tiles per compute
@@ -67,36 +84,43 @@ int32_t choose_kernel(const tpp_brgemm_kernel_s& h, const tpp::BrgemmParams& p) 
   bool vec = h.vec_ok;
   if (p.fused) vec = vec && (p.a_step_m % 8 == 0) && (p.b_step_n % 8 == 0);
   if (!vec) return tpp::K_BF16_GENERIC;
+  // Direct global->LDS instances when k is a multiple of 32 (64-k stages when it is a multiple of
+  // 64: whole 128-byte lines of B per load), except for pointer lists, whose scattered pair
+  // blocks stream better through registers; register staging otherwise.
+  const bool dl_kind = h.desc.k % 32 == 0 && h.desc.kind != TPP_BR_ADDRESS;
+  const bool bk64 = h.desc.k % 64 == 0;
   if (const char* env = std::getenv("TPP_FORCE_KERNEL")) {
     const int id = std::atoi(env);
-    const bool is_dl = id >= tpp::K_BF16_DL_256x256 && id <= tpp::K_BF16_PP_256x256;
+    const bool is_dl = id >= tpp::K_BF16_DL_256x256 && id != tpp::K_BF16_GENERIC &&
+                       id != tpp::K_F32_GENERIC;
+    const bool id_bk64 = id >= tpp::K_BF16_DL64K_256x256;
     if (id >= 0 && id < tpp::K_COUNT && id != tpp::K_BF16_GENERIC && id != tpp::K_F32_GENERIC &&
-        (!is_dl || h.desc.k % 32 == 0))
+        (!is_dl || (h.desc.k % (id_bk64 ? 64 : 32) == 0 &&
+                    dl_offsets_fit(h, p, tpp::kernel_tile_m(id), tpp::kernel_tile_n(id)))))
       return id;
   }
-  struct Cand { int32_t id; int bm, bn; };
-  // k a multiple of 32: the direct global->LDS instances (the 256x256 one in its ping-pong
-  // schedule), except for pointer lists, whose scattered pair blocks stream better through
-  // registers; otherwise register staging.
-  const bool dl = h.desc.k % 32 == 0 && h.desc.kind != TPP_BR_ADDRESS;
-  const Cand cands[] = {{dl ? tpp::K_BF16_PP_256x256 : tpp::K_BF16_256x256, 256, 256},
-                        {dl ? tpp::K_BF16_DL_128x128 : tpp::K_BF16_128x128, 128, 128},
-                        {dl ? tpp::K_BF16_DL_64x64 : tpp::K_BF16_64x64, 64, 64}};
+  struct Cand { int32_t dl_id, vec_id; int bm, bn; };
+  const Cand cands[] = {
+      {bk64 ? tpp::K_BF16_DL64K_256x256 : tpp::K_BF16_PP_256x256, tpp::K_BF16_256x256, 256, 256},
+      {bk64 ? tpp::K_BF16_DL64K_128x128 : tpp::K_BF16_DL_128x128, tpp::K_BF16_128x128, 128, 128},
+      {tpp::K_BF16_DL_64x64, tpp::K_BF16_64x64, 64, 64}};
   for (const Cand& c : cands) {
     // never pad a virtual C out to a larger tile (the 64x64 tile is the floor)
-    if ((c.bm > p.vrows && c.bm > 64) || (c.bn > p.vcols && c.bn > 64)) continue;
+    const bool last = c.bm == 64;
+    if (!last && (c.bm > p.vrows || c.bn > p.vcols)) continue;
     const int64_t tiles = p.groups * ((p.vrows + c.bm - 1) / c.bm) * ((p.vcols + c.bn - 1) / c.bn);
     // two tiles per compute unit: one workgroup's barriers and epilogue overlap the other's MFMAs
-    if (tiles >= 512) return c.id;
+    if (tiles >= 512 || last)
+      return (dl_kind && dl_offsets_fit(h, p, c.bm, c.bn)) ? c.dl_id : c.vec_id;
   }
-  return dl ? tpp::K_BF16_DL_64x64 : tpp::K_BF16_64x64;
+  return tpp::K_BF16_64x64;
 }
 
 tpp_status launch(const tpp_brgemm_kernel_s* h, tpp::BrgemmParams& p, void* stream) {
-  // the kernels count stages (pairs x k-steps of 64) and tiles in 32 bits
-  const int64_t ksteps = (h->desc.k + 63) / 64;
+  // the kernels count stages (pairs x k-steps of 32 or 64) and tiles in 32 bits
+  const int64_t ksteps = (h->desc.k + 31) / 32;
   if (p.kind != TPP_BR_ADDRESS && p.count * ksteps >= (1LL << 31))
-    return fail(TPP_ERR_UNSUPPORTED, "count * ceil(k/64) must be below 2^31");
+    return fail(TPP_ERR_UNSUPPORTED, "count * ceil(k/32) must be below 2^31");
   // Stride kind: every pair base is a + i*stride_a (+ an instance step), so 16-byte alignment of
   // all of them follows from the base pointers and the element steps, checked here once.
   if (p.kind == TPP_BR_STRIDE) {
