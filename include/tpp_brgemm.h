@@ -92,7 +92,11 @@ tpp_status tpp_brgemm_dispatch(const tpp_brgemm_desc* desc, tpp_brgemm_handle* o
  *   stride:  A_i = a + i * stride_a, B_i = b + i * stride_b
  *   offset:  A_i = a + offs_a[i],    B_i = b + offs_b[i]      (device int64 arrays, elements)
  *   address: A_i = ptrs_a[i],        B_i = ptrs_b[i]          (device arrays of device pointers)
- * Errors: INVALID_ARG for a NULL handle, count < 0, or a NULL pointer the call needs. */
+ * An fp32 call whose output is only a few 64 x 64 tiles splits the pair list over several
+ * workgroups; their partial sums go to a device work buffer the library keeps per GPU and per
+ * stream (as tpp_reduce) and are added in a fixed order, so results do not vary between runs.
+ * Errors: INVALID_ARG for a NULL handle, count < 0, or a NULL pointer the call needs; NO_MEMORY
+ * if that work buffer cannot be allocated. */
 tpp_status tpp_brgemm_execute_stride(tpp_brgemm_handle h, const void* a, const void* b, void* c,
                                      const float* bias, int64_t count, void* stream);
 tpp_status tpp_brgemm_execute_offset(tpp_brgemm_handle h, const void* a, const void* b,
@@ -151,10 +155,10 @@ tpp_status tpp_brgemm_describe(tpp_brgemm_handle h, char* buf, size_t len);
  *   f(x) = x into out_x when TPP_RED_X is set, f(x) = x*x into out_x2 when TPP_RED_X2 is set
  *   (both may be set: one pass, two outputs).  fold: SUM (from 0), MUL (from 1), MIN, MAX.
  *   Outputs are device fp32 arrays.  Arithmetic is fp32; the summation order is unspecified.
- * The library keeps a small device work buffer per GPU for partial results (allocated on first
- * use and kept until the process ends).  Exactly one of BY_COLS / BY_ROWS, and at least one of
- * X / X2, must be set.  Errors: INVALID_ARG for m, n <= 0, ld < m, bad flags, NULL pointers;
- * NO_MEMORY if the work buffer cannot be allocated. */
+ * Partial results go to a device work buffer the library keeps per GPU and per stream (allocated
+ * on first use, kept until the process ends; growing it synchronises the device).  Exactly one of
+ * BY_COLS / BY_ROWS, and at least one of X / X2, must be set.  Errors: INVALID_ARG for m, n <= 0,
+ * ld < m, bad flags, NULL pointers; NO_MEMORY if the work buffer cannot be allocated. */
 typedef enum { TPP_RED_SUM = 0, TPP_RED_MUL = 1, TPP_RED_MIN = 2, TPP_RED_MAX = 3 } tpp_reduce_op;
 enum {
   TPP_RED_BY_COLS = 1u << 0,

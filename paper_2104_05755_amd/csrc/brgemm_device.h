@@ -85,8 +85,9 @@ struct TileCoord {
   int32_t col0;     // first virtual column of the tile
 };
 
-__device__ __forceinline__ TileCoord decode_tile(const BrgemmParams& p, int bm, int bn) {
-  const int64_t t = xcd_tile(blockIdx.x, p.total_tiles);
+__device__ __forceinline__ TileCoord decode_tile_at(const BrgemmParams& p, int bm, int bn,
+                                                   int64_t bid) {
+  const int64_t t = xcd_tile(bid, p.total_tiles);
   const int64_t per_group = (int64_t)p.tiles_m * p.tiles_n;
   TileCoord tc;
   tc.g = t / per_group;
@@ -102,6 +103,10 @@ __device__ __forceinline__ TileCoord decode_tile(const BrgemmParams& p, int bm, 
   tc.row0 = (b0 + (int32_t)(tb % bh)) * bm;
   tc.col0 = (int32_t)(tb / bh) * bn;
   return tc;
+}
+
+__device__ __forceinline__ TileCoord decode_tile(const BrgemmParams& p, int bm, int bn) {
+  return decode_tile_at(p, bm, bn, blockIdx.x);
 }
 
 // Virtual row R -> element offset of that row inside A (relative to the instance's A base) and

@@ -88,9 +88,8 @@ __device__ __forceinline__ int swz_a(int k) {
     return ((k >> 1) & 1) << 2;
 }
 
-// SCHED: 0 = every wave loads, reads and multiplies in turn; 1 = ping-pong, memory half = fragment
-// reads + load issue; 2 = ping-pong, memory half = load issue only, the next stage's fragments
-// read during the MFMAs.
+// SCHED: 0 = every wave loads, reads and multiplies in turn; 1 = ping-pong (memory half = fragment
+// reads + load issue, compute half = MFMAs, two wave groups offset by a half-period).
 // BKT: k per stage, 32 or 64.  At 64 every stage reads whole 128-byte lines of the K-contiguous B
 // blocks (a column of a 64-k block is 128 bytes); at 32 each B column load covers half a line.
 template <int BM, int BN, int WAVES_M, int WAVES_N, bool FULL, int KIND, bool ALIGNED, int SCHED,
@@ -113,8 +112,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void brgemm_bf16_dl_kernel(
   // LDS ring slots: three 32-k stages in flight (a fifth slot, which fits, measured slower), or
   // one 64-k stage (two 64 KB slots for the 256x256 tile).
   constexpr int SLOTS = BKT == 64 ? 2 : 4;
-  static_assert(BKT == 32 || SCHED == 0 || SCHED == 3,
-                "the ping-pong schedules keep three stages in flight");
+  static_assert(BKT == 32 || SCHED == 0, "the ping-pong schedule keeps three stages in flight");
   static_assert(SLOTS * SLOT <= LDS_MAX, "ring fits in LDS");
   constexpr int LDS_BYTES = (SLOTS * SLOT > EP_BYTES) ? SLOTS * SLOT : EP_BYTES;
   static_assert(A_BYTES % (1024 * NW) == 0 && B_BYTES % (1024 * NW) == 0, "whole wave-loads");
@@ -314,44 +312,6 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void brgemm_bf16_dl_kernel(
       if (s + SLOTS - 1 < stages) issue();   // stage s + SLOTS - 1 refills the slot of s - 1
       compute(s % SLOTS);
     }
-  } else if constexpr (SCHED == 3) {
-    // As schedule 0, with stage s + SLOTS - 1's wave-loads spread between the MFMA groups of stage
-    // s (a group: one A fragment times all B fragments) instead of issued in a burst after the
-    // barrier, where every wave would stall at the load unit before its first MFMA; and with
-    // k-step kq + 1's fragments read while k-step kq's MFMAs run.  (Loop indices that select
-    // registers are compile-time constants after unrolling.)
-    constexpr int GROUPS = KQ * TM;
-    for (int32_t s = 0; s < stages; ++s) {
-      wait_loads(lmin(stages - 1 - s, SLOTS - 2));
-      lds_barrier();
-      const bool more = s + SLOTS - 1 < stages;
-      if (more) stage_begin();
-      const int sl = s % SLOTS;
-      bf16x8 af[2][TM], bfr[2][TN];
-      read_frags(sl, 0, af[0], bfr[0]);
-#pragma unroll
-      for (int kq = 0; kq < KQ; ++kq) {
-        const int cur = kq & 1;
-        if (kq + 1 < KQ) read_frags(sl, kq + 1, af[cur ^ 1], bfr[cur ^ 1]);
-#pragma unroll
-        for (int tm = 0; tm < TM; ++tm) {
-#pragma unroll
-          for (int tn = 0; tn < TN; ++tn)
-            acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][tm], bfr[cur][tn],
-                                                                  acc[tm][tn], 0, 0, 0);
-          const int grp = kq * TM + tm;
-#pragma unroll
-          for (int r = grp * LPS / GROUPS; r < (grp + 1) * LPS / GROUPS; ++r) {
-            if (more) {
-              __builtin_amdgcn_sched_barrier(0);
-              issue_load(r);
-              __builtin_amdgcn_sched_barrier(0);
-            }
-          }
-        }
-      }
-      if (more) stage_end();
-    }
   } else if constexpr (SCHED == 1) {
     // Ping-pong: waves 0-3 (one per SIMD) lead, waves 4-7 lag by one half-period.  Each stage is
     // a memory half (fragment reads of the stage, global->LDS issue of stage s + SLOTS - 1) and a compute
@@ -400,52 +360,6 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void brgemm_bf16_dl_kernel(
       if (lead && s + 1 < stages) wait_loads(later);
       lds_barrier();
     }
-    if (lead) lds_barrier();
-  } else {
-    // Ping-pong with the fragment reads moved into the compute half: stage t's compute half runs
-    // its MFMAs on fragments already in registers and reads stage t + 1's fragments from LDS
-    // meanwhile; the memory half only issues stage t + SLOTS - 1's global->LDS loads.  Waves 0-3
-    // lead, waves 4-7 lag by one half-period:
-    //   barrier j:  leading waves end L(j/2) (j even) or C(j/2) (j odd);
-    //               lagging waves end C(j/2 - 1) (j even, the first one is the offset barrier) or
-    //               L(j/2) (j odd).
-    // Stage t + 1 is read during C(t), so it must have landed before barrier 2t, the one that
-    // opens the leading waves' C(t): leading waves wait at the end of L(t), lagging ones at the end
-    // of C(t - 1) (each with its loads of later stages still in flight).  The slot refilled in L(t)
-    // held stage t - 1, whose last reads (lagging C(t - 2)) ended before barrier 2t - 2.
-    static_assert(NW == 8, "two groups of four waves");
-    const bool lead = wave < 4;
-    bf16x8 af[2][KQ][TM], bfr[2][KQ][TN];
-    wait_loads(lmin(stages - 1, SLOTS - 2));   // stage 0 landed everywhere ...
-    lds_barrier();
-#pragma unroll
-    for (int kq = 0; kq < KQ; ++kq) read_frags(0, kq, af[0][kq], bfr[0][kq]);   // ... and read
-    if (!lead) {
-      if (stages > 1) wait_loads(lmin(stages - 2, SLOTS - 3));   // stage 1, before barrier 0
-      lds_barrier();
-    }
-    // Two iterations per trip so that the fragment buffers are indexed by constants.
-    auto step = [&](int32_t s, bf16x8 (&fa)[KQ][TM], bf16x8 (&fb)[KQ][TN],
-                    bf16x8 (&na)[KQ][TM], bf16x8 (&nb)[KQ][TN]) {
-      // L(s)
-      if (s + SLOTS - 1 < stages) issue();   // stage s + SLOTS - 1
-      if (lead && s + 1 < stages) wait_loads(lmin(stages - 2 - s, SLOTS - 2));
-      lds_barrier();
-      // C(s)
-#pragma unroll
-      for (int kq = 0; kq < KQ; ++kq) {
-        if (s + 1 < stages) read_frags((s + 1) % SLOTS, kq, na[kq], nb[kq]);
-        mfmas(fa[kq], fb[kq]);
-      }
-      if (!lead && s + 2 < stages) wait_loads(lmin(stages - 3 - s, SLOTS - 3));
-      lds_barrier();
-    };
-    int32_t s = 0;
-    for (; s + 1 < stages; s += 2) {
-      step(s, af[0], bfr[0], af[1], bfr[1]);
-      step(s + 1, af[1], bfr[1], af[0], bfr[0]);
-    }
-    if (s < stages) step(s, af[0], bfr[0], af[1], bfr[1]);
     if (lead) lds_barrier();
   }
   __syncthreads();

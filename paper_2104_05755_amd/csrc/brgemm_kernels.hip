@@ -611,10 +611,16 @@ __global__ __launch_bounds__(NT) void brgemm_f32_kernel(BrgemmParams p) {
   __shared__ float Bs[F_BN * F_BROW];
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int wm = wave & 1, wn = wave >> 1;
-  const TileCoord tc = decode_tile(p, F_BM, F_BN);
+  // With a split, workgroup bid takes chunk bid % split of tile bid / split's pair list.
+  const int32_t split = p.split > 1 ? p.split : 1;
+  const int64_t tile_bid = (int64_t)blockIdx.x / split;
+  const int32_t chunk = (int32_t)((int64_t)blockIdx.x - tile_bid * split);
+  const TileCoord tc = decode_tile_at(p, F_BM, F_BN, tile_bid);
   const Instance in = instance_of(p, tc.g);
+  const int64_t pair_lo = in.npairs * chunk / split;
+  const int64_t pair_hi = in.npairs * (chunk + 1) / split;
   const int32_t ksteps = (p.k + F_BK - 1) / F_BK;
-  const int64_t stages = in.npairs * ksteps;
+  const int64_t stages = (pair_hi - pair_lo) * ksteps;
 
   // A element e = t + 256*j: row t%64 (fixed), k = t/64 + 4*j.
   const int a_r = t & 63, a_k0 = t >> 6;
@@ -639,7 +645,7 @@ __global__ __launch_bounds__(NT) void brgemm_f32_kernel(BrgemmParams p) {
     const int32_t kk = (int32_t)(s - i * ksteps) * F_BK;
     const float* pa;
     const float* pb;
-    pair_bases<float>(p, in, i, pa, pb);
+    pair_bases<float>(p, in, pair_lo + i, pa, pb);
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int32_t ka = kk + a_k0 + 4 * j;
@@ -665,12 +671,52 @@ __global__ __launch_bounds__(NT) void brgemm_f32_kernel(BrgemmParams p) {
     }
     __syncthreads();
   }
+  if (split > 1) {
+    // raw partial sums: tile-local column-major 64 x 64 block of this (tile, chunk)
+    float* w = p.ws + ((size_t)tile_bid * split + chunk) * (F_BM * F_BN);
+    const int c_local = wn * 32 + (lane & 31);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int r_local = wm * 32 + q * 8 + (lane >> 5) * 4;
+      gst<f32x4>(w + c_local * F_BM + r_local,
+                 (f32x4){acc[q * 4 + 0], acc[q * 4 + 1], acc[q * 4 + 2], acc[q * 4 + 3]});
+    }
+    return;
+  }
   const int32_t C = tc.col0 + wn * 32 + (lane & 31);
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const int32_t R0 = tc.row0 + wm * 32 + q * 8 + (lane >> 5) * 4;
     const float v[4] = {acc[q * 4 + 0], acc[q * 4 + 1], acc[q * 4 + 2], acc[q * 4 + 3]};
     store_group<true>(p, in, R0, C, v);
+  }
+}
+
+// Finishing step of a split fp32 launch: one workgroup per tile sums the split partial tiles in
+// chunk order (so the result does not depend on timing) and applies beta * C, bias, activation
+// and the store, exactly as the unsplit kernel's epilogue.
+__global__ __launch_bounds__(NT) void brgemm_f32_split_finish(BrgemmParams p) {
+  const int t = threadIdx.x;
+  const int64_t tile_bid = blockIdx.x;
+  const TileCoord tc = decode_tile_at(p, F_BM, F_BN, tile_bid);
+  const Instance in = instance_of(p, tc.g);
+  const int c_local = t & 63, r0 = (t >> 6) * 16;   // 16 consecutive rows of one column
+  float sum[16];
+#pragma unroll
+  for (int e = 0; e < 16; ++e) sum[e] = 0.0f;
+  const float* w = p.ws + (size_t)tile_bid * p.split * (F_BM * F_BN) + c_local * F_BM + r0;
+  for (int32_t ch = 0; ch < p.split; ++ch) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const f32x4 v = gld<f32x4>(w + (size_t)ch * (F_BM * F_BN) + q * 4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) sum[q * 4 + e] += v[e];
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const float v[4] = {sum[q * 4 + 0], sum[q * 4 + 1], sum[q * 4 + 2], sum[q * 4 + 3]};
+    store_group<true>(p, in, tc.row0 + r0 + q * 4, tc.col0 + c_local, v);
   }
 }
 
@@ -757,10 +803,20 @@ hipError_t launch_brgemm(BrgemmParams& p, int32_t id, hipStream_t stream) {
       hipLaunchKernelGGL((brgemm_bf16_kernel<64, 64, 2, 2, true>), grid, block, 0, stream, p);
       break;
     default:
-      hipLaunchKernelGGL(brgemm_f32_kernel, grid, block, 0, stream, p);
+      if (p.split > 1) {
+        hipLaunchKernelGGL(brgemm_f32_kernel, dim3((unsigned)(p.total_tiles * p.split)), block, 0,
+                           stream, p);
+        hipLaunchKernelGGL(brgemm_f32_split_finish, grid, block, 0, stream, p);
+      } else {
+        hipLaunchKernelGGL(brgemm_f32_kernel, grid, block, 0, stream, p);
+      }
       break;
   }
   return hipGetLastError();
+}
+
+int64_t f32_split_ws_floats(int32_t split, int64_t total_tiles) {
+  return (int64_t)split * total_tiles * F_BM * F_BN;
 }
 
 }  // namespace tpp

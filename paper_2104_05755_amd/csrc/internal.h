@@ -45,6 +45,11 @@ struct BrgemmParams {
   int32_t tiles_m, tiles_n;  // tiles per group
   int64_t groups;            // 1 (strided) or G (explicit)
   int64_t total_tiles;
+  // Split over the pair list (fp32 kernel, grids too small to fill the GPU): split > 1 chunks of
+  // each instance's pairs are reduced by separate workgroups into ws (split x total_tiles tiles of
+  // 64 x 64 fp32), then summed in chunk order by a finishing kernel that applies the epilogue.
+  int32_t split;             // 1: no split
+  float* ws;
 };
 
 // Kernel instances of the bf16 family (tile shape + load path) and the fp32 kernel.
@@ -66,6 +71,8 @@ enum KernelId : int32_t {
 
 const char* kernel_name(int32_t id);
 int kernel_tile_m(int32_t id);   // tile rows of kernel instance id
+// fp32 workspace floats a split launch of the fp32 kernel needs (split x tiles x 64 x 64).
+int64_t f32_split_ws_floats(int32_t split, int64_t total_tiles);
 int kernel_tile_n(int32_t id);   // tile columns
 
 // Fill the tiling fields of p for kernel `id` and launch on `stream`.

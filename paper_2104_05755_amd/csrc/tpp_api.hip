@@ -9,7 +9,9 @@
 #include <cstdio>
 #include <cstring>
 #include <memory>
+#include <map>
 #include <mutex>
+#include <tuple>
 #include <string>
 #include <vector>
 
@@ -84,11 +86,12 @@ int32_t choose_kernel(const tpp_brgemm_kernel_s& h, const tpp::BrgemmParams& p) 
   bool vec = h.vec_ok;
   if (p.fused) vec = vec && (p.a_step_m % 8 == 0) && (p.b_step_n % 8 == 0);
   if (!vec) return tpp::K_BF16_GENERIC;
-  // Direct global->LDS instances when k is a multiple of 32 (64-k stages when it is a multiple of
-  // 64: whole 128-byte lines of B per load), except for pointer lists, whose scattered pair
-  // blocks stream better through registers; register staging otherwise.
-  const bool dl_kind = h.desc.k % 32 == 0 && h.desc.kind != TPP_BR_ADDRESS;
+  // Direct buffer->LDS instances when k is a multiple of 32, with 64-k stages when it is a
+  // multiple of 64 (whole 128-byte lines of B per load); pointer lists only with 64-k stages
+  // (measured faster than register staging there, slower with 32-k stages); register staging
+  // otherwise.
   const bool bk64 = h.desc.k % 64 == 0;
+  const bool dl_kind = h.desc.k % 32 == 0 && (h.desc.kind != TPP_BR_ADDRESS || bk64);
   if (const char* env = std::getenv("TPP_FORCE_KERNEL")) {
     const int id = std::atoi(env);
     const bool is_dl = id >= tpp::K_BF16_DL_256x256 && id != tpp::K_BF16_GENERIC &&
@@ -116,6 +119,39 @@ int32_t choose_kernel(const tpp_brgemm_kernel_s& h, const tpp::BrgemmParams& p) 
   return tpp::K_BF16_64x64;
 }
 
+// Device work buffers for partial results, one per (device, stream, purpose) so that calls on
+// different streams never share one; allocated on first use, grown when a call needs more (after
+// a device synchronisation, since queued work may still use the old one), kept until exit.
+enum WorkPurpose { WORK_REDUCE = 0, WORK_SPLIT = 1 };
+struct WorkBuffer {
+  float* ptr = nullptr;
+  int64_t floats = 0;
+};
+std::mutex g_work_mu;
+std::map<std::tuple<int, void*, int>, WorkBuffer> g_work;
+
+tpp_status work_buffer(int purpose, void* stream, int64_t floats, float** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(TPP_ERR_HIP, "hipGetDevice failed");
+  std::lock_guard<std::mutex> lock(g_work_mu);
+  WorkBuffer& wb = g_work[std::make_tuple(dev, stream, purpose)];
+  if (wb.floats < floats) {
+    if (wb.ptr) {
+      if (hipDeviceSynchronize() != hipSuccess || hipFree(wb.ptr) != hipSuccess)
+        return fail(TPP_ERR_HIP, "could not release the old work buffer");
+      wb.ptr = nullptr;
+      wb.floats = 0;
+    }
+    void* ptr = nullptr;
+    if (hipMalloc(&ptr, (size_t)floats * sizeof(float)) != hipSuccess)
+      return fail(TPP_ERR_NO_MEMORY, "work buffer of %lld floats", (long long)floats);
+    wb.ptr = static_cast<float*>(ptr);
+    wb.floats = floats;
+  }
+  *out = wb.ptr;
+  return TPP_OK;
+}
+
 tpp_status launch(const tpp_brgemm_kernel_s* h, tpp::BrgemmParams& p, void* stream) {
   // the kernels count stages (pairs x k-steps of 32 or 64) and tiles in 32 bits
   const int64_t ksteps = (h->desc.k + 31) / 32;
@@ -130,9 +166,27 @@ tpp_status launch(const tpp_brgemm_kernel_s* h, tpp::BrgemmParams& p, void* stre
                 (p.fused || p.grid_form || (!p.a_off && !p.b_off));
   }
   const int32_t id = choose_kernel(*h, p);
+  p.split = 1;
+  p.ws = nullptr;
+  if (id == tpp::K_F32_GENERIC && p.kind != TPP_BR_ADDRESS && p.count >= 2) {
+    // A grid of few 64 x 64 tiles leaves most of the GPU idle while each workgroup walks the
+    // whole pair list: split the list into chunks reduced by separate workgroups (about 256 in
+    // all) and sum the chunks in a finishing kernel.
+    const int64_t tiles = p.groups * ((p.vrows + 63) / 64) * ((p.vcols + 63) / 64);
+    if (tiles < 128) {
+      int64_t split = 256 / tiles;
+      if (split > p.count) split = p.count;
+      if (split > 1) {
+        p.split = (int32_t)split;
+        const tpp_status st =
+            work_buffer(WORK_SPLIT, stream, tpp::f32_split_ws_floats(p.split, tiles), &p.ws);
+        if (st != TPP_OK) return st;
+      }
+    }
+  }
   if (std::getenv("TPP_LOG"))
-    std::fprintf(stderr, "[tpp] %s: G=%lld vrows=%d vcols=%d fused=%d -> %s\n", h->name,
-                 (long long)p.groups, p.vrows, p.vcols, p.fused, tpp::kernel_name(id));
+    std::fprintf(stderr, "[tpp] %s: G=%lld vrows=%d vcols=%d fused=%d split=%d -> %s\n", h->name,
+                 (long long)p.groups, p.vrows, p.vcols, p.fused, p.split, tpp::kernel_name(id));
   const hipError_t e = tpp::launch_brgemm(p, id, static_cast<hipStream_t>(stream));
   if (e != hipSuccess)
     return fail(TPP_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
@@ -172,13 +226,6 @@ tpp_status run_single(const tpp_brgemm_kernel_s* h, tpp::BrgemmParams& p, void* 
   p.vcols = p.n;
   return launch(h, p, stream);
 }
-
-struct WorkBuffer {
-  float* ptr = nullptr;
-  int64_t floats = 0;
-};
-std::mutex g_work_mu;
-std::vector<WorkBuffer> g_work;   // one per device
 
 }  // namespace
 
@@ -390,26 +437,8 @@ tpp_status tpp_reduce(int32_t m, int32_t n, int64_t ld, int32_t in_type, const v
   const int64_t need = tpp::reduce_work_floats(p);
   float* work = nullptr;
   if (need > 0) {
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess) return fail(TPP_ERR_HIP, "hipGetDevice failed");
-    std::lock_guard<std::mutex> lock(g_work_mu);
-    if ((int)g_work.size() <= dev) g_work.resize(dev + 1);
-    WorkBuffer& wb = g_work[dev];
-    if (wb.floats < need) {
-      // Growing waits for the device: the old buffer may still be read by queued reductions.
-      if (wb.ptr) {
-        if (hipDeviceSynchronize() != hipSuccess || hipFree(wb.ptr) != hipSuccess)
-          return fail(TPP_ERR_HIP, "could not release the old work buffer");
-        wb.ptr = nullptr;
-        wb.floats = 0;
-      }
-      void* ptr = nullptr;
-      if (hipMalloc(&ptr, (size_t)need * sizeof(float)) != hipSuccess)
-        return fail(TPP_ERR_NO_MEMORY, "work buffer of %lld floats", (long long)need);
-      wb.ptr = static_cast<float*>(ptr);
-      wb.floats = need;
-    }
-    work = wb.ptr;
+    const tpp_status st = work_buffer(WORK_REDUCE, stream, need, &work);
+    if (st != TPP_OK) return st;
   }
   const hipError_t e = tpp::launch_reduce(p, work, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(TPP_ERR_HIP, "reduce launch failed: %s", hipGetErrorString(e));

@@ -140,6 +140,17 @@ def test_three_variants_bit_identical_on_gpu():
     assert np.array_equal(outs[0], outs[1]) and np.array_equal(outs[0], outs[2])
 
 
+def test_fp32_split_pair_list_is_deterministic():
+    """A one-tile fp32 call splits its pair list over workgroups and adds the chunk sums in a fixed
+    order: repeated calls give identical bits, within the fp32 bar of the oracle."""
+    wl = wk.fp32_single()
+    first = run_gpu(wl)["c"]
+    again = run_gpu(wl)["c"]
+    assert np.array_equal(first.view(np.uint32), again.view(np.uint32))
+    ref, _ = run_oracle(wl)
+    check_close(first, ref, wl.calls[0], "fp32 split")
+
+
 def test_single_call_entry_points_match_batched():
     """The paper-shaped single calls (stride / offset / address) equal one-instance batches."""
     import paper_2104_05755_amd as tpp
