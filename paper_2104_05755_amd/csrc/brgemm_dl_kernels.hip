@@ -93,8 +93,10 @@ __device__ __forceinline__ int swz_a(int k) {
 // BKT: k per stage, 32 or 64.  At 64 every stage reads whole 128-byte lines of the K-contiguous B
 // blocks (a column of a 64-k block is 128 bytes); at 32 each B column load covers half a line.
 template <int BM, int BN, int WAVES_M, int WAVES_N, bool FULL, int KIND, bool ALIGNED, int SCHED,
-          int BKT>
-__global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void brgemm_bf16_dl_kernel(BrgemmParams p) {
+          int BKT, int SLOTS_T>
+// Four-wave instances run two workgroups per CU, i.e. two waves per SIMD: at most 256 registers.
+__global__ __launch_bounds__(64 * WAVES_M * WAVES_N, (WAVES_M * WAVES_N == 4) ? 2 : 1)
+void brgemm_bf16_dl_kernel(BrgemmParams p) {
   constexpr int DL_BK = BKT;
   static_assert(BKT == 32 || BKT == 64, "stage depth");
   constexpr int NW = WAVES_M * WAVES_N;
@@ -111,7 +113,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void brgemm_bf16_dl_kernel(
   constexpr int EP_BYTES = NW * 32 * (WTM + 4) * 4;
   // LDS ring slots: three 32-k stages in flight (a fifth slot, which fits, measured slower), or
   // one 64-k stage (two 64 KB slots for the 256x256 tile).
-  constexpr int SLOTS = BKT == 64 ? 2 : 4;
+  constexpr int SLOTS = SLOTS_T > 0 ? SLOTS_T : (BKT == 64 ? 2 : 4);
   static_assert(BKT == 32 || SCHED == 0, "the ping-pong schedule keeps three stages in flight");
   static_assert(SLOTS * SLOT <= LDS_MAX, "ring fits in LDS");
   constexpr int LDS_BYTES = (SLOTS * SLOT > EP_BYTES) ? SLOTS * SLOT : EP_BYTES;
@@ -370,34 +372,34 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void brgemm_bf16_dl_kernel(
                                             reinterpret_cast<float*>(lds), acc);
 }
 
-template <int BM, int BN, int WM, int WN, bool FULL, int KIND, int PP, int BKT>
+template <int BM, int BN, int WM, int WN, bool FULL, int KIND, int PP, int BKT, int SL>
 void launch_dl_k(const BrgemmParams& p, dim3 grid, hipStream_t stream) {
   const dim3 block(64 * WM * WN);
   if constexpr (KIND == TPP_BR_STRIDE) {
     if (p.aligned) {
-      hipLaunchKernelGGL((brgemm_bf16_dl_kernel<BM, BN, WM, WN, FULL, KIND, true, PP, BKT>), grid, block,
+      hipLaunchKernelGGL((brgemm_bf16_dl_kernel<BM, BN, WM, WN, FULL, KIND, true, PP, BKT, SL>), grid, block,
                          0, stream, p);
       return;
     }
   }
-  hipLaunchKernelGGL((brgemm_bf16_dl_kernel<BM, BN, WM, WN, FULL, KIND, false, PP, BKT>), grid, block, 0,
+  hipLaunchKernelGGL((brgemm_bf16_dl_kernel<BM, BN, WM, WN, FULL, KIND, false, PP, BKT, SL>), grid, block, 0,
                      stream, p);
 }
 
-template <int BM, int BN, int WM, int WN, int PP = 0, int BKT = 32>
+template <int BM, int BN, int WM, int WN, int PP = 0, int BKT = 32, int SL = 0>
 void launch_dl(const BrgemmParams& p, bool full, dim3 grid, hipStream_t stream) {
   switch (p.kind) {
     case TPP_BR_STRIDE:
-      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_STRIDE, PP, BKT>(p, grid, stream)
-           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_STRIDE, PP, BKT>(p, grid, stream);
+      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_STRIDE, PP, BKT, SL>(p, grid, stream)
+           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_STRIDE, PP, BKT, SL>(p, grid, stream);
       break;
     case TPP_BR_OFFSET:
-      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_OFFSET, PP, BKT>(p, grid, stream)
-           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_OFFSET, PP, BKT>(p, grid, stream);
+      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_OFFSET, PP, BKT, SL>(p, grid, stream)
+           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_OFFSET, PP, BKT, SL>(p, grid, stream);
       break;
     default:
-      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_ADDRESS, PP, BKT>(p, grid, stream)
-           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_ADDRESS, PP, BKT>(p, grid, stream);
+      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_ADDRESS, PP, BKT, SL>(p, grid, stream)
+           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_ADDRESS, PP, BKT, SL>(p, grid, stream);
       break;
   }
 }
@@ -412,7 +414,6 @@ hipError_t launch_brgemm_dl(const BrgemmParams& p, int32_t id, bool full, dim3 g
     case K_BF16_DL_64x64: launch_dl<64, 64, 2, 2>(p, full, grid, stream); break;
     case K_BF16_PP_256x256: launch_dl<256, 256, 4, 2, 1>(p, full, grid, stream); break;
     case K_BF16_DL64K_256x256: launch_dl<256, 256, 4, 2, 0, 64>(p, full, grid, stream); break;
-    case K_BF16_DL64K_256x128: launch_dl<256, 128, 4, 2, 0, 64>(p, full, grid, stream); break;
     case K_BF16_DL64K_128x128: launch_dl<128, 128, 2, 2, 0, 64>(p, full, grid, stream); break;
     default: return hipErrorInvalidValue;
   }

@@ -736,7 +736,6 @@ constexpr KernelInfo kInfo[K_COUNT] = {
     {"bf16_64x64_w4_direct_lds", 64, 64},
     {"bf16_256x256_w8_direct_lds_pingpong", 256, 256},
     {"bf16_256x256_w8_direct_lds_bk64", 256, 256},
-    {"bf16_256x128_w8_direct_lds_bk64", 256, 128},
     {"bf16_128x128_w4_direct_lds_bk64", 128, 128},
 };
 
@@ -796,7 +795,6 @@ hipError_t launch_brgemm(BrgemmParams& p, int32_t id, hipStream_t stream) {
     case K_BF16_DL_64x64:
     case K_BF16_PP_256x256:
     case K_BF16_DL64K_256x256:
-    case K_BF16_DL64K_256x128:
     case K_BF16_DL64K_128x128:
       return launch_brgemm_dl(p, id, full, grid, stream);
     case K_BF16_GENERIC:

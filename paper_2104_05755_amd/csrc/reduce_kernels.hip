@@ -12,7 +12,7 @@
 //     LDS.  Column ranges of different workgroups meet in a second, tiny pass.
 // Arithmetic is fp32.  When a shape needs several partial results per output (row segments or
 // column ranges), they go to a device work buffer and a second kernel folds them in a fixed
-// order, so results do not depend on scheduling.
+// order (which depends only on the shape), so results do not depend on scheduling.
 #include <hip/hip_runtime.h>
 
 #include <math.h>
@@ -134,20 +134,48 @@ __global__ __launch_bounds__(RT) void reduce_cols_kernel(ReduceParams p, int32_t
 #pragma unroll
   for (int e = 0; e < V; ++e) ax[e] = ax2[e] = fold_identity<OP>();
   const bool full = r0 + V <= p.m;
-  for (int32_t c = c_lo + tc; c < c_hi; c += TC) {
+  auto load_vec = [&](int32_t c, float (&x)[V]) {
     const int64_t base = (int64_t)c * p.ld + r0;
-    float x[V];
     if (V > 1 && full) {
       loadv<BF16, V>(p.in, base, x);
     } else {
 #pragma unroll
       for (int e = 0; e < V; ++e) x[e] = (r0 + e < p.m) ? load1<BF16>(p.in, base + e) : 0.0f;
     }
+  };
+  // Four columns per trip, all loads issued before any is folded, into four accumulator sets
+  // (combined in a fixed order below): four loads in flight per thread instead of one.
+  float bx[4][V], bx2[4][V];
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+#pragma unroll
+    for (int e = 0; e < V; ++e) bx[u][e] = bx2[u][e] = fold_identity<OP>();
+  int32_t c = c_lo + tc;
+  for (; c + 3 * TC < c_hi; c += 4 * TC) {
+    float x[4][V];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) load_vec(c + u * TC, x[u]);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int e = 0; e < V; ++e) {
+        bx[u][e] = fold<OP>(bx[u][e], x[u][e]);
+        bx2[u][e] = fold<OP>(bx2[u][e], x[u][e] * x[u][e]);
+      }
+  }
+  for (; c < c_hi; c += TC) {
+    float x[V];
+    load_vec(c, x);
 #pragma unroll
     for (int e = 0; e < V; ++e) {
-      ax[e] = fold<OP>(ax[e], x[e]);
-      ax2[e] = fold<OP>(ax2[e], x[e] * x[e]);
+      bx[0][e] = fold<OP>(bx[0][e], x[e]);
+      bx2[0][e] = fold<OP>(bx2[0][e], x[e] * x[e]);
     }
+  }
+#pragma unroll
+  for (int e = 0; e < V; ++e) {
+    ax[e] = fold<OP>(fold<OP>(bx[0][e], bx[1][e]), fold<OP>(bx[2][e], bx[3][e]));
+    ax2[e] = fold<OP>(fold<OP>(bx2[0][e], bx2[1][e]), fold<OP>(bx2[2][e], bx2[3][e]));
   }
 #pragma unroll
   for (int e = 0; e < V; ++e) {
@@ -197,6 +225,50 @@ __global__ __launch_bounds__(RT) void reduce_combine_kernel(const float* work, i
   }
 }
 
+// Second pass for many outputs: workgroup b folds outputs [64 b, 64 b + 64), lane = output, so
+// every partial load is a coalesced 256-byte row; wave w folds partials s = w, w + 4, ... in
+// increasing s, and the four wave results are folded in wave order.
+template <int OP>
+__global__ __launch_bounds__(RT) void reduce_combine_wide_kernel(const float* work, int32_t n_out,
+                                                                 int32_t nseg, uint32_t flags,
+                                                                 float* out_x, float* out_x2) {
+  __shared__ float sx[4][64], sx2[4][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t o = (int64_t)blockIdx.x * 64 + lane;
+  float fx = fold_identity<OP>(), fx2 = fold_identity<OP>();
+  if (o < n_out) {
+    const float* px = work + o;
+    const float* px2 = work + (int64_t)nseg * n_out + o;
+    int32_t s = w;
+    for (; s + 12 < nseg; s += 16) {   // four partials of each half in flight
+      float a[4], b[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        a[u] = px[(int64_t)(s + 4 * u) * n_out];
+        b[u] = px2[(int64_t)(s + 4 * u) * n_out];
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        fx = fold<OP>(fx, a[u]);
+        fx2 = fold<OP>(fx2, b[u]);
+      }
+    }
+    for (; s < nseg; s += 4) {
+      fx = fold<OP>(fx, px[(int64_t)s * n_out]);
+      fx2 = fold<OP>(fx2, px2[(int64_t)s * n_out]);
+    }
+  }
+  sx[w][lane] = fx;
+  sx2[w][lane] = fx2;
+  __syncthreads();
+  if (w == 0 && o < n_out) {
+    fx = fold<OP>(fold<OP>(sx[0][lane], sx[1][lane]), fold<OP>(sx[2][lane], sx[3][lane]));
+    fx2 = fold<OP>(fold<OP>(sx2[0][lane], sx2[1][lane]), fold<OP>(sx2[2][lane], sx2[3][lane]));
+    if (flags & TPP_RED_X) out_x[o] = fx;
+    if (flags & TPP_RED_X2) out_x2[o] = fx2;
+  }
+}
+
 struct Plan {
   bool by_cols;
   int v;          // elements per load (1, 4 or 8)
@@ -224,17 +296,20 @@ Plan make_plan(const ReduceParams& p) {
     pl.nseg = (int32_t)((p.m + pl.seg - 1) / pl.seg);
     pl.blocks = ((int64_t)p.n * pl.nseg + (RT / 64) - 1) / (RT / 64);
   } else {
+    // Up to 64 row vectors per workgroup (at least four column lanes): a tall input gets more
+    // row blocks rather than more column ranges, which keeps the partials per output few.
     const int64_t vecs = (p.m + pl.v - 1) / pl.v;
     int32_t tr = 1;
-    while (tr < vecs && tr < RT) tr <<= 1;
+    while (tr < vecs && tr < RT / 4) tr <<= 1;
     pl.tr = tr;
     pl.nrb = (int32_t)((p.m + (int64_t)tr * pl.v - 1) / ((int64_t)tr * pl.v));
     const int32_t tc = RT / tr;
-    // aim for ~512 workgroups, each walking at least 4 columns per column lane
-    int64_t nseg = (512 + pl.nrb - 1) / pl.nrb;
-    const int64_t max_seg = (p.n + 4LL * tc - 1) / (4LL * tc);
+    // aim for ~1024 workgroups (four per CU), each walking at least 8 columns per column lane,
+    // and at most 512 partial results per output for the combine pass
+    int64_t nseg = (1024 + pl.nrb - 1) / pl.nrb;
+    const int64_t max_seg = (p.n + 8LL * tc - 1) / (8LL * tc);
     nseg = nseg < 1 ? 1 : (nseg > max_seg ? max_seg : nseg);
-    if (nseg > 256) nseg = 256;
+    if (nseg > 512) nseg = 512;
     pl.seg = (int32_t)((p.n + nseg - 1) / nseg);
     pl.nseg = (int32_t)((p.n + pl.seg - 1) / pl.seg);
     pl.blocks = (int64_t)pl.nrb * pl.nseg;
@@ -263,8 +338,12 @@ void launch_op(const ReduceParams& p, const Plan& pl, float* work, hipStream_t s
   }
   if (pl.nseg > 1) {
     const int32_t n_out = pl.by_cols ? p.m : p.n;
-    hipLaunchKernelGGL(reduce_combine_kernel<OP>, dim3((unsigned)((n_out + 3) / 4)),
-                       dim3(RT), 0, stream, work, n_out, pl.nseg, p.flags, p.out_x, p.out_x2);
+    if (n_out >= 512)   // many outputs: coalesced over outputs
+      hipLaunchKernelGGL(reduce_combine_wide_kernel<OP>, dim3((unsigned)((n_out + 63) / 64)),
+                         dim3(RT), 0, stream, work, n_out, pl.nseg, p.flags, p.out_x, p.out_x2);
+    else                // few outputs: one wavefront per output, lanes over the partials
+      hipLaunchKernelGGL(reduce_combine_kernel<OP>, dim3((unsigned)((n_out + 3) / 4)),
+                         dim3(RT), 0, stream, work, n_out, pl.nseg, p.flags, p.out_x, p.out_x2);
   }
 }
 

@@ -54,8 +54,11 @@ def check(got, ref, absdata, op, by, what):
         assert np.all(np.abs(got - ref) <= rtol * np.abs(ref) + 1e-30), what
 
 
+# (1024, 4096) by columns and (8192, 1024) by rows fold over 100+ and 4 partial results per
+# output in the many-outputs combine pass.
 SHAPES = [(1, 1, 1), (3, 5, 3), (64, 100, 64), (64, 100, 67), (37, 513, 40), (1000, 7, 1000),
-          (100000, 3, 100003), (8, 200000, 8), (257, 1031, 264), (4096, 64, 4096)]
+          (100000, 3, 100003), (8, 200000, 8), (257, 1031, 264), (4096, 64, 4096),
+          (1024, 4096, 1024), (8192, 1024, 8192)]
 
 
 @pytest.mark.parametrize("m,n,ld", SHAPES)
