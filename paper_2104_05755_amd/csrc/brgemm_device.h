@@ -361,35 +361,45 @@ __device__ __forceinline__ void epilogue_bf16_act(const BrgemmParams& p, const I
   const bool has_bias = (p.flags & TPP_EPI_BIAS) != 0;
   const int half = lane >> 5;                  // rows 4*half.. of each 8-row group
   // Bias of the lane's rows, all issued before any is used: for group tm and q, the four rows
-  // 32 tm + 8 q + 4 half + e (an 8-row chunk never straddles an instance: m % 8 == 0).
+  // 32 tm + 8 q + 4 half + e (an 8-row chunk never straddles an instance: m % 8 == 0).  The
+  // chunks are 8 rows apart, so the instance row and bias index advance by additions.
   f32x4 bias4[TM][4];
+  {
+    const int32_t R0 = row_base + 4 * half;
+    int32_t gi = 0, r = R0;
+    if (p.fused) {
+      gi = R0 / p.m;
+      r = R0 - gi * p.m;
+    }
+    int64_t idx = p.fused ? (int64_t)gi * p.bias_step_m + r : in.bias + R0;
 #pragma unroll
-  for (int tm = 0; tm < TM; ++tm)
+    for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int32_t R = row_base + tm * 32 + 8 * q + 4 * half;
-      int64_t idx;
-      bool ok;
-      if (p.fused) {
-        const int32_t gi = R / p.m, r = R - gi * p.m;
-        idx = (int64_t)gi * p.bias_step_m + r;
-        ok = FULL || R < p.vrows;
-      } else {
-        idx = in.bias + R;
-        ok = FULL || R < p.m;
-      }
-      f32x4 b = {0.0f, 0.0f, 0.0f, 0.0f};
-      if (has_bias && ok) {
-        const float* bp = p.bias + idx;
-        if ((reinterpret_cast<uintptr_t>(bp) & 15) == 0) {
-          b = gld<f32x4>(bp);
-        } else {
+      for (int q = 0; q < 4; ++q) {
+        const int32_t R = R0 + tm * 32 + 8 * q;
+        const bool ok = FULL || R < (p.fused ? p.vrows : p.m);
+        f32x4 b = {0.0f, 0.0f, 0.0f, 0.0f};
+        if (has_bias && ok) {
+          const float* bp = p.bias + idx;
+          if ((reinterpret_cast<uintptr_t>(bp) & 15) == 0) {
+            b = gld<f32x4>(bp);
+          } else {
 #pragma unroll
-          for (int e = 0; e < 4; ++e) b[e] = gld<float>(bp + e);
+            for (int e = 0; e < 4; ++e) b[e] = gld<float>(bp + e);
+          }
+        }
+        bias4[tm][q] = b;
+        // next chunk, 8 rows on
+        idx += 8;
+        if (p.fused) {
+          r += 8;
+          while (r >= p.m) {
+            r -= p.m;
+            idx += p.bias_step_m - p.m;
+          }
         }
       }
-      bias4[tm][q] = b;
-    }
+  }
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm) {
 #pragma unroll
@@ -427,24 +437,28 @@ __device__ __forceinline__ void epilogue_bf16_act(const BrgemmParams& p, const I
     row_ok = FULL || R < p.m;
     row_off = R;
   }
+  // Columns advance by COLS_PER_IT per iteration: track the instance column and offset by
+  // additions (one division per lane).
+  int32_t C = tc.col0 + wn * WTN + csub;
+  int32_t cin = C;
+  int64_t col_off;
+  if (p.fused) {
+    const int32_t gi = C / p.n;
+    cin = C - gi * p.n;
+    col_off = (int64_t)gi * p.c_step_n + (int64_t)cin * p.ldc;
+  } else {
+    col_off = (int64_t)C * p.ldc;
+  }
+  const int32_t c_lim = p.fused ? p.vcols : p.n;
+  const int64_t wrap = p.c_step_n - (int64_t)p.n * p.ldc;   // next instance, column 0
+  uint16_t* const cbase = static_cast<uint16_t*>(p.c) + in.c + row_off;
 #pragma unroll 4
   for (int it = 0; it < WTN / COLS_PER_IT; ++it) {
     const int col_local = it * COLS_PER_IT + csub;
     const u32x4 w = *reinterpret_cast<const u32x4*>(
         slab + col_local * COL_BYTES + ((chunk ^ (col_local & (CPC - 1))) << 4));
-    const int32_t C = tc.col0 + wn * WTN + col_local;
-    bool col_ok;
-    int64_t col_off;
-    if (p.fused) {
-      const int32_t gi = C / p.n, c = C - gi * p.n;
-      col_ok = FULL || C < p.vcols;
-      col_off = (int64_t)gi * p.c_step_n + (int64_t)c * p.ldc;
-    } else {
-      col_ok = FULL || C < p.n;
-      col_off = (int64_t)C * p.ldc;
-    }
-    if (row_ok && col_ok) {
-      uint16_t* cp = static_cast<uint16_t*>(p.c) + in.c + row_off + col_off;
+    if (row_ok && (FULL || C < c_lim)) {
+      uint16_t* cp = cbase + col_off;
       if ((reinterpret_cast<uintptr_t>(cp) & 15) == 0) {
         gst<u32x4>(cp, w);
       } else {
@@ -454,6 +468,15 @@ __device__ __forceinline__ void epilogue_bf16_act(const BrgemmParams& p, const I
           gst<uint16_t>(cp + 2 * e, (uint16_t)(d[e] & 0xffffu));
           gst<uint16_t>(cp + 2 * e + 1, (uint16_t)(d[e] >> 16));
         }
+      }
+    }
+    C += COLS_PER_IT;
+    col_off += (int64_t)COLS_PER_IT * p.ldc;
+    if (p.fused) {
+      cin += COLS_PER_IT;
+      while (cin >= p.n) {
+        cin -= p.n;
+        col_off += wrap;
       }
     }
   }
