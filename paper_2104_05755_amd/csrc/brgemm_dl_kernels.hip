@@ -280,12 +280,17 @@ void brgemm_bf16_dl_kernel(BrgemmParams p) {
       for (int tn = 0; tn < TN; ++tn)
         acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[tm], bfr[tn], acc[tm][tn], 0, 0, 0);
   };
+  // One stage's MFMAs with the fragments double-buffered: k-step kq + 1's reads are issued
+  // before k-step kq's MFMAs (a scheduling barrier keeps the compiler from sinking them to their
+  // use), so the MFMAs do not wait on LDS latency at each k-step.
   auto compute = [&](int slot_idx) {
+    bf16x8 af[2][TM], bfr[2][TN];
+    read_frags(slot_idx, 0, af[0], bfr[0]);
 #pragma unroll
     for (int kq = 0; kq < KQ; ++kq) {
-      bf16x8 af[TM], bfr[TN];
-      read_frags(slot_idx, kq, af, bfr);
-      mfmas(af, bfr);
+      if (kq + 1 < KQ) read_frags(slot_idx, kq + 1, af[(kq + 1) & 1], bfr[(kq + 1) & 1]);
+      __builtin_amdgcn_sched_barrier(0);   // keep the reads ahead of the MFMAs
+      mfmas(af[kq & 1], bfr[kq & 1]);
     }
   };
   // Wait until this wave's loads of the stage `ahead` stages before its newest issued one landed.
