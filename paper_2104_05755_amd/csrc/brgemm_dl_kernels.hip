@@ -184,10 +184,40 @@ void brgemm_bf16_dl_kernel(BrgemmParams p) {
   i32x4 ra, rb;
   char* slot = lds;
   bool aligned = true;
+  // Offset and pointer lists: lane j holds pair j's two entries (the first 64 pairs), loaded
+  // once; a stage picks its pair's with readlane instead of a memory load per stage.
+  uint64_t pair_a = 0, pair_b = 0;
+  if constexpr (KIND == TPP_BR_OFFSET) {
+    if (lane < in.npairs) {
+      pair_a = (uint64_t)p.offs_a[lane];
+      pair_b = (uint64_t)p.offs_b[lane];
+    }
+  } else if constexpr (KIND == TPP_BR_ADDRESS) {
+    if (lane < in.npairs) {
+      pair_a = reinterpret_cast<uint64_t>(p.ptrs_a[in.pair0 + lane]);
+      pair_b = reinterpret_cast<uint64_t>(p.ptrs_b[in.pair0 + lane]);
+    }
+  }
+  auto lane_u64 = [](uint64_t v, int32_t src) {
+    const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)v, src);
+    const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(v >> 32), src);
+    return ((uint64_t)hi << 32) | lo;
+  };
   auto stage_begin = [&]() {
     const uint16_t* pa;
     const uint16_t* pb;
-    pair_bases_k<KIND, uint16_t>(p, in, iss_i, pa, pb);
+    if (KIND != TPP_BR_STRIDE && iss_i < 64) {
+      const uint64_t ea = lane_u64(pair_a, iss_i), eb = lane_u64(pair_b, iss_i);
+      if constexpr (KIND == TPP_BR_OFFSET) {
+        pa = static_cast<const uint16_t*>(p.a) + in.a + (int64_t)ea;
+        pb = static_cast<const uint16_t*>(p.b) + in.b + (int64_t)eb;
+      } else {
+        pa = reinterpret_cast<const uint16_t*>(ea);
+        pb = reinterpret_cast<const uint16_t*>(eb);
+      }
+    } else {
+      pair_bases_k<KIND, uint16_t>(p, in, iss_i, pa, pb);
+    }
     ua = reinterpret_cast<const char*>(pa + base_a) + (int64_t)iss_kk * p.lda * 2;
     ub = reinterpret_cast<const char*>(pb + base_b) + (int64_t)iss_kk * 2;
     ra = raw_buffer(ua);
@@ -420,6 +450,7 @@ hipError_t launch_brgemm_dl(const BrgemmParams& p, int32_t id, bool full, dim3 g
     case K_BF16_PP_256x256: launch_dl<256, 256, 4, 2, 1>(p, full, grid, stream); break;
     case K_BF16_DL64K_256x256: launch_dl<256, 256, 4, 2, 0, 64>(p, full, grid, stream); break;
     case K_BF16_DL64K_128x128: launch_dl<128, 128, 2, 2, 0, 64>(p, full, grid, stream); break;
+    case K_BF16_DL64K_64x64: launch_dl<64, 64, 2, 2, 0, 64>(p, full, grid, stream); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -692,32 +692,31 @@ __global__ __launch_bounds__(NT) void brgemm_f32_kernel(BrgemmParams p) {
   }
 }
 
-// Finishing step of a split fp32 launch: one workgroup per tile sums the split partial tiles in
-// chunk order (so the result does not depend on timing) and applies beta * C, bias, activation
-// and the store, exactly as the unsplit kernel's epilogue.
+// Finishing step of a split fp32 launch: four workgroups per tile, each thread four consecutive
+// rows of one column (16 rows x 64 columns per workgroup).  It sums the split partial tiles in
+// chunk order (so the result does not depend on timing), eight chunk loads in flight at a time,
+// and applies beta * C, bias, activation and the store exactly as the unsplit kernel's epilogue.
 __global__ __launch_bounds__(NT) void brgemm_f32_split_finish(BrgemmParams p) {
   const int t = threadIdx.x;
-  const int64_t tile_bid = blockIdx.x;
+  const int64_t tile_bid = blockIdx.x / 4;
+  const int quarter = (int)(blockIdx.x - tile_bid * 4);
   const TileCoord tc = decode_tile_at(p, F_BM, F_BN, tile_bid);
   const Instance in = instance_of(p, tc.g);
-  const int c_local = t & 63, r0 = (t >> 6) * 16;   // 16 consecutive rows of one column
-  float sum[16];
-#pragma unroll
-  for (int e = 0; e < 16; ++e) sum[e] = 0.0f;
+  const int c_local = t & 63, r0 = quarter * 16 + (t >> 6) * 4;
   const float* w = p.ws + (size_t)tile_bid * p.split * (F_BM * F_BN) + c_local * F_BM + r0;
-  for (int32_t ch = 0; ch < p.split; ++ch) {
+  const size_t step = F_BM * F_BN;
+  f32x4 sum = {0.0f, 0.0f, 0.0f, 0.0f};
+  int32_t ch = 0;
+  for (; ch + 8 <= p.split; ch += 8) {
+    f32x4 v[8];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const f32x4 v = gld<f32x4>(w + (size_t)ch * (F_BM * F_BN) + q * 4);
+    for (int u = 0; u < 8; ++u) v[u] = gld<f32x4>(w + (size_t)(ch + u) * step);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) sum[q * 4 + e] += v[e];
-    }
+    for (int u = 0; u < 8; ++u) sum += v[u];
   }
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const float v[4] = {sum[q * 4 + 0], sum[q * 4 + 1], sum[q * 4 + 2], sum[q * 4 + 3]};
-    store_group<true>(p, in, tc.row0 + r0 + q * 4, tc.col0 + c_local, v);
-  }
+  for (; ch < p.split; ++ch) sum += gld<f32x4>(w + (size_t)ch * step);
+  const float v4[4] = {sum[0], sum[1], sum[2], sum[3]};
+  store_group<true>(p, in, tc.row0 + r0, tc.col0 + c_local, v4);
 }
 
 struct KernelInfo {
@@ -737,6 +736,7 @@ constexpr KernelInfo kInfo[K_COUNT] = {
     {"bf16_256x256_w8_direct_lds_pingpong", 256, 256},
     {"bf16_256x256_w8_direct_lds_bk64", 256, 256},
     {"bf16_128x128_w4_direct_lds_bk64", 128, 128},
+    {"bf16_64x64_w4_direct_lds_bk64", 64, 64},
 };
 
 }  // namespace
@@ -796,6 +796,7 @@ hipError_t launch_brgemm(BrgemmParams& p, int32_t id, hipStream_t stream) {
     case K_BF16_PP_256x256:
     case K_BF16_DL64K_256x256:
     case K_BF16_DL64K_128x128:
+    case K_BF16_DL64K_64x64:
       return launch_brgemm_dl(p, id, full, grid, stream);
     case K_BF16_GENERIC:
       hipLaunchKernelGGL((brgemm_bf16_kernel<64, 64, 2, 2, true>), grid, block, 0, stream, p);
@@ -804,7 +805,8 @@ hipError_t launch_brgemm(BrgemmParams& p, int32_t id, hipStream_t stream) {
       if (p.split > 1) {
         hipLaunchKernelGGL(brgemm_f32_kernel, dim3((unsigned)(p.total_tiles * p.split)), block, 0,
                            stream, p);
-        hipLaunchKernelGGL(brgemm_f32_split_finish, grid, block, 0, stream, p);
+        hipLaunchKernelGGL(brgemm_f32_split_finish, dim3((unsigned)(p.total_tiles * 4)), block, 0,
+                           stream, p);
       } else {
         hipLaunchKernelGGL(brgemm_f32_kernel, grid, block, 0, stream, p);
       }

@@ -65,7 +65,8 @@ enum KernelId : int32_t {
   K_BF16_PP_256x256 = 8,  // direct global->LDS staging, 8 waves in two alternating groups
   K_BF16_DL64K_256x256 = 9,  // direct global->LDS staging, 8 waves, 64-k stages (k % 64 == 0)
   K_BF16_DL64K_128x128 = 10, // as 9, 128x128 tiles, 4 waves (two workgroups per CU)
-  K_COUNT = 11
+  K_BF16_DL64K_64x64 = 11,   // as 9, 64x64 tiles, 4 waves
+  K_COUNT = 12
 };
 
 const char* kernel_name(int32_t id);

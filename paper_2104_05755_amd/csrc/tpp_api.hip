@@ -106,7 +106,7 @@ int32_t choose_kernel(const tpp_brgemm_kernel_s& h, const tpp::BrgemmParams& p) 
   const Cand cands[] = {
       {bk64 ? tpp::K_BF16_DL64K_256x256 : tpp::K_BF16_PP_256x256, tpp::K_BF16_256x256, 256, 256},
       {bk64 ? tpp::K_BF16_DL64K_128x128 : tpp::K_BF16_DL_128x128, tpp::K_BF16_128x128, 128, 128},
-      {tpp::K_BF16_DL_64x64, tpp::K_BF16_64x64, 64, 64}};
+      {bk64 ? tpp::K_BF16_DL64K_64x64 : tpp::K_BF16_DL_64x64, tpp::K_BF16_64x64, 64, 64}};
   for (const Cand& c : cands) {
     // never pad a virtual C out to a larger tile (the 64x64 tile is the floor)
     const bool last = c.bm == 64;

@@ -269,7 +269,7 @@ def test_device_bf16_narrowing_is_rne():
 # ----------------------------------------------------------------------------------------------
 # Every tile instance of the 16-byte-load family, forced one at a time (complete and ragged tiles)
 # ----------------------------------------------------------------------------------------------
-VEC_KERNEL_IDS = [0, 1, 2, 5, 6, 7, 8, 9, 10]
+VEC_KERNEL_IDS = [0, 1, 2, 5, 6, 7, 8, 9, 10, 11]
 
 
 @pytest.mark.parametrize("kid", VEC_KERNEL_IDS)
