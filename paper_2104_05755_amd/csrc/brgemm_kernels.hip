@@ -722,21 +722,22 @@ __global__ __launch_bounds__(NT) void brgemm_f32_split_finish(BrgemmParams p) {
 struct KernelInfo {
   const char* name;
   int bm, bn;
+  int kstep;   // k must be a multiple of this (direct buffer->LDS stages); 1 = any k
 };
 
 constexpr KernelInfo kInfo[K_COUNT] = {
-    {"bf16_256x256_w8_vec", 256, 256},
-    {"bf16_128x128_w4_vec", 128, 128},
-    {"bf16_64x64_w4_vec", 64, 64},
-    {"bf16_64x64_generic", 64, 64},
-    {"f32_64x64_generic", 64, 64},
-    {"bf16_256x256_w8_direct_lds", 256, 256},
-    {"bf16_128x128_w4_direct_lds", 128, 128},
-    {"bf16_64x64_w4_direct_lds", 64, 64},
-    {"bf16_256x256_w8_direct_lds_pingpong", 256, 256},
-    {"bf16_256x256_w8_direct_lds_bk64", 256, 256},
-    {"bf16_128x128_w4_direct_lds_bk64", 128, 128},
-    {"bf16_64x64_w4_direct_lds_bk64", 64, 64},
+    {"bf16_256x256_w8_vec", 256, 256, 1},
+    {"bf16_128x128_w4_vec", 128, 128, 1},
+    {"bf16_64x64_w4_vec", 64, 64, 1},
+    {"bf16_64x64_generic", 64, 64, 1},
+    {"f32_64x64_generic", 64, 64, 1},
+    {"bf16_256x256_w8_direct_lds", 256, 256, 32},
+    {"bf16_128x128_w4_direct_lds", 128, 128, 32},
+    {"bf16_64x64_w4_direct_lds", 64, 64, 32},
+    {"bf16_256x256_w8_direct_lds_pingpong", 256, 256, 32},
+    {"bf16_256x256_w8_direct_lds_bk64", 256, 256, 64},
+    {"bf16_128x128_w4_direct_lds_bk64", 128, 128, 64},
+    {"bf16_64x64_w4_direct_lds_bk64", 64, 64, 64},
 };
 
 }  // namespace
@@ -744,6 +745,7 @@ constexpr KernelInfo kInfo[K_COUNT] = {
 const char* kernel_name(int32_t id) { return (id >= 0 && id < K_COUNT) ? kInfo[id].name : "?"; }
 int kernel_tile_m(int32_t id) { return (id >= 0 && id < K_COUNT) ? kInfo[id].bm : 64; }
 int kernel_tile_n(int32_t id) { return (id >= 0 && id < K_COUNT) ? kInfo[id].bn : 64; }
+int kernel_k_step(int32_t id) { return (id >= 0 && id < K_COUNT) ? kInfo[id].kstep : 1; }
 
 template <int BM, int BN, int WM, int WN, bool FULL, int KIND>
 void launch_vec_k(const BrgemmParams& p, dim3 grid, hipStream_t stream) {

@@ -74,6 +74,7 @@ int kernel_tile_m(int32_t id);   // tile rows of kernel instance id
 // fp32 workspace floats a split launch of the fp32 kernel needs (split x tiles x 64 x 64).
 int64_t f32_split_ws_floats(int32_t split, int64_t total_tiles);
 int kernel_tile_n(int32_t id);   // tile columns
+int kernel_k_step(int32_t id);   // k granularity the instance needs (1 = any k)
 
 // Fill the tiling fields of p for kernel `id` and launch on `stream`.
 hipError_t launch_brgemm(BrgemmParams& p, int32_t id, hipStream_t stream);

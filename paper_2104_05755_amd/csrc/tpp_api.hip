@@ -94,11 +94,9 @@ int32_t choose_kernel(const tpp_brgemm_kernel_s& h, const tpp::BrgemmParams& p) 
   const bool dl_kind = h.desc.k % 32 == 0 && (h.desc.kind != TPP_BR_ADDRESS || bk64);
   if (const char* env = std::getenv("TPP_FORCE_KERNEL")) {
     const int id = std::atoi(env);
-    const bool is_dl = id >= tpp::K_BF16_DL_256x256 && id != tpp::K_BF16_GENERIC &&
-                       id != tpp::K_F32_GENERIC;
-    const bool id_bk64 = id >= tpp::K_BF16_DL64K_256x256;
+    const bool is_dl = tpp::kernel_k_step(id) > 1;
     if (id >= 0 && id < tpp::K_COUNT && id != tpp::K_BF16_GENERIC && id != tpp::K_F32_GENERIC &&
-        (!is_dl || (h.desc.k % (id_bk64 ? 64 : 32) == 0 &&
+        (!is_dl || (h.desc.k % tpp::kernel_k_step(id) == 0 &&
                     dl_offsets_fit(h, p, tpp::kernel_tile_m(id), tpp::kernel_tile_n(id)))))
       return id;
   }
