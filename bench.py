@@ -31,7 +31,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=50)
-    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target wall time of the oracle CPU baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-per-config", action="store_true")
@@ -263,7 +263,7 @@ def run_cpu_baseline(seconds: float, wl):
         t0 = time.perf_counter()
         run_oracle(wl, 0, sel=sel)
         dt = time.perf_counter() - t0
-        if dt >= seconds * 0.5 or n >= call.G:
+        if dt >= seconds * 0.7 or n >= call.G:
             break
         n = min(call.G, max(2 * n, int(n * seconds / max(dt, 1e-3))))
     flops = 2 * call.m * call.n * call.k * call.count * len(sel)
