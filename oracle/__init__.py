@@ -1,4 +1,5 @@
-"""Plain CPU oracle for the batch-reduce GEMM TPP, its fused epilogue and the Reduce TPP.
+"""Plain CPU oracle for the batch-reduce GEMM TPP, its fused epilogue, the Reduce TPP and the
+Transform TPP.
 
 TEST INFRASTRUCTURE ONLY.  The product path (the HIP library and its Python binding) never
 imports, links or calls anything in this package; only ``tests/``, the smoke check and the
@@ -27,6 +28,7 @@ STRIDE, OFFSET, ADDRESS = 0, 1, 2
 EPI_BIAS, EPI_RELU, EPI_GELU_TANH = 1, 2, 4
 RED_SUM, RED_MUL, RED_MIN, RED_MAX = 0, 1, 2, 3
 RED_BY_COLS, RED_BY_ROWS, RED_X, RED_X2 = 1, 2, 4, 8
+TR_TRANSPOSE, TR_VNNI, TR_VNNI_TO_VNNI_T = 0, 1, 2
 
 _DTYPES = {"f32": F32, "bf16": BF16}
 _KINDS = {"stride": STRIDE, "offset": OFFSET, "address": ADDRESS}
@@ -74,6 +76,8 @@ def lib():
                                                vp, i64, vp, vp, ctypes.c_int]
         _lib.oracle_reduce.restype = ctypes.c_int
         _lib.oracle_reduce.argtypes = [i32, i32, i64, i32, vp, i32, ctypes.c_uint32, vp, vp]
+        _lib.oracle_transform.restype = ctypes.c_int
+        _lib.oracle_transform.argtypes = [i32, i32, i32, i64, i64, i32, i32, vp, vp]
         _lib.oracle_f32_to_bf16.restype = ctypes.c_uint16
         _lib.oracle_f32_to_bf16.argtypes = [ctypes.c_float]
         _lib.oracle_f32_to_bf16_array.restype = None
@@ -215,6 +219,30 @@ def reduce(x, m: int, n: int, ld: int, in_type: str, op: str, by: str, want=("x"
     if rc != 0:
         raise ValueError("oracle_reduce rejected its arguments")
     return ox, ox2
+
+
+_TR_KINDS = {"transpose": TR_TRANSPOSE, "vnni": TR_VNNI, "vnni_t": TR_VNNI_TO_VNNI_T}
+
+
+def transform_out_len(kind: str, m: int, n: int, ld_out: int, alpha: int) -> int:
+    """Elements of an output buffer that holds every position the transformation defines."""
+    if m == 0 or n == 0:
+        return 0
+    groups = {"transpose": m, "vnni": -(-n // alpha), "vnni_t": -(-m // alpha)}[kind]
+    return ld_out * groups
+
+
+def transform(kind: str, m: int, n: int, ld_in: int, ld_out: int, dtype: str, alpha: int,
+              x: np.ndarray, out: np.ndarray) -> np.ndarray:
+    """Transform TPP (kind "transpose", "vnni" or "vnni_t") from host array x into host array
+    out, in place; positions the transformation does not define keep their values."""
+    _check_dtype(x, dtype, "x")
+    _check_dtype(out, dtype, "out")
+    es = 4 if dtype == "f32" else 2
+    rc = lib().oracle_transform(_TR_KINDS[kind], m, n, ld_in, ld_out, es, alpha, _ptr(x), _ptr(out))
+    if rc != 0:
+        raise ValueError("oracle_transform rejected its arguments")
+    return out
 
 
 def f32_to_bf16(x: float) -> int:

@@ -289,3 +289,62 @@ int oracle_reduce(int32_t m, int32_t n, int64_t ld, int32_t in_type, const void*
   }
   return 0;
 }
+
+/* Transform TPP (Table 1; Sec. 3.1 defines the three transformations; the VNNI layout is the
+ * [K/alpha][M][alpha] reformatting of Sec. 3.2.2).  Entries are moved as raw bytes. */
+static void move_entry(void* out, int64_t oi, const void* in, int64_t ii, int32_t es) {
+  memcpy((char*)out + oi * es, (const char*)in + ii * es, (size_t)es);
+}
+
+static void zero_entry(void* out, int64_t oi, int32_t es) {
+  memset((char*)out + oi * es, 0, (size_t)es);
+}
+
+int oracle_transform(int32_t kind, int32_t m, int32_t n, int64_t ld_in, int64_t ld_out,
+                     int32_t es, int32_t alpha, const void* in, void* out) {
+  if (m < 0 || n < 0 || (es != 2 && es != 4)) return -1;
+  if (alpha != 1 && alpha != 2 && alpha != 4) return -1;
+  if (kind == ORACLE_TR_TRANSPOSE) {
+    if (ld_in < m || ld_out < n) return -1;
+  } else if (kind == ORACLE_TR_VNNI) {
+    if (ld_in < m || ld_out < (int64_t)m * alpha) return -1;
+  } else if (kind == ORACLE_TR_VNNI_TO_VNNI_T) {
+    if (ld_in < (int64_t)m * alpha || ld_out < (int64_t)n * alpha) return -1;
+  } else {
+    return -1;
+  }
+  if (m == 0 || n == 0) return 0;
+  if (!in || !out) return -1;
+  if (kind == ORACLE_TR_TRANSPOSE) {
+    for (int32_t c = 0; c < n; ++c)
+      for (int32_t r = 0; r < m; ++r)
+        move_entry(out, (int64_t)c + (int64_t)r * ld_out, in, (int64_t)r + (int64_t)c * ld_in, es);
+  } else if (kind == ORACLE_TR_VNNI) {
+    const int32_t groups = (n + alpha - 1) / alpha;
+    for (int32_t g = 0; g < groups; ++g)
+      for (int32_t r = 0; r < m; ++r)
+        for (int32_t a = 0; a < alpha; ++a) {
+          const int32_t c = g * alpha + a;
+          const int64_t oi = (int64_t)g * ld_out + (int64_t)r * alpha + a;
+          if (c < n)
+            move_entry(out, oi, in, (int64_t)r + (int64_t)c * ld_in, es);
+          else
+            zero_entry(out, oi, es);
+        }
+  } else {
+    /* output group g holds rows r = alpha*g + a of the input as its columns of n entries */
+    const int32_t groups = (m + alpha - 1) / alpha;
+    for (int32_t g = 0; g < groups; ++g)
+      for (int32_t c = 0; c < n; ++c)
+        for (int32_t a = 0; a < alpha; ++a) {
+          const int32_t r = g * alpha + a;
+          const int64_t oi = (int64_t)g * ld_out + (int64_t)c * alpha + a;
+          if (r < m)
+            move_entry(out, oi, in, (int64_t)(c / alpha) * ld_in + (int64_t)r * alpha + c % alpha,
+                       es);
+          else
+            zero_entry(out, oi, es);
+        }
+  }
+  return 0;
+}

@@ -12,6 +12,8 @@
  *     RELU, GELU; Table 2 Add with column broadcast, Sec. 2.2), applied as Alg. 6 applies its UNARY
  *     to the finished C block.
  *   - Unary Reduce TPP, Table 1 and Sec. 3.1 (reduction-by-columns turns M x N into M x 1).
+ *   - Unary Transform TPP, Table 1 and Sec. 3.1: Transpose, VNNI formatting and VNNI to
+ *     VNNI-transpose (entry permutations; no arithmetic).
  *
  * Storage reading: every 2D block is column-major with a leading dimension (element (r, c) of an
  * m x n block sits at base + r + c*ld), which is how Alg. 6 lays out its blocked tensors (the
@@ -31,6 +33,7 @@ enum { ORACLE_STRIDE = 0, ORACLE_OFFSET = 1, ORACLE_ADDRESS = 2 };
 enum { ORACLE_EPI_BIAS = 1u, ORACLE_EPI_RELU = 2u, ORACLE_EPI_GELU_TANH = 4u };
 enum { ORACLE_RED_SUM = 0, ORACLE_RED_MUL = 1, ORACLE_RED_MIN = 2, ORACLE_RED_MAX = 3 };
 enum { ORACLE_RED_BY_COLS = 1u, ORACLE_RED_BY_ROWS = 2u, ORACLE_RED_X = 4u, ORACLE_RED_X2 = 8u };
+enum { ORACLE_TR_TRANSPOSE = 0, ORACLE_TR_VNNI = 1, ORACLE_TR_VNNI_TO_VNNI_T = 2 };
 
 typedef struct {
   int32_t m, n, k;           /* C is m x n, A_i is m x k, B_i is k x n                        */
@@ -72,6 +75,23 @@ int oracle_brgemm_batched(const oracle_desc* d, const oracle_grid* grid, int64_t
  * both may be set.  Outputs are unrounded doubles. */
 int oracle_reduce(int32_t m, int32_t n, int64_t ld, int32_t in_type, const void* in,
                   int32_t op, uint32_t flags, double* out_x, double* out_x2);
+
+/* Transform TPP (Table 1; Sec. 3.1): a permutation of the entries of an m x n input whose entry
+ * (r, c) sits at in + r + c*ld_in (elements of es bytes: 4 for fp32, 2 for bf16).
+ *   TRANSPOSE       the matrix transpose: the n x m output has entry (c, r) = in(r, c) at
+ *                   out + c + r*ld_out (ld_in >= m, ld_out >= n; alpha unused).
+ *   VNNI            the logical tensor [D1][D0] = [n][m] (columns of m contiguous rows) laid out
+ *                   as [D1/alpha][D0][alpha]: column c = alpha*g + a goes to
+ *                   out + g*ld_out + r*alpha + a (ld_in >= m, ld_out >= m*alpha).  A last group
+ *                   with fewer than alpha columns is completed with zero entries.
+ *   VNNI_TO_VNNI_T  the input is an m x n tensor in that layout (group stride ld_in >= m*alpha);
+ *                   the output is its transpose (n x m) in the same layout with the same alpha
+ *                   (group stride ld_out >= n*alpha), i.e. [D1/a][D0][a] -> [D0/a][D1][a];
+ *                   zero entries complete the output's last group when m % alpha != 0.
+ * alpha is 1, 2 or 4.  Positions of out outside these (gaps when ld_out exceeds the extent) are
+ * left as they were.  m == 0 or n == 0 writes nothing.  Returns 0, or -1 for a bad argument. */
+int oracle_transform(int32_t kind, int32_t m, int32_t n, int64_t ld_in, int64_t ld_out,
+                     int32_t es, int32_t alpha, const void* in, void* out);
 
 /* Helpers the tests pin on their own: exact widening and the round-to-nearest-even narrowing
  * used for every output element. */

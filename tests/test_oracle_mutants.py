@@ -40,6 +40,22 @@ MUTANTS = {
                         "ax = (op == ORACLE_RED_MUL) ? 1.0 : 0.0;"),
 }
 
+# Transform TPP mutants, caught by the transform pins.
+TRANSFORM_MUTANTS = {
+    "transpose_output_index": ("move_entry(out, (int64_t)c + (int64_t)r * ld_out, in,",
+                               "move_entry(out, (int64_t)r + (int64_t)c * ld_out, in,"),
+    "vnni_planar_not_interleaved": ("const int64_t oi = (int64_t)g * ld_out + (int64_t)r * alpha + a;",
+                                    "const int64_t oi = (int64_t)g * ld_out + (int64_t)a * m + r;"),
+    "vnni_group_of_column": ("const int32_t c = g * alpha + a;", "const int32_t c = a * alpha + g;"),
+    "vnni_no_zero_fill": ("          if (c < n)\n            move_entry(out, oi, in, (int64_t)r + (int64_t)c * ld_in, es);\n          else\n            zero_entry(out, oi, es);",
+                          "          if (c < n)\n            move_entry(out, oi, in, (int64_t)r + (int64_t)c * ld_in, es);"),
+    "vnni_t_input_group": ("(int64_t)(c / alpha) * ld_in + (int64_t)r * alpha + c % alpha",
+                           "(int64_t)(c % alpha) * ld_in + (int64_t)r * alpha + c / alpha"),
+    "vnni_t_row_of_group": ("const int32_t r = g * alpha + a;", "const int32_t r = g + a * alpha;"),
+    "vnni_t_pad_not_zero": ("          if (r < m)\n            move_entry(out, oi, in, (int64_t)(c / alpha) * ld_in",
+                            "          if (r < m || 1)\n            move_entry(out, oi, in, (int64_t)(c / alpha) * ld_in"),
+}
+
 
 @pytest.fixture(scope="module")
 def source():
@@ -47,9 +63,7 @@ def source():
         return f.read()
 
 
-@pytest.mark.parametrize("name", sorted(MUTANTS))
-def test_pins_catch_planted_mistake(name, source, tmp_path):
-    old, new = MUTANTS[name]
+def _caught(old, new, pins, source, tmp_path, name):
     assert source.count(old) == 1, f"mutation site for {name} not unique"
     mutated = source.replace(old, new)
     src = tmp_path / "oracle.c"
@@ -60,6 +74,18 @@ def test_pins_catch_planted_mistake(name, source, tmp_path):
                     str(src), "-lm"], check=True)
     env = dict(os.environ, ORACLE_LIB_OVERRIDE=str(so), OMP_NUM_THREADS="2")
     r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
-                        os.path.join(ROOT, "tests", "test_oracle_pins.py")],
+                        os.path.join(ROOT, "tests", pins)],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, f"no pin caught mutant {name}:\n{r.stdout[-2000:]}"
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_catch_planted_mistake(name, source, tmp_path):
+    old, new = MUTANTS[name]
+    _caught(old, new, "test_oracle_pins.py", source, tmp_path, name)
+
+
+@pytest.mark.parametrize("name", sorted(TRANSFORM_MUTANTS))
+def test_transform_pins_catch_planted_mistake(name, source, tmp_path):
+    old, new = TRANSFORM_MUTANTS[name]
+    _caught(old, new, "test_oracle_transform_pins.py", source, tmp_path, name)
