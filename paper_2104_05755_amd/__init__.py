@@ -1,4 +1,5 @@
-"""MI355X (gfx950) batch-reduce GEMM TPP: thin Python binding of the C ABI in include/tpp_brgemm.h.
+"""MI355X (gfx950) TPP library: thin Python binding of the C ABI in include/tpp_brgemm.h and
+include/tpp_transform.h.
 
 Argument marshalling only: every step of the computation runs in the HIP kernels of
 ``libtpp_mi355x.so``.  The functions keep the C names; pointers are plain integers (device
@@ -29,6 +30,7 @@ TPP_BR_STRIDE, TPP_BR_OFFSET, TPP_BR_ADDRESS = 0, 1, 2
 TPP_EPI_BIAS, TPP_EPI_RELU, TPP_EPI_GELU_TANH = 1, 2, 4
 TPP_RED_SUM, TPP_RED_MUL, TPP_RED_MIN, TPP_RED_MAX = 0, 1, 2, 3
 TPP_RED_BY_COLS, TPP_RED_BY_ROWS, TPP_RED_X, TPP_RED_X2 = 1, 2, 4, 8
+TPP_TR_TRANSPOSE, TPP_TR_VNNI, TPP_TR_VNNI_TO_VNNI_T = 0, 1, 2
 
 _c_void_p, _i64, _i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
 
@@ -76,6 +78,8 @@ _sig("tpp_brgemm_release", None, _c_void_p)
 _sig("tpp_brgemm_describe", _i32, _c_void_p, ctypes.c_char_p, ctypes.c_size_t)
 _sig("tpp_reduce", _i32, _i32, _i32, _i64, _i32, _c_void_p, _i32, ctypes.c_uint32, _c_void_p,
      _c_void_p, _c_void_p)
+_sig("tpp_transform", _i32, _i32, _i32, _i32, _i64, _i64, _i32, _i32, _c_void_p, _c_void_p,
+     _c_void_p)
 
 
 def _p(x):
@@ -147,6 +151,11 @@ def tpp_brgemm_describe(h) -> str:
 def tpp_reduce(m, n, ld, in_type, x, op, flags, out_x, out_x2, stream=None):
     _check(_lib.tpp_reduce(m, n, ld, in_type, _p(x), op, flags, _p(out_x), _p(out_x2), stream),
            "tpp_reduce")
+
+
+def tpp_transform(kind, m, n, ld_in, ld_out, dtype, alpha, x, out, stream=None):
+    _check(_lib.tpp_transform(kind, m, n, ld_in, ld_out, dtype, alpha, _p(x), _p(out), stream),
+           "tpp_transform")
 
 
 def tpp_status_string(s: int) -> str:

@@ -5,6 +5,7 @@
 #include <stdint.h>
 
 #include "tpp_brgemm.h"
+#include "tpp_transform.h"
 
 namespace tpp {
 
@@ -96,5 +97,20 @@ struct ReduceParams {
 // Number of floats of work space a reduce of this shape needs (0 if none).
 int64_t reduce_work_floats(const ReduceParams& p);
 hipError_t launch_reduce(const ReduceParams& p, float* work, hipStream_t stream);
+
+// Transform TPP launcher (transform_kernels.hip).  kind: 0 transpose, 1 VNNI, 2 VNNI to
+// VNNI-transpose; es: entry bytes (2 or 4); vec: both operands 16-byte aligned with leading
+// dimensions of whole 16-byte units (the vector paths).  tiles_m is filled by the launcher.
+// hipErrorInvalidConfiguration when one launch would need more than 2^31 - 1 workgroups.
+struct TransformParams {
+  const void* in;
+  void* out;
+  int32_t kind, m, n;
+  int64_t ld_in, ld_out;
+  int32_t es, alpha;
+  int32_t vec;
+  int64_t tiles_m;
+};
+hipError_t launch_transform(TransformParams& p, hipStream_t stream);
 
 }  // namespace tpp

@@ -1,6 +1,6 @@
-// tpp_api.hip -- the C ABI of include/tpp_brgemm.h: argument checks, the dispatch cache, kernel
-// selection and launches.  Host code only; the kernels live in brgemm_kernels.hip and
-// reduce_kernels.hip.
+// tpp_api.hip -- the C ABI of include/tpp_brgemm.h and include/tpp_transform.h: argument checks,
+// the dispatch cache, kernel selection and launches.  Host code only; the kernels live in
+// brgemm_kernels.hip, brgemm_dl_kernels.hip, reduce_kernels.hip and transform_kernels.hip.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -440,6 +440,38 @@ tpp_status tpp_reduce(int32_t m, int32_t n, int64_t ld, int32_t in_type, const v
   }
   const hipError_t e = tpp::launch_reduce(p, work, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(TPP_ERR_HIP, "reduce launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+tpp_status tpp_transform(int32_t kind, int32_t m, int32_t n, int64_t ld_in, int64_t ld_out,
+                         int32_t dtype, int32_t alpha, const void* in, void* out, void* stream) {
+  if (kind < TPP_TR_TRANSPOSE || kind > TPP_TR_VNNI_TO_VNNI_T)
+    return fail(TPP_ERR_INVALID_ARG, "unknown transform kind %d", kind);
+  if (!valid_dtype(dtype)) return fail(TPP_ERR_INVALID_ARG, "unknown datatype code");
+  if (m < 0 || n < 0) return fail(TPP_ERR_INVALID_ARG, "m, n must be >= 0");
+  if (kind == TPP_TR_TRANSPOSE) {
+    alpha = 1;
+    if (ld_in < m || ld_out < n) return fail(TPP_ERR_INVALID_ARG, "ld_in < m or ld_out < n");
+  } else {
+    if (alpha != 1 && alpha != 2 && alpha != 4)
+      return fail(TPP_ERR_INVALID_ARG, "alpha must be 1, 2 or 4");
+    if (kind == TPP_TR_VNNI && (ld_in < m || ld_out < (int64_t)m * alpha))
+      return fail(TPP_ERR_INVALID_ARG, "VNNI needs ld_in >= m and ld_out >= m * alpha");
+    if (kind == TPP_TR_VNNI_TO_VNNI_T &&
+        (ld_in < (int64_t)m * alpha || ld_out < (int64_t)n * alpha))
+      return fail(TPP_ERR_INVALID_ARG,
+                  "VNNI to VNNI-transpose needs ld_in >= m * alpha and ld_out >= n * alpha");
+  }
+  if (m == 0 || n == 0) return ok();
+  if (!in || !out) return fail(TPP_ERR_INVALID_ARG, "NULL input or output");
+  const int32_t es = dtype == TPP_DT_F32 ? 4 : 2;
+  const bool vec = ((reinterpret_cast<uintptr_t>(in) | reinterpret_cast<uintptr_t>(out)) & 15) == 0 &&
+                   (ld_in * es) % 16 == 0 && (ld_out * es) % 16 == 0;
+  tpp::TransformParams p{in, out, kind, m, n, ld_in, ld_out, es, alpha, vec ? 1 : 0, 0};
+  const hipError_t e = tpp::launch_transform(p, static_cast<hipStream_t>(stream));
+  if (e == hipErrorInvalidConfiguration)
+    return fail(TPP_ERR_UNSUPPORTED, "transform needs more than 2^31 - 1 workgroups");
+  if (e != hipSuccess) return fail(TPP_ERR_HIP, "transform launch failed: %s", hipGetErrorString(e));
   return ok();
 }
 

@@ -1,16 +1,17 @@
 """The C-ABI library on the host: it loads, exports every declared symbol, and its host-only
 paths (dispatch validation, the handle cache, argument checks that precede any launch) behave
-as include/tpp_brgemm.h states.  No device work happens here."""
+as include/tpp_brgemm.h and include/tpp_transform.h state.  No device work happens here."""
 from __future__ import annotations
 
 import ctypes
+import glob
 import os
 import re
 
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "tpp_brgemm.h")
+HEADERS = sorted(glob.glob(os.path.join(ROOT, "include", "*.h")))
 
 
 @pytest.fixture(scope="module")
@@ -20,14 +21,16 @@ def tpp():
 
 
 def declared_functions():
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(tpp_[a-z_]+)\s*\(", text)))
+    names = set()
+    for h in HEADERS:
+        text = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names |= set(re.findall(r"\b(tpp_[a-z_]+)\s*\(", text))
+    return sorted(names)
 
 
 def test_library_exports_every_declared_function(tpp):
     names = declared_functions()
-    assert "tpp_brgemm_dispatch" in names and "tpp_reduce" in names
+    assert {"tpp_brgemm_dispatch", "tpp_reduce", "tpp_transform"} <= set(names)
     lib = ctypes.CDLL(tpp.LIB_PATH)
     missing = [n for n in names if not hasattr(lib, n)]
     assert not missing, f"not exported: {missing}"
@@ -142,3 +145,31 @@ def test_reduce_argument_checks(tpp, args):
     with pytest.raises(tpp.TppError) as e:
         tpp.tpp_reduce(m, n, ld, dt, fake if x else None, op, flags, fake, None)
     assert e.value.status == tpp.TPP_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("args,status", [
+    ((3, 4, 4, 4, 4, 0, 1), "INVALID_ARG"),            # unknown kind
+    ((0, -1, 4, 4, 4, 1, 1), "INVALID_ARG"),           # m < 0
+    ((0, 4, 4, 3, 4, 1, 1), "INVALID_ARG"),            # ld_in < m
+    ((0, 4, 4, 4, 3, 1, 1), "INVALID_ARG"),            # ld_out < n
+    ((1, 4, 4, 4, 7, 1, 2), "INVALID_ARG"),            # VNNI ld_out < m * alpha
+    ((1, 4, 4, 4, 8, 1, 3), "INVALID_ARG"),            # alpha 3
+    ((2, 4, 4, 7, 8, 1, 2), "INVALID_ARG"),            # VNNI_T ld_in < m * alpha
+    ((2, 4, 4, 8, 7, 1, 2), "INVALID_ARG"),            # VNNI_T ld_out < n * alpha
+    ((0, 4, 4, 4, 4, 7, 1), "INVALID_ARG"),            # unknown dtype
+])
+def test_transform_argument_checks(tpp, args, status):
+    kind, m, n, ld_in, ld_out, dtype, alpha = args
+    with pytest.raises(tpp.TppError) as e:
+        tpp.tpp_transform(kind, m, n, ld_in, ld_out, dtype, alpha, 16, 16)
+    assert e.value.status == getattr(tpp, f"TPP_ERR_{status}")
+
+
+def test_transform_null_pointers_and_empty_shapes(tpp):
+    with pytest.raises(tpp.TppError) as e:
+        tpp.tpp_transform(tpp.TPP_TR_TRANSPOSE, 4, 4, 4, 4, tpp.TPP_DT_BF16, 1, None, 16)
+    assert e.value.status == tpp.TPP_ERR_INVALID_ARG
+    # nothing to move: no pointer is looked at, nothing is launched
+    for kind in (tpp.TPP_TR_TRANSPOSE, tpp.TPP_TR_VNNI, tpp.TPP_TR_VNNI_TO_VNNI_T):
+        tpp.tpp_transform(kind, 0, 5, 8, 8 * 2, tpp.TPP_DT_BF16, 2, None, None)
+        tpp.tpp_transform(kind, 5, 0, 16, 16, tpp.TPP_DT_BF16, 2, None, None)
