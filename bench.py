@@ -8,7 +8,8 @@ two batched BRGEMM launches (8192 instances x 16 pairs, then 2048 instances x 64
 launches).  ``roofline`` takes the dominant launch's mean duration over K more steps with a
 timing-only (fence-free) HIP event on its stream around each launch.  The same run also
 times the other workloads (fp32 single BRGEMM, MLP fully-connected layer, 3x3 convolution with
-batchnorm statistics via the Reduce TPP, gathered address-based BRGEMM) under ``per_config``,
+batchnorm statistics via the Reduce TPP, gathered address-based BRGEMM, and the Transform TPP's
+transpose and VNNI formatting of a 64 MB tensor) under ``per_config``,
 and the CPU oracle on a bounded sample of the headline workload under ``cpu_baseline``.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
@@ -327,6 +328,36 @@ def per_config(args, torch, tpp, torch_io, wk, np, stream):
                                "hbm_frac": round(rb / (per[1] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
         out[str(cfg)] = entry
         del dev, dcs, fns
+        torch.cuda.empty_cache()
+    out.update(transform_entries(args, torch, tpp, stream))
+    return out
+
+
+def transform_entries(args, torch, tpp, stream):
+    """Transform TPP on the MLP block's hidden activations (8192 tokens x 4096 features, bf16,
+    64 MB): its transpose and its VNNI formatting (alpha 2), each timed over max(steps, 50)
+    back-to-back launches.  HBM bound: every entry is read once and written once."""
+    m, n = 8192, 4096
+    es = 2
+    out = {}
+    for name, kind, alpha in (("transform_transpose", tpp.TPP_TR_TRANSPOSE, 1),
+                              ("transform_vnni", tpp.TPP_TR_VNNI, 2)):
+        ld_out = n if kind == tpp.TPP_TR_TRANSPOSE else m * alpha
+        groups = m if kind == tpp.TPP_TR_TRANSPOSE else n // alpha
+        x = torch.randint(-32768, 32767, (m * n,), dtype=torch.int16, device="cuda")
+        o = torch.empty(ld_out * groups, dtype=torch.int16, device="cuda")
+
+        def f(kind=kind, alpha=alpha, ld_out=ld_out, x=x, o=o):
+            tpp.tpp_transform(kind, m, n, m, ld_out, tpp.TPP_DT_BF16, alpha, x, o, stream)
+        time_steps([f], min(max(args.steps, 50), args.warmup), 0, torch)   # warm-up
+        ms = time_bursts([f], max(args.steps, 50), torch)[0]
+        byts = 2 * m * n * es
+        gbs = byts / (ms * 1e-3) / 1e9
+        out[name] = {"workload": f"{name.split('_')[1]} of a {m} x {n} bf16 tensor (64 MB), "
+                                 f"alpha {alpha}", "launch_us": round(ms * 1e3, 2),
+                     "alg_bytes": byts, "hbm_gbs": round(gbs, 1),
+                     "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)}
+        del x, o
         torch.cuda.empty_cache()
     return out
 

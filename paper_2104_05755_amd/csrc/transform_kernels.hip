@@ -12,7 +12,7 @@
 //   - VNNI: no LDS: each thread writes one 16-byte chunk of an output group, gathering its
 //     alpha columns with one (16 / alpha)-byte load each.
 //   - VNNI to VNNI-transpose: the tiled kernel with both sides addressed in the VNNI layout,
-//     entry by entry.
+//     16-byte chunks on whole aligned tiles, entry by entry otherwise.
 #include <hip/hip_runtime.h>
 
 #include "brgemm_device.h"
@@ -113,19 +113,43 @@ __global__ __launch_bounds__(TPB) void transpose_kernel(TransformParams p) {
 }
 
 // VNNI to VNNI-transpose: logical tile rows [r0, r0 + 64), columns [c0, c0 + 64) (both multiples
-// of alpha, so groups never straddle tiles).  Reads walk the input's contiguous order (c % alpha
-// fastest, then r), writes the output's (r % alpha fastest, then c).  Output rows from m up to
-// the next multiple of alpha are the zero completion of the last group.
+// of alpha, so groups never straddle tiles), staged as lds[c][r].  Reads walk the input's
+// contiguous order (c % alpha fastest, then r), writes the output's (r % alpha fastest, then c).
+// Whole tiles with aligned operands move 16-byte chunks on both sides: an input chunk is
+// V / alpha rows of one group's alpha columns, an output chunk V / alpha columns of one output
+// group's alpha rows.  Output rows from m up to the next multiple of alpha are the zero
+// completion of the last group (never in a whole tile).
 template <int ES, int ALPHA>
 __global__ __launch_bounds__(TPB) void vnni_t_kernel(TransformParams p) {
   using T = typename Entry<ES>::T;
+  constexpr int V = 16 / ES, CPG = TT * ALPHA / V;   // 16-byte chunks per group of a tile
   __shared__ T lds[TT][TT + 1];
   const int t = threadIdx.x;
   const int64_t bid = blockIdx.x;
   const int32_t r0 = (int32_t)(bid % p.tiles_m) * TT, c0 = (int32_t)(bid / p.tiles_m) * TT;
-  const int32_t m_pad = (p.m + ALPHA - 1) / ALPHA * ALPHA;
   const T* in = static_cast<const T*>(p.in);
   T* out = static_cast<T*>(p.out);
+  if (r0 + TT <= p.m && c0 + TT <= p.n && p.vec) {
+    for (int q = t; q < TT * TT / V; q += TPB) {
+      const int gi = q / CPG, j0 = (q % CPG) * V, rr0 = j0 / ALPHA;
+      const u32x4 w4 = gld<u32x4>(in + (int64_t)(c0 / ALPHA + gi) * p.ld_in +
+                                  (int64_t)(r0 + rr0) * ALPHA);
+      const uint32_t w[4] = {w4[0], w4[1], w4[2], w4[3]};
+#pragma unroll
+      for (int e = 0; e < V; ++e) lds[gi * ALPHA + e % ALPHA][rr0 + e / ALPHA] = entry_of<ES>(w, e);
+    }
+    __syncthreads();
+    for (int q = t; q < TT * TT / V; q += TPB) {
+      const int gi = q / CPG, j0 = (q % CPG) * V, cc0 = j0 / ALPHA;
+      T v[V];
+#pragma unroll
+      for (int e = 0; e < V; ++e) v[e] = lds[cc0 + e / ALPHA][gi * ALPHA + e % ALPHA];
+      gst<u32x4>(out + (int64_t)(r0 / ALPHA + gi) * p.ld_out + (int64_t)(c0 + cc0) * ALPHA,
+                 pack16<ES>(v));
+    }
+    return;
+  }
+  const int32_t m_pad = (p.m + ALPHA - 1) / ALPHA * ALPHA;
   for (int q = t; q < TT * TT; q += TPB) {
     const int a = q % ALPHA, rr = (q / ALPHA) % TT, cc = (q / (ALPHA * TT)) * ALPHA + a;
     const int32_t r = r0 + rr, c = c0 + cc;
