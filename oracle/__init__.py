@@ -1,5 +1,5 @@
-"""Plain CPU oracle for the batch-reduce GEMM TPP, its fused epilogue, the Reduce TPP and the
-Transform TPP.
+"""Plain CPU oracle for the batch-reduce GEMM TPP, its fused epilogue (forward, and the inverse
+activations of back-propagation), the Reduce TPP and the Transform TPP.
 
 TEST INFRASTRUCTURE ONLY.  The product path (the HIP library and its Python binding) never
 imports, links or calls anything in this package; only ``tests/``, the smoke check and the
@@ -26,6 +26,10 @@ _SRC = os.path.join(_HERE, "oracle.c")
 F32, BF16 = 0, 1
 STRIDE, OFFSET, ADDRESS = 0, 1, 2
 EPI_BIAS, EPI_RELU, EPI_GELU_TANH = 1, 2, 4
+EPI_RELU_INV, EPI_GELU_TANH_INV, EPI_SAVE_PREACT = 8, 16, 32
+_EPI_BITS = {"bias": EPI_BIAS, "relu": EPI_RELU, "gelu_tanh": EPI_GELU_TANH,
+             "relu_inv": EPI_RELU_INV, "gelu_tanh_inv": EPI_GELU_TANH_INV,
+             "save_preact": EPI_SAVE_PREACT}
 RED_SUM, RED_MUL, RED_MIN, RED_MAX = 0, 1, 2, 3
 RED_BY_COLS, RED_BY_ROWS, RED_X, RED_X2 = 1, 2, 4, 8
 TR_TRANSPOSE, TR_VNNI, TR_VNNI_TO_VNNI_T = 0, 1, 2
@@ -74,6 +78,18 @@ def lib():
         _lib.oracle_brgemm_batched.argtypes = [ctypes.POINTER(_Desc), ctypes.POINTER(_Grid), i64,
                                                vp, vp, vp, vp, vp, vp, vp, vp, i64, vp, vp, vp, vp,
                                                vp, i64, vp, vp, ctypes.c_int]
+        _lib.oracle_brgemm_batched_aux.restype = ctypes.c_int
+        _lib.oracle_brgemm_batched_aux.argtypes = [ctypes.POINTER(_Desc), ctypes.POINTER(_Grid),
+                                                   i64, vp, vp, vp, vp, vp, vp, vp, vp, vp, i64,
+                                                   vp, vp, vp, vp, vp, i64, vp, vp, ctypes.c_int]
+        _lib.oracle_reduce_batched.restype = ctypes.c_int
+        _lib.oracle_reduce_batched.argtypes = [i32, i32, i64, i32, vp, i64, i64, i32,
+                                               ctypes.c_uint32, vp, vp, i64]
+        _lib.oracle_transform_batched.restype = ctypes.c_int
+        _lib.oracle_transform_batched.argtypes = [i32, i32, i32, i64, i64, i32, i32, vp, i64, vp,
+                                                  i64, i64]
+        _lib.oracle_gelu_tanh_grad.restype = ctypes.c_double
+        _lib.oracle_gelu_tanh_grad.argtypes = [ctypes.c_double]
         _lib.oracle_reduce.restype = ctypes.c_int
         _lib.oracle_reduce.argtypes = [i32, i32, i64, i32, vp, i32, ctypes.c_uint32, vp, vp]
         _lib.oracle_transform.restype = ctypes.c_int
@@ -105,11 +121,13 @@ class Desc:
     kind: str = "stride"
     stride_a: int = 0
     stride_b: int = 0
-    flags: set = field(default_factory=set)   # subset of {"bias", "relu", "gelu_tanh"}
+    # subset of {"bias", "relu", "gelu_tanh", "relu_inv", "gelu_tanh_inv", "save_preact"}
+    flags: set = field(default_factory=set)
 
     def _c(self) -> _Desc:
-        fl = (EPI_BIAS if "bias" in self.flags else 0) | (EPI_RELU if "relu" in self.flags else 0) \
-            | (EPI_GELU_TANH if "gelu_tanh" in self.flags else 0)
+        fl = 0
+        for f in self.flags:
+            fl |= _EPI_BITS[f]
         return _Desc(self.m, self.n, self.k, self.lda, self.ldb, self.ldc, _DTYPES[self.ab_type],
                      _DTYPES[self.c_type], float(self.beta), _KINDS[self.kind], self.stride_a,
                      self.stride_b, fl)
@@ -139,18 +157,22 @@ def _pointer_list(base: np.ndarray, elem_offsets, es: int):
 
 def brgemm_batched(desc: Desc, a, b, c, bias=None, *, grid=None, G=1, a_off=None, b_off=None,
                    c_off=None, bias_off=None, count=0, offs_a=None, offs_b=None, begin=None,
-                   idx_a=None, idx_b=None, sel=None, want_ref64=False, nthreads=0):
+                   idx_a=None, idx_b=None, sel=None, want_ref64=False, nthreads=0, aux=None):
     """Run G BRGEMM instances in place on ``c``.
 
     grid: dict with gm, gn, a_step_m, b_step_n, c_step_m, c_step_n, bias_step_m (strided form),
     or None for the explicit per-instance offset arrays.  Address variant: ``idx_a``/``idx_b`` are
     element offsets into the pools ``a``/``b``; they become host addresses here, and ``begin``
     (G+1 entries) splits them into per-instance lists.  Returns the unrounded fp64 results of the
-    selected instances when ``want_ref64``.
+    selected instances when ``want_ref64``.  ``aux``: the tensor of C's type and layout that
+    "save_preact" writes and "relu_inv" / "gelu_tanh_inv" read (in place).
     """
     _check_dtype(a, desc.ab_type, "a")
     _check_dtype(b, desc.ab_type, "b")
     _check_dtype(c, desc.c_type, "c")
+    _check_dtype(aux, desc.c_type, "aux")
+    if aux is not None and (aux.shape != c.shape or not aux.flags.c_contiguous):
+        raise ValueError("aux must be a contiguous array shaped as c")
     if bias is not None and bias.dtype != np.float32:
         raise TypeError("bias must be float32")
     for arr in (a, b, c, bias):
@@ -173,11 +195,11 @@ def brgemm_batched(desc: Desc, a, b, c, bias=None, *, grid=None, G=1, a_off=None
     sel_arr = None if sel is None else _as_i64(sel)
     n_sel = G if sel_arr is None else len(sel_arr)
     ref = np.empty((n_sel, desc.n, desc.m), dtype=np.float64) if want_ref64 else None
-    rc = lib().oracle_brgemm_batched(
+    rc = lib().oracle_brgemm_batched_aux(
         ctypes.byref(d), ctypes.byref(g) if g is not None else None, G,
         _ptr(a_off), _ptr(b_off), _ptr(c_off), _ptr(bias_off),
         _ptr(a) if desc.kind != "address" else None, _ptr(b) if desc.kind != "address" else None,
-        _ptr(c), _ptr(bias), count, _ptr(offs_a), _ptr(offs_b), _ptr(begin), _ptr(ptrs_a),
+        _ptr(c), _ptr(aux), _ptr(bias), count, _ptr(offs_a), _ptr(offs_b), _ptr(begin), _ptr(ptrs_a),
         _ptr(ptrs_b), n_sel, _ptr(sel_arr), _ptr(ref), nthreads)
     if rc != 0:
         raise ValueError("oracle_brgemm_batched rejected its arguments")
@@ -221,6 +243,26 @@ def reduce(x, m: int, n: int, ld: int, in_type: str, op: str, by: str, want=("x"
     return ox, ox2
 
 
+def reduce_batched(x, m: int, n: int, ld: int, in_type: str, G: int, in_stride: int, op: str,
+                   by: str, want=("x",), out_stride=None):
+    """G Reduce TPP calls on blocks ``in_stride`` elements apart; returns (G x outputs) arrays
+    (the outputs of call g start g*out_stride apart; default: packed)."""
+    _check_dtype(x, in_type, "x")
+    ops = {"sum": RED_SUM, "mul": RED_MUL, "min": RED_MIN, "max": RED_MAX}
+    flags = (RED_BY_COLS if by == "cols" else RED_BY_ROWS)
+    flags |= (RED_X if "x" in want else 0) | (RED_X2 if "x2" in want else 0)
+    outn = m if by == "cols" else n
+    ostride = outn if out_stride is None else out_stride
+    size = (G - 1) * ostride + outn if G > 0 else 0
+    ox = np.zeros(size, dtype=np.float64) if "x" in want else None
+    ox2 = np.zeros(size, dtype=np.float64) if "x2" in want else None
+    rc = lib().oracle_reduce_batched(m, n, ld, _DTYPES[in_type], _ptr(x), G, in_stride, ops[op],
+                                     flags, _ptr(ox), _ptr(ox2), ostride)
+    if rc != 0:
+        raise ValueError("oracle_reduce_batched rejected its arguments")
+    return ox, ox2
+
+
 _TR_KINDS = {"transpose": TR_TRANSPOSE, "vnni": TR_VNNI, "vnni_t": TR_VNNI_TO_VNNI_T}
 
 
@@ -245,6 +287,21 @@ def transform(kind: str, m: int, n: int, ld_in: int, ld_out: int, dtype: str, al
     return out
 
 
+def transform_batched(kind: str, m: int, n: int, ld_in: int, ld_out: int, dtype: str,
+                      alpha: int, x: np.ndarray, in_stride: int, out: np.ndarray,
+                      out_stride: int, G: int) -> np.ndarray:
+    """G Transform TPP calls: block g of x (``in_stride`` elements apart) into block g of out
+    (``out_stride`` apart), in place on out."""
+    _check_dtype(x, dtype, "x")
+    _check_dtype(out, dtype, "out")
+    es = 4 if dtype == "f32" else 2
+    rc = lib().oracle_transform_batched(_TR_KINDS[kind], m, n, ld_in, ld_out, es, alpha, _ptr(x),
+                                        in_stride, _ptr(out), out_stride, G)
+    if rc != 0:
+        raise ValueError("oracle_transform_batched rejected its arguments")
+    return out
+
+
 def f32_to_bf16(x: float) -> int:
     return int(lib().oracle_f32_to_bf16(float(x)))
 
@@ -262,6 +319,10 @@ def bf16_to_f32(h: int) -> float:
 
 def gelu_tanh(x: float) -> float:
     return float(lib().oracle_gelu_tanh(float(x)))
+
+
+def gelu_tanh_grad(x: float) -> float:
+    return float(lib().oracle_gelu_tanh_grad(float(x)))
 
 
 def max_threads() -> int:

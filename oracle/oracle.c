@@ -61,6 +61,15 @@ double oracle_gelu_tanh(double x) {
   return 0.5 * x * (1.0 + tanh(c * (x + 0.044715 * x * x * x)));
 }
 
+/* Derivative of that GELU form (the GELU_inv of Table 1, used by back-propagation):
+ * with u = sqrt(2/pi) (x + 0.044715 x^3) and t = tanh(u),
+ *   d/dx [0.5 x (1 + t)] = 0.5 (1 + t) + 0.5 x (1 - t^2) sqrt(2/pi) (1 + 3 * 0.044715 x^2). */
+double oracle_gelu_tanh_grad(double x) {
+  const double c = sqrt(2.0 / 3.14159265358979323846);
+  const double t = tanh(c * (x + 0.044715 * x * x * x));
+  return 0.5 * (1.0 + t) + 0.5 * x * (1.0 - t * t) * c * (1.0 + 3.0 * 0.044715 * x * x);
+}
+
 int oracle_max_threads(void) {
 #ifdef _OPENMP
   return omp_get_max_threads();
@@ -108,7 +117,18 @@ static int check_desc(const oracle_desc* d) {
   if (d->lda < d->m || d->ldb < d->k || d->ldc < d->m) return -1;
   if (d->ab_type != ORACLE_F32 && d->ab_type != ORACLE_BF16) return -1;
   if (d->c_type != ORACLE_F32 && d->c_type != ORACLE_BF16) return -1;
-  if ((d->flags & ORACLE_EPI_RELU) && (d->flags & ORACLE_EPI_GELU_TANH)) return -1;
+  const uint32_t f = d->flags;
+  const uint32_t known = ORACLE_EPI_BIAS | ORACLE_EPI_RELU | ORACLE_EPI_GELU_TANH |
+                         ORACLE_EPI_RELU_INV | ORACLE_EPI_GELU_TANH_INV | ORACLE_EPI_SAVE_PREACT;
+  if (f & ~known) return -1;
+  if ((f & ORACLE_EPI_RELU) && (f & ORACLE_EPI_GELU_TANH)) return -1;
+  if ((f & ORACLE_EPI_RELU_INV) && (f & ORACLE_EPI_GELU_TANH_INV)) return -1;
+  /* an inverse activation multiplies the block by a derivative: no forward activation with it */
+  if ((f & (ORACLE_EPI_RELU_INV | ORACLE_EPI_GELU_TANH_INV)) &&
+      (f & (ORACLE_EPI_RELU | ORACLE_EPI_GELU_TANH | ORACLE_EPI_SAVE_PREACT)))
+    return -1;
+  /* the pre-activation is only worth keeping when an activation follows it */
+  if ((f & ORACLE_EPI_SAVE_PREACT) && !(f & (ORACLE_EPI_RELU | ORACLE_EPI_GELU_TANH))) return -1;
   if (d->kind < ORACLE_STRIDE || d->kind > ORACLE_ADDRESS) return -1;
   return 0;
 }
@@ -118,10 +138,16 @@ static int check_desc(const oracle_desc* d) {
  *   s   = sum_i sum_p A_i(r, p) * B_i(p, c)          (Table 3, Sec. 2.3)
  *   v   = beta * C(r, c) + s                         (C read only when beta != 0)
  *   v  += bias[r]                                    (Add with a column broadcast over n)
+ *   aux(r, c) = round(v)                             (SAVE_PREACT: the pre-activation kept for
+ *                                                     back-propagation, in C's type and layout)
  *   v   = relu(v) or gelu_tanh(v)                    (unary TPP on the finished block, Alg. 6)
- *   C(r, c) = round(v)                               (Identity with conversion)            */
+ *   v   = v * act'(z), z = aux(r, c)                 (RELU_INV / GELU_TANH_INV, Table 1: the
+ *                                                     incoming gradient times the activation's
+ *                                                     derivative at the saved pre-activation)
+ *   C(r, c) = round(v)                               (Identity with conversion)
+ * ReLU's derivative is taken as 1 for z > 0 and 0 otherwise.                                 */
 static void brgemm_resolved(const oracle_desc* d, const char* const* pa, const char* const* pb,
-                            int64_t count, void* c, const float* bias, double* ref64) {
+                            int64_t count, void* c, const float* bias, void* aux, double* ref64) {
   for (int32_t col = 0; col < d->n; ++col) {
     for (int32_t row = 0; row < d->m; ++row) {
       double s = 0.0;
@@ -136,12 +162,23 @@ static void brgemm_resolved(const oracle_desc* d, const char* const* pa, const c
       double v = s;
       if (d->beta != 0.0) v = d->beta * oracle_widen(c, ci, d->c_type) + s;
       if (d->flags & ORACLE_EPI_BIAS) v += (double)bias[row];
+      if (d->flags & ORACLE_EPI_SAVE_PREACT) store_rounded(aux, ci, d->c_type, v);
       if (d->flags & ORACLE_EPI_RELU) v = v > 0.0 ? v : 0.0;
       if (d->flags & ORACLE_EPI_GELU_TANH) v = oracle_gelu_tanh(v);
+      if (d->flags & ORACLE_EPI_RELU_INV) {
+        const double z = oracle_widen(aux, ci, d->c_type);
+        v = z > 0.0 ? v : 0.0;
+      }
+      if (d->flags & ORACLE_EPI_GELU_TANH_INV)
+        v = v * oracle_gelu_tanh_grad(oracle_widen(aux, ci, d->c_type));
       if (ref64) ref64[(int64_t)row + (int64_t)col * d->m] = v;
       store_rounded(c, ci, d->c_type, v);
     }
   }
+}
+
+static int needs_aux(const oracle_desc* d) {
+  return (d->flags & (ORACLE_EPI_RELU_INV | ORACLE_EPI_GELU_TANH_INV | ORACLE_EPI_SAVE_PREACT)) != 0;
 }
 
 static int check_pairs(const oracle_desc* d, const void* a, const void* b, int64_t count,
@@ -156,7 +193,7 @@ static int check_pairs(const oracle_desc* d, const void* a, const void* b, int64
 
 /* One call: resolve the count block addresses, then run the definition. */
 static int brgemm_one(const oracle_desc* d, const void* a, const void* b, void* c,
-                      const float* bias, int64_t count, const int64_t* offs_a,
+                      const float* bias, void* aux, int64_t count, const int64_t* offs_a,
                       const int64_t* offs_b, const void* const* ptrs_a,
                       const void* const* ptrs_b, double* ref64) {
   if (check_pairs(d, a, b, count, offs_a, offs_b, ptrs_a, ptrs_b) != 0) return -1;
@@ -168,7 +205,7 @@ static int brgemm_one(const oracle_desc* d, const void* a, const void* b, void* 
     return -1;
   }
   pair_addresses(d, a, b, count, offs_a, offs_b, ptrs_a, ptrs_b, pa, pb);
-  brgemm_resolved(d, pa, pb, count, c, bias, ref64);
+  brgemm_resolved(d, pa, pb, count, c, bias, aux, ref64);
   free(pa);
   free(pb);
   return 0;
@@ -179,8 +216,18 @@ int oracle_brgemm(const oracle_desc* d, const void* a, const void* b, void* c, c
                   const void* const* ptrs_a, const void* const* ptrs_b, double* ref64) {
   if (check_desc(d) != 0 || !c) return -1;
   if ((d->flags & ORACLE_EPI_BIAS) && !bias) return -1;
-  return brgemm_one(d, a, b, c, bias, count, offs_a, offs_b, ptrs_a, ptrs_b, ref64);
+  if (needs_aux(d)) return -1;   /* single calls carry no aux tensor */
+  return brgemm_one(d, a, b, c, bias, NULL, count, offs_a, offs_b, ptrs_a, ptrs_b, ref64);
 }
+
+int oracle_brgemm_batched_aux(const oracle_desc* d, const oracle_grid* grid, int64_t G,
+                              const int64_t* a_off, const int64_t* b_off, const int64_t* c_off,
+                              const int64_t* bias_off,
+                              const void* a, const void* b, void* c, void* aux, const float* bias,
+                              int64_t count, const int64_t* offs_a, const int64_t* offs_b,
+                              const int64_t* begin, const void* const* ptrs_a,
+                              const void* const* ptrs_b, int64_t n_sel, const int64_t* sel,
+                              double* ref64, int nthreads);
 
 /* The loops around the BRGEMM call that Alg. 6 (FC layer: ib_n, ib_m over output blocks) and
  * Alg. 7 (dilated convolution: pos) write out: G independent calls, each with its own bases.
@@ -196,8 +243,25 @@ int oracle_brgemm_batched(const oracle_desc* d, const oracle_grid* grid, int64_t
                           int64_t count, const int64_t* offs_a, const int64_t* offs_b,
                           const int64_t* begin, const void* const* ptrs_a, const void* const* ptrs_b,
                           int64_t n_sel, const int64_t* sel, double* ref64, int nthreads) {
+  if (d && needs_aux(d)) return -1;
+  return oracle_brgemm_batched_aux(d, grid, G, a_off, b_off, c_off, bias_off, a, b, c, NULL, bias,
+                                   count, offs_a, offs_b, begin, ptrs_a, ptrs_b, n_sel, sel, ref64,
+                                   nthreads);
+}
+
+/* As oracle_brgemm_batched, with the aux tensor: shaped and laid out as C (same leading
+ * dimension, same per-instance offsets) and of C's type. */
+int oracle_brgemm_batched_aux(const oracle_desc* d, const oracle_grid* grid, int64_t G,
+                              const int64_t* a_off, const int64_t* b_off, const int64_t* c_off,
+                              const int64_t* bias_off,
+                              const void* a, const void* b, void* c, void* aux, const float* bias,
+                              int64_t count, const int64_t* offs_a, const int64_t* offs_b,
+                              const int64_t* begin, const void* const* ptrs_a,
+                              const void* const* ptrs_b, int64_t n_sel, const int64_t* sel,
+                              double* ref64, int nthreads) {
   if (check_desc(d) != 0 || G < 0 || !c) return -1;
   if ((d->flags & ORACLE_EPI_BIAS) && !bias) return -1;
+  if (needs_aux(d) && !aux) return -1;
   if (grid && (grid->gm <= 0 || grid->gn <= 0 || grid->gm * grid->gn != G)) return -1;
   if (d->kind == ORACLE_ADDRESS && G > 0 && !begin) return -1;
   if (!sel) n_sel = G;
@@ -228,18 +292,19 @@ int oracle_brgemm_batched(const oracle_desc* d, const oracle_grid* grid, int64_t
       zo = bias_off ? bias_off[g] : 0;
     }
     void* cg = (char*)c + co * es_c;
+    void* xg = aux ? (char*)aux + co * es_c : NULL;
     const float* zg = bias ? bias + zo : NULL;
     double* rg = ref64 ? ref64 + s * (int64_t)d->m * d->n : NULL;
     int rc;
     if (d->kind == ORACLE_ADDRESS) {
       const int64_t lo = begin[g], hi = begin[g + 1];
       rc = (hi < lo) ? -1
-                     : brgemm_one(d, NULL, NULL, cg, zg, hi - lo, NULL, NULL,
+                     : brgemm_one(d, NULL, NULL, cg, zg, xg, hi - lo, NULL, NULL,
                                   ptrs_a ? ptrs_a + lo : NULL, ptrs_b ? ptrs_b + lo : NULL, rg);
     } else {
       const void* ag = a ? (const char*)a + ao * es_ab : NULL;
       const void* bg = b ? (const char*)b + bo * es_ab : NULL;
-      rc = brgemm_one(d, ag, bg, cg, zg, count, offs_a, offs_b, NULL, NULL, rg);
+      rc = brgemm_one(d, ag, bg, cg, zg, xg, count, offs_a, offs_b, NULL, NULL, rg);
     }
     if (rc != 0) failed |= 1;
   }
@@ -345,6 +410,36 @@ int oracle_transform(int32_t kind, int32_t m, int32_t n, int64_t ld_in, int64_t 
           else
             zero_entry(out, oi, es);
         }
+  }
+  return 0;
+}
+
+/* The loop Alg. 6 writes around a TPP call, for the Reduce and Transform TPPs: G independent
+ * calls on blocks in_stride elements apart, whose results are out_stride elements (outputs)
+ * apart. */
+int oracle_reduce_batched(int32_t m, int32_t n, int64_t ld, int32_t in_type, const void* in,
+                          int64_t G, int64_t in_stride, int32_t op, uint32_t flags,
+                          double* out_x, double* out_x2, int64_t out_stride) {
+  if (G < 0 || in_stride < 0 || out_stride < 0) return -1;
+  const int es = elem_size(in_type);
+  for (int64_t g = 0; g < G; ++g) {
+    const int rc = oracle_reduce(m, n, ld, in_type, (const char*)in + g * in_stride * es, op,
+                                 flags, out_x ? out_x + g * out_stride : NULL,
+                                 out_x2 ? out_x2 + g * out_stride : NULL);
+    if (rc != 0) return rc;
+  }
+  return 0;
+}
+
+int oracle_transform_batched(int32_t kind, int32_t m, int32_t n, int64_t ld_in, int64_t ld_out,
+                             int32_t es, int32_t alpha, const void* in, int64_t in_stride,
+                             void* out, int64_t out_stride, int64_t G) {
+  if (G < 0 || in_stride < 0 || out_stride < 0) return -1;
+  for (int64_t g = 0; g < G; ++g) {
+    const int rc = oracle_transform(kind, m, n, ld_in, ld_out, es, alpha,
+                                    in ? (const char*)in + g * in_stride * es : NULL,
+                                    out ? (char*)out + g * out_stride * es : NULL);
+    if (rc != 0) return rc;
   }
   return 0;
 }

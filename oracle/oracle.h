@@ -14,6 +14,10 @@
  *   - Unary Reduce TPP, Table 1 and Sec. 3.1 (reduction-by-columns turns M x N into M x 1).
  *   - Unary Transform TPP, Table 1 and Sec. 3.1: Transpose, VNNI formatting and VNNI to
  *     VNNI-transpose (entry permutations; no arithmetic).
+ *   - For back-propagation through the fused layers (Sec. 5.2.2 implements the backward pass of
+ *     the fully-connected layer with TPPs as well): the RELU_inv / GELU_inv TPPs of Table 1 fused
+ *     after the BRGEMM, the pre-activation kept by the forward call, and the loops of Alg. 6 around
+ *     the Reduce and Transform TPPs.
  *
  * Storage reading: every 2D block is column-major with a leading dimension (element (r, c) of an
  * m x n block sits at base + r + c*ld), which is how Alg. 6 lays out its blocked tensors (the
@@ -30,7 +34,8 @@ extern "C" {
 
 enum { ORACLE_F32 = 0, ORACLE_BF16 = 1 };
 enum { ORACLE_STRIDE = 0, ORACLE_OFFSET = 1, ORACLE_ADDRESS = 2 };
-enum { ORACLE_EPI_BIAS = 1u, ORACLE_EPI_RELU = 2u, ORACLE_EPI_GELU_TANH = 4u };
+enum { ORACLE_EPI_BIAS = 1u, ORACLE_EPI_RELU = 2u, ORACLE_EPI_GELU_TANH = 4u,
+       ORACLE_EPI_RELU_INV = 8u, ORACLE_EPI_GELU_TANH_INV = 16u, ORACLE_EPI_SAVE_PREACT = 32u };
 enum { ORACLE_RED_SUM = 0, ORACLE_RED_MUL = 1, ORACLE_RED_MIN = 2, ORACLE_RED_MAX = 3 };
 enum { ORACLE_RED_BY_COLS = 1u, ORACLE_RED_BY_ROWS = 2u, ORACLE_RED_X = 4u, ORACLE_RED_X2 = 8u };
 enum { ORACLE_TR_TRANSPOSE = 0, ORACLE_TR_VNNI = 1, ORACLE_TR_VNNI_TO_VNNI_T = 2 };
@@ -70,6 +75,20 @@ int oracle_brgemm_batched(const oracle_desc* d, const oracle_grid* grid, int64_t
                           const int64_t* begin, const void* const* ptrs_a, const void* const* ptrs_b,
                           int64_t n_sel, const int64_t* sel, double* ref64, int nthreads);
 
+/* As oracle_brgemm_batched, with an aux tensor of C's type, shaped and laid out as C (same
+ * leading dimension and per-instance offsets).  SAVE_PREACT (with RELU or GELU_TANH) writes the
+ * pre-activation beta*C + sum + bias, rounded to C's type, into aux before the activation;
+ * RELU_INV / GELU_TANH_INV (Table 1's inverse activations for back-propagation) multiply the
+ * block by the activation's derivative at z = aux.  Calls without these flags may pass NULL. */
+int oracle_brgemm_batched_aux(const oracle_desc* d, const oracle_grid* grid, int64_t G,
+                              const int64_t* a_off, const int64_t* b_off, const int64_t* c_off,
+                              const int64_t* bias_off,
+                              const void* a, const void* b, void* c, void* aux, const float* bias,
+                              int64_t count, const int64_t* offs_a, const int64_t* offs_b,
+                              const int64_t* begin, const void* const* ptrs_a,
+                              const void* const* ptrs_b, int64_t n_sel, const int64_t* sel,
+                              double* ref64, int nthreads);
+
 /* Reduce TPP on an m x n column-major tensor.  BY_COLS folds across the n columns (m outputs),
  * BY_ROWS folds across the m rows (n outputs).  X / X2 select the input x or its square x*x;
  * both may be set.  Outputs are unrounded doubles. */
@@ -93,6 +112,16 @@ int oracle_reduce(int32_t m, int32_t n, int64_t ld, int32_t in_type, const void*
 int oracle_transform(int32_t kind, int32_t m, int32_t n, int64_t ld_in, int64_t ld_out,
                      int32_t es, int32_t alpha, const void* in, void* out);
 
+/* G calls of the Reduce / Transform TPP on blocks in_stride elements apart (the loops Alg. 6
+ * writes around a TPP); outputs of call g start out_stride elements (doubles for the reduce)
+ * after those of call g - 1. */
+int oracle_reduce_batched(int32_t m, int32_t n, int64_t ld, int32_t in_type, const void* in,
+                          int64_t G, int64_t in_stride, int32_t op, uint32_t flags,
+                          double* out_x, double* out_x2, int64_t out_stride);
+int oracle_transform_batched(int32_t kind, int32_t m, int32_t n, int64_t ld_in, int64_t ld_out,
+                             int32_t es, int32_t alpha, const void* in, int64_t in_stride,
+                             void* out, int64_t out_stride, int64_t G);
+
 /* Helpers the tests pin on their own: exact widening and the round-to-nearest-even narrowing
  * used for every output element. */
 double   oracle_widen(const void* base, int64_t idx, int32_t dtype);
@@ -100,6 +129,7 @@ uint16_t oracle_f32_to_bf16(float f);
 void     oracle_f32_to_bf16_array(const float* in, uint16_t* out, int64_t n);
 float    oracle_bf16_to_f32(uint16_t h);
 double   oracle_gelu_tanh(double x);
+double   oracle_gelu_tanh_grad(double x);
 int      oracle_max_threads(void);
 
 #ifdef __cplusplus

@@ -27,7 +27,8 @@ MUTANTS = {
     "bias_by_column": ("v += (double)bias[row];", "v += (double)bias[col % d->m];"),
     "relu_sign": ("v = v > 0.0 ? v : 0.0;", "v = v < 0.0 ? v : 0.0;"),
     "gelu_sign": ("(1.0 + tanh(", "(1.0 - tanh("),
-    "gelu_cubic": ("0.044715 * x * x * x", "0.044715 * x * x"),
+    "gelu_cubic": ("(1.0 + tanh(c * (x + 0.044715 * x * x * x)))",
+                   "(1.0 + tanh(c * (x + 0.044715 * x * x)))"),
     "rne_ties_up": ("rest > 0x8000u ||", "rest >= 0x8000u ||"),
     "grid_swapped": ("co = gi_m * grid->c_step_m + gi_n * grid->c_step_n;",
                      "co = gi_n * grid->c_step_m + gi_m * grid->c_step_n;"),
@@ -54,6 +55,25 @@ TRANSFORM_MUTANTS = {
     "vnni_t_row_of_group": ("const int32_t r = g * alpha + a;", "const int32_t r = g + a * alpha;"),
     "vnni_t_pad_not_zero": ("          if (r < m)\n            move_entry(out, oi, in, (int64_t)(c / alpha) * ld_in",
                             "          if (r < m || 1)\n            move_entry(out, oi, in, (int64_t)(c / alpha) * ld_in"),
+}
+
+# Back-propagation mutants (inverse activations, saved pre-activation, batched loops), caught by
+# the backward pins.
+BACKWARD_MUTANTS = {
+    "gelu_grad_dropped_term": (" + 0.5 * x * (1.0 - t * t) * c * (1.0 + 3.0 * 0.044715 * x * x);",
+                               ";"),
+    "gelu_grad_cubic_factor": ("(1.0 + 3.0 * 0.044715 * x * x)", "(1.0 + 0.044715 * x * x)"),
+    "relu_inv_at_zero": ("v = z > 0.0 ? v : 0.0;", "v = z >= 0.0 ? v : 0.0;"),
+    "gelu_inv_at_output": ("v = v * oracle_gelu_tanh_grad(oracle_widen(aux, ci, d->c_type));",
+                           "v = v * oracle_gelu_tanh_grad(v);"),
+    "preact_saved_after_act": (
+        "if (d->flags & ORACLE_EPI_SAVE_PREACT) store_rounded(aux, ci, d->c_type, v);\n"
+        "      if (d->flags & ORACLE_EPI_RELU) v = v > 0.0 ? v : 0.0;",
+        "if (d->flags & ORACLE_EPI_RELU) v = v > 0.0 ? v : 0.0;\n"
+        "      if (d->flags & ORACLE_EPI_SAVE_PREACT) store_rounded(aux, ci, d->c_type, v);"),
+    "transform_batch_stride_bytes": ("(const char*)in + g * in_stride * es,",
+                                     "(const char*)in + g * in_stride,"),
+    "reduce_batch_out_packed": ("out_x ? out_x + g * out_stride : NULL", "out_x ? out_x + g * m : NULL"),
 }
 
 
@@ -89,3 +109,9 @@ def test_pins_catch_planted_mistake(name, source, tmp_path):
 def test_transform_pins_catch_planted_mistake(name, source, tmp_path):
     old, new = TRANSFORM_MUTANTS[name]
     _caught(old, new, "test_oracle_transform_pins.py", source, tmp_path, name)
+
+
+@pytest.mark.parametrize("name", sorted(BACKWARD_MUTANTS))
+def test_backward_pins_catch_planted_mistake(name, source, tmp_path):
+    old, new = BACKWARD_MUTANTS[name]
+    _caught(old, new, "test_oracle_backward_pins.py", source, tmp_path, name)

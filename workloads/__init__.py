@@ -17,6 +17,10 @@ base + r + c*ld, the way Alg. 6 lays out its blocked tensors with the b_m / b_k 
                 block) drawn from pools of blocks, beta = 1, fp32 out
   reduce_bn     the Reduce TPP on a conv output: per-channel sum and sum of squares (the
                 statistics step of batchnorm, Sec. 5.1.2)
+  mlp_backward  the transformer MLP trained: GEMM1 keeping its pre-activation, then the backward
+                pass through both layers (weight transposes, GELU_inv fused into the data
+                gradient, weight gradients batch-reduced over token blocks, bias gradients by the
+                Reduce TPP)
 
 The default sizes are the full sizes; every generator takes smaller sizes for oracle-speed tests.
 """
@@ -74,6 +78,7 @@ class Call:
     b: Optional[str] = None
     c: Optional[str] = None
     bias: Optional[str] = None
+    aux: Optional[str] = None              # tensor shaped as C: saved / read pre-activation
 
     @property
     def pairs(self) -> int:
@@ -88,12 +93,47 @@ class Call:
 
 
 @dataclass
+class TransformStep:
+    """G Transform TPP calls over blocks ``in_stride`` / ``out_stride`` elements apart."""
+    kind: str
+    m: int
+    n: int
+    ld_in: int
+    ld_out: int
+    dtype: str
+    src: str
+    dst: str
+    G: int = 1
+    in_stride: int = 0
+    out_stride: int = 0
+    alpha: int = 1
+
+
+@dataclass
+class ReduceStep:
+    """G Reduce TPP calls; outputs of call g start ``out_stride`` floats after call g - 1's."""
+    src: str
+    m: int
+    n: int
+    ld: int
+    in_type: str
+    op: str
+    by: str
+    dst_x: Optional[str] = None
+    dst_x2: Optional[str] = None
+    G: int = 1
+    in_stride: int = 0
+    out_stride: int = 0
+
+
+@dataclass
 class Workload:
     name: str
     arrays: dict
     calls: list
     reduce: Optional[dict] = None
     notes: str = ""
+    steps: Optional[list] = None   # ordered Call / TransformStep / ReduceStep (chained workloads)
 
     @property
     def flops(self) -> int:
@@ -212,6 +252,85 @@ def gathered(seed: int = 5, n_out: int = 4096, pool: int = 8192, m: int = 128, n
                 idx_a=(ia * m * k).astype(np.int64), idx_b=(ib * k * n).astype(np.int64),
                 a="apool", b="bpool", c="c")
     return Workload("gathered", dict(apool=apool, bpool=bpool, c=c), [call])
+
+
+def mlp_backward(seed: int = 6, tokens: int = 8192, hidden: int = 1024,
+                 inter: int = 4096) -> Workload:
+    """One training step's worth of the transformer MLP's first layer forward and both layers'
+    backward, on the blocked layouts of :func:`mlp_block` (column-major 64 x 64 blocks).
+
+    Forward (kept for back-propagation): Z = W1 X + b1 saved in ``z`` (bf16, H's layout), H =
+    gelu(Z) in ``h``.  The incoming gradient dY (N(0,1), Y's layout [Nb][Hb][64n][64h]) then gives
+      dZ  = (W2^T dY) * gelu'(Z)      B1: A = W2 blocks transposed, GELU_inv fused, bf16
+      dW2 = sum over tokens dY H^T    B2: A = dY, B = H blocks transposed, fp32
+      db2 = sum over tokens dY        two Reduce TPP calls (over token blocks, then within one)
+      dX  = W1^T dZ                   B3: A = W1 blocks transposed, bf16
+      dW1 = sum over tokens dZ X^T    B4: A = dZ, B = X blocks transposed, fp32
+      db1 = sum over tokens dZ        two Reduce TPP calls
+    Every transposed operand is a batched Transform TPP (transpose of each 64 x 64 block in place
+    of the block).  The weight gradients keep W's blocked layout, dX keeps X's.
+    """
+    rng = np.random.default_rng(seed)
+    nb, hb, ib = tokens // BLK, hidden // BLK, inter // BLK
+    blk = BLK * BLK
+    x = bf16_bits(_normal(rng, (nb, hb, BLK, BLK), 1.0))
+    w1 = bf16_bits(_normal(rng, (ib, hb, BLK, BLK), 0.02))
+    b1 = _normal(rng, (inter,), 0.02)
+    w2 = bf16_bits(_normal(rng, (hb, ib, BLK, BLK), 0.02))
+    dy = bf16_bits(_normal(rng, (nb, hb, BLK, BLK), 1.0))
+    nan16 = lambda shape: np.full(shape, 0x7FC0, dtype=np.uint16)
+    nan32 = lambda shape: np.full(shape, np.nan, dtype=np.float32)
+    arrays = dict(x=x, w1=w1, b1=b1, w2=w2, dy=dy,
+                  z=nan16((nb, ib, BLK, BLK)), h=nan16((nb, ib, BLK, BLK)),
+                  w1t=nan16((ib, hb, BLK, BLK)), w2t=nan16((hb, ib, BLK, BLK)),
+                  ht=nan16((nb, ib, BLK, BLK)), xt=nan16((nb, hb, BLK, BLK)),
+                  dz=nan16((nb, ib, BLK, BLK)), dx=nan16((nb, hb, BLK, BLK)),
+                  dw1=nan32((ib, hb, BLK, BLK)), dw2=nan32((hb, ib, BLK, BLK)),
+                  p1=nan32((ib * blk,)), p2=nan32((hb * blk,)),
+                  db1=nan32((inter,)), db2=nan32((hidden,)))
+    sq = lambda **kw: dict(dict(gm=1, gn=1, a_step_m=0, b_step_n=0, c_step_m=0, c_step_n=0,
+                                bias_step_m=0), **kw)
+    fwd = Call(BLK, BLK, BLK, BLK, BLK, BLK, "bf16", "bf16", 0.0, "stride", blk, blk,
+               {"bias", "gelu_tanh", "save_preact"}, G=ib * nb,
+               grid=sq(gm=ib, gn=nb, a_step_m=hb * blk, b_step_n=hb * blk, c_step_m=blk,
+                       c_step_n=ib * blk, bias_step_m=BLK),
+               count=hb, a="w1", b="x", c="h", bias="b1", aux="z")
+    tr = lambda src, dst, g: TransformStep("transpose", BLK, BLK, BLK, BLK, "bf16", src, dst,
+                                           G=g, in_stride=blk, out_stride=blk)
+    # dZ[nb][ib] (i x n) = gelu'(Z) * sum_hb W2[hb][ib]^T (i x h) dY[nb][hb] (h x n)
+    b1c = Call(BLK, BLK, BLK, BLK, BLK, BLK, "bf16", "bf16", 0.0, "stride", ib * blk, blk,
+               {"gelu_tanh_inv"}, G=ib * nb,
+               grid=sq(gm=ib, gn=nb, a_step_m=blk, b_step_n=hb * blk, c_step_m=blk,
+                       c_step_n=ib * blk),
+               count=hb, a="w2t", b="dy", c="dz", aux="z")
+    # dW2[hb][ib] (h x i) = sum_nb dY[nb][hb] (h x n) H[nb][ib]^T (n x i)
+    b2c = Call(BLK, BLK, BLK, BLK, BLK, BLK, "bf16", "f32", 0.0, "stride", hb * blk, ib * blk,
+               set(), G=hb * ib,
+               grid=sq(gm=hb, gn=ib, a_step_m=blk, b_step_n=blk, c_step_m=ib * blk,
+                       c_step_n=blk),
+               count=nb, a="dy", b="ht", c="dw2")
+    # dX[nb][hb] (h x n) = sum_ib W1[ib][hb]^T (h x i) dZ[nb][ib] (i x n)
+    b3c = Call(BLK, BLK, BLK, BLK, BLK, BLK, "bf16", "bf16", 0.0, "stride", hb * blk, blk,
+               set(), G=hb * nb,
+               grid=sq(gm=hb, gn=nb, a_step_m=blk, b_step_n=ib * blk, c_step_m=blk,
+                       c_step_n=hb * blk),
+               count=ib, a="w1t", b="dz", c="dx")
+    # dW1[ib][hb] (i x h) = sum_nb dZ[nb][ib] (i x n) X[nb][hb]^T (n x h)
+    b4c = Call(BLK, BLK, BLK, BLK, BLK, BLK, "bf16", "f32", 0.0, "stride", ib * blk, hb * blk,
+               set(), G=ib * hb,
+               grid=sq(gm=ib, gn=hb, a_step_m=blk, b_step_n=blk, c_step_m=hb * blk,
+                       c_step_n=blk),
+               count=nb, a="dz", b="xt", c="dw1")
+    # bias gradients: rows (feature within block, token within block, feature block) of the
+    # gradient summed over the token blocks, then each 64 x 64 block's columns summed
+    red = lambda src, fb, p, db: [
+        ReduceStep(src, fb * blk, nb, fb * blk, "bf16", "sum", "cols", dst_x=p),
+        ReduceStep(p, BLK, BLK, BLK, "f32", "sum", "cols", dst_x=db, G=fb, in_stride=blk,
+                   out_stride=BLK)]
+    steps = [fwd, tr("w2", "w2t", hb * ib), tr("w1", "w1t", ib * hb), tr("h", "ht", nb * ib),
+             tr("x", "xt", nb * hb), b1c, b2c, *red("dy", hb, "p2", "db2"), b3c, b4c,
+             *red("dz", ib, "p1", "db1")]
+    return Workload("mlp_backward", arrays, [fwd, b1c, b2c, b3c, b4c], steps=steps)
 
 
 CONFIGS = {
