@@ -13,6 +13,8 @@
  *     GELU and Identity-with-conversion), applied to the finished C block as Alg. 6 applies its
  *     UNARY:  C = cvt( act( beta * C + sum_i A_i B_i + bias[row] ) );
  *   - the unary Reduce TPP, Table 1 (rows or columns, SUM / MUL / MIN / MAX, of x or x*x).
+ * For back-propagation the epilogue also takes Table 1's inverse activations (RELU_inv, GELU_inv)
+ * and can keep the forward pre-activation for them, and the Reduce TPP runs as a batch of calls.
  *
  * Conventions for every entry point
  *   - 2D blocks are column-major with a leading dimension: element (r, c) of an m x n block lives
@@ -55,11 +57,25 @@ typedef enum {
   TPP_BR_ADDRESS = 2   /* address_A_i = ptrs_a[i]                                               */
 } tpp_br_kind;
 
-/* Epilogue bits.  RELU and GELU_TANH exclude each other. */
+/* Epilogue bits.  RELU and GELU_TANH exclude each other.
+ * The last three serve back-propagation (Table 1 pairs RELU and GELU with the inverses that the
+ * backward pass uses; Sec. 5.2.2 builds the backward pass of the fully-connected layer from the
+ * same TPPs).  They use an AUX tensor of C's type, shaped and laid out exactly as C (same ldc,
+ * same per-instance offsets), and need tpp_brgemm_execute_batched_aux:
+ *   SAVE_PREACT    with RELU or GELU_TANH: aux = the pre-activation beta C + sum + bias, rounded
+ *                  to C's type, written before the activation (the forward call of training).
+ *   RELU_INV       C = v * (z > 0 ? 1 : 0), z = aux: the incoming gradient v masked where the
+ *                  saved pre-activation was not positive.
+ *   GELU_TANH_INV  C = v * gelu'(z), z = aux, gelu' the derivative of the GELU_TANH form.
+ * RELU_INV and GELU_TANH_INV exclude each other and RELU, GELU_TANH and SAVE_PREACT; v is
+ * beta C + sum (+ bias[row] when BIAS is set). */
 enum {
   TPP_EPI_BIAS = 1u << 0,      /* + bias[row]: fp32 column vector of length m, broadcast over n  */
   TPP_EPI_RELU = 1u << 1,      /* x > 0 ? x : +0                                                 */
-  TPP_EPI_GELU_TANH = 1u << 2  /* 0.5 x (1 + tanh(sqrt(2/pi) (x + 0.044715 x^3)))                */
+  TPP_EPI_GELU_TANH = 1u << 2, /* 0.5 x (1 + tanh(sqrt(2/pi) (x + 0.044715 x^3)))                */
+  TPP_EPI_RELU_INV = 1u << 3,
+  TPP_EPI_GELU_TANH_INV = 1u << 4,
+  TPP_EPI_SAVE_PREACT = 1u << 5
 };
 
 /* Problem description: the dispatch-time fields of the TPP (Sec. 2.2: rows, columns, leading
@@ -82,8 +98,9 @@ typedef struct tpp_brgemm_kernel_s* tpp_brgemm_handle;
 
 /* Dispatch (Sec. 3): validate the description and return the cached handle for it; equal
  * descriptions return the same handle.  Host-only: no device work, safe without a GPU.
- * Errors: INVALID_ARG for sizes <= 0, ld too small, RELU together with GELU_TANH, unknown kind
- * or flag bits, NULL desc/out; UNSUPPORTED for other type combinations. */
+ * Errors: INVALID_ARG for sizes <= 0, ld too small, RELU together with GELU_TANH, an excluded
+ * combination of the back-propagation bits, unknown kind or flag bits, NULL desc/out;
+ * UNSUPPORTED for other type combinations. */
 tpp_status tpp_brgemm_dispatch(const tpp_brgemm_desc* desc, tpp_brgemm_handle* out);
 
 /* The call API for one BRGEMM (Sec. 2.3 / Alg. 2): C = epi(beta C + sum_{i<count} A_i B_i).
@@ -95,8 +112,9 @@ tpp_status tpp_brgemm_dispatch(const tpp_brgemm_desc* desc, tpp_brgemm_handle* o
  * An fp32 call whose output is only a few 64 x 64 tiles splits the pair list over several
  * workgroups; their partial sums go to a device work buffer the library keeps per GPU and per
  * stream (as tpp_reduce) and are added in a fixed order, so results do not vary between runs.
- * Errors: INVALID_ARG for a NULL handle, count < 0, or a NULL pointer the call needs; NO_MEMORY
- * if that work buffer cannot be allocated. */
+ * Errors: INVALID_ARG for a NULL handle, count < 0, a NULL pointer the call needs, or a handle
+ * with an AUX bit (those run through tpp_brgemm_execute_batched_aux); NO_MEMORY if that work
+ * buffer cannot be allocated. */
 tpp_status tpp_brgemm_execute_stride(tpp_brgemm_handle h, const void* a, const void* b, void* c,
                                      const float* bias, int64_t count, void* stream);
 tpp_status tpp_brgemm_execute_offset(tpp_brgemm_handle h, const void* a, const void* b,
@@ -140,6 +158,21 @@ tpp_status tpp_brgemm_execute_batched(tpp_brgemm_handle h, const tpp_grid_stride
                                       const void* const* d_ptrs_a, const void* const* d_ptrs_b,
                                       void* stream);
 
+/* tpp_brgemm_execute_batched with the AUX tensor of TPP_EPI_SAVE_PREACT, TPP_EPI_RELU_INV and
+ * TPP_EPI_GELU_TANH_INV (device, C's type, laid out as C: instance g's block at the offset of its
+ * C block).  aux is written (SAVE_PREACT) or only read (the inverses); it must not overlap C or
+ * any A_i / B_i.  A handle without AUX bits ignores aux (it may be NULL).
+ * Errors: those of tpp_brgemm_execute_batched, plus INVALID_ARG for a NULL aux the handle needs. */
+tpp_status tpp_brgemm_execute_batched_aux(tpp_brgemm_handle h, const tpp_grid_strided* grid,
+                                          int64_t G, const int64_t* d_a_off,
+                                          const int64_t* d_b_off, const int64_t* d_c_off,
+                                          const int64_t* d_bias_off, const void* a,
+                                          const void* b, void* c, void* aux, const float* bias,
+                                          int64_t count, const int64_t* d_offs_a,
+                                          const int64_t* d_offs_b, const int64_t* d_begin,
+                                          const void* const* d_ptrs_a,
+                                          const void* const* d_ptrs_b, void* stream);
+
 /* Handles live in the cache until the process ends; release is a no-op kept for symmetry with
  * dispatch, and is safe on NULL. */
 void tpp_brgemm_release(tpp_brgemm_handle h);
@@ -168,6 +201,16 @@ enum {
 };
 tpp_status tpp_reduce(int32_t m, int32_t n, int64_t ld, int32_t in_type, const void* in,
                       int32_t op, uint32_t flags, float* out_x, float* out_x2, void* stream);
+
+/* G Reduce TPP calls in one launch (the loop Alg. 6 writes around a TPP, here for the bias
+ * gradients of a blocked layer): call g folds the m x n block at in + g * in_stride (elements)
+ * and writes its outputs at out_x + g * out_stride and out_x2 + g * out_stride (floats).  Every
+ * call has the shape, op and flags above.  G == 0 is a no-op.
+ * Errors: those of tpp_reduce, plus INVALID_ARG for G, in_stride or out_stride < 0;
+ * UNSUPPORTED when one launch would need more than 2^31 - 1 workgroups. */
+tpp_status tpp_reduce_batched(int32_t m, int32_t n, int64_t ld, int32_t in_type, const void* in,
+                              int64_t G, int64_t in_stride, int32_t op, uint32_t flags,
+                              float* out_x, float* out_x2, int64_t out_stride, void* stream);
 
 /* Static text for a status code, and the last error's detail for the calling thread. */
 const char* tpp_status_string(tpp_status s);

@@ -53,6 +53,17 @@ typedef enum {
 tpp_status tpp_transform(int32_t kind, int32_t m, int32_t n, int64_t ld_in, int64_t ld_out,
                          int32_t dtype, int32_t alpha, const void* in, void* out, void* stream);
 
+/* G Transform TPP calls in one launch (the loop Alg. 6 writes around a TPP; e.g. the transpose
+ * of every 64 x 64 block of a blocked weight tensor that the backward pass multiplies by):
+ * call g transforms the block at in + g * in_stride into out + g * out_stride (elements), each
+ * as tpp_transform does with the arguments above.  G == 0 is a no-op.  No output block may
+ * overlap an input block or another output block.
+ * Errors: those of tpp_transform, plus INVALID_ARG for G, in_stride or out_stride < 0. */
+tpp_status tpp_transform_batched(int32_t kind, int32_t m, int32_t n, int64_t ld_in,
+                                 int64_t ld_out, int32_t dtype, int32_t alpha, const void* in,
+                                 int64_t in_stride, void* out, int64_t out_stride, int64_t G,
+                                 void* stream);
+
 #ifdef __cplusplus
 }
 #endif

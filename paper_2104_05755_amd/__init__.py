@@ -28,6 +28,7 @@ TPP_OK, TPP_ERR_INVALID_ARG, TPP_ERR_UNSUPPORTED, TPP_ERR_HIP, TPP_ERR_NO_MEMORY
 TPP_DT_F32, TPP_DT_BF16 = 0, 1
 TPP_BR_STRIDE, TPP_BR_OFFSET, TPP_BR_ADDRESS = 0, 1, 2
 TPP_EPI_BIAS, TPP_EPI_RELU, TPP_EPI_GELU_TANH = 1, 2, 4
+TPP_EPI_RELU_INV, TPP_EPI_GELU_TANH_INV, TPP_EPI_SAVE_PREACT = 8, 16, 32
 TPP_RED_SUM, TPP_RED_MUL, TPP_RED_MIN, TPP_RED_MAX = 0, 1, 2, 3
 TPP_RED_BY_COLS, TPP_RED_BY_ROWS, TPP_RED_X, TPP_RED_X2 = 1, 2, 4, 8
 TPP_TR_TRANSPOSE, TPP_TR_VNNI, TPP_TR_VNNI_TO_VNNI_T = 0, 1, 2
@@ -74,12 +75,19 @@ _sig("tpp_brgemm_execute_address", _i32, _c_void_p, _c_void_p, _c_void_p, _c_voi
 _sig("tpp_brgemm_execute_batched", _i32, _c_void_p, ctypes.POINTER(tpp_grid_strided), _i64,
      _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p,
      _i64, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p)
+_sig("tpp_brgemm_execute_batched_aux", _i32, _c_void_p, ctypes.POINTER(tpp_grid_strided), _i64,
+     _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p,
+     _c_void_p, _i64, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p)
 _sig("tpp_brgemm_release", None, _c_void_p)
 _sig("tpp_brgemm_describe", _i32, _c_void_p, ctypes.c_char_p, ctypes.c_size_t)
 _sig("tpp_reduce", _i32, _i32, _i32, _i64, _i32, _c_void_p, _i32, ctypes.c_uint32, _c_void_p,
      _c_void_p, _c_void_p)
 _sig("tpp_transform", _i32, _i32, _i32, _i32, _i64, _i64, _i32, _i32, _c_void_p, _c_void_p,
      _c_void_p)
+_sig("tpp_reduce_batched", _i32, _i32, _i32, _i64, _i32, _c_void_p, _i64, _i64, _i32,
+     ctypes.c_uint32, _c_void_p, _c_void_p, _i64, _c_void_p)
+_sig("tpp_transform_batched", _i32, _i32, _i32, _i32, _i64, _i64, _i32, _i32, _c_void_p, _i64,
+     _c_void_p, _i64, _i64, _c_void_p)
 
 
 def _p(x):
@@ -124,18 +132,31 @@ def tpp_brgemm_execute_address(h, ptrs_a, ptrs_b, c, bias, count, stream=None):
                                            stream), "tpp_brgemm_execute_address")
 
 
+def _grid(grid):
+    if grid is None or isinstance(grid, tpp_grid_strided):
+        return grid
+    return tpp_grid_strided(*(int(grid[f]) for f in ("gm", "gn", "a_step_m", "b_step_n",
+                                                     "c_step_m", "c_step_n", "bias_step_m")))
+
+
 def tpp_brgemm_execute_batched(h, grid, G, a_off, b_off, c_off, bias_off, a, b, c, bias, count,
                                offs_a, offs_b, begin, ptrs_a, ptrs_b, stream=None):
     """grid: tpp_grid_strided, a dict with its fields, or None (explicit offset arrays)."""
-    g = None
-    if grid is not None:
-        g = grid if isinstance(grid, tpp_grid_strided) else tpp_grid_strided(
-            *(int(grid[f]) for f in ("gm", "gn", "a_step_m", "b_step_n", "c_step_m",
-                                     "c_step_n", "bias_step_m")))
+    g = _grid(grid)
     _check(_lib.tpp_brgemm_execute_batched(
         h, ctypes.byref(g) if g is not None else None, G, _p(a_off), _p(b_off), _p(c_off),
         _p(bias_off), _p(a), _p(b), _p(c), _p(bias), count, _p(offs_a), _p(offs_b), _p(begin),
         _p(ptrs_a), _p(ptrs_b), stream), "tpp_brgemm_execute_batched")
+
+
+def tpp_brgemm_execute_batched_aux(h, grid, G, a_off, b_off, c_off, bias_off, a, b, c, aux, bias,
+                                   count, offs_a, offs_b, begin, ptrs_a, ptrs_b, stream=None):
+    """tpp_brgemm_execute_batched with the aux tensor (shaped and laid out as c)."""
+    g = _grid(grid)
+    _check(_lib.tpp_brgemm_execute_batched_aux(
+        h, ctypes.byref(g) if g is not None else None, G, _p(a_off), _p(b_off), _p(c_off),
+        _p(bias_off), _p(a), _p(b), _p(c), _p(aux), _p(bias), count, _p(offs_a), _p(offs_b),
+        _p(begin), _p(ptrs_a), _p(ptrs_b), stream), "tpp_brgemm_execute_batched_aux")
 
 
 def tpp_brgemm_release(h):
@@ -158,6 +179,18 @@ def tpp_transform(kind, m, n, ld_in, ld_out, dtype, alpha, x, out, stream=None):
            "tpp_transform")
 
 
+def tpp_reduce_batched(m, n, ld, in_type, x, G, in_stride, op, flags, out_x, out_x2, out_stride,
+                       stream=None):
+    _check(_lib.tpp_reduce_batched(m, n, ld, in_type, _p(x), G, in_stride, op, flags, _p(out_x),
+                                   _p(out_x2), out_stride, stream), "tpp_reduce_batched")
+
+
+def tpp_transform_batched(kind, m, n, ld_in, ld_out, dtype, alpha, x, in_stride, out, out_stride,
+                          G, stream=None):
+    _check(_lib.tpp_transform_batched(kind, m, n, ld_in, ld_out, dtype, alpha, _p(x), in_stride,
+                                      _p(out), out_stride, G, stream), "tpp_transform_batched")
+
+
 def tpp_status_string(s: int) -> str:
     return _lib.tpp_status_string(s).decode()
 
@@ -169,10 +202,13 @@ def tpp_last_error_message() -> str:
 def make_desc(m, n, k, lda, ldb, ldc, ab_type="bf16", c_type="f32", beta=0.0, kind="stride",
               stride_a=0, stride_b=0, flags=()) -> tpp_brgemm_desc:
     """Convenience: a descriptor from readable names (dtype "f32"/"bf16", kind
-    "stride"/"offset"/"address", flags from {"bias", "relu", "gelu_tanh"})."""
+    "stride"/"offset"/"address", flags from {"bias", "relu", "gelu_tanh", "relu_inv",
+    "gelu_tanh_inv", "save_preact"})."""
     dt = {"f32": TPP_DT_F32, "bf16": TPP_DT_BF16}
     kd = {"stride": TPP_BR_STRIDE, "offset": TPP_BR_OFFSET, "address": TPP_BR_ADDRESS}
-    fl = {"bias": TPP_EPI_BIAS, "relu": TPP_EPI_RELU, "gelu_tanh": TPP_EPI_GELU_TANH}
+    fl = {"bias": TPP_EPI_BIAS, "relu": TPP_EPI_RELU, "gelu_tanh": TPP_EPI_GELU_TANH,
+          "relu_inv": TPP_EPI_RELU_INV, "gelu_tanh_inv": TPP_EPI_GELU_TANH_INV,
+          "save_preact": TPP_EPI_SAVE_PREACT}
     bits = 0
     for f in flags:
         bits |= fl[f]

@@ -71,6 +71,107 @@ __device__ __forceinline__ float activate(float v, uint32_t flags) {
   return v;
 }
 
+// Derivative of gelu_tanh, for GELU_inv (Table 1).  With s = 0.5 (1 + tanh u) = 1 / (1 + e^(-2u))
+// the GELU is x s, so its derivative is s + 2 x s (1 - s) u', where 1 - s = e^(-2u) s (no
+// cancellation) and u' = sqrt(2/pi) (1 + 3 * 0.044715 x^2).  The argument is clamped to [-9, 9]:
+// beyond it the derivative is 0 or 1 to within 3e-27, and the clamp keeps e^(-2u) finite and s a
+// normal number, so no inf * 0 arises.
+__device__ __forceinline__ float gelu_tanh_grad(float z) {
+  const float x = fminf(fmaxf(z, -9.0f), 9.0f);
+  const float k1 = -2.3022082f;    // -2 log2(e) sqrt(2/pi), as in gelu_tanh
+  const float k2 = -0.10294324f;   // k1 * 0.044715
+  const float e = __builtin_amdgcn_exp2f(x * __builtin_fmaf(k2, x * x, k1));   // e^(-2u)
+  const float s = __builtin_amdgcn_rcpf(1.0f + e);
+  const float c2 = 1.5957691f;     // 2 sqrt(2/pi)
+  return s * __builtin_fmaf(c2 * x * (e * s), __builtin_fmaf(0.134145f, x * x, 1.0f), 1.0f);
+}
+
+// The aux tensor of the back-propagation epilogue bits has C's type and layout: N consecutive
+// rows of one column start at element e0, exactly where C's do.
+template <int N>
+__device__ __forceinline__ void aux_load(const BrgemmParams& p, int64_t e0, float (&z)[N]) {
+  if (p.c_bf16) {
+    const uint16_t* ap = static_cast<const uint16_t*>(p.aux) + e0;
+    if constexpr (N == 8) {
+      if ((reinterpret_cast<uintptr_t>(ap) & 15) == 0) {
+        const u32x4 w = gld<u32x4>(ap);
+        const uint32_t d[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          z[2 * e] = bf16_bits_to_f32(d[e] & 0xffffu);
+          z[2 * e + 1] = bf16_bits_to_f32(d[e] >> 16);
+        }
+        return;
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < N; ++e) z[e] = bf16_bits_to_f32(gld<uint16_t>(ap + e));
+  } else {
+    const float* ap = static_cast<const float*>(p.aux) + e0;
+    if constexpr (N % 4 == 0) {
+      if ((reinterpret_cast<uintptr_t>(ap) & 15) == 0) {
+#pragma unroll
+        for (int q = 0; q < N / 4; ++q) {
+          const f32x4 w = gld<f32x4>(ap + 4 * q);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) z[4 * q + e] = w[e];
+        }
+        return;
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < N; ++e) z[e] = gld<float>(ap + e);
+  }
+}
+
+template <int N>
+__device__ __forceinline__ void aux_store(const BrgemmParams& p, int64_t e0, const float (&v)[N]) {
+  if (p.c_bf16) {
+    uint16_t* ap = static_cast<uint16_t*>(p.aux) + e0;
+    if constexpr (N == 8) {
+      if ((reinterpret_cast<uintptr_t>(ap) & 15) == 0) {
+        gst<u32x4>(ap, (u32x4){pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                               pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])});
+        return;
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < N; ++e) gst<uint16_t>(ap + e, f32_to_bf16_bits(v[e]));
+  } else {
+    float* ap = static_cast<float*>(p.aux) + e0;
+    if constexpr (N % 4 == 0) {
+      if ((reinterpret_cast<uintptr_t>(ap) & 15) == 0) {
+#pragma unroll
+        for (int q = 0; q < N / 4; ++q)
+          gst<f32x4>(ap + 4 * q, (f32x4){v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]});
+        return;
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < N; ++e) gst<float>(ap + e, v[e]);
+  }
+}
+
+// The aux steps of the epilogue on N consecutive rows of one column (element e0 of C's layout),
+// after beta*C and the bias: SAVE_PREACT keeps v (rounded to C's type) before the activation;
+// RELU_INV / GELU_TANH_INV, which never come with an activation, multiply v by the activation's
+// derivative at the saved pre-activation z.  activate() then runs on the result as usual.
+template <int N>
+__device__ __forceinline__ void epi_aux(const BrgemmParams& p, int64_t e0, float (&v)[N]) {
+  if (p.flags & TPP_EPI_SAVE_PREACT) aux_store<N>(p, e0, v);
+  if (p.flags & (TPP_EPI_RELU_INV | TPP_EPI_GELU_TANH_INV)) {
+    float z[N];
+    aux_load<N>(p, e0, z);
+    if (p.flags & TPP_EPI_RELU_INV) {
+#pragma unroll
+      for (int e = 0; e < N; ++e) v[e] = z[e] > 0.0f ? v[e] : 0.0f;
+    } else {
+#pragma unroll
+      for (int e = 0; e < N; ++e) v[e] = v[e] * gelu_tanh_grad(z[e]);
+    }
+  }
+}
+
 // XCD-aware tile order: workgroups are handed to the 8 XCDs round-robin, so consecutive block
 // ids land on different L2s.  Remapping gives each XCD a contiguous run of tiles (neighbouring
 // tiles share A rows or B columns and so share that XCD's L2).
@@ -307,9 +408,12 @@ __device__ __forceinline__ void epilogue_via_lds(const BrgemmParams& p, const In
               v[2 * e + 1] = p.beta * bf16_bits_to_f32(d[e] >> 16) + v[2 * e + 1];
             }
           }
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] += bias8[e];
+          if (p.flags & EPI_AUX_MASK) epi_aux<8>(p, e0, v);
           uint32_t o[8];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) o[e] = f32_to_bf16_bits(activate(v[e] + bias8[e], p.flags));
+          for (int e = 0; e < 8; ++e) o[e] = f32_to_bf16_bits(activate(v[e], p.flags));
           if (vec) {
             gst<u32x4>(cp, (u32x4){o[0] | (o[1] << 16), o[2] | (o[3] << 16),
                                    o[4] | (o[5] << 16), o[6] | (o[7] << 16)});
@@ -325,7 +429,10 @@ __device__ __forceinline__ void epilogue_via_lds(const BrgemmParams& p, const In
             for (int e = 0; e < 8; ++e) v[e] = p.beta * gld<float>(cp + e) + v[e];
           }
 #pragma unroll
-          for (int e = 0; e < 8; ++e) v[e] = activate(v[e] + bias8[e], p.flags);
+          for (int e = 0; e < 8; ++e) v[e] += bias8[e];
+          if (p.flags & EPI_AUX_MASK) epi_aux<8>(p, e0, v);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] = activate(v[e], p.flags);
           if (vec) {
             gst<f32x4>(cp, (f32x4){v[0], v[1], v[2], v[3]});
             gst<f32x4>(cp + 4, (f32x4){v[4], v[5], v[6], v[7]});
@@ -341,7 +448,7 @@ __device__ __forceinline__ void epilogue_via_lds(const BrgemmParams& p, const In
 }
 
 // ---------------------------------------------------------------------------------------------
-// Epilogue for a bf16 C that is not read (beta = 0).  Bias and activation are applied to the
+// Epilogue for a bf16 C that is not read (beta = 0) and no aux tensor.  Bias and activation are applied to the
 // accumulators where they are, each lane narrows its four consecutive rows of a column to bf16
 // and parks them in its own wave's LDS slab (column-major, WTM rows per column, 16-byte row
 // chunks XOR-swizzled by the column), and the wave then stores the slab as 16-byte runs of 8

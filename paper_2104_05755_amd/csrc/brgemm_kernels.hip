@@ -79,6 +79,7 @@ __device__ __forceinline__ void store_group(const BrgemmParams& p, const Instanc
       }
       if (has_bias)
         for (int e = 0; e < 4; ++e) v[e] += bias[bias_idx + e];
+      if (p.flags & EPI_AUX_MASK) epi_aux<4>(p, e0, v);
       uint32_t o[4];
       for (int e = 0; e < 4; ++e) o[e] = f32_to_bf16_bits(activate(v[e], p.flags));
       if (vec) {
@@ -100,6 +101,7 @@ __device__ __forceinline__ void store_group(const BrgemmParams& p, const Instanc
       }
       if (has_bias)
         for (int e = 0; e < 4; ++e) v[e] += bias[bias_idx + e];
+      if (p.flags & EPI_AUX_MASK) epi_aux<4>(p, e0, v);
       for (int e = 0; e < 4; ++e) v[e] = activate(v[e], p.flags);
       if (vec) {
         *reinterpret_cast<float4*>(cp) = make_float4(v[0], v[1], v[2], v[3]);
@@ -122,17 +124,19 @@ __device__ __forceinline__ void store_group(const BrgemmParams& p, const Instanc
         bias_idx = in.bias + R;
       }
       const int64_t ei = in.c + row_off + col_off;
-      float v = v_in[e];
+      float v1[1] = {v_in[e]};
       if (p.c_bf16) {
         uint16_t* cp = static_cast<uint16_t*>(p.c) + ei;
-        if (p.beta != 0.0f) v = p.beta * bf16_bits_to_f32(*cp) + v;
-        if (has_bias) v += bias[bias_idx];
-        *cp = f32_to_bf16_bits(activate(v, p.flags));
+        if (p.beta != 0.0f) v1[0] = p.beta * bf16_bits_to_f32(*cp) + v1[0];
+        if (has_bias) v1[0] += bias[bias_idx];
+        if (p.flags & EPI_AUX_MASK) epi_aux<1>(p, ei, v1);
+        *cp = f32_to_bf16_bits(activate(v1[0], p.flags));
       } else {
         float* cp = static_cast<float*>(p.c) + ei;
-        if (p.beta != 0.0f) v = p.beta * *cp + v;
-        if (has_bias) v += bias[bias_idx];
-        *cp = activate(v, p.flags);
+        if (p.beta != 0.0f) v1[0] = p.beta * *cp + v1[0];
+        if (has_bias) v1[0] += bias[bias_idx];
+        if (p.flags & EPI_AUX_MASK) epi_aux<1>(p, ei, v1);
+        *cp = activate(v1[0], p.flags);
       }
     }
   }

@@ -51,7 +51,12 @@ struct BrgemmParams {
   // 64 x 64 fp32), then summed in chunk order by a finishing kernel that applies the epilogue.
   int32_t split;             // 1: no split
   float* ws;
+  // Tensor of C's type and layout read or written by the back-propagation epilogue bits.
+  void* aux;
 };
+
+// Epilogue bits that use the aux tensor.
+constexpr uint32_t EPI_AUX_MASK = TPP_EPI_RELU_INV | TPP_EPI_GELU_TANH_INV | TPP_EPI_SAVE_PREACT;
 
 // Kernel instances of the bf16 family (tile shape + load path) and the fp32 kernel.
 enum KernelId : int32_t {
@@ -93,8 +98,14 @@ struct ReduceParams {
   uint32_t flags;
   float* out_x;
   float* out_x2;
+  // Batch of G calls: call g reads in + g * in_stride (elements), writes outputs g * out_stride
+  // floats on.
+  int64_t G;
+  int64_t in_stride;
+  int64_t out_stride;
 };
-// Number of floats of work space a reduce of this shape needs (0 if none).
+// Number of floats of work space a reduce of this shape (and batch) needs: 0 if none, -1 if one
+// of its launches would need more than 2^31 - 1 workgroups.
 int64_t reduce_work_floats(const ReduceParams& p);
 hipError_t launch_reduce(const ReduceParams& p, float* work, hipStream_t stream);
 
@@ -110,6 +121,10 @@ struct TransformParams {
   int32_t es, alpha;
   int32_t vec;
   int64_t tiles_m;
+  // Batch of G calls: call g reads in + g * in_stride and writes out + g * out_stride (elements).
+  int64_t G;
+  int64_t in_stride;
+  int64_t out_stride;
 };
 hipError_t launch_transform(TransformParams& p, hipStream_t stream);
 

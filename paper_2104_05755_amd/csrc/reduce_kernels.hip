@@ -10,6 +10,8 @@
 //   BY_COLS (out[r] = fold over c): a thread owns 16 bytes of consecutive rows and walks the
 //     columns of its workgroup's column range; the column lanes of a workgroup then meet in
 //     LDS.  Column ranges of different workgroups meet in a second, tiny pass.
+// A batch of G calls (the loop of Alg. 6 around the TPP) runs as one launch: each pass has its
+// per-call workgroups G times over, and workgroup b serves call b / per.
 // Arithmetic is fp32.  When a shape needs several partial results per output (row segments or
 // column ranges), they go to a device work buffer and a second kernel folds them in a fixed
 // order (which depends only on the shape), so results do not depend on scheduling.
@@ -70,13 +72,31 @@ __device__ __forceinline__ void loadv(const void* base, int64_t idx, float out[V
   }
 }
 
+// Batched calls: workgroup b of a launch works on call g = b / per (per workgroups per call).
+// Moves p's input and outputs and the work buffer to call g's and returns the workgroup's index
+// within its call.  Each call's partials take wsize floats of the work buffer.
+template <bool BF16>
+__device__ __forceinline__ int64_t batch_of(ReduceParams& p, int64_t per, float*& work,
+                                            int64_t wsize) {
+  const int64_t bid = blockIdx.x;
+  const int64_t g = bid / per;
+  if (g > 0) {
+    p.in = static_cast<const char*>(p.in) + g * p.in_stride * (BF16 ? 2 : 4);
+    if (p.out_x) p.out_x += g * p.out_stride;
+    if (p.out_x2) p.out_x2 += g * p.out_stride;
+    if (work) work += g * wsize;
+  }
+  return bid - g * per;
+}
+
 // BY_ROWS: wavefront wid folds rows [s*seg_rows, min(m, (s+1)*seg_rows)) of column c, where
 // c = wid % n, s = wid / n.  V == 1 means element loads.
 template <int OP, bool BF16, int V>
 __global__ __launch_bounds__(RT) void reduce_rows_kernel(ReduceParams p, int32_t seg_rows,
-                                                         int32_t nseg, float* work) {
+                                                         int32_t nseg, float* work, int64_t per) {
   const int lane = threadIdx.x & 63;
-  const int64_t wid = (int64_t)blockIdx.x * (RT / 64) + (threadIdx.x >> 6);
+  const int64_t lb = batch_of<BF16>(p, per, work, 2LL * nseg * p.n);
+  const int64_t wid = lb * (RT / 64) + (threadIdx.x >> 6);
   if (wid >= (int64_t)p.n * nseg) return;
   const int32_t c = (int32_t)(wid % p.n), s = (int32_t)(wid / p.n);
   const int32_t r_lo = s * seg_rows;
@@ -121,13 +141,14 @@ __global__ __launch_bounds__(RT) void reduce_rows_kernel(ReduceParams p, int32_t
 template <int OP, bool BF16, int V>
 __global__ __launch_bounds__(RT) void reduce_cols_kernel(ReduceParams p, int32_t TR,
                                                          int32_t col_seg, int32_t nseg,
-                                                         int32_t nrb, float* work) {
+                                                         int32_t nrb, float* work, int64_t per) {
   __shared__ float sx[RT * V];
   __shared__ float sx2[RT * V];
   const int t = threadIdx.x;
   const int TC = RT / TR;
   const int tr = t % TR, tc = t / TR;
-  const int32_t rb = (int32_t)(blockIdx.x % nrb), s = (int32_t)(blockIdx.x / nrb);
+  const int64_t lb = batch_of<BF16>(p, per, work, 2LL * nseg * p.m);
+  const int32_t rb = (int32_t)(lb % nrb), s = (int32_t)(lb / nrb);
   const int32_t r0 = rb * TR * V + tr * V;
   const int32_t c_lo = s * col_seg, c_hi = min(p.n, c_lo + col_seg);
   float ax[V], ax2[V];
@@ -205,12 +226,29 @@ __global__ __launch_bounds__(RT) void reduce_cols_kernel(ReduceParams p, int32_t
 
 // Second pass: out[o] = fold over s < nseg of work[s * n_out + o] (x part, then x2 part).
 // One wavefront per output: lanes take every 64th partial, then fold across the wavefront.
+// Moves the combine pass's pointers to call g = blockIdx.x / per of a batch and returns the
+// workgroup's index within its call.
+__device__ __forceinline__ int64_t combine_batch(int64_t per, int32_t n_out, int32_t nseg,
+                                                 int64_t out_stride, const float*& work,
+                                                 float*& out_x, float*& out_x2) {
+  const int64_t bid = blockIdx.x;
+  const int64_t g = bid / per;
+  if (g > 0) {
+    work += g * 2LL * nseg * n_out;
+    if (out_x) out_x += g * out_stride;
+    if (out_x2) out_x2 += g * out_stride;
+  }
+  return bid - g * per;
+}
+
 template <int OP>
 __global__ __launch_bounds__(RT) void reduce_combine_kernel(const float* work, int32_t n_out,
                                                             int32_t nseg, uint32_t flags,
-                                                            float* out_x, float* out_x2) {
+                                                            float* out_x, float* out_x2,
+                                                            int64_t per, int64_t out_stride) {
   const int lane = threadIdx.x & 63;
-  const int64_t o = (int64_t)blockIdx.x * (RT / 64) + (threadIdx.x >> 6);
+  const int64_t lb = combine_batch(per, n_out, nseg, out_stride, work, out_x, out_x2);
+  const int64_t o = lb * (RT / 64) + (threadIdx.x >> 6);
   if (o >= n_out) return;
   float fx = fold_identity<OP>(), fx2 = fold_identity<OP>();
   for (int32_t s = lane; s < nseg; s += 64) {
@@ -231,10 +269,12 @@ __global__ __launch_bounds__(RT) void reduce_combine_kernel(const float* work, i
 template <int OP>
 __global__ __launch_bounds__(RT) void reduce_combine_wide_kernel(const float* work, int32_t n_out,
                                                                  int32_t nseg, uint32_t flags,
-                                                                 float* out_x, float* out_x2) {
+                                                                 float* out_x, float* out_x2,
+                                                                 int64_t per, int64_t out_stride) {
   __shared__ float sx[4][64], sx2[4][64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int64_t o = (int64_t)blockIdx.x * 64 + lane;
+  const int64_t lb = combine_batch(per, n_out, nseg, out_stride, work, out_x, out_x2);
+  const int64_t o = lb * 64 + lane;
   float fx = fold_identity<OP>(), fx2 = fold_identity<OP>();
   if (o < n_out) {
     const float* px = work + o;
@@ -319,12 +359,15 @@ Plan make_plan(const ReduceParams& p) {
 
 template <int OP, bool BF16, int V>
 void launch_first(const ReduceParams& p, const Plan& pl, float* work, hipStream_t stream) {
+  // with one partial per output the first pass writes the outputs itself (no work buffer)
+  float* w = pl.nseg > 1 ? work : nullptr;
+  const dim3 grid((unsigned)(pl.blocks * p.G));
   if (!pl.by_cols)
-    hipLaunchKernelGGL((reduce_rows_kernel<OP, BF16, V>), dim3((unsigned)pl.blocks), dim3(RT), 0,
-                       stream, p, pl.seg, pl.nseg, work);
+    hipLaunchKernelGGL((reduce_rows_kernel<OP, BF16, V>), grid, dim3(RT), 0, stream, p, pl.seg,
+                       pl.nseg, w, pl.blocks);
   else
-    hipLaunchKernelGGL((reduce_cols_kernel<OP, BF16, V>), dim3((unsigned)pl.blocks), dim3(RT), 0,
-                       stream, p, pl.tr, pl.seg, pl.nseg, pl.nrb, work);
+    hipLaunchKernelGGL((reduce_cols_kernel<OP, BF16, V>), grid, dim3(RT), 0, stream, p, pl.tr,
+                       pl.seg, pl.nseg, pl.nrb, w, pl.blocks);
 }
 
 template <int OP>
@@ -338,12 +381,17 @@ void launch_op(const ReduceParams& p, const Plan& pl, float* work, hipStream_t s
   }
   if (pl.nseg > 1) {
     const int32_t n_out = pl.by_cols ? p.m : p.n;
-    if (n_out >= 512)   // many outputs: coalesced over outputs
-      hipLaunchKernelGGL(reduce_combine_wide_kernel<OP>, dim3((unsigned)((n_out + 63) / 64)),
-                         dim3(RT), 0, stream, work, n_out, pl.nseg, p.flags, p.out_x, p.out_x2);
-    else                // few outputs: one wavefront per output, lanes over the partials
-      hipLaunchKernelGGL(reduce_combine_kernel<OP>, dim3((unsigned)((n_out + 3) / 4)),
-                         dim3(RT), 0, stream, work, n_out, pl.nseg, p.flags, p.out_x, p.out_x2);
+    if (n_out >= 512) {   // many outputs: coalesced over outputs
+      const int64_t per = (n_out + 63) / 64;
+      hipLaunchKernelGGL(reduce_combine_wide_kernel<OP>, dim3((unsigned)(per * p.G)), dim3(RT), 0,
+                         stream, work, n_out, pl.nseg, p.flags, p.out_x, p.out_x2, per,
+                         p.out_stride);
+    } else {              // few outputs: one wavefront per output, lanes over the partials
+      const int64_t per = (n_out + 3) / 4;
+      hipLaunchKernelGGL(reduce_combine_kernel<OP>, dim3((unsigned)(per * p.G)), dim3(RT), 0,
+                         stream, work, n_out, pl.nseg, p.flags, p.out_x, p.out_x2, per,
+                         p.out_stride);
+    }
   }
 }
 
@@ -351,8 +399,12 @@ void launch_op(const ReduceParams& p, const Plan& pl, float* work, hipStream_t s
 
 int64_t reduce_work_floats(const ReduceParams& p) {
   const Plan pl = make_plan(p);
+  const int32_t n_out = pl.by_cols ? p.m : p.n;
+  // every pass of the launch (first pass, combine) must fit 2^31 - 1 workgroups
+  const int64_t per = pl.blocks > (n_out + 3) / 4 ? pl.blocks : (n_out + 3) / 4;
+  if (per > 0x7fffffff / (p.G > 0 ? p.G : 1)) return -1;
   if (pl.nseg <= 1) return 0;
-  return 2LL * pl.nseg * (pl.by_cols ? p.m : p.n);
+  return 2LL * pl.nseg * n_out * p.G;
 }
 
 hipError_t launch_reduce(const ReduceParams& p, float* work, hipStream_t stream) {

@@ -166,7 +166,8 @@ tpp_status launch(const tpp_brgemm_kernel_s* h, tpp::BrgemmParams& p, void* stre
   const int32_t id = choose_kernel(*h, p);
   p.split = 1;
   p.ws = nullptr;
-  if (id == tpp::K_F32_GENERIC && p.kind != TPP_BR_ADDRESS && p.count >= 2) {
+  if (id == tpp::K_F32_GENERIC && p.kind != TPP_BR_ADDRESS && p.count >= 2 &&
+      !(p.flags & tpp::EPI_AUX_MASK)) {
     // A grid of few 64 x 64 tiles leaves most of the GPU idle while each workgroup walks the
     // whole pair list: split the list into chunks reduced by separate workgroups (about 256 in
     // all) and sum the chunks in a finishing kernel.
@@ -215,6 +216,14 @@ tpp_status check_bias(const tpp_brgemm_kernel_s* h, const float* bias) {
   return TPP_OK;
 }
 
+// The calls without an aux argument cannot run a handle whose epilogue reads or writes one.
+tpp_status check_no_aux(const tpp_brgemm_kernel_s* h) {
+  if (h->desc.flags & tpp::EPI_AUX_MASK)
+    return fail(TPP_ERR_INVALID_ARG,
+                "the handle's epilogue uses an aux tensor: call tpp_brgemm_execute_batched_aux");
+  return TPP_OK;
+}
+
 // Single call = a batched call with one instance of a 1x1 strided grid.
 tpp_status run_single(const tpp_brgemm_kernel_s* h, tpp::BrgemmParams& p, void* stream) {
   p.fused = 1;
@@ -260,10 +269,18 @@ tpp_status tpp_brgemm_dispatch(const tpp_brgemm_desc* desc, tpp_brgemm_handle* o
     return fail(TPP_ERR_UNSUPPORTED, "accumulation is fp32 only");
   if (d.kind != TPP_BR_STRIDE && d.kind != TPP_BR_OFFSET && d.kind != TPP_BR_ADDRESS)
     return fail(TPP_ERR_INVALID_ARG, "unknown batch kind %d", d.kind);
-  if (d.flags & ~(uint32_t)(TPP_EPI_BIAS | TPP_EPI_RELU | TPP_EPI_GELU_TANH))
+  if (d.flags & ~(uint32_t)(TPP_EPI_BIAS | TPP_EPI_RELU | TPP_EPI_GELU_TANH | tpp::EPI_AUX_MASK))
     return fail(TPP_ERR_INVALID_ARG, "unknown epilogue flag bits 0x%x", d.flags);
   if ((d.flags & TPP_EPI_RELU) && (d.flags & TPP_EPI_GELU_TANH))
     return fail(TPP_ERR_INVALID_ARG, "RELU and GELU_TANH exclude each other");
+  const uint32_t inv = TPP_EPI_RELU_INV | TPP_EPI_GELU_TANH_INV;
+  if ((d.flags & inv) == inv)
+    return fail(TPP_ERR_INVALID_ARG, "RELU_INV and GELU_TANH_INV exclude each other");
+  if ((d.flags & inv) && (d.flags & (TPP_EPI_RELU | TPP_EPI_GELU_TANH | TPP_EPI_SAVE_PREACT)))
+    return fail(TPP_ERR_INVALID_ARG,
+                "an inverse activation excludes RELU, GELU_TANH and SAVE_PREACT");
+  if ((d.flags & TPP_EPI_SAVE_PREACT) && !(d.flags & (TPP_EPI_RELU | TPP_EPI_GELU_TANH)))
+    return fail(TPP_ERR_INVALID_ARG, "SAVE_PREACT needs RELU or GELU_TANH");
   if (!std::isfinite(d.beta)) return fail(TPP_ERR_INVALID_ARG, "beta must be finite");
 
   std::lock_guard<std::mutex> lock(g_cache_mu);
@@ -305,6 +322,7 @@ tpp_status tpp_brgemm_execute_stride(tpp_brgemm_handle h, const void* a, const v
   if (!c) return fail(TPP_ERR_INVALID_ARG, "NULL c");
   if (count > 0 && (!a || !b)) return fail(TPP_ERR_INVALID_ARG, "NULL a or b");
   if (tpp_status s = check_bias(h, bias)) return s;
+  if (tpp_status s = check_no_aux(h)) return s;
   tpp::BrgemmParams p;
   fill_common(h, p);
   p.a = a; p.b = b; p.c = c; p.bias = bias;
@@ -323,6 +341,7 @@ tpp_status tpp_brgemm_execute_offset(tpp_brgemm_handle h, const void* a, const v
   if (count > 0 && (!a || !b || !offs_a || !offs_b))
     return fail(TPP_ERR_INVALID_ARG, "NULL a, b or offset array");
   if (tpp_status s = check_bias(h, bias)) return s;
+  if (tpp_status s = check_no_aux(h)) return s;
   tpp::BrgemmParams p;
   fill_common(h, p);
   p.a = a; p.b = b; p.c = c; p.bias = bias;
@@ -341,6 +360,7 @@ tpp_status tpp_brgemm_execute_address(tpp_brgemm_handle h, const void* const* pt
   if (!c) return fail(TPP_ERR_INVALID_ARG, "NULL c");
   if (count > 0 && (!ptrs_a || !ptrs_b)) return fail(TPP_ERR_INVALID_ARG, "NULL pointer list");
   if (tpp_status s = check_bias(h, bias)) return s;
+  if (tpp_status s = check_no_aux(h)) return s;
   tpp::BrgemmParams p;
   fill_common(h, p);
   p.c = c; p.bias = bias;
@@ -353,15 +373,17 @@ tpp_status tpp_brgemm_execute_address(tpp_brgemm_handle h, const void* const* pt
   return run_single(h, p, stream);
 }
 
-tpp_status tpp_brgemm_execute_batched(tpp_brgemm_handle h, const tpp_grid_strided* grid,
-                                      int64_t G, const int64_t* d_a_off, const int64_t* d_b_off,
-                                      const int64_t* d_c_off, const int64_t* d_bias_off,
-                                      const void* a, const void* b, void* c, const float* bias,
-                                      int64_t count, const int64_t* d_offs_a,
-                                      const int64_t* d_offs_b, const int64_t* d_begin,
-                                      const void* const* d_ptrs_a, const void* const* d_ptrs_b,
-                                      void* stream) {
-  if (tpp_status s = check_handle(h)) return s;
+}  // extern "C"
+
+namespace {
+
+tpp_status execute_batched(tpp_brgemm_handle h, const tpp_grid_strided* grid, int64_t G,
+                           const int64_t* d_a_off, const int64_t* d_b_off, const int64_t* d_c_off,
+                           const int64_t* d_bias_off, const void* a, const void* b, void* c,
+                           void* aux, const float* bias, int64_t count, const int64_t* d_offs_a,
+                           const int64_t* d_offs_b, const int64_t* d_begin,
+                           const void* const* d_ptrs_a, const void* const* d_ptrs_b,
+                           void* stream) {
   const tpp_brgemm_desc& d = h->desc;
   if (G < 0) return fail(TPP_ERR_INVALID_ARG, "G < 0");
   if (grid) {
@@ -375,6 +397,8 @@ tpp_status tpp_brgemm_execute_batched(tpp_brgemm_handle h, const tpp_grid_stride
   if (G == 0) return ok();
   if (!c) return fail(TPP_ERR_INVALID_ARG, "NULL c");
   if (tpp_status s = check_bias(h, bias)) return s;
+  if ((d.flags & tpp::EPI_AUX_MASK) && !aux)
+    return fail(TPP_ERR_INVALID_ARG, "the handle's epilogue needs the aux tensor (NULL aux)");
   if (d.kind == TPP_BR_ADDRESS) {
     if (!d_begin) return fail(TPP_ERR_INVALID_ARG, "address kind needs d_begin");
     if (!d_ptrs_a || !d_ptrs_b) return fail(TPP_ERR_INVALID_ARG, "NULL pointer list");
@@ -391,6 +415,7 @@ tpp_status tpp_brgemm_execute_batched(tpp_brgemm_handle h, const tpp_grid_stride
   p.offs_a = d_offs_a; p.offs_b = d_offs_b;
   p.begin = d_begin; p.ptrs_a = d_ptrs_a; p.ptrs_b = d_ptrs_b;
   p.a_off = d_a_off; p.b_off = d_b_off; p.c_off = d_c_off; p.bias_off = d_bias_off;
+  p.aux = (d.flags & tpp::EPI_AUX_MASK) ? aux : nullptr;
   if (grid) {
     p.gm = grid->gm; p.gn = grid->gn;
     p.a_step_m = grid->a_step_m; p.b_step_n = grid->b_step_n;
@@ -417,9 +442,48 @@ tpp_status tpp_brgemm_execute_batched(tpp_brgemm_handle h, const tpp_grid_stride
   return launch(h, p, stream);
 }
 
-tpp_status tpp_reduce(int32_t m, int32_t n, int64_t ld, int32_t in_type, const void* in,
-                      int32_t op, uint32_t flags, float* out_x, float* out_x2, void* stream) {
+}  // namespace
+
+extern "C" {
+
+tpp_status tpp_brgemm_execute_batched(tpp_brgemm_handle h, const tpp_grid_strided* grid,
+                                      int64_t G, const int64_t* d_a_off, const int64_t* d_b_off,
+                                      const int64_t* d_c_off, const int64_t* d_bias_off,
+                                      const void* a, const void* b, void* c, const float* bias,
+                                      int64_t count, const int64_t* d_offs_a,
+                                      const int64_t* d_offs_b, const int64_t* d_begin,
+                                      const void* const* d_ptrs_a, const void* const* d_ptrs_b,
+                                      void* stream) {
+  if (tpp_status s = check_handle(h)) return s;
+  if (tpp_status s = check_no_aux(h)) return s;
+  return execute_batched(h, grid, G, d_a_off, d_b_off, d_c_off, d_bias_off, a, b, c, nullptr,
+                         bias, count, d_offs_a, d_offs_b, d_begin, d_ptrs_a, d_ptrs_b, stream);
+}
+
+tpp_status tpp_brgemm_execute_batched_aux(tpp_brgemm_handle h, const tpp_grid_strided* grid,
+                                          int64_t G, const int64_t* d_a_off,
+                                          const int64_t* d_b_off, const int64_t* d_c_off,
+                                          const int64_t* d_bias_off, const void* a,
+                                          const void* b, void* c, void* aux, const float* bias,
+                                          int64_t count, const int64_t* d_offs_a,
+                                          const int64_t* d_offs_b, const int64_t* d_begin,
+                                          const void* const* d_ptrs_a,
+                                          const void* const* d_ptrs_b, void* stream) {
+  if (tpp_status s = check_handle(h)) return s;
+  return execute_batched(h, grid, G, d_a_off, d_b_off, d_c_off, d_bias_off, a, b, c, aux, bias,
+                         count, d_offs_a, d_offs_b, d_begin, d_ptrs_a, d_ptrs_b, stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+tpp_status reduce_impl(int32_t m, int32_t n, int64_t ld, int32_t in_type, const void* in,
+                       int64_t G, int64_t in_stride, int32_t op, uint32_t flags, float* out_x,
+                       float* out_x2, int64_t out_stride, void* stream) {
   if (m <= 0 || n <= 0) return fail(TPP_ERR_INVALID_ARG, "m, n must be > 0");
+  if (G < 0 || in_stride < 0 || out_stride < 0)
+    return fail(TPP_ERR_INVALID_ARG, "G, in_stride and out_stride must be >= 0");
   if (ld < m) return fail(TPP_ERR_INVALID_ARG, "ld < m");
   if (!valid_dtype(in_type)) return fail(TPP_ERR_INVALID_ARG, "unknown datatype code");
   if (!in) return fail(TPP_ERR_INVALID_ARG, "NULL input");
@@ -431,8 +495,11 @@ tpp_status tpp_reduce(int32_t m, int32_t n, int64_t ld, int32_t in_type, const v
   if (!(flags & (TPP_RED_X | TPP_RED_X2))) return fail(TPP_ERR_INVALID_ARG, "set X and/or X2");
   if ((flags & TPP_RED_X) && !out_x) return fail(TPP_ERR_INVALID_ARG, "NULL out_x");
   if ((flags & TPP_RED_X2) && !out_x2) return fail(TPP_ERR_INVALID_ARG, "NULL out_x2");
-  tpp::ReduceParams p{in, m, n, ld, in_type == TPP_DT_BF16, op, flags, out_x, out_x2};
+  if (G == 0) return ok();
+  tpp::ReduceParams p{in, m, n, ld, in_type == TPP_DT_BF16, op, flags, out_x, out_x2,
+                      G, in_stride, out_stride};
   const int64_t need = tpp::reduce_work_floats(p);
+  if (need < 0) return fail(TPP_ERR_UNSUPPORTED, "reduce needs more than 2^31 - 1 workgroups");
   float* work = nullptr;
   if (need > 0) {
     const tpp_status st = work_buffer(WORK_REDUCE, stream, need, &work);
@@ -443,8 +510,11 @@ tpp_status tpp_reduce(int32_t m, int32_t n, int64_t ld, int32_t in_type, const v
   return ok();
 }
 
-tpp_status tpp_transform(int32_t kind, int32_t m, int32_t n, int64_t ld_in, int64_t ld_out,
-                         int32_t dtype, int32_t alpha, const void* in, void* out, void* stream) {
+tpp_status transform_impl(int32_t kind, int32_t m, int32_t n, int64_t ld_in, int64_t ld_out,
+                          int32_t dtype, int32_t alpha, const void* in, int64_t in_stride,
+                          void* out, int64_t out_stride, int64_t G, void* stream) {
+  if (G < 0 || in_stride < 0 || out_stride < 0)
+    return fail(TPP_ERR_INVALID_ARG, "G, in_stride and out_stride must be >= 0");
   if (kind < TPP_TR_TRANSPOSE || kind > TPP_TR_VNNI_TO_VNNI_T)
     return fail(TPP_ERR_INVALID_ARG, "unknown transform kind %d", kind);
   if (!valid_dtype(dtype)) return fail(TPP_ERR_INVALID_ARG, "unknown datatype code");
@@ -462,17 +532,50 @@ tpp_status tpp_transform(int32_t kind, int32_t m, int32_t n, int64_t ld_in, int6
       return fail(TPP_ERR_INVALID_ARG,
                   "VNNI to VNNI-transpose needs ld_in >= m * alpha and ld_out >= n * alpha");
   }
-  if (m == 0 || n == 0) return ok();
+  if (m == 0 || n == 0 || G == 0) return ok();
   if (!in || !out) return fail(TPP_ERR_INVALID_ARG, "NULL input or output");
   const int32_t es = dtype == TPP_DT_F32 ? 4 : 2;
+  // the 16-byte paths need every block of the batch aligned: the bases, the leading dimensions
+  // and (for G > 1) the block strides in whole 16-byte units
   const bool vec = ((reinterpret_cast<uintptr_t>(in) | reinterpret_cast<uintptr_t>(out)) & 15) == 0 &&
-                   (ld_in * es) % 16 == 0 && (ld_out * es) % 16 == 0;
-  tpp::TransformParams p{in, out, kind, m, n, ld_in, ld_out, es, alpha, vec ? 1 : 0, 0};
+                   (ld_in * es) % 16 == 0 && (ld_out * es) % 16 == 0 &&
+                   (G == 1 || ((in_stride * es) % 16 == 0 && (out_stride * es) % 16 == 0));
+  tpp::TransformParams p{in, out, kind, m, n, ld_in, ld_out, es, alpha, vec ? 1 : 0, 0,
+                         G, in_stride, out_stride};
   const hipError_t e = tpp::launch_transform(p, static_cast<hipStream_t>(stream));
   if (e == hipErrorInvalidConfiguration)
     return fail(TPP_ERR_UNSUPPORTED, "transform needs more than 2^31 - 1 workgroups");
   if (e != hipSuccess) return fail(TPP_ERR_HIP, "transform launch failed: %s", hipGetErrorString(e));
   return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+tpp_status tpp_reduce(int32_t m, int32_t n, int64_t ld, int32_t in_type, const void* in,
+                      int32_t op, uint32_t flags, float* out_x, float* out_x2, void* stream) {
+  return reduce_impl(m, n, ld, in_type, in, 1, 0, op, flags, out_x, out_x2, 0, stream);
+}
+
+tpp_status tpp_reduce_batched(int32_t m, int32_t n, int64_t ld, int32_t in_type, const void* in,
+                              int64_t G, int64_t in_stride, int32_t op, uint32_t flags,
+                              float* out_x, float* out_x2, int64_t out_stride, void* stream) {
+  return reduce_impl(m, n, ld, in_type, in, G, in_stride, op, flags, out_x, out_x2, out_stride,
+                     stream);
+}
+
+tpp_status tpp_transform(int32_t kind, int32_t m, int32_t n, int64_t ld_in, int64_t ld_out,
+                         int32_t dtype, int32_t alpha, const void* in, void* out, void* stream) {
+  return transform_impl(kind, m, n, ld_in, ld_out, dtype, alpha, in, 0, out, 0, 1, stream);
+}
+
+tpp_status tpp_transform_batched(int32_t kind, int32_t m, int32_t n, int64_t ld_in,
+                                 int64_t ld_out, int32_t dtype, int32_t alpha, const void* in,
+                                 int64_t in_stride, void* out, int64_t out_stride, int64_t G,
+                                 void* stream) {
+  return transform_impl(kind, m, n, ld_in, ld_out, dtype, alpha, in, in_stride, out, out_stride,
+                        G, stream);
 }
 
 }  // extern "C"

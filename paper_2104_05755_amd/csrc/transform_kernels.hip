@@ -68,18 +68,31 @@ __device__ __forceinline__ int tile_pos(int c, int r) {
   return c * TT + (((r / V) ^ ((c / V) % CH)) * V) + r % V;
 }
 
+// Workgroup b of a batched launch works on call g = b / per (per workgroups per call), whose
+// blocks start g * in_stride and g * out_stride entries on; returns the workgroup's index within
+// its call.
+template <typename T>
+__device__ __forceinline__ int64_t batch_of(const TransformParams& p, int64_t per, const T*& in,
+                                            T*& out) {
+  const int64_t bid = blockIdx.x;
+  const int64_t g = bid / per;
+  in = static_cast<const T*>(p.in) + g * p.in_stride;
+  out = static_cast<T*>(p.out) + g * p.out_stride;
+  return bid - g * per;
+}
+
 // Transpose: the n x m output's entry (c, r) = in(r, c).  Tile (r0, c0) of a flattened grid
-// (tiles_m tiles along m).
+// (tiles_m tiles along m, per tiles per call).
 template <int ES>
-__global__ __launch_bounds__(TPB) void transpose_kernel(TransformParams p) {
+__global__ __launch_bounds__(TPB) void transpose_kernel(TransformParams p, int64_t per) {
   using T = typename Entry<ES>::T;
   constexpr int V = 16 / ES, CH = TT / V;
   __shared__ __attribute__((aligned(16))) T lds[TT * TT];
   const int t = threadIdx.x;
-  const int64_t bid = blockIdx.x;
+  const T* in;
+  T* out;
+  const int64_t bid = batch_of<T>(p, per, in, out);
   const int32_t r0 = (int32_t)(bid % p.tiles_m) * TT, c0 = (int32_t)(bid / p.tiles_m) * TT;
-  const T* in = static_cast<const T*>(p.in);
-  T* out = static_cast<T*>(p.out);
   const bool whole = r0 + TT <= p.m && c0 + TT <= p.n;
   if (whole && p.vec) {
     // chunk q: input column c0 + q / CH, rows r0 + (q % CH) * V .. + V - 1
@@ -120,15 +133,15 @@ __global__ __launch_bounds__(TPB) void transpose_kernel(TransformParams p) {
 // group's alpha rows.  Output rows from m up to the next multiple of alpha are the zero
 // completion of the last group (never in a whole tile).
 template <int ES, int ALPHA>
-__global__ __launch_bounds__(TPB) void vnni_t_kernel(TransformParams p) {
+__global__ __launch_bounds__(TPB) void vnni_t_kernel(TransformParams p, int64_t per) {
   using T = typename Entry<ES>::T;
   constexpr int V = 16 / ES, CPG = TT * ALPHA / V;   // 16-byte chunks per group of a tile
   __shared__ T lds[TT][TT + 1];
   const int t = threadIdx.x;
-  const int64_t bid = blockIdx.x;
+  const T* in;
+  T* out;
+  const int64_t bid = batch_of<T>(p, per, in, out);
   const int32_t r0 = (int32_t)(bid % p.tiles_m) * TT, c0 = (int32_t)(bid / p.tiles_m) * TT;
-  const T* in = static_cast<const T*>(p.in);
-  T* out = static_cast<T*>(p.out);
   if (r0 + TT <= p.m && c0 + TT <= p.n && p.vec) {
     for (int q = t; q < TT * TT / V; q += TPB) {
       const int gi = q / CPG, j0 = (q % CPG) * V, rr0 = j0 / ALPHA;
@@ -184,16 +197,18 @@ __device__ __forceinline__ void load_words(const void* src, uint32_t* w) {
 // cover the group's m * ALPHA entries): entries j0 .. j0 + V - 1, i.e. rows j0 / ALPHA ..
 // (j0 + V) / ALPHA - 1 of the group's ALPHA columns.  Columns past n are the zero completion.
 template <int ES, int ALPHA>
-__global__ __launch_bounds__(TPB) void vnni_kernel(TransformParams p, int64_t cpg, int64_t total) {
+__global__ __launch_bounds__(TPB) void vnni_kernel(TransformParams p, int64_t cpg, int64_t total,
+                                                   int64_t per) {
   using T = typename Entry<ES>::T;
   constexpr int V = 16 / ES, ROWS = V / ALPHA;
-  const int64_t q = (int64_t)blockIdx.x * TPB + threadIdx.x;
+  const T* in;
+  T* out;
+  const int64_t q = batch_of<T>(p, per, in, out) * TPB + threadIdx.x;
   if (q >= total) return;
   const int64_t g = q / cpg;
   const int64_t j0 = (q - g * cpg) * V;
   const int64_t extent = (int64_t)p.m * ALPHA;
-  const T* in = static_cast<const T*>(p.in);
-  T* o = static_cast<T*>(p.out) + g * p.ld_out + j0;
+  T* o = out + g * p.ld_out + j0;
   if (p.vec && j0 + V <= extent) {
     const int64_t r0 = j0 / ALPHA;
     T v[V];
@@ -214,34 +229,41 @@ __global__ __launch_bounds__(TPB) void vnni_kernel(TransformParams p, int64_t cp
   }
 }
 
+// A launch of per workgroups for each of the G calls: at most 2^31 - 1 workgroups in all.
+inline bool grid_fits(int64_t per, int64_t G) { return per <= 0x7fffffff / (G > 0 ? G : 1); }
+
 template <int ES>
 hipError_t launch_es(TransformParams& p, hipStream_t stream) {
   const int64_t tiles_n = (p.n + TT - 1) / TT;
+  const int64_t G = p.G;
   if (p.kind == 0) {
     p.tiles_m = (p.m + TT - 1) / TT;
     const int64_t tiles = p.tiles_m * tiles_n;
-    if (tiles > 0x7fffffff) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL(transpose_kernel<ES>, dim3((uint32_t)tiles), dim3(TPB), 0, stream, p);
+    if (!grid_fits(tiles, G)) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL(transpose_kernel<ES>, dim3((uint32_t)(tiles * G)), dim3(TPB), 0, stream, p,
+                       tiles);
   } else if (p.kind == 1) {
     constexpr int V = 16 / ES;
     const int64_t cpg = ((int64_t)p.m * p.alpha + V - 1) / V;
     const int64_t total = cpg * ((p.n + p.alpha - 1) / p.alpha);
     const int64_t blocks = (total + TPB - 1) / TPB;
-    if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
+    if (!grid_fits(blocks, G)) return hipErrorInvalidConfiguration;
+    const dim3 grid((uint32_t)(blocks * G));
     switch (p.alpha) {
-      case 1: hipLaunchKernelGGL((vnni_kernel<ES, 1>), dim3((uint32_t)blocks), dim3(TPB), 0, stream, p, cpg, total); break;
-      case 2: hipLaunchKernelGGL((vnni_kernel<ES, 2>), dim3((uint32_t)blocks), dim3(TPB), 0, stream, p, cpg, total); break;
-      default: hipLaunchKernelGGL((vnni_kernel<ES, 4>), dim3((uint32_t)blocks), dim3(TPB), 0, stream, p, cpg, total); break;
+      case 1: hipLaunchKernelGGL((vnni_kernel<ES, 1>), grid, dim3(TPB), 0, stream, p, cpg, total, blocks); break;
+      case 2: hipLaunchKernelGGL((vnni_kernel<ES, 2>), grid, dim3(TPB), 0, stream, p, cpg, total, blocks); break;
+      default: hipLaunchKernelGGL((vnni_kernel<ES, 4>), grid, dim3(TPB), 0, stream, p, cpg, total, blocks); break;
     }
   } else {
     const int64_t m_pad = ((int64_t)p.m + p.alpha - 1) / p.alpha * p.alpha;
     p.tiles_m = (m_pad + TT - 1) / TT;
     const int64_t tiles = p.tiles_m * tiles_n;
-    if (tiles > 0x7fffffff) return hipErrorInvalidConfiguration;
+    if (!grid_fits(tiles, G)) return hipErrorInvalidConfiguration;
+    const dim3 grid((uint32_t)(tiles * G));
     switch (p.alpha) {
-      case 1: hipLaunchKernelGGL((vnni_t_kernel<ES, 1>), dim3((uint32_t)tiles), dim3(TPB), 0, stream, p); break;
-      case 2: hipLaunchKernelGGL((vnni_t_kernel<ES, 2>), dim3((uint32_t)tiles), dim3(TPB), 0, stream, p); break;
-      default: hipLaunchKernelGGL((vnni_t_kernel<ES, 4>), dim3((uint32_t)tiles), dim3(TPB), 0, stream, p); break;
+      case 1: hipLaunchKernelGGL((vnni_t_kernel<ES, 1>), grid, dim3(TPB), 0, stream, p, tiles); break;
+      case 2: hipLaunchKernelGGL((vnni_t_kernel<ES, 2>), grid, dim3(TPB), 0, stream, p, tiles); break;
+      default: hipLaunchKernelGGL((vnni_t_kernel<ES, 4>), grid, dim3(TPB), 0, stream, p, tiles); break;
     }
   }
   return hipGetLastError();

@@ -36,6 +36,7 @@ class DeviceCall:
     b: Optional[torch.Tensor]
     c: torch.Tensor
     bias: Optional[torch.Tensor]
+    aux: Optional[torch.Tensor] = None
     a_off: Optional[torch.Tensor] = None
     b_off: Optional[torch.Tensor] = None
     c_off: Optional[torch.Tensor] = None
@@ -70,7 +71,8 @@ def prepare(call, dev: dict, device="cuda") -> DeviceCall:
     h = tpp.tpp_brgemm_dispatch(descriptor(call))
     a = dev[call.a] if call.a else None
     b = dev[call.b] if call.b else None
-    dc = DeviceCall(h, call, a, b, dev[call.c], dev[call.bias] if call.bias else None)
+    dc = DeviceCall(h, call, a, b, dev[call.c], dev[call.bias] if call.bias else None,
+                    dev[call.aux] if getattr(call, "aux", None) else None)
     if call.grid is None:
         dc.a_off, dc.b_off = _i64(call.a_off, device), _i64(call.b_off, device)
         dc.c_off, dc.bias_off = _i64(call.c_off, device), _i64(call.bias_off, device)
@@ -88,10 +90,51 @@ def launch(dc: DeviceCall, stream: Optional[int] = None):
     call = dc.call
     if stream is None:
         stream = tpp.current_stream()
+    a = dc.a if call.kind != "address" else None
+    b = dc.b if call.kind != "address" else None
+    if dc.aux is not None:
+        tpp.tpp_brgemm_execute_batched_aux(
+            dc.handle, call.grid, call.G, dc.a_off, dc.b_off, dc.c_off, dc.bias_off, a, b, dc.c,
+            dc.aux, dc.bias, call.count, dc.offs_a, dc.offs_b, dc.begin, dc.ptrs_a, dc.ptrs_b,
+            stream)
+        return
     tpp.tpp_brgemm_execute_batched(
-        dc.handle, call.grid, call.G, dc.a_off, dc.b_off, dc.c_off, dc.bias_off,
-        dc.a if call.kind != "address" else None, dc.b if call.kind != "address" else None,
+        dc.handle, call.grid, call.G, dc.a_off, dc.b_off, dc.c_off, dc.bias_off, a, b,
         dc.c, dc.bias, call.count, dc.offs_a, dc.offs_b, dc.begin, dc.ptrs_a, dc.ptrs_b, stream)
+
+
+_DT = {"f32": tpp.TPP_DT_F32, "bf16": tpp.TPP_DT_BF16}
+_TR = {"transpose": tpp.TPP_TR_TRANSPOSE, "vnni": tpp.TPP_TR_VNNI,
+       "vnni_t": tpp.TPP_TR_VNNI_TO_VNNI_T}
+_RED = {"sum": tpp.TPP_RED_SUM, "mul": tpp.TPP_RED_MUL, "min": tpp.TPP_RED_MIN,
+        "max": tpp.TPP_RED_MAX}
+
+
+def prepare_step(step, dev: dict, device="cuda"):
+    """A chained workload's step ready to launch: a DeviceCall for a BRGEMM call, the step itself
+    for a Transform or Reduce step (their arguments are all sizes and array names)."""
+    if hasattr(step, "kind") and hasattr(step, "grid"):
+        return prepare(step, dev, device)
+    return step
+
+
+def launch_step(st, dev: dict, stream: Optional[int] = None):
+    """One step of a chained workload (see ``workloads.TransformStep`` / ``ReduceStep``)."""
+    if stream is None:
+        stream = tpp.current_stream()
+    if isinstance(st, DeviceCall):
+        launch(st, stream)
+    elif hasattr(st, "ld_in"):      # transform
+        tpp.tpp_transform_batched(_TR[st.kind], st.m, st.n, st.ld_in, st.ld_out, _DT[st.dtype],
+                                  st.alpha, dev[st.src], st.in_stride, dev[st.dst], st.out_stride,
+                                  st.G, stream)
+    else:                           # reduce
+        flags = tpp.TPP_RED_BY_COLS if st.by == "cols" else tpp.TPP_RED_BY_ROWS
+        flags |= (tpp.TPP_RED_X if st.dst_x else 0) | (tpp.TPP_RED_X2 if st.dst_x2 else 0)
+        tpp.tpp_reduce_batched(st.m, st.n, st.ld, _DT[st.in_type], dev[st.src], st.G,
+                               st.in_stride, _RED[st.op], flags,
+                               dev[st.dst_x] if st.dst_x else None,
+                               dev[st.dst_x2] if st.dst_x2 else None, st.out_stride, stream)
 
 
 def upload(wl, device="cuda") -> dict:

@@ -69,8 +69,12 @@ def test_dispatch_caches_equal_descriptors(tpp):
 @pytest.mark.parametrize("field,value,status", [
     ("m", 0, -1), ("n", -3, -1), ("k", 0, -1),
     ("lda", 10, -1), ("ldb", 5, -1), ("ldc", 1, -1),
-    ("a_type", 7, -1), ("comp_type", 1, -2), ("kind", 3, -1), ("flags", 8, -1),
+    ("a_type", 7, -1), ("comp_type", 1, -2), ("kind", 3, -1), ("flags", 64, -1),
     ("flags", 2 | 4, -1), ("beta", float("nan"), -1),
+    # back-propagation bits: the inverses exclude each other and every forward activation,
+    # SAVE_PREACT needs an activation
+    ("flags", 8 | 16, -1), ("flags", 8 | 2, -1), ("flags", 16 | 4, -1), ("flags", 16 | 32 | 4, -1),
+    ("flags", 32, -1), ("flags", 32 | 1, -1),
 ])
 def test_dispatch_rejects(tpp, field, value, status):
     d = tpp.make_desc(16, 16, 16, 16, 16, 16, "bf16", "f32")
@@ -121,6 +125,41 @@ def test_execute_argument_checks_precede_any_launch(tpp):
         with pytest.raises(tpp.TppError) as e:
             f()
         assert e.value.status == tpp.TPP_ERR_INVALID_ARG, i
+
+
+def test_aux_handles_need_the_aux_call(tpp):
+    fake = 1 << 40   # never dereferenced
+    grid = dict(gm=1, gn=1, a_step_m=0, b_step_n=0, c_step_m=0, c_step_n=0, bias_step_m=0)
+    for flags in (["relu_inv"], ["gelu_tanh_inv"], ["bias", "gelu_tanh", "save_preact"]):
+        h = tpp.tpp_brgemm_dispatch(tpp.make_desc(16, 16, 16, 16, 16, 16, "bf16", "bf16",
+                                                  flags=flags))
+        bias = fake if "bias" in flags else None
+        bad = [
+            lambda: tpp.tpp_brgemm_execute_stride(h, fake, fake, fake, bias, 1),
+            lambda: tpp.tpp_brgemm_execute_batched(h, grid, 1, None, None, None, None, fake, fake,
+                                                   fake, bias, 1, None, None, None, None, None),
+            lambda: tpp.tpp_brgemm_execute_batched_aux(h, grid, 1, None, None, None, None, fake,
+                                                       fake, fake, None, bias, 1, None, None,
+                                                       None, None, None),   # aux missing
+        ]
+        for i, f in enumerate(bad):
+            with pytest.raises(tpp.TppError) as e:
+                f()
+            assert e.value.status == tpp.TPP_ERR_INVALID_ARG, (flags, i)
+
+
+def test_batched_reduce_and_transform_argument_checks(tpp):
+    fake = 1 << 40
+    for G, si, so in ((-1, 0, 0), (2, -1, 4), (2, 16, -4)):
+        with pytest.raises(tpp.TppError) as e:
+            tpp.tpp_reduce_batched(4, 4, 4, 0, fake, G, si, 0, 1 | 4, fake, None, so)
+        assert e.value.status == tpp.TPP_ERR_INVALID_ARG
+        with pytest.raises(tpp.TppError) as e:
+            tpp.tpp_transform_batched(0, 4, 4, 4, 4, 0, 1, fake, si, fake, so, G)
+        assert e.value.status == tpp.TPP_ERR_INVALID_ARG
+    # G == 0 does nothing (the pointers are never touched)
+    tpp.tpp_reduce_batched(4, 4, 4, 0, fake, 0, 16, 0, 1 | 4, fake, None, 4)
+    tpp.tpp_transform_batched(0, 4, 4, 4, 4, 0, 1, fake, 16, fake, 16, 0)
 
 
 def test_zero_instances_is_a_no_op(tpp):
