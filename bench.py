@@ -8,8 +8,9 @@ two batched BRGEMM launches (8192 instances x 16 pairs, then 2048 instances x 64
 launches).  ``roofline`` takes the dominant launch's mean duration over K more steps with a
 timing-only (fence-free) HIP event on its stream around each launch.  The same run also
 times the other workloads (fp32 single BRGEMM, MLP fully-connected layer, 3x3 convolution with
-batchnorm statistics via the Reduce TPP, gathered address-based BRGEMM, and the Transform TPP's
-transpose and VNNI formatting of a 64 MB tensor) under ``per_config``,
+batchnorm statistics via the Reduce TPP, gathered address-based BRGEMM, the Transform TPP's
+transpose and VNNI formatting of a 64 MB tensor, and the MLP block's backward pass) under
+``per_config``,
 and the CPU oracle on a bounded sample of the headline workload under ``cpu_baseline``.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
@@ -330,6 +331,63 @@ def per_config(args, torch, tpp, torch_io, wk, np, stream):
         del dev, dcs, fns
         torch.cuda.empty_cache()
     out.update(transform_entries(args, torch, tpp, stream))
+    out["mlp_backward"] = backward_entry(args, torch, tpp, torch_io, wk, stream)
+    return out
+
+
+def backward_entry(args, torch, tpp, torch_io, wk, stream):
+    """The transformer MLP's backward pass at the headline size (see workloads.mlp_backward): the
+    four weight / activation transposes, the four gradient BRGEMMs (GELU_inv fused into dZ) and
+    the bias-gradient reduces, timed as one step over K steps (nothing between the launches), and
+    each launch's mean duration inside the step from fence-free events.  The forward call that
+    keeps the pre-activation (GEMM1 + SAVE_PREACT) runs once before and is timed on its own."""
+    wl = wk.mlp_backward()
+    dev = torch_io.upload(wl)
+    sts = [torch_io.prepare_step(st, dev) for st in wl.steps]
+    fns = [lambda st=st: torch_io.launch_step(st, dev, stream) for st in sts]
+    fwd, bwd = fns[0], fns[1:]
+    steps = max(10, args.steps // 4)
+    ms_fwd = time_bursts([fwd], steps, torch)[0]
+    elapsed = time_steps(bwd, steps, max(3, args.warmup // 10), torch)
+    per = time_in_steps(bwd, steps, torch, stream)
+    bw_calls = wl.calls[1:]
+    bw_flops = sum(c.flops for c in bw_calls)
+    launches = []
+    names = {1: "transpose W2 blocks", 2: "transpose W1 blocks", 3: "transpose H blocks",
+             4: "transpose X blocks", 5: "dZ = (W2^T dY) * gelu'(Z)  [GELU_inv fused]",
+             6: "dW2 = sum_tokens dY H^T", 7: "db2 (sum over token blocks)",
+             8: "db2 (sum within a block)", 9: "dX = W1^T dZ", 10: "dW1 = sum_tokens dZ X^T",
+             11: "db1 (sum over token blocks)", 12: "db1 (sum within a block)"}
+    brgemm_ms = 0.0
+    for i, (st, ms) in enumerate(zip(wl.steps[1:], per), start=1):
+        e = {"what": names[i], "launch_us": round(ms * 1e3, 2)}
+        if isinstance(st, wk.Call):
+            tfl = st.flops / (ms * 1e-3) / 1e12
+            brgemm_ms += ms
+            e.update(kernel=tpp.tpp_brgemm_describe(sts[i].handle), instances=st.G,
+                     pairs=st.pairs, tflops=round(tfl, 1), mfma_frac=round(tfl / PEAK_BF16_TFLOPS, 4))
+        elif isinstance(st, wk.TransformStep):
+            byts = 2 * st.G * st.m * st.n * 2
+            e.update(alg_bytes=byts, hbm_frac=round(byts / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4))
+        else:
+            es = 2 if st.in_type == "bf16" else 4
+            byts = st.G * st.m * st.n * es
+            e.update(alg_bytes=byts, hbm_frac=round(byts / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4))
+        launches.append(e)
+    out = {"workload": "backward of the transformer MLP block (8192 tokens, 1024 -> 4096 -> 1024, "
+                       "bf16 64x64 blocks): dZ, dW2, db2, dX, dW1, db1",
+           "ms_per_step": round(elapsed / steps * 1e3, 3),
+           "brgemm_flops": bw_flops,
+           "step_tflops": round(bw_flops / (elapsed / steps) / 1e12, 1),
+           "brgemm_tflops": round(bw_flops / (brgemm_ms * 1e-3) / 1e12, 1),
+           "launches": launches,
+           "forward_save_preact": {
+               "what": "GEMM1 1024->4096 bias+GELU keeping the pre-activation Z (aux store)",
+               "kernel": tpp.tpp_brgemm_describe(sts[0].handle),
+               "launch_us": round(ms_fwd * 1e3, 2),
+               "tflops": round(wl.calls[0].flops / (ms_fwd * 1e-3) / 1e12, 1)}}
+    del dev, sts, fns
+    torch.cuda.empty_cache()
     return out
 
 

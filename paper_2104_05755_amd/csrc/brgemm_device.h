@@ -14,6 +14,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 // Global-memory accesses through address-space-1 pointers, so that they compile to global_*
 // instructions.  (Through generic pointers they become flat_* instructions, which also count
@@ -92,6 +93,16 @@ template <int N>
 __device__ __forceinline__ void aux_load(const BrgemmParams& p, int64_t e0, float (&z)[N]) {
   if (p.c_bf16) {
     const uint16_t* ap = static_cast<const uint16_t*>(p.aux) + e0;
+    if constexpr (N == 4) {
+      if ((reinterpret_cast<uintptr_t>(ap) & 7) == 0) {
+        const u32x2 w = gld<u32x2>(ap);
+        z[0] = bf16_bits_to_f32(w[0] & 0xffffu);
+        z[1] = bf16_bits_to_f32(w[0] >> 16);
+        z[2] = bf16_bits_to_f32(w[1] & 0xffffu);
+        z[3] = bf16_bits_to_f32(w[1] >> 16);
+        return;
+      }
+    }
     if constexpr (N == 8) {
       if ((reinterpret_cast<uintptr_t>(ap) & 15) == 0) {
         const u32x4 w = gld<u32x4>(ap);
@@ -128,6 +139,12 @@ template <int N>
 __device__ __forceinline__ void aux_store(const BrgemmParams& p, int64_t e0, const float (&v)[N]) {
   if (p.c_bf16) {
     uint16_t* ap = static_cast<uint16_t*>(p.aux) + e0;
+    if constexpr (N == 4) {
+      if ((reinterpret_cast<uintptr_t>(ap) & 7) == 0) {
+        gst<u32x2>(ap, (u32x2){pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])});
+        return;
+      }
+    }
     if constexpr (N == 8) {
       if ((reinterpret_cast<uintptr_t>(ap) & 15) == 0) {
         gst<u32x4>(ap, (u32x4){pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
@@ -448,13 +465,19 @@ __device__ __forceinline__ void epilogue_via_lds(const BrgemmParams& p, const In
 }
 
 // ---------------------------------------------------------------------------------------------
-// Epilogue for a bf16 C that is not read (beta = 0) and no aux tensor.  Bias and activation are applied to the
+// Epilogue for a bf16 C that is not read (beta = 0).  Bias and activation are applied to the
 // accumulators where they are, each lane narrows its four consecutive rows of a column to bf16
 // and parks them in its own wave's LDS slab (column-major, WTM rows per column, 16-byte row
 // chunks XOR-swizzled by the column), and the wave then stores the slab as 16-byte runs of 8
 // rows, so every global store instruction writes whole 128-byte lines.  A wave touches only its
 // own slab, so no workgroup barrier is involved; the caller has passed one after the last LDS
-// read of the main loop.  ACT: 0 none, 1 ReLU, 2 GELU-tanh.
+// read of the main loop.  ACT: 0 none, 1 ReLU, 2 GELU-tanh, 3 ReLU_inv, 4 GELU-tanh_inv.
+// For the inverse activations the aux tensor (C's layout) is first loaded into the slab with the
+// store's 16-byte runs, and each lane reads its saved pre-activations from the very 8 bytes
+// where it then parks its result.  LDS operations of one wave complete in order, so every read
+// sees the wave's earlier writes and every write lands after the wave's earlier reads.
+// (Keeping the pre-activation, SAVE_PREACT, takes the fp32-slab epilogue: a second slab pass
+// here ran the 256x256 kernels out of registers.)
 // ---------------------------------------------------------------------------------------------
 template <int WTM, int WTN, int TM, int TN, bool FULL, int ACT>
 __device__ __forceinline__ void epilogue_bf16_act(const BrgemmParams& p, const Instance& in,
@@ -507,65 +530,58 @@ __device__ __forceinline__ void epilogue_bf16_act(const BrgemmParams& p, const I
         }
       }
   }
-#pragma unroll
-  for (int tm = 0; tm < TM; ++tm) {
-#pragma unroll
-    for (int tn = 0; tn < TN; ++tn) {
-      const int col = tn * 32 + (lane & 31);
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        float v[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          float x = acc[tm][tn][4 * q + e] + bias4[tm][q][e];
-          if constexpr (ACT == 1) x = x > 0.0f ? x : 0.0f;
-          if constexpr (ACT == 2) x = gelu_tanh(x);
-          v[e] = x;
-        }
-        const int ch = tm * 4 + q;             // 16-byte chunk of this lane's 8-row group
-        *reinterpret_cast<uint2*>(slab + col * COL_BYTES + ((ch ^ (col & (CPC - 1))) << 4) +
-                                  half * 8) = make_uint2(pack_bf16x2(v[0], v[1]),
-                                                         pack_bf16x2(v[2], v[3]));
-      }
-    }
-  }
-  // Read back: 64 lanes = 64 / CPC columns x CPC chunks per instruction.  LDS operations of one
-  // wave complete in order, so the reads see this wave's writes.
+  // The slab <-> global walk: 64 lanes = 64 / CPC columns x CPC chunks per instruction, columns
+  // advancing by COLS_PER_IT (instance column and offset tracked by additions, one division per
+  // lane).  fn(slab chunk, global element offset relative to the instance's C base, valid).
   constexpr int COLS_PER_IT = 64 / CPC;
   const int chunk = lane % CPC, csub = lane / CPC;
-  const int32_t R = row_base + chunk * 8;
-  bool row_ok;
-  int64_t row_off;
-  if (p.fused) {
-    const int32_t gi = R / p.m, r = R - gi * p.m;
-    row_ok = FULL || R < p.vrows;
-    row_off = (int64_t)gi * p.c_step_m + r;
-  } else {
-    row_ok = FULL || R < p.m;
-    row_off = R;
-  }
-  // Columns advance by COLS_PER_IT per iteration: track the instance column and offset by
-  // additions (one division per lane).
-  int32_t C = tc.col0 + wn * WTN + csub;
-  int32_t cin = C;
-  int64_t col_off;
-  if (p.fused) {
-    const int32_t gi = C / p.n;
-    cin = C - gi * p.n;
-    col_off = (int64_t)gi * p.c_step_n + (int64_t)cin * p.ldc;
-  } else {
-    col_off = (int64_t)C * p.ldc;
-  }
-  const int32_t c_lim = p.fused ? p.vcols : p.n;
-  const int64_t wrap = p.c_step_n - (int64_t)p.n * p.ldc;   // next instance, column 0
-  uint16_t* const cbase = static_cast<uint16_t*>(p.c) + in.c + row_off;
+  auto walk = [&](auto&& fn) {
+    const int32_t R = row_base + chunk * 8;
+    bool row_ok;
+    int64_t row_off;
+    if (p.fused) {
+      const int32_t gi = R / p.m, r = R - gi * p.m;
+      row_ok = FULL || R < p.vrows;
+      row_off = (int64_t)gi * p.c_step_m + r;
+    } else {
+      row_ok = FULL || R < p.m;
+      row_off = R;
+    }
+    int32_t C = tc.col0 + wn * WTN + csub;
+    int32_t cin = C;
+    int64_t col_off;
+    if (p.fused) {
+      const int32_t gi = C / p.n;
+      cin = C - gi * p.n;
+      col_off = (int64_t)gi * p.c_step_n + (int64_t)cin * p.ldc;
+    } else {
+      col_off = (int64_t)C * p.ldc;
+    }
+    const int32_t c_lim = p.fused ? p.vcols : p.n;
+    const int64_t wrap = p.c_step_n - (int64_t)p.n * p.ldc;   // next instance, column 0
 #pragma unroll 4
-  for (int it = 0; it < WTN / COLS_PER_IT; ++it) {
-    const int col_local = it * COLS_PER_IT + csub;
-    const u32x4 w = *reinterpret_cast<const u32x4*>(
-        slab + col_local * COL_BYTES + ((chunk ^ (col_local & (CPC - 1))) << 4));
-    if (row_ok && (FULL || C < c_lim)) {
-      uint16_t* cp = cbase + col_off;
+    for (int it = 0; it < WTN / COLS_PER_IT; ++it) {
+      const int col_local = it * COLS_PER_IT + csub;
+      char* sp = slab + col_local * COL_BYTES + ((chunk ^ (col_local & (CPC - 1))) << 4);
+      fn(sp, in.c + row_off + col_off, row_ok && (FULL || C < c_lim));
+      C += COLS_PER_IT;
+      col_off += (int64_t)COLS_PER_IT * p.ldc;
+      if (p.fused) {
+        cin += COLS_PER_IT;
+        while (cin >= p.n) {
+          cin -= p.n;
+          col_off += wrap;
+        }
+      }
+    }
+  };
+  // slab -> tensor at base (C or aux): 16-byte runs of 8 rows
+  auto store_slab = [&](void* base) {
+    uint16_t* const b16 = static_cast<uint16_t*>(base);
+    walk([&](const char* sp, int64_t off, bool ok) {
+      const u32x4 w = *reinterpret_cast<const u32x4*>(sp);
+      if (!ok) return;
+      uint16_t* cp = b16 + off;
       if ((reinterpret_cast<uintptr_t>(cp) & 15) == 0) {
         gst<u32x4>(cp, w);
       } else {
@@ -576,29 +592,78 @@ __device__ __forceinline__ void epilogue_bf16_act(const BrgemmParams& p, const I
           gst<uint16_t>(cp + 2 * e + 1, (uint16_t)(d[e] >> 16));
         }
       }
-    }
-    C += COLS_PER_IT;
-    col_off += (int64_t)COLS_PER_IT * p.ldc;
-    if (p.fused) {
-      cin += COLS_PER_IT;
-      while (cin >= p.n) {
-        cin -= p.n;
-        col_off += wrap;
-      }
-    }
+    });
+  };
+  // Each lane's four rows of one column in the slab: the 8 bytes of its 8-row group's chunk.
+  auto slab_at = [&](int tm, int tn, int q) -> char* {
+    const int col = tn * 32 + (lane & 31);
+    const int ch = tm * 4 + q;                 // 16-byte chunk of this lane's 8-row group
+    return slab + col * COL_BYTES + ((ch ^ (col & (CPC - 1))) << 4) + half * 8;
+  };
+  // The accumulators + bias, through activation A, narrowed into the slab.
+  auto park = [&](auto act_now) {
+    constexpr int A = decltype(act_now)::value;
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          char* sp = slab_at(tm, tn, q);
+          float v[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = acc[tm][tn][4 * q + e] + bias4[tm][q][e];
+          if constexpr (A == 3 || A == 4) {
+            const uint2 zb = *reinterpret_cast<const uint2*>(sp);   // saved pre-activations
+            const float z[4] = {bf16_bits_to_f32(zb.x & 0xffffu), bf16_bits_to_f32(zb.x >> 16),
+                                bf16_bits_to_f32(zb.y & 0xffffu), bf16_bits_to_f32(zb.y >> 16)};
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              v[e] = A == 3 ? (z[e] > 0.0f ? v[e] : 0.0f) : v[e] * gelu_tanh_grad(z[e]);
+          }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if constexpr (A == 1) v[e] = v[e] > 0.0f ? v[e] : 0.0f;
+            if constexpr (A == 2) v[e] = gelu_tanh(v[e]);
+          }
+          *reinterpret_cast<uint2*>(sp) = make_uint2(pack_bf16x2(v[0], v[1]),
+                                                     pack_bf16x2(v[2], v[3]));
+        }
+  };
+  if constexpr (ACT == 3 || ACT == 4) {
+    // aux -> slab with the store's 16-byte runs (out-of-range rows / columns are never read back
+    // into a stored value, so they are left as they are)
+    const uint16_t* const a16 = static_cast<const uint16_t*>(p.aux);
+    walk([&](char* sp, int64_t off, bool ok) {
+      if (!ok) return;
+      const uint16_t* ap = a16 + off;
+      *reinterpret_cast<u32x4*>(sp) =
+          (reinterpret_cast<uintptr_t>(ap) & 15) == 0 ? ld16(ap) : ld16_unaligned(ap);
+    });
   }
+  park(IntC<ACT>());
+  store_slab(p.c);
 }
 
 template <int WTM, int WTN, int TM, int TN, bool FULL>
 __device__ __forceinline__ void epilogue_bf16(const BrgemmParams& p, const Instance& in,
                                               const TileCoord& tc, int wm, int wn, int lane,
                                               int wave, char* lds, f32x16 (&acc)[TM][TN]) {
-  if (p.flags & TPP_EPI_GELU_TANH)
-    epilogue_bf16_act<WTM, WTN, TM, TN, FULL, 2>(p, in, tc, wm, wn, lane, wave, lds, acc);
-  else if (p.flags & TPP_EPI_RELU)
-    epilogue_bf16_act<WTM, WTN, TM, TN, FULL, 1>(p, in, tc, wm, wn, lane, wave, lds, acc);
-  else
-    epilogue_bf16_act<WTM, WTN, TM, TN, FULL, 0>(p, in, tc, wm, wn, lane, wave, lds, acc);
+  const uint32_t f = p.flags;
+#define TPP_EPI_BF16(A) \
+  epilogue_bf16_act<WTM, WTN, TM, TN, FULL, A>(p, in, tc, wm, wn, lane, wave, lds, acc)
+  if (f & TPP_EPI_GELU_TANH_INV) {
+    TPP_EPI_BF16(4);
+  } else if (f & TPP_EPI_RELU_INV) {
+    TPP_EPI_BF16(3);
+  } else if (f & TPP_EPI_GELU_TANH) {
+    TPP_EPI_BF16(2);
+  } else if (f & TPP_EPI_RELU) {
+    TPP_EPI_BF16(1);
+  } else {
+    TPP_EPI_BF16(0);
+  }
+#undef TPP_EPI_BF16
 }
 
 }  // namespace dev

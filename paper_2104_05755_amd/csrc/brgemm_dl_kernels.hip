@@ -400,7 +400,7 @@ void brgemm_bf16_dl_kernel(BrgemmParams p) {
     if (lead) lds_barrier();
   }
   __syncthreads();
-  if (p.c_bf16 && p.beta == 0.0f && !(p.flags & EPI_AUX_MASK))
+  if (p.c_bf16 && p.beta == 0.0f && !(p.flags & TPP_EPI_SAVE_PREACT))
     epilogue_bf16<WTM, WTN, TM, TN, FULL>(p, in, tc, wm, wn, lane, wave, lds, acc);
   else
     epilogue_via_lds<WTM, WTN, TM, TN, FULL>(p, in, tc, wm, wn, lane, wave,
