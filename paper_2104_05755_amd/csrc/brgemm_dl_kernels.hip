@@ -127,10 +127,19 @@ void brgemm_bf16_dl_kernel(BrgemmParams p) {
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);   // wave-uniform: kept in SGPRs
   const int wm = wave % WAVES_M, wn = wave / WAVES_M;
-  const TileCoord tc = decode_tile(p, BM, BN);
+  // Split launches (p.split > 1): workgroup b reduces chunk b / total_tiles of the stage list of
+  // tile b % total_tiles (consecutive block ids still alternate over the XCDs, as the tile order
+  // assumes) into a partial tile of the work buffer; a finishing kernel adds the chunks.
+  const int64_t bid = blockIdx.x;
+  const int32_t chunk = p.split > 1 ? (int32_t)(bid / p.total_tiles) : 0;
+  const int64_t tile_bid = bid - (int64_t)chunk * p.total_tiles;
+  const TileCoord tc = decode_tile_at(p, BM, BN, tile_bid);
   const Instance in = instance_of(p, tc.g);
   const int32_t ksteps = p.k / DL_BK;
-  const int32_t stages = (int32_t)(in.npairs * ksteps);
+  const int32_t all_stages = (int32_t)(in.npairs * ksteps);
+  const int32_t s_first = p.split > 1 ? (int32_t)((int64_t)all_stages * chunk / p.split) : 0;
+  const int32_t stages =
+      p.split > 1 ? (int32_t)((int64_t)all_stages * (chunk + 1) / p.split) - s_first : all_stages;
 
   // Element offsets of the first instance block the tile touches in A and in B: every row / column
   // offset of the tile is at least this (the host takes this kernel only for non-negative steps
@@ -178,7 +187,7 @@ void brgemm_bf16_dl_kernel(BrgemmParams p) {
   // Stages are issued in order; (iss_i, iss_kk) is the pair and k offset of the next one, so no
   // stage index is ever divided.  A stage's wave-loads can be spread over other work:
   // stage_begin(), issue_load(r) for r < LPS (A loads first, then B), stage_end().
-  int32_t iss_i = 0, iss_kk = 0, iss_s = 0;
+  int32_t iss_i = s_first / ksteps, iss_kk = (s_first - iss_i * ksteps) * DL_BK, iss_s = 0;
   const char* ua = nullptr;
   const char* ub = nullptr;
   i32x4 ra, rb;
@@ -400,6 +409,21 @@ void brgemm_bf16_dl_kernel(BrgemmParams p) {
     if (lead) lds_barrier();
   }
   __syncthreads();
+  if (p.split > 1) {
+    // the chunk's partial tile: f32x16 (tm, tn) accumulators of each lane, lane-contiguous
+    float* w = p.ws + (size_t)(chunk * p.total_tiles + tile_bid) * (BM * BN) +
+               (size_t)wave * (TM * TN * 1024) + lane * 16;
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          gst<f32x4>(w + (tm * TN + tn) * 1024 + 4 * q,
+                     (f32x4){acc[tm][tn][4 * q], acc[tm][tn][4 * q + 1], acc[tm][tn][4 * q + 2],
+                             acc[tm][tn][4 * q + 3]});
+    return;
+  }
   if (p.c_bf16 && p.beta == 0.0f && !(p.flags & TPP_EPI_SAVE_PREACT))
     epilogue_bf16<WTM, WTN, TM, TN, FULL>(p, in, tc, wm, wn, lane, wave, lds, acc);
   else
@@ -440,6 +464,19 @@ void launch_dl(const BrgemmParams& p, bool full, dim3 grid, hipStream_t stream) 
 }
 
 }  // namespace
+
+bool dl_wave_grid(int32_t id, int& waves_m, int& waves_n) {
+  switch (id) {
+    case K_BF16_DL_256x256: waves_m = 2; waves_n = 4; return true;
+    case K_BF16_PP_256x256:
+    case K_BF16_DL64K_256x256: waves_m = 4; waves_n = 2; return true;
+    case K_BF16_DL_128x128:
+    case K_BF16_DL_64x64:
+    case K_BF16_DL64K_128x128:
+    case K_BF16_DL64K_64x64: waves_m = 2; waves_n = 2; return true;
+    default: return false;
+  }
+}
 
 hipError_t launch_brgemm_dl(const BrgemmParams& p, int32_t id, bool full, dim3 grid,
                             hipStream_t stream) {

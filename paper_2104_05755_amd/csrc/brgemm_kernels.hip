@@ -723,6 +723,43 @@ __global__ __launch_bounds__(NT) void brgemm_f32_split_finish(BrgemmParams p) {
   store_group<true>(p, in, tc.row0 + r0, tc.col0 + c_local, v4);
 }
 
+// Finishing step of a split direct-LDS launch.  A partial tile holds, for each wave (waves_m x
+// waves_n of them, a WTM x WTN tile each) and 32x32 block (tm, tn), every lane's 16 accumulators
+// (f32x16, lane-contiguous).  Thread item i = ((wave * TM + tm) * TN + tn) * 256 + lane * 4 + q
+// takes the four consecutive rows of MFMA register group q (rows 32 tm + 8 q + 4 (lane / 32) ..
+// + 3 and column 32 tn + lane % 32 of the wave tile), so consecutive threads read consecutive 16
+// bytes.  It sums them over the chunks in chunk order (the result does not depend on timing) and
+// applies beta * C, bias, activation, the aux steps and the store as an unsplit epilogue does.
+__global__ __launch_bounds__(NT) void brgemm_dl_split_finish(BrgemmParams p, int32_t bm,
+                                                             int32_t bn, int32_t waves_m,
+                                                             int32_t waves_n, int32_t per_tile) {
+  const int64_t tile_bid = blockIdx.x / per_tile;
+  const int32_t item = (int32_t)(blockIdx.x - tile_bid * per_tile) * NT + threadIdx.x;
+  const TileCoord tc = decode_tile_at(p, bm, bn, tile_bid);
+  const Instance in = instance_of(p, tc.g);
+  const int32_t wtm = bm / waves_m, wtn = bn / waves_n;
+  const int32_t tms = wtm / 32, tns = wtn / 32;
+  const int32_t lane = (item & 255) >> 2, q = item & 3;
+  const int32_t rest = item >> 8;
+  const int32_t tn = rest % tns, tm = (rest / tns) % tms, wave = rest / (tns * tms);
+  const int32_t wm = wave % waves_m, wn = wave / waves_m;
+  const float* w = p.ws + (size_t)tile_bid * (bm * bn) + (size_t)item * 4;
+  const size_t step = (size_t)p.total_tiles * bm * bn;
+  f32x4 sum = {0.0f, 0.0f, 0.0f, 0.0f};
+  int32_t ch = 0;
+  for (; ch + 4 <= p.split; ch += 4) {
+    f32x4 v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = gld<f32x4>(w + (size_t)(ch + u) * step);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) sum += v[u];
+  }
+  for (; ch < p.split; ++ch) sum += gld<f32x4>(w + (size_t)ch * step);
+  const float v4[4] = {sum[0], sum[1], sum[2], sum[3]};
+  store_group<false>(p, in, tc.row0 + wm * wtm + tm * 32 + 8 * q + 4 * (lane >> 5),
+                     tc.col0 + wn * wtn + tn * 32 + (lane & 31), v4);
+}
+
 struct KernelInfo {
   const char* name;
   int bm, bn;
@@ -802,8 +839,19 @@ hipError_t launch_brgemm(BrgemmParams& p, int32_t id, hipStream_t stream) {
     case K_BF16_PP_256x256:
     case K_BF16_DL64K_256x256:
     case K_BF16_DL64K_128x128:
-    case K_BF16_DL64K_64x64:
-      return launch_brgemm_dl(p, id, full, grid, stream);
+    case K_BF16_DL64K_64x64: {
+      if (p.split <= 1) return launch_brgemm_dl(p, id, full, grid, stream);
+      // split over the stage list: chunk partials, then the finishing sum and epilogue
+      const hipError_t e =
+          launch_brgemm_dl(p, id, full, dim3((unsigned)(p.total_tiles * p.split)), stream);
+      if (e != hipSuccess) return e;
+      int wm = 0, wn = 0;
+      if (!dl_wave_grid(id, wm, wn)) return hipErrorInvalidValue;
+      const int32_t per_tile = bm * bn / 4 / NT;
+      hipLaunchKernelGGL(brgemm_dl_split_finish, dim3((unsigned)(p.total_tiles * per_tile)),
+                         block, 0, stream, p, bm, bn, wm, wn, per_tile);
+      break;
+    }
     case K_BF16_GENERIC:
       hipLaunchKernelGGL((brgemm_bf16_kernel<64, 64, 2, 2, true>), grid, block, 0, stream, p);
       break;

@@ -46,9 +46,10 @@ struct BrgemmParams {
   int32_t tiles_m, tiles_n;  // tiles per group
   int64_t groups;            // 1 (strided) or G (explicit)
   int64_t total_tiles;
-  // Split over the pair list (fp32 kernel, grids too small to fill the GPU): split > 1 chunks of
-  // each instance's pairs are reduced by separate workgroups into ws (split x total_tiles tiles of
-  // 64 x 64 fp32), then summed in chunk order by a finishing kernel that applies the epilogue.
+  // Split over the pair list (grids too small to fill the GPU): split > 1 chunks of each
+  // instance's pairs (fp32 kernel) or stages (direct-to-LDS kernels) are reduced by separate
+  // workgroups into ws (split x total_tiles fp32 tiles), then summed in chunk order by a
+  // finishing kernel that applies the epilogue.
   int32_t split;             // 1: no split
   float* ws;
   // Tensor of C's type and layout read or written by the back-propagation epilogue bits.
@@ -85,8 +86,11 @@ int kernel_k_step(int32_t id);   // k granularity the instance needs (1 = any k)
 // Fill the tiling fields of p for kernel `id` and launch on `stream`.
 hipError_t launch_brgemm(BrgemmParams& p, int32_t id, hipStream_t stream);
 // The direct-to-LDS instances (brgemm_dl_kernels.hip); p's tiling fields already filled.
+// With p.split > 1, grid covers total_tiles * split workgroups writing partial tiles to p.ws.
 hipError_t launch_brgemm_dl(const BrgemmParams& p, int32_t id, bool full, dim3 grid,
                             hipStream_t stream);
+// Wave layout (waves along m, along n) of a direct-to-LDS instance; false for other ids.
+bool dl_wave_grid(int32_t id, int& waves_m, int& waves_n);
 
 // Reduce TPP launcher; `work` is a device buffer of `work_floats` floats for partial results.
 struct ReduceParams {

@@ -105,14 +105,19 @@ int32_t choose_kernel(const tpp_brgemm_kernel_s& h, const tpp::BrgemmParams& p) 
       {bk64 ? tpp::K_BF16_DL64K_256x256 : tpp::K_BF16_PP_256x256, tpp::K_BF16_256x256, 256, 256},
       {bk64 ? tpp::K_BF16_DL64K_128x128 : tpp::K_BF16_DL_128x128, tpp::K_BF16_128x128, 128, 128},
       {bk64 ? tpp::K_BF16_DL64K_64x64 : tpp::K_BF16_DL_64x64, tpp::K_BF16_64x64, 64, 64}};
+  // total k of one instance's batch reduction (address kind: per instance, not known here)
+  const int64_t ktot = h.desc.kind == TPP_BR_ADDRESS ? 0 : p.count * (int64_t)h.desc.k;
   for (const Cand& c : cands) {
     // never pad a virtual C out to a larger tile (the 64x64 tile is the floor)
     const bool last = c.bm == 64;
     if (!last && (c.bm > p.vrows || c.bn > p.vcols)) continue;
     const int64_t tiles = p.groups * ((p.vrows + c.bm - 1) / c.bm) * ((p.vcols + c.bn - 1) / c.bn);
+    const bool dl = dl_kind && dl_offsets_fit(h, p, c.bm, c.bn);
     // two tiles per compute unit: one workgroup's barriers and epilogue overlap the other's MFMAs
-    if (tiles >= 512 || last)
-      return (dl_kind && dl_offsets_fit(h, p, c.bm, c.bn)) ? c.dl_id : c.vec_id;
+    if (tiles >= 512 || last) return dl ? c.dl_id : c.vec_id;
+    // a long batch reduction (weight gradients: all token blocks) makes up the parallelism by
+    // splitting its stage list instead (see launch), keeping the large tile's operand reuse
+    if (dl && bk64 && c.bm == 256 && ktot >= 8192 && tiles * 8 >= 256) return c.dl_id;
   }
   return tpp::K_BF16_64x64;
 }
@@ -181,6 +186,28 @@ tpp_status launch(const tpp_brgemm_kernel_s* h, tpp::BrgemmParams& p, void* stre
             work_buffer(WORK_SPLIT, stream, tpp::f32_split_ws_floats(p.split, tiles), &p.ws);
         if (st != TPP_OK) return st;
       }
+    }
+  }
+  if (p.split == 1 && tpp::kernel_k_step(id) > 1 && p.kind != TPP_BR_ADDRESS && p.count > 0) {
+    // Direct-to-LDS kernel on a grid of fewer tiles than compute units: split every tile's
+    // stage list into chunks reduced by separate workgroups (about 256 in all, at least 8 stages
+    // each) and add the chunks in a finishing kernel.  TPP_SPLIT overrides the count.
+    const int bm = tpp::kernel_tile_m(id), bn = tpp::kernel_tile_n(id);
+    const int64_t tiles = p.groups * ((p.vrows + bm - 1) / bm) * ((p.vcols + bn - 1) / bn);
+    const int64_t stages = p.count * (h->desc.k / tpp::kernel_k_step(id));
+    int64_t split = 1;
+    if (tiles < 256 && stages >= 16) {
+      split = 256 / tiles;
+      if (split > 8) split = 8;
+      if (split > stages / 8) split = stages / 8;
+    }
+    if (const char* env = std::getenv("TPP_SPLIT")) split = std::atoi(env);
+    if (split > stages) split = stages;
+    if (split > 1) {
+      p.split = (int32_t)split;
+      const tpp_status st =
+          work_buffer(WORK_SPLIT, stream, split * tiles * (int64_t)bm * bn, &p.ws);
+      if (st != TPP_OK) return st;
     }
   }
   if (std::getenv("TPP_LOG"))

@@ -289,3 +289,54 @@ def test_mlp_backward_full_size_sampled():
         blk = np.ascontiguousarray(dz[:, i]).reshape(-1)   # 64 x (nb * 64), column-major
         o, _ = oracle.reduce(blk, BLK, nb * BLK, BLK, "bf16", "sum", "cols")
         assert rel_fro(got["db1"][i * BLK:(i + 1) * BLK], o) <= 5e-3
+
+
+# ---- split stage lists (long batch reductions on grids of few tiles) -----------------------
+DL_KERNELS = [5, 6, 7, 8, 9, 10, 11]
+
+
+@pytest.mark.parametrize("split", [2, 3, 5])
+@pytest.mark.parametrize("kid", DL_KERNELS)
+def test_split_stage_list_integer_bit_exact(kid, split, monkeypatch):
+    """Every direct-LDS instance with its stage list split into chunks (partial tiles summed in
+    chunk order by the finishing kernel): bit-exact on small-integer data, with the bias, the
+    ReLU_inv aux step and a ragged strided grid, for bf16 and fp32 outputs."""
+    monkeypatch.setenv("TPP_FORCE_KERNEL", str(kid))
+    monkeypatch.setenv("TPP_SPLIT", str(split))
+    rng = np.random.default_rng(kid * 10 + split)
+    m, n, k, count, gm, gn = 72, 64, 64, 7, 3, 2
+    draw = lambda s: rng.integers(-3, 4, size=s).astype(np.float32)
+    for ct in ("bf16", "f32"):
+        a = wk.bf16_bits(draw((gm * count * k * m,)))
+        b = wk.bf16_bits(draw((gn * count * n * k,)))
+        zv = draw((gm * gn * m * n,))
+        fill = np.full(gm * gn * m * n, 0x7FC0, np.uint16) if ct == "bf16" else \
+            np.full(gm * gn * m * n, np.nan, np.float32)
+        arrays = dict(a=a, b=b, c=fill, bias=draw((gm * m,)),
+                      z=wk.bf16_bits(zv) if ct == "bf16" else zv)
+        call = wk.Call(m, n, k, m, k, m, "bf16", ct, 0.0, "stride", k * m, n * k,
+                       {"bias", "relu_inv"}, G=gm * gn,
+                       grid=dict(gm=gm, gn=gn, a_step_m=count * k * m, b_step_n=count * n * k,
+                                 c_step_m=m * n, c_step_n=gm * m * n, bias_step_m=m),
+                       count=count, a="a", b="b", c="c", bias="bias", aux="z")
+        say(f"split {split} kernel {kid} {ct}")
+        ref = {k2: np.array(v, copy=True) for k2, v in arrays.items()}
+        run_call_oracle(call, ref)
+        got = gpu_steps([call], arrays, ["c"])["c"]
+        assert np.array_equal(got, ref["c"])
+
+
+@pytest.mark.parametrize("split", [2, 4])
+@pytest.mark.parametrize("kid", [9, 10])
+def test_split_mlp_block_matches_oracle(kid, split, monkeypatch):
+    """The MLP block's two calls (bias + GELU, bias) with split stage lists, random data."""
+    monkeypatch.setenv("TPP_FORCE_KERNEL", str(kid))
+    monkeypatch.setenv("TPP_SPLIT", str(split))
+    wl = wk.mlp_block(seed=43, tokens=512, hidden=512, inter=512)
+    say(f"split {split} kernel {kid} mlp_block")
+    ref = run_steps_oracle(wk.Workload(wl.name, wl.arrays, wl.calls, steps=wl.calls))
+    got = gpu_steps(wl.calls, wl.arrays, ["h", "y"])
+    _compare("h", got["h"], ref["h"], wl.calls[0])
+    _compare("y", got["y"], ref["y"], wl.calls[1])
+    again = gpu_steps(wl.calls, wl.arrays, ["y"])   # chunk-order sums: the same bits every run
+    assert np.array_equal(again["y"], got["y"])
