@@ -88,6 +88,9 @@ def lib():
         _lib.oracle_transform_batched.restype = ctypes.c_int
         _lib.oracle_transform_batched.argtypes = [i32, i32, i32, i64, i64, i32, i32, vp, i64, vp,
                                                   i64, i64]
+        _lib.oracle_embedding_bag.restype = ctypes.c_int
+        _lib.oracle_embedding_bag.argtypes = [i64, i32, i32, vp, i64, i64, vp, vp, i32, vp, i64,
+                                              vp]
         _lib.oracle_gelu_tanh_grad.restype = ctypes.c_double
         _lib.oracle_gelu_tanh_grad.argtypes = [ctypes.c_double]
         _lib.oracle_reduce.restype = ctypes.c_int
@@ -319,6 +322,22 @@ def bf16_to_f32(h: int) -> float:
 
 def gelu_tanh(x: float) -> float:
     return float(lib().oracle_gelu_tanh(float(x)))
+
+
+def embedding_bag(w: np.ndarray, M: int, E: int, ldw: int, w_type: str, begin, idx,
+                  out: np.ndarray, ldo: int, out_type: str, want_ref64=False):
+    """Sparse embedding gather-reduce (Alg. 5) into ``out`` (in place); returns the unrounded
+    sums (n_bags x E) when ``want_ref64``."""
+    _check_dtype(w, w_type, "w")
+    _check_dtype(out, out_type, "out")
+    begin, idx = _as_i64(begin), _as_i64(idx)
+    n_bags = len(begin) - 1
+    ref = np.empty((n_bags, E), dtype=np.float64) if want_ref64 else None
+    rc = lib().oracle_embedding_bag(M, E, _DTYPES[w_type], _ptr(w), ldw, n_bags, _ptr(begin),
+                                    _ptr(idx), _DTYPES[out_type], _ptr(out), ldo, _ptr(ref))
+    if rc != 0:
+        raise ValueError("oracle_embedding_bag rejected its arguments")
+    return ref
 
 
 def gelu_tanh_grad(x: float) -> float:

@@ -443,3 +443,34 @@ int oracle_transform_batched(int32_t kind, int32_t m, int32_t n, int64_t ld_in, 
   }
   return 0;
 }
+
+/* Sparse embedding gather-reduce (Alg. 5): the output row of bag b is o = a^T W with a the
+ * multi-hot vector of the bag's indices, i.e. the sum of the table rows the bag lists,
+ *   out[b][e] = sum_{j = begin[b]}^{begin[b+1]-1} W[idx[j]][e]      (e < E),
+ * a listed index counted as often as it is listed (the loop of Alg. 5 over the indices).  Row r
+ * of the table starts at W + r*ldw.  Sums are fp64, rounded once to the output type.  An empty
+ * bag gives zeros.  Returns -1 for an index outside [0, M) or a decreasing begin. */
+int oracle_embedding_bag(int64_t M, int32_t E, int32_t w_type, const void* W, int64_t ldw,
+                         int64_t n_bags, const int64_t* begin, const int64_t* idx,
+                         int32_t out_type, void* out, int64_t ldo, double* ref64) {
+  if (M < 0 || E <= 0 || n_bags < 0 || ldw < E || ldo < E) return -1;
+  if (w_type != ORACLE_F32 && w_type != ORACLE_BF16) return -1;
+  if (out_type != ORACLE_F32 && out_type != ORACLE_BF16) return -1;
+  if (n_bags == 0) return 0;
+  if (!begin || !out) return -1;
+  for (int64_t b = 0; b < n_bags; ++b) {
+    if (begin[b + 1] < begin[b]) return -1;
+    for (int64_t j = begin[b]; j < begin[b + 1]; ++j)
+      if (idx[j] < 0 || idx[j] >= M) return -1;
+  }
+  for (int64_t b = 0; b < n_bags; ++b) {
+    for (int32_t e = 0; e < E; ++e) {
+      double s = 0.0;
+      for (int64_t j = begin[b]; j < begin[b + 1]; ++j)
+        s += oracle_widen(W, idx[j] * ldw + e, w_type);
+      if (ref64) ref64[b * (int64_t)E + e] = s;
+      store_rounded(out, b * ldo + e, out_type, s);
+    }
+  }
+  return 0;
+}

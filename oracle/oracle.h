@@ -18,6 +18,7 @@
  *     the fully-connected layer with TPPs as well): the RELU_inv / GELU_inv TPPs of Table 1 fused
  *     after the BRGEMM, the pre-activation kept by the forward call, and the loops of Alg. 6 around
  *     the Reduce and Transform TPPs.
+ *   - The sparse embedding gather-reduce of Alg. 5 (a multi-hot vector times a table).
  *
  * Storage reading: every 2D block is column-major with a leading dimension (element (r, c) of an
  * m x n block sits at base + r + c*ld), which is how Alg. 6 lays out its blocked tensors (the
@@ -121,6 +122,15 @@ int oracle_reduce_batched(int32_t m, int32_t n, int64_t ld, int32_t in_type, con
 int oracle_transform_batched(int32_t kind, int32_t m, int32_t n, int64_t ld_in, int64_t ld_out,
                              int32_t es, int32_t alpha, const void* in, int64_t in_stride,
                              void* out, int64_t out_stride, int64_t G);
+
+/* Sparse embedding gather-reduce (Alg. 5): out[b][e] = sum over j in [begin[b], begin[b+1]) of
+ * W[idx[j]][e] (row r at W + r*ldw, output row b at out + b*ldo), fp64 sums rounded once to
+ * out_type; repeated indices count as often as listed; an empty bag gives zeros.  ref64
+ * (optional): n_bags x E unrounded sums.  Returns -1 for an index outside [0, M), a decreasing
+ * begin, or a bad size. */
+int oracle_embedding_bag(int64_t M, int32_t E, int32_t w_type, const void* W, int64_t ldw,
+                         int64_t n_bags, const int64_t* begin, const int64_t* idx,
+                         int32_t out_type, void* out, int64_t ldo, double* ref64);
 
 /* Helpers the tests pin on their own: exact widening and the round-to-nearest-even narrowing
  * used for every output element. */

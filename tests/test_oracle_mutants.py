@@ -76,6 +76,18 @@ BACKWARD_MUTANTS = {
     "reduce_batch_out_packed": ("out_x ? out_x + g * out_stride : NULL", "out_x ? out_x + g * m : NULL"),
 }
 
+# Embedding gather-reduce mutants, caught by the embedding pins.
+EMBEDDING_MUTANTS = {
+    "emb_first_index_dropped": ("for (int64_t j = begin[b]; j < begin[b + 1]; ++j)\n        s +=",
+                                "for (int64_t j = begin[b] + 1; j < begin[b + 1]; ++j)\n        s +="),
+    "emb_row_stride": ("s += oracle_widen(W, idx[j] * ldw + e, w_type);",
+                       "s += oracle_widen(W, idx[j] * E + e, w_type);"),
+    "emb_out_stride": ("store_rounded(out, b * ldo + e, out_type, s);",
+                       "store_rounded(out, b * E + e, out_type, s);"),
+    "emb_index_as_position": ("s += oracle_widen(W, idx[j] * ldw + e, w_type);",
+                              "s += oracle_widen(W, j * ldw + e, w_type);"),
+}
+
 
 @pytest.fixture(scope="module")
 def source():
@@ -115,3 +127,9 @@ def test_transform_pins_catch_planted_mistake(name, source, tmp_path):
 def test_backward_pins_catch_planted_mistake(name, source, tmp_path):
     old, new = BACKWARD_MUTANTS[name]
     _caught(old, new, "test_oracle_backward_pins.py", source, tmp_path, name)
+
+
+@pytest.mark.parametrize("name", sorted(EMBEDDING_MUTANTS))
+def test_embedding_pins_catch_planted_mistake(name, source, tmp_path):
+    old, new = EMBEDDING_MUTANTS[name]
+    _caught(old, new, "test_oracle_embedding_pins.py", source, tmp_path, name)

@@ -17,6 +17,7 @@ base + r + c*ld, the way Alg. 6 lays out its blocked tensors with the b_m / b_k 
                 block) drawn from pools of blocks, beta = 1, fp32 out
   reduce_bn     the Reduce TPP on a conv output: per-channel sum and sum of squares (the
                 statistics step of batchnorm, Sec. 5.1.2)
+  embedding_bag sparse embedding lookups (Alg. 5): per bag, the sum of the table rows it lists
   mlp_backward  the transformer MLP trained: GEMM1 keeping its pre-activation, then the backward
                 pass through both layers (weight transposes, GELU_inv fused into the data
                 gradient, weight gradients batch-reduced over token blocks, bias gradients by the
@@ -124,6 +125,26 @@ class ReduceStep:
     G: int = 1
     in_stride: int = 0
     out_stride: int = 0
+
+
+@dataclass
+class EmbeddingStep:
+    """Sparse embedding gather-reduce (Alg. 5): out row b = sum of the table rows idx[j] for j in
+    [begin[b], begin[b+1]); table rows ldw apart, output rows ldo apart."""
+    M: int
+    E: int
+    ldw: int
+    ldo: int
+    w_type: str
+    out_type: str
+    w: str = "w"
+    begin: str = "begin"
+    idx: str = "idx"
+    out: str = "out"
+
+    @property
+    def n_bags(self) -> int:
+        return -1   # from the begin array's length - 1
 
 
 @dataclass
@@ -331,6 +352,28 @@ def mlp_backward(seed: int = 6, tokens: int = 8192, hidden: int = 1024,
              tr("x", "xt", nb * hb), b1c, b2c, *red("dy", hb, "p2", "db2"), b3c, b4c,
              *red("dz", ib, "p1", "db1")]
     return Workload("mlp_backward", arrays, [fwd, b1c, b2c, b3c, b4c], steps=steps)
+
+
+def embedding_bag(seed: int = 7, rows: int = 1_000_000, dim: int = 128, bags: int = 16384,
+                  min_pool: int = 1, max_pool: int = 64, w_type: str = "f32",
+                  out_type: str = "f32", pad: int = 0) -> Workload:
+    """DLRM-style sparse embedding lookups (Alg. 5): a table of ``rows`` x ``dim`` entries, U[-1,1];
+    ``bags`` multi-hot lookups of a pooling factor uniform on {min_pool..max_pool}, indices
+    uniform on the table with replacement (CSR: begin[bags + 1], idx).  ``pad`` widens the table's
+    and the output's row strides.  The paper defers DLRM's table sizes to earlier work; these
+    sizes stand in for one large table of its MLPerf-style configuration."""
+    rng = np.random.default_rng(seed)
+    ldw, ldo = dim + pad, dim + pad
+    wv = _uniform(rng, (rows * ldw,))
+    w = wv if w_type == "f32" else bf16_bits(wv)
+    lens = rng.integers(min_pool, max_pool + 1, size=bags)
+    begin = np.zeros(bags + 1, dtype=np.int64)
+    begin[1:] = np.cumsum(lens)
+    idx = rng.integers(0, rows, size=int(begin[-1])).astype(np.int64)
+    out = np.full(bags * ldo, np.nan, np.float32) if out_type == "f32" else \
+        np.full(bags * ldo, 0x7FC0, np.uint16)
+    st = EmbeddingStep(rows, dim, ldw, ldo, w_type, out_type)
+    return Workload("embedding_bag", dict(w=w, begin=begin, idx=idx, out=out), [], steps=[st])
 
 
 CONFIGS = {
