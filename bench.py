@@ -9,8 +9,8 @@ launches).  ``roofline`` takes the dominant launch's mean duration over K more s
 timing-only (fence-free) HIP event on its stream around each launch.  The same run also
 times the other workloads (fp32 single BRGEMM, MLP fully-connected layer, 3x3 convolution with
 batchnorm statistics via the Reduce TPP, gathered address-based BRGEMM, the Transform TPP's
-transpose and VNNI formatting of a 64 MB tensor, and the MLP block's backward pass) under
-``per_config``,
+transpose and VNNI formatting of a 64 MB tensor, the MLP block's backward pass, and the sparse
+embedding gather-reduce) under ``per_config``,
 and the CPU oracle on a bounded sample of the headline workload under ``cpu_baseline``.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
@@ -332,7 +332,33 @@ def per_config(args, torch, tpp, torch_io, wk, np, stream):
         torch.cuda.empty_cache()
     out.update(transform_entries(args, torch, tpp, stream))
     out["mlp_backward"] = backward_entry(args, torch, tpp, torch_io, wk, stream)
+    out["embedding_bag"] = embedding_entry(args, torch, tpp, torch_io, wk, stream)
     return out
+
+
+def embedding_entry(args, torch, tpp, torch_io, wk, stream):
+    """The sparse embedding gather-reduce (Alg. 5) on the DLRM-style lookup workload: one launch
+    timed over max(steps, 50) back-to-back launches.  HBM bound: its algorithmic bytes are every
+    listed row once per listing (the gather), the index and bag lists, and the output rows."""
+    wl = wk.embedding_bag()
+    dev = torch_io.upload(wl)
+    st = wl.steps[0]
+    pst = torch_io.prepare_step(st, dev)
+    f = lambda: torch_io.launch_step(pst, dev, stream)
+    time_steps([f], min(max(args.steps, 50), args.warmup), 0, torch)   # warm-up
+    ms = time_bursts([f], max(args.steps, 50), torch)[0]
+    n_bags = len(wl.arrays["begin"]) - 1
+    lookups = int(wl.arrays["begin"][-1])
+    es = 4 if st.w_type == "f32" else 2
+    byts = lookups * st.E * es + 8 * lookups + 8 * (n_bags + 1) + n_bags * st.E * 4
+    gbs = byts / (ms * 1e-3) / 1e9
+    del dev, pst
+    torch.cuda.empty_cache()
+    return {"workload": f"{n_bags} bags of 1..64 lookups ({lookups} in all) into a {st.M} x "
+                        f"{st.E} {st.w_type} table ({st.M * st.E * es / 1e6:.0f} MB), fp32 out",
+            "launch_us": round(ms * 1e3, 2), "alg_bytes": byts, "hbm_gbs": round(gbs, 1),
+            "hbm_frac": round(gbs / PEAK_HBM_GBS, 4),
+            "lookups_per_s": round(lookups / (ms * 1e-3) / 1e9, 2), "lookups_unit": "G/s"}
 
 
 def backward_entry(args, torch, tpp, torch_io, wk, stream):

@@ -1,5 +1,5 @@
-"""MI355X (gfx950) TPP library: thin Python binding of the C ABI in include/tpp_brgemm.h and
-include/tpp_transform.h.
+"""MI355X (gfx950) TPP library: thin Python binding of the C ABI in include/tpp_brgemm.h,
+include/tpp_transform.h and include/tpp_embedding.h.
 
 Argument marshalling only: every step of the computation runs in the HIP kernels of
 ``libtpp_mi355x.so``.  The functions keep the C names; pointers are plain integers (device
@@ -84,6 +84,8 @@ _sig("tpp_reduce", _i32, _i32, _i32, _i64, _i32, _c_void_p, _i32, ctypes.c_uint3
      _c_void_p, _c_void_p)
 _sig("tpp_transform", _i32, _i32, _i32, _i32, _i64, _i64, _i32, _i32, _c_void_p, _c_void_p,
      _c_void_p)
+_sig("tpp_embedding_bag", _i32, _i64, _i32, _i32, _c_void_p, _i64, _i64, _c_void_p, _c_void_p,
+     _i32, _c_void_p, _i64, _c_void_p)
 _sig("tpp_reduce_batched", _i32, _i32, _i32, _i64, _i32, _c_void_p, _i64, _i64, _i32,
      ctypes.c_uint32, _c_void_p, _c_void_p, _i64, _c_void_p)
 _sig("tpp_transform_batched", _i32, _i32, _i32, _i32, _i64, _i64, _i32, _i32, _c_void_p, _i64,
@@ -189,6 +191,11 @@ def tpp_transform_batched(kind, m, n, ld_in, ld_out, dtype, alpha, x, in_stride,
                           G, stream=None):
     _check(_lib.tpp_transform_batched(kind, m, n, ld_in, ld_out, dtype, alpha, _p(x), in_stride,
                                       _p(out), out_stride, G, stream), "tpp_transform_batched")
+
+
+def tpp_embedding_bag(M, E, w_type, W, ldw, n_bags, begin, idx, out_type, out, ldo, stream=None):
+    _check(_lib.tpp_embedding_bag(M, E, w_type, _p(W), ldw, n_bags, _p(begin), _p(idx), out_type,
+                                  _p(out), ldo, stream), "tpp_embedding_bag")
 
 
 def tpp_status_string(s: int) -> str:

@@ -5,6 +5,7 @@
 #include <stdint.h>
 
 #include "tpp_brgemm.h"
+#include "tpp_embedding.h"
 #include "tpp_transform.h"
 
 namespace tpp {
@@ -131,5 +132,21 @@ struct TransformParams {
   int64_t out_stride;
 };
 hipError_t launch_transform(TransformParams& p, hipStream_t stream);
+
+// Embedding gather-reduce launcher (embedding_kernels.hip).  hipErrorInvalidConfiguration when
+// one launch would need more than 2^31 - 1 workgroups.
+struct EmbeddingParams {
+  int64_t M;
+  int32_t E;
+  int32_t w_bf16, out_bf16;
+  const void* W;
+  int64_t ldw;
+  int64_t n_bags;
+  const int64_t* begin;
+  const int64_t* idx;
+  void* out;
+  int64_t ldo;
+};
+hipError_t launch_embedding(const EmbeddingParams& p, hipStream_t stream);
 
 }  // namespace tpp

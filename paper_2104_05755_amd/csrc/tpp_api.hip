@@ -1,6 +1,8 @@
-// tpp_api.hip -- the C ABI of include/tpp_brgemm.h and include/tpp_transform.h: argument checks,
+// tpp_api.hip -- the C ABI of include/tpp_brgemm.h, include/tpp_transform.h and
+// include/tpp_embedding.h: argument checks,
 // the dispatch cache, kernel selection and launches.  Host code only; the kernels live in
-// brgemm_kernels.hip, brgemm_dl_kernels.hip, reduce_kernels.hip and transform_kernels.hip.
+// brgemm_kernels.hip, brgemm_dl_kernels.hip, reduce_kernels.hip, transform_kernels.hip and
+// embedding_kernels.hip.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -595,6 +597,26 @@ tpp_status tpp_reduce_batched(int32_t m, int32_t n, int64_t ld, int32_t in_type,
 tpp_status tpp_transform(int32_t kind, int32_t m, int32_t n, int64_t ld_in, int64_t ld_out,
                          int32_t dtype, int32_t alpha, const void* in, void* out, void* stream) {
   return transform_impl(kind, m, n, ld_in, ld_out, dtype, alpha, in, 0, out, 0, 1, stream);
+}
+
+tpp_status tpp_embedding_bag(int64_t M, int32_t E, int32_t w_type, const void* W, int64_t ldw,
+                             int64_t n_bags, const int64_t* d_begin, const int64_t* d_idx,
+                             int32_t out_type, void* out, int64_t ldo, void* stream) {
+  if (M < 0 || E <= 0 || n_bags < 0)
+    return fail(TPP_ERR_INVALID_ARG, "M, n_bags must be >= 0 and E > 0");
+  if (ldw < E || ldo < E) return fail(TPP_ERR_INVALID_ARG, "ldw and ldo must be >= E");
+  if (!valid_dtype(w_type) || !valid_dtype(out_type))
+    return fail(TPP_ERR_INVALID_ARG, "unknown datatype code");
+  if (n_bags == 0) return ok();
+  if (!d_begin || !out || (M > 0 && (!W || !d_idx)))
+    return fail(TPP_ERR_INVALID_ARG, "NULL table, list or output");
+  tpp::EmbeddingParams p{M, E, w_type == TPP_DT_BF16, out_type == TPP_DT_BF16, W, ldw, n_bags,
+                         d_begin, d_idx, out, ldo};
+  const hipError_t e = tpp::launch_embedding(p, static_cast<hipStream_t>(stream));
+  if (e == hipErrorInvalidConfiguration)
+    return fail(TPP_ERR_UNSUPPORTED, "embedding needs more than 2^31 - 1 workgroups");
+  if (e != hipSuccess) return fail(TPP_ERR_HIP, "embedding launch failed: %s", hipGetErrorString(e));
+  return ok();
 }
 
 tpp_status tpp_transform_batched(int32_t kind, int32_t m, int32_t n, int64_t ld_in,

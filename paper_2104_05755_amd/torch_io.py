@@ -119,11 +119,16 @@ def prepare_step(step, dev: dict, device="cuda"):
 
 
 def launch_step(st, dev: dict, stream: Optional[int] = None):
-    """One step of a chained workload (see ``workloads.TransformStep`` / ``ReduceStep``)."""
+    """One step of a chained workload (see ``workloads.TransformStep``, ``ReduceStep`` and
+    ``EmbeddingStep``)."""
     if stream is None:
         stream = tpp.current_stream()
     if isinstance(st, DeviceCall):
         launch(st, stream)
+    elif hasattr(st, "ldw"):        # embedding gather-reduce
+        begin = dev[st.begin]
+        tpp.tpp_embedding_bag(st.M, st.E, _DT[st.w_type], dev[st.w], st.ldw, begin.numel() - 1,
+                              begin, dev[st.idx], _DT[st.out_type], dev[st.out], st.ldo, stream)
     elif hasattr(st, "ld_in"):      # transform
         tpp.tpp_transform_batched(_TR[st.kind], st.m, st.n, st.ld_in, st.ld_out, _DT[st.dtype],
                                   st.alpha, dev[st.src], st.in_stride, dev[st.dst], st.out_stride,

@@ -212,3 +212,17 @@ def test_transform_null_pointers_and_empty_shapes(tpp):
     for kind in (tpp.TPP_TR_TRANSPOSE, tpp.TPP_TR_VNNI, tpp.TPP_TR_VNNI_TO_VNNI_T):
         tpp.tpp_transform(kind, 0, 5, 8, 8 * 2, tpp.TPP_DT_BF16, 2, None, None)
         tpp.tpp_transform(kind, 5, 0, 16, 16, tpp.TPP_DT_BF16, 2, None, None)
+
+
+def test_embedding_argument_checks(tpp):
+    fake = 1 << 40   # never dereferenced: every call below fails its checks first
+    bad = [(-1, 8, 0, 8, 1, 8), (10, 0, 0, 8, 1, 8), (10, 8, 0, 7, 1, 8), (10, 8, 0, 8, 1, 7),
+           (10, 8, 5, 8, 1, 8), (10, 8, 0, 8, -1, 8)]
+    for M, E, wt, ldw, nb, ldo in bad:
+        with pytest.raises(tpp.TppError) as e:
+            tpp.tpp_embedding_bag(M, E, wt, fake, ldw, nb, fake, fake, 0, fake, ldo)
+        assert e.value.status == tpp.TPP_ERR_INVALID_ARG
+    with pytest.raises(tpp.TppError) as e:
+        tpp.tpp_embedding_bag(10, 8, 0, fake, 8, 1, None, fake, 0, fake, 8)
+    assert e.value.status == tpp.TPP_ERR_INVALID_ARG
+    tpp.tpp_embedding_bag(10, 8, 0, fake, 8, 0, fake, fake, 0, fake, 8)   # no bags: a no-op
