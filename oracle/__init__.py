@@ -91,6 +91,12 @@ def lib():
         _lib.oracle_embedding_bag.restype = ctypes.c_int
         _lib.oracle_embedding_bag.argtypes = [i64, i32, i32, vp, i64, i64, vp, vp, i32, vp, i64,
                                               vp]
+        _lib.oracle_eq_scores.restype = ctypes.c_int
+        _lib.oracle_eq_scores.argtypes = [vp, i32, i32, vp]
+        _lib.oracle_eq_plan.restype = ctypes.c_int
+        _lib.oracle_eq_plan.argtypes = [vp, i32, i32, vp, vp, vp, vp]
+        _lib.oracle_eq_eval.restype = ctypes.c_int
+        _lib.oracle_eq_eval.argtypes = [vp, i32, i32, i32, i32, vp, i32, vp, i64, i32, vp]
         _lib.oracle_gelu_tanh_grad.restype = ctypes.c_double
         _lib.oracle_gelu_tanh_grad.argtypes = [ctypes.c_double]
         _lib.oracle_reduce.restype = ctypes.c_int
@@ -337,6 +343,76 @@ def embedding_bag(w: np.ndarray, M: int, E: int, ldw: int, w_type: str, begin, i
                                     _ptr(idx), _DTYPES[out_type], _ptr(out), ldo, _ptr(ref))
     if rc != 0:
         raise ValueError("oracle_embedding_bag rejected its arguments")
+    return ref
+
+
+# ---- TPP matrix equations (Sec. 4) ----------------------------------------------------------
+EQ_OPS = {"identity": 0, "neg": 1, "exp": 2, "tanh": 3, "relu": 4, "gelu_tanh": 5, "sqrt": 6,
+          "rcp": 7, "square": 8, "sigmoid": 9, "add": 16, "sub": 17, "mul": 18, "div": 19,
+          "max": 20, "min": 21, "muladd": 32}
+EQ_BCAST = {"none": 0, "col": 1, "row": 2, "scalar": 3}
+
+
+class _EqNode(ctypes.Structure):
+    _fields_ = [("arity", ctypes.c_int32), ("op", ctypes.c_int32),
+                ("child", ctypes.c_int32 * 3), ("leaf", ctypes.c_int32)]
+
+
+class _EqLeaf(ctypes.Structure):
+    _fields_ = [("ptr", ctypes.c_void_p), ("ld", ctypes.c_int64), ("dtype", ctypes.c_int32),
+                ("bcast", ctypes.c_int32)]
+
+
+def _eq_nodes(nodes):
+    """nodes: list of ("leaf", leaf_index) or (op_name, child, ...) tuples."""
+    arr = (_EqNode * len(nodes))()
+    for i, nd in enumerate(nodes):
+        if nd[0] == "leaf":
+            arr[i].arity, arr[i].op, arr[i].leaf = 0, 0, nd[1]
+            arr[i].child[:] = [-1, -1, -1]
+        else:
+            kids = list(nd[1:])
+            arr[i].arity, arr[i].op, arr[i].leaf = len(kids), EQ_OPS[nd[0]], -1
+            arr[i].child[:] = kids + [-1] * (3 - len(kids))
+    return arr
+
+
+def eq_scores(nodes, root):
+    """Alg. 3: register score of every node."""
+    arr = _eq_nodes(nodes)
+    sc = (ctypes.c_int32 * len(nodes))()
+    if lib().oracle_eq_scores(arr, len(nodes), root, sc) != 0:
+        raise ValueError("malformed equation tree")
+    return list(sc)
+
+
+def eq_plan(nodes, root):
+    """Alg. 4: (timestamps, tmp ids, number of tmps) of every node (leaves -1)."""
+    arr = _eq_nodes(nodes)
+    n = len(nodes)
+    sc = (ctypes.c_int32 * n)()
+    if lib().oracle_eq_scores(arr, n, root, sc) != 0:
+        raise ValueError("malformed equation tree")
+    ts, tm, nt = (ctypes.c_int32 * n)(), (ctypes.c_int32 * n)(), ctypes.c_int32()
+    if lib().oracle_eq_plan(arr, n, root, sc, ts, tm, ctypes.byref(nt)) != 0:
+        raise ValueError("malformed equation tree")
+    return list(ts), list(tm), nt.value
+
+
+def eq_eval(nodes, root, m, n, leaves, out, ldo, out_type, want_ref64=False):
+    """The equation's value on an m x n output (in place on ``out``).  leaves: list of
+    (array, ld, dtype, bcast) with bcast in "none"/"col"/"row"/"scalar"."""
+    arr = _eq_nodes(nodes)
+    lv = (_EqLeaf * max(1, len(leaves)))()
+    for i, (a, ld, dt, bc) in enumerate(leaves):
+        _check_dtype(a, dt, f"leaf {i}")
+        lv[i].ptr, lv[i].ld, lv[i].dtype, lv[i].bcast = a.ctypes.data, ld, _DTYPES[dt], EQ_BCAST[bc]
+    _check_dtype(out, out_type, "out")
+    ref = np.empty((n, m), dtype=np.float64) if want_ref64 else None
+    rc = lib().oracle_eq_eval(arr, len(nodes), root, m, n, lv, len(leaves), _ptr(out), ldo,
+                              _DTYPES[out_type], _ptr(ref))
+    if rc != 0:
+        raise ValueError("oracle_eq_eval rejected its arguments")
     return ref
 
 

@@ -474,3 +474,189 @@ int oracle_embedding_bag(int64_t M, int32_t E, int32_t w_type, const void* W, in
   }
   return 0;
 }
+
+/* ---- TPP matrix equations (Sec. 4) ---------------------------------------------------------- */
+
+static int eq_check(const oracle_eq_node* nodes, int32_t n_nodes, int32_t r, int depth) {
+  if (r < 0 || r >= n_nodes || depth > n_nodes) return -1;
+  const oracle_eq_node* x = &nodes[r];
+  if (x->arity < ORACLE_EQ_LEAF || x->arity > ORACLE_EQ_TERNARY) return -1;
+  for (int c = 0; c < x->arity; ++c)
+    if (eq_check(nodes, n_nodes, x->child[c], depth + 1) != 0) return -1;
+  return 0;
+}
+
+/* Alg. 3, recursively.  Unary: 1 over a leaf, else the child's score.  Binary: the children's
+ * score plus one when they are equal, else the larger.  Ternary: 1 when all three children are
+ * leaves, else the largest of 3 and the children's scores (as the algorithm prints it). */
+static int32_t eq_score(const oracle_eq_node* nodes, int32_t r, int32_t* score) {
+  const oracle_eq_node* x = &nodes[r];
+  int32_t v = 0;
+  if (x->arity == ORACLE_EQ_UNARY) {
+    const int32_t c = eq_score(nodes, x->child[0], score);
+    v = nodes[x->child[0]].arity == ORACLE_EQ_LEAF ? 1 : c;
+  } else if (x->arity == ORACLE_EQ_BINARY) {
+    const int32_t l = eq_score(nodes, x->child[0], score);
+    const int32_t rr = eq_score(nodes, x->child[1], score);
+    v = l == rr ? l + 1 : (l > rr ? l : rr);
+  } else if (x->arity == ORACLE_EQ_TERNARY) {
+    const int32_t l = eq_score(nodes, x->child[0], score);
+    const int32_t mm = eq_score(nodes, x->child[1], score);
+    const int32_t rr = eq_score(nodes, x->child[2], score);
+    int all_leaves = 1;
+    for (int c = 0; c < 3; ++c) all_leaves &= nodes[x->child[c]].arity == ORACLE_EQ_LEAF;
+    if (all_leaves) {
+      v = 1;
+    } else {
+      v = 3;
+      if (l > v) v = l;
+      if (mm > v) v = mm;
+      if (rr > v) v = rr;
+    }
+  }
+  score[r] = v;
+  return v;
+}
+
+int oracle_eq_scores(const oracle_eq_node* nodes, int32_t n_nodes, int32_t root, int32_t* score) {
+  if (!nodes || !score || eq_check(nodes, n_nodes, root, 0) != 0) return -1;
+  for (int32_t i = 0; i < n_nodes; ++i) score[i] = 0;
+  eq_score(nodes, root, score);
+  return 0;
+}
+
+/* The pool of temporary tensors of Alg. 4: Reserve_Tmp hands out the lowest free id,
+ * Recycle_Tmp returns one (a leaf has none to return). */
+typedef struct { int32_t used[64]; int32_t high; } eq_pool;
+
+static int32_t eq_reserve(eq_pool* p) {
+  for (int32_t i = 0; i < 64; ++i)
+    if (!p->used[i]) {
+      p->used[i] = 1;
+      if (i + 1 > p->high) p->high = i + 1;
+      return i;
+    }
+  return -1;
+}
+
+static void eq_recycle(eq_pool* p, int32_t t) {
+  if (t >= 0) p->used[t] = 0;
+}
+
+/* Alg. 4, recursively: children in order of decreasing register score (ties: the earlier child
+ * first), then the node's timestamp; its tmp is a new one when every child is a leaf, else the tmp
+ * of its first non-leaf child in the order Left, Right, Middle, the other children's tmps
+ * recycled. */
+static void eq_visit(const oracle_eq_node* nodes, int32_t r, const int32_t* score, int32_t* ts,
+                     int32_t* tmp, int32_t* clock, eq_pool* pool) {
+  const oracle_eq_node* x = &nodes[r];
+  if (x->arity == ORACLE_EQ_LEAF) return;
+  /* children by decreasing score, the earlier child first among equals */
+  int32_t seq[3], nseq = 0, taken[3] = {0, 0, 0};
+  for (int k = 0; k < x->arity; ++k) {
+    int best = -1;
+    for (int c = 0; c < x->arity; ++c)
+      if (!taken[c] && (best < 0 || score[x->child[c]] > score[x->child[best]])) best = c;
+    taken[best] = 1;
+    seq[nseq++] = best;
+  }
+  for (int k = 0; k < nseq; ++k) eq_visit(nodes, x->child[seq[k]], score, ts, tmp, clock, pool);
+  ts[r] = (*clock)++;
+  int all_leaves = 1;
+  for (int c = 0; c < x->arity; ++c) all_leaves &= nodes[x->child[c]].arity == ORACLE_EQ_LEAF;
+  if (all_leaves) {
+    tmp[r] = eq_reserve(pool);
+    return;
+  }
+  /* the child whose tmp the node takes: Left, else (ternary) Right, else Middle / Right */
+  int keep;
+  if (nodes[x->child[0]].arity != ORACLE_EQ_LEAF) {
+    keep = 0;
+  } else if (x->arity == ORACLE_EQ_TERNARY && nodes[x->child[2]].arity != ORACLE_EQ_LEAF) {
+    keep = 2;
+  } else {
+    keep = 1;
+  }
+  tmp[r] = tmp[x->child[keep]];
+  for (int c = 0; c < x->arity; ++c)
+    if (c != keep) eq_recycle(pool, tmp[x->child[c]]);
+}
+
+int oracle_eq_plan(const oracle_eq_node* nodes, int32_t n_nodes, int32_t root,
+                   const int32_t* score, int32_t* timestamp, int32_t* tmp, int32_t* n_tmps) {
+  if (!nodes || !score || !timestamp || !tmp || !n_tmps) return -1;
+  if (eq_check(nodes, n_nodes, root, 0) != 0) return -1;
+  for (int32_t i = 0; i < n_nodes; ++i) timestamp[i] = tmp[i] = -1;
+  eq_pool pool;
+  memset(&pool, 0, sizeof pool);
+  int32_t clock = 0;
+  eq_visit(nodes, root, score, timestamp, tmp, &clock, &pool);
+  *n_tmps = pool.high;
+  return 0;
+}
+
+static double eq_value(const oracle_eq_node* nodes, int32_t r, const oracle_eq_leaf* leaves,
+                       int32_t row, int32_t col) {
+  const oracle_eq_node* x = &nodes[r];
+  if (x->arity == ORACLE_EQ_LEAF) {
+    const oracle_eq_leaf* L = &leaves[x->leaf];
+    int64_t at = 0;
+    if (L->bcast == ORACLE_BC_NONE) at = (int64_t)row + (int64_t)col * L->ld;
+    else if (L->bcast == ORACLE_BC_COL) at = row;
+    else if (L->bcast == ORACLE_BC_ROW) at = col;
+    return oracle_widen(L->ptr, at, L->dtype);
+  }
+  const double a = eq_value(nodes, x->child[0], leaves, row, col);
+  if (x->arity == ORACLE_EQ_UNARY) {
+    switch (x->op) {
+      case ORACLE_EQ_IDENTITY: return a;
+      case ORACLE_EQ_NEG: return -a;
+      case ORACLE_EQ_EXP: return exp(a);
+      case ORACLE_EQ_TANH: return tanh(a);
+      case ORACLE_EQ_RELU: return a > 0.0 ? a : 0.0;
+      case ORACLE_EQ_GELU_TANH: return oracle_gelu_tanh(a);
+      case ORACLE_EQ_SQRT: return sqrt(a);
+      case ORACLE_EQ_RCP: return 1.0 / a;
+      case ORACLE_EQ_SQUARE: return a * a;
+      default: return 1.0 / (1.0 + exp(-a));   /* sigmoid */
+    }
+  }
+  const double b = eq_value(nodes, x->child[1], leaves, row, col);
+  if (x->arity == ORACLE_EQ_BINARY) {
+    switch (x->op) {
+      case ORACLE_EQ_ADD: return a + b;
+      case ORACLE_EQ_SUB: return a - b;
+      case ORACLE_EQ_MUL: return a * b;
+      case ORACLE_EQ_DIV: return a / b;
+      case ORACLE_EQ_MAX: return a > b ? a : b;
+      default: return a < b ? a : b;             /* min */
+    }
+  }
+  const double c = eq_value(nodes, x->child[2], leaves, row, col);
+  return a * b + c;                               /* muladd */
+}
+
+static int eq_op_ok(const oracle_eq_node* x) {
+  if (x->arity == ORACLE_EQ_UNARY) return x->op >= ORACLE_EQ_IDENTITY && x->op <= ORACLE_EQ_SIGMOID;
+  if (x->arity == ORACLE_EQ_BINARY) return x->op >= ORACLE_EQ_ADD && x->op <= ORACLE_EQ_MIN;
+  if (x->arity == ORACLE_EQ_TERNARY) return x->op == ORACLE_EQ_MULADD;
+  return 1;
+}
+
+int oracle_eq_eval(const oracle_eq_node* nodes, int32_t n_nodes, int32_t root, int32_t m,
+                   int32_t n, const oracle_eq_leaf* leaves, int32_t n_leaves, void* out,
+                   int64_t ldo, int32_t out_type, double* ref64) {
+  if (!nodes || eq_check(nodes, n_nodes, root, 0) != 0 || m < 0 || n < 0 || ldo < m) return -1;
+  for (int32_t i = 0; i < n_nodes; ++i) {
+    if (!eq_op_ok(&nodes[i])) return -1;
+    if (nodes[i].arity == ORACLE_EQ_LEAF && (nodes[i].leaf < 0 || nodes[i].leaf >= n_leaves))
+      return -1;
+  }
+  for (int32_t col = 0; col < n; ++col)
+    for (int32_t row = 0; row < m; ++row) {
+      const double v = eq_value(nodes, root, leaves, row, col);
+      if (ref64) ref64[(int64_t)row + (int64_t)col * m] = v;
+      store_rounded(out, (int64_t)row + (int64_t)col * ldo, out_type, v);
+    }
+  return 0;
+}

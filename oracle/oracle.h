@@ -19,6 +19,8 @@
  *     after the BRGEMM, the pre-activation kept by the forward call, and the loops of Alg. 6 around
  *     the Reduce and Transform TPPs.
  *   - The sparse embedding gather-reduce of Alg. 5 (a multi-hot vector times a table).
+ *   - TPP matrix equations (Sec. 4): the register scores of Alg. 3, the execution plan of
+ *     Alg. 4, and the value of an elementwise equation tree.
  *
  * Storage reading: every 2D block is column-major with a leading dimension (element (r, c) of an
  * m x n block sits at base + r + c*ld), which is how Alg. 6 lays out its blocked tensors (the
@@ -131,6 +133,36 @@ int oracle_transform_batched(int32_t kind, int32_t m, int32_t n, int64_t ld_in, 
 int oracle_embedding_bag(int64_t M, int32_t E, int32_t w_type, const void* W, int64_t ldw,
                          int64_t n_bags, const int64_t* begin, const int64_t* idx,
                          int32_t out_type, void* out, int64_t ldo, double* ref64);
+
+/* TPP matrix equations (Sec. 4): a tree whose internal nodes are unary / binary / ternary TPPs
+ * and whose leaves are the 2D input tensors.  Node i: arity (0 = leaf), op, children (node
+ * indices; first, second, third = Left, Middle / Right as the paper names them), leaf = the
+ * input index of a leaf. */
+enum { ORACLE_EQ_LEAF = 0, ORACLE_EQ_UNARY = 1, ORACLE_EQ_BINARY = 2, ORACLE_EQ_TERNARY = 3 };
+enum { ORACLE_EQ_IDENTITY = 0, ORACLE_EQ_NEG = 1, ORACLE_EQ_EXP = 2, ORACLE_EQ_TANH = 3,
+       ORACLE_EQ_RELU = 4, ORACLE_EQ_GELU_TANH = 5, ORACLE_EQ_SQRT = 6, ORACLE_EQ_RCP = 7,
+       ORACLE_EQ_SQUARE = 8, ORACLE_EQ_SIGMOID = 9,
+       ORACLE_EQ_ADD = 16, ORACLE_EQ_SUB = 17, ORACLE_EQ_MUL = 18, ORACLE_EQ_DIV = 19,
+       ORACLE_EQ_MAX = 20, ORACLE_EQ_MIN = 21,
+       ORACLE_EQ_MULADD = 32 };
+/* Leaf broadcast (Sec. 2.2): 0 a full m x n tensor, 1 a column of m entries repeated over the n
+ * columns, 2 a row of n entries repeated over the m rows, 3 one scalar. */
+enum { ORACLE_BC_NONE = 0, ORACLE_BC_COL = 1, ORACLE_BC_ROW = 2, ORACLE_BC_SCALAR = 3 };
+typedef struct { int32_t arity, op, child[3], leaf; } oracle_eq_node;
+typedef struct { const void* ptr; int64_t ld; int32_t dtype, bcast; } oracle_eq_leaf;
+
+/* Alg. 3: register score of every node (leaves 0).  Returns -1 for a malformed tree. */
+int oracle_eq_scores(const oracle_eq_node* nodes, int32_t n_nodes, int32_t root, int32_t* score);
+/* Alg. 4 on the scores of Alg. 3: evaluation timestamp and temporary tensor id of every internal
+ * node (leaves: -1), and the number of temporaries the plan uses. */
+int oracle_eq_plan(const oracle_eq_node* nodes, int32_t n_nodes, int32_t root,
+                   const int32_t* score, int32_t* timestamp, int32_t* tmp, int32_t* n_tmps);
+/* The equation's value at every (r, c) of an m x n output: the tree evaluated recursively in
+ * fp64 (libm transcendentals), rounded once to out_type; ref64 (optional, m x n column-major)
+ * gets the unrounded values. */
+int oracle_eq_eval(const oracle_eq_node* nodes, int32_t n_nodes, int32_t root, int32_t m,
+                   int32_t n, const oracle_eq_leaf* leaves, int32_t n_leaves, void* out,
+                   int64_t ldo, int32_t out_type, double* ref64);
 
 /* Helpers the tests pin on their own: exact widening and the round-to-nearest-even narrowing
  * used for every output element. */

@@ -4,7 +4,8 @@ from __future__ import annotations
 import numpy as np
 
 import oracle
-from workloads import Call, EmbeddingStep, ReduceStep, TransformStep, Workload, bf16_values
+from workloads import (Call, EmbeddingStep, EquationStep, ReduceStep, TransformStep, Workload,
+                       bf16_values)
 
 
 def oracle_desc(call: Call) -> oracle.Desc:
@@ -41,6 +42,10 @@ def run_step_oracle(step, arrs: dict, nthreads=0):
         for d, o in ((step.dst_x, ox), (step.dst_x2, ox2)):
             if d:
                 arrs[d].reshape(-1)[: o.size] = o.astype(np.float32)
+    elif isinstance(step, EquationStep):
+        leaves = [(arrs[name], ld, dt, bc) for name, ld, dt, bc in step.leaves]
+        oracle.eq_eval(step.nodes, step.root, step.m, step.n, leaves, arrs[step.out], step.ldo,
+                       step.out_type)
     elif isinstance(step, EmbeddingStep):
         oracle.embedding_bag(arrs[step.w], step.M, step.E, step.ldw, step.w_type,
                              arrs[step.begin], arrs[step.idx], arrs[step.out], step.ldo,

@@ -88,6 +88,21 @@ EMBEDDING_MUTANTS = {
                               "s += oracle_widen(W, j * ldw + e, w_type);"),
 }
 
+# Matrix-equation mutants (Alg. 3, Alg. 4, the tree's value), caught by the equation pins.
+EQUATION_MUTANTS = {
+    "eq_binary_no_increment": ("v = l == rr ? l + 1 : (l > rr ? l : rr);", "v = l > rr ? l : rr;"),
+    "eq_unary_over_leaf": ("v = nodes[x->child[0]].arity == ORACLE_EQ_LEAF ? 1 : c;", "v = c;"),
+    "eq_plan_min_first": ("(best < 0 || score[x->child[c]] > score[x->child[best]])",
+                          "(best < 0 || score[x->child[c]] < score[x->child[best]])"),
+    "eq_keeps_right_tmp": ("if (nodes[x->child[0]].arity != ORACLE_EQ_LEAF) {\n    keep = 0;",
+                           "if (0) {\n    keep = 0;"),
+    "eq_reserve_skips_zero": ("for (int32_t i = 0; i < 64; ++i)\n    if (!p->used[i])",
+                              "for (int32_t i = 1; i < 64; ++i)\n    if (!p->used[i])"),
+    "eq_bcast_col_as_row": ("else if (L->bcast == ORACLE_BC_COL) at = row;",
+                            "else if (L->bcast == ORACLE_BC_COL) at = col;"),
+    "eq_div_swapped": ("case ORACLE_EQ_DIV: return a / b;", "case ORACLE_EQ_DIV: return b / a;"),
+}
+
 
 @pytest.fixture(scope="module")
 def source():
@@ -133,3 +148,9 @@ def test_backward_pins_catch_planted_mistake(name, source, tmp_path):
 def test_embedding_pins_catch_planted_mistake(name, source, tmp_path):
     old, new = EMBEDDING_MUTANTS[name]
     _caught(old, new, "test_oracle_embedding_pins.py", source, tmp_path, name)
+
+
+@pytest.mark.parametrize("name", sorted(EQUATION_MUTANTS))
+def test_equation_pins_catch_planted_mistake(name, source, tmp_path):
+    old, new = EQUATION_MUTANTS[name]
+    _caught(old, new, "test_oracle_equation_pins.py", source, tmp_path, name)

@@ -18,6 +18,8 @@ base + r + c*ld, the way Alg. 6 lays out its blocked tensors with the b_m / b_k 
   reduce_bn     the Reduce TPP on a conv output: per-channel sum and sum of squares (the
                 statistics step of batchnorm, Sec. 5.1.2)
   embedding_bag sparse embedding lookups (Alg. 5): per bag, the sum of the table rows it lists
+  equation_example / layernorm  TPP matrix equations (Sec. 4): the paper's example tree, and a
+                layer norm from a Reduce TPP and equations
   mlp_backward  the transformer MLP trained: GEMM1 keeping its pre-activation, then the backward
                 pass through both layers (weight transposes, GELU_inv fused into the data
                 gradient, weight gradients batch-reduced over token blocks, bias gradients by the
@@ -145,6 +147,21 @@ class EmbeddingStep:
     @property
     def n_bags(self) -> int:
         return -1   # from the begin array's length - 1
+
+
+@dataclass
+class EquationStep:
+    """A TPP matrix equation (Sec. 4) over an m x n output: ``nodes`` as ("leaf", i) or
+    (op, child, ...) tuples, ``leaves`` as (array name, ld, dtype, broadcast) with broadcast in
+    "none" / "col" / "row" / "scalar"."""
+    nodes: list
+    root: int
+    m: int
+    n: int
+    leaves: list
+    out: str
+    ldo: int
+    out_type: str
 
 
 @dataclass
@@ -374,6 +391,62 @@ def embedding_bag(seed: int = 7, rows: int = 1_000_000, dim: int = 128, bags: in
         np.full(bags * ldo, 0x7FC0, np.uint16)
     st = EmbeddingStep(rows, dim, ldw, ldo, w_type, out_type)
     return Workload("embedding_bag", dict(w=w, begin=begin, idx=idx, out=out), [], steps=[st])
+
+
+# The paper's example equation Out = Tanh(T0) + (T1 x T2) / (T3 - T4), elementwise.
+EXAMPLE_EQUATION = [("leaf", 0), ("leaf", 1), ("leaf", 2), ("leaf", 3), ("leaf", 4),
+                    ("tanh", 0), ("mul", 1, 2), ("sub", 3, 4), ("div", 6, 7), ("add", 5, 8)]
+
+
+def equation_example(seed: int = 8, m: int = 4096, n: int = 4096) -> Workload:
+    """The example equation of Sec. 4 on m x n fp32 tensors: T0 U[-2,2], T1 and T2 U[-1,1],
+    T3 U[1,2] and T4 U[-2,-1] (the divisor stays at least 2 away from zero); fp32 output."""
+    rng = np.random.default_rng(seed)
+    t = [rng.uniform(lo, hi, m * n).astype(np.float32)
+         for lo, hi in ((-2, 2), (-1, 1), (-1, 1), (1, 2), (-2, -1))]
+    arrays = {f"t{i}": t[i] for i in range(5)}
+    arrays["out"] = np.full(m * n, np.nan, np.float32)
+    st = EquationStep(EXAMPLE_EQUATION, 9, m, n, [(f"t{i}", m, "f32", "none") for i in range(5)],
+                      "out", m, "f32")
+    return Workload("equation_example", arrays, [], steps=[st])
+
+
+def layernorm(seed: int = 9, features: int = 1024, tokens: int = 8192, eps: float = 1e-5) -> Workload:
+    """Layer normalization over the features of each token, from TPPs (Sec. 5.1.2 builds its
+    norms from reduce and equation TPPs): X (features x tokens, bf16, column per token) ->
+      1. Reduce by rows: per token, sum of x and of x^2 (fp32)
+      2. equation on 1 x tokens: mu = s / F, rs = 1 / sqrt(s2 / F - mu^2 + eps), two outputs as two
+         equations (mu, then rs)
+      3. equation on features x tokens: Y = (X - mu) * rs * gamma + beta, mu and rs broadcast over
+         the rows, gamma and beta over the columns; bf16 output.
+    X ~ N(0.5, 1), gamma ~ N(1, 0.1), beta ~ N(0, 0.1)."""
+    rng = np.random.default_rng(seed)
+    x = bf16_bits((rng.standard_normal(features * tokens) + 0.5).astype(np.float32))
+    gamma = (1.0 + 0.1 * rng.standard_normal(features)).astype(np.float32)
+    beta = (0.1 * rng.standard_normal(features)).astype(np.float32)
+    inv_f = np.array([1.0 / features], np.float32)
+    eps_a = np.array([eps], np.float32)
+    nan = lambda k: np.full(k, np.nan, np.float32)
+    arrays = dict(x=x, gamma=gamma, beta=beta, inv_f=inv_f, eps=eps_a, s=nan(tokens),
+                  s2=nan(tokens), mu=nan(tokens), rs=nan(tokens),
+                  y=np.full(features * tokens, 0x7FC0, np.uint16))
+    red = ReduceStep("x", features, tokens, features, "bf16", "sum", "rows", dst_x="s",
+                     dst_x2="s2")
+    mu = EquationStep([("leaf", 0), ("leaf", 1), ("mul", 0, 1)], 2, 1, tokens,
+                      [("s", 1, "f32", "none"), ("inv_f", 1, "f32", "scalar")], "mu", 1, "f32")
+    # rs = rcp(sqrt(s2 * (1/F) - square(mu) + eps))
+    rs = EquationStep([("leaf", 0), ("leaf", 1), ("leaf", 2), ("leaf", 3), ("mul", 0, 1),
+                       ("square", 2), ("sub", 4, 5), ("add", 6, 3), ("sqrt", 7), ("rcp", 8)], 9,
+                      1, tokens, [("s2", 1, "f32", "none"), ("inv_f", 1, "f32", "scalar"),
+                                  ("mu", 1, "f32", "none"), ("eps", 1, "f32", "scalar")],
+                      "rs", 1, "f32")
+    # Y = muladd(mul(sub(x, mu), rs), gamma, beta)
+    y = EquationStep([("leaf", 0), ("leaf", 1), ("leaf", 2), ("leaf", 3), ("leaf", 4),
+                      ("sub", 0, 1), ("mul", 5, 2), ("muladd", 6, 3, 4)], 7, features, tokens,
+                     [("x", features, "bf16", "none"), ("mu", 1, "f32", "row"),
+                      ("rs", 1, "f32", "row"), ("gamma", 1, "f32", "col"),
+                      ("beta", 1, "f32", "col")], "y", features, "bf16")
+    return Workload("layernorm", arrays, [], steps=[red, mu, rs, y])
 
 
 CONFIGS = {
