@@ -9,8 +9,8 @@ launches).  ``roofline`` takes the dominant launch's mean duration over K more s
 timing-only (fence-free) HIP event on its stream around each launch.  The same run also
 times the other workloads (fp32 single BRGEMM, MLP fully-connected layer, 3x3 convolution with
 batchnorm statistics via the Reduce TPP, gathered address-based BRGEMM, the Transform TPP's
-transpose and VNNI formatting of a 64 MB tensor, the MLP block's backward pass, and the sparse
-embedding gather-reduce) under ``per_config``,
+transpose and VNNI formatting of a 64 MB tensor, the MLP block's backward pass, the sparse
+embedding gather-reduce, and two TPP matrix equations) under ``per_config``,
 and the CPU oracle on a bounded sample of the headline workload under ``cpu_baseline``.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
@@ -333,6 +333,40 @@ def per_config(args, torch, tpp, torch_io, wk, np, stream):
     out.update(transform_entries(args, torch, tpp, stream))
     out["mlp_backward"] = backward_entry(args, torch, tpp, torch_io, wk, stream)
     out["embedding_bag"] = embedding_entry(args, torch, tpp, torch_io, wk, stream)
+    out.update(equation_entries(args, torch, tpp, torch_io, wk, stream))
+    return out
+
+
+def equation_entries(args, torch, tpp, torch_io, wk, stream):
+    """TPP matrix equations (Sec. 4): the paper's example tree on 4096 x 4096 fp32 tensors, and a
+    layer norm over 1024 features of 8192 tokens (Reduce TPP, then equations for the statistics
+    and the normalization), each timed over max(steps, 50) back-to-back runs.  HBM bound: the
+    algorithmic bytes are every leaf tensor read once and the output written once (for the layer
+    norm: X read twice, Y written once)."""
+    out = {}
+    steps = max(args.steps, 50)
+    for name, wl in (("equation_example", wk.equation_example()),
+                     ("layernorm", wk.layernorm())):
+        dev = torch_io.upload(wl)
+        sts = [torch_io.prepare_step(st, dev) for st in wl.steps]
+        fns = [lambda st=st: torch_io.launch_step(st, dev, stream) for st in sts]
+        time_steps(fns, min(steps, args.warmup), 0, torch)   # warm-up
+        elapsed = time_steps(fns, steps, 0, torch)
+        ms = elapsed / steps * 1e3
+        if name == "equation_example":
+            st = wl.steps[0]
+            byts = 6 * st.m * st.n * 4
+            what = f"Tanh(T0) + (T1 x T2) / (T3 - T4), elementwise, {st.m} x {st.n} fp32"
+        else:
+            y = wl.steps[-1]
+            byts = 2 * y.m * y.n * 2 + y.m * y.n * 2
+            what = f"layer norm over {y.m} features of {y.n} tokens, bf16 (Reduce + 3 equations)"
+        gbs = byts / (ms * 1e-3) / 1e9
+        out[name] = {"workload": what, "launch_us": round(ms * 1e3, 2), "launches": len(fns),
+                     "alg_bytes": byts, "hbm_gbs": round(gbs, 1),
+                     "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)}
+        del dev, sts, fns
+        torch.cuda.empty_cache()
     return out
 
 

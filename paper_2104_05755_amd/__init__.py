@@ -1,5 +1,5 @@
 """MI355X (gfx950) TPP library: thin Python binding of the C ABI in include/tpp_brgemm.h,
-include/tpp_transform.h and include/tpp_embedding.h.
+include/tpp_transform.h, include/tpp_embedding.h and include/tpp_equation.h.
 
 Argument marshalling only: every step of the computation runs in the HIP kernels of
 ``libtpp_mi355x.so``.  The functions keep the C names; pointers are plain integers (device
@@ -84,6 +84,27 @@ _sig("tpp_reduce", _i32, _i32, _i32, _i64, _i32, _c_void_p, _i32, ctypes.c_uint3
      _c_void_p, _c_void_p)
 _sig("tpp_transform", _i32, _i32, _i32, _i32, _i64, _i64, _i32, _i32, _c_void_p, _c_void_p,
      _c_void_p)
+class tpp_eq_node(ctypes.Structure):
+    _fields_ = [("arity", _i32), ("op", _i32), ("child", _i32 * 3), ("leaf", _i32)]
+
+
+class tpp_eq_plan_node(ctypes.Structure):
+    _fields_ = [("score", _i32), ("timestamp", _i32), ("tmp", _i32)]
+
+
+class tpp_eq_arg(ctypes.Structure):
+    _fields_ = [("ptr", _c_void_p), ("ld", _i64), ("dtype", _i32), ("bcast", _i32)]
+
+
+TPP_EQ_OPS = {"identity": 0, "neg": 1, "exp": 2, "tanh": 3, "relu": 4, "gelu_tanh": 5, "sqrt": 6,
+              "rcp": 7, "square": 8, "sigmoid": 9, "add": 16, "sub": 17, "mul": 18, "div": 19,
+              "max": 20, "min": 21, "muladd": 32}
+TPP_BC = {"none": 0, "col": 1, "row": 2, "scalar": 3}
+
+_sig("tpp_equation_plan", _i32, ctypes.POINTER(tpp_eq_node), _i32, _i32,
+     ctypes.POINTER(tpp_eq_plan_node), ctypes.POINTER(_i32))
+_sig("tpp_equation_execute", _i32, ctypes.POINTER(tpp_eq_node), _i32, _i32, _i32, _i32,
+     ctypes.POINTER(tpp_eq_arg), _i32, _c_void_p, _i64, _i32, _c_void_p)
 _sig("tpp_embedding_bag", _i32, _i64, _i32, _i32, _c_void_p, _i64, _i64, _c_void_p, _c_void_p,
      _i32, _c_void_p, _i64, _c_void_p)
 _sig("tpp_reduce_batched", _i32, _i32, _i32, _i64, _i32, _c_void_p, _i64, _i64, _i32,
@@ -196,6 +217,40 @@ def tpp_transform_batched(kind, m, n, ld_in, ld_out, dtype, alpha, x, in_stride,
 def tpp_embedding_bag(M, E, w_type, W, ldw, n_bags, begin, idx, out_type, out, ldo, stream=None):
     _check(_lib.tpp_embedding_bag(M, E, w_type, _p(W), ldw, n_bags, _p(begin), _p(idx), out_type,
                                   _p(out), ldo, stream), "tpp_embedding_bag")
+
+
+def eq_nodes(nodes):
+    """An equation tree from ("leaf", argument index) and (op name, child, ...) tuples."""
+    arr = (tpp_eq_node * len(nodes))()
+    for i, nd in enumerate(nodes):
+        if nd[0] == "leaf":
+            arr[i].arity, arr[i].op, arr[i].leaf = 0, 0, nd[1]
+            arr[i].child[:] = [-1, -1, -1]
+        else:
+            kids = list(nd[1:])
+            arr[i].arity, arr[i].op, arr[i].leaf = len(kids), TPP_EQ_OPS[nd[0]], -1
+            arr[i].child[:] = kids + [-1] * (3 - len(kids))
+    return arr
+
+
+def tpp_equation_plan(nodes, root):
+    """(scores, timestamps, tmp ids, number of tmps) of an equation tree (host only)."""
+    arr = eq_nodes(nodes)
+    plan = (tpp_eq_plan_node * len(nodes))()
+    nt = _i32()
+    _check(_lib.tpp_equation_plan(arr, len(nodes), root, plan, ctypes.byref(nt)),
+           "tpp_equation_plan")
+    return ([p.score for p in plan], [p.timestamp for p in plan], [p.tmp for p in plan], nt.value)
+
+
+def tpp_equation_execute(nodes, root, m, n, args, out, ldo, out_type, stream=None):
+    """args: list of (tensor or address, ld, dtype code, broadcast name)."""
+    arr = eq_nodes(nodes)
+    ga = (tpp_eq_arg * max(1, len(args)))()
+    for i, (x, ld, dt, bc) in enumerate(args):
+        ga[i].ptr, ga[i].ld, ga[i].dtype, ga[i].bcast = _p(x), ld, dt, TPP_BC[bc]
+    _check(_lib.tpp_equation_execute(arr, len(nodes), root, m, n, ga, len(args), _p(out), ldo,
+                                     out_type, stream), "tpp_equation_execute")
 
 
 def tpp_status_string(s: int) -> str:

@@ -9,7 +9,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 LIB = os.path.join(PKG, "libtpp_mi355x.so")
 SOURCES = ["tpp_api.hip", "brgemm_kernels.hip", "brgemm_dl_kernels.hip", "reduce_kernels.hip",
-           "transform_kernels.hip", "embedding_kernels.hip"]
+           "transform_kernels.hip", "embedding_kernels.hip", "equation.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

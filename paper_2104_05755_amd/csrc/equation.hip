@@ -1,0 +1,314 @@
+// equation.hip -- TPP matrix equations (Sec. 4) for gfx950: the planner of Alg. 3 / Alg. 4 on the
+// host, and an executor that evaluates the planned instruction list per output element.
+//
+// Executor (see equation_kernel): eight output elements per thread; each instruction of the plan
+// dispatches once and then runs over the eight elements.  The temporaries of the plan are named
+// registers, so the plan's reuse of temporaries is register reuse: the paper's Strategy 2.  The
+// instruction list lives in the kernel arguments and is read with scalar loads.
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+
+#include <vector>
+
+#include "brgemm_device.h"
+#include "internal.h"
+
+namespace tpp {
+
+// ---- planner (host) --------------------------------------------------------------------------
+namespace {
+
+bool op_fits(int32_t arity, int32_t op) {
+  switch (arity) {
+    case TPP_EQ_LEAF: return true;
+    case TPP_EQ_UNARY: return op >= TPP_EQ_IDENTITY && op <= TPP_EQ_SIGMOID;
+    case TPP_EQ_BINARY: return op >= TPP_EQ_ADD && op <= TPP_EQ_MIN;
+    case TPP_EQ_TERNARY: return op == TPP_EQ_MULADD;
+    default: return false;
+  }
+}
+
+bool is_leaf(const tpp_eq_node* nodes, int32_t i) { return nodes[i].arity == TPP_EQ_LEAF; }
+
+// Nodes reachable from the root in post-order (children before parents), checking that every
+// reachable node is reached once and well formed.  Iterative, with an explicit stack.
+const char* post_order(const tpp_eq_node* nodes, int32_t n_nodes, int32_t root,
+                       std::vector<int32_t>& order) {
+  if (root < 0 || root >= n_nodes) return "root index out of range";
+  std::vector<char> seen(n_nodes, 0);
+  std::vector<std::pair<int32_t, int32_t>> stack;   // (node, next child to visit)
+  stack.push_back({root, 0});
+  seen[root] = 1;
+  while (!stack.empty()) {
+    auto& top = stack.back();
+    const tpp_eq_node& x = nodes[top.first];
+    if (x.arity < TPP_EQ_LEAF || x.arity > TPP_EQ_TERNARY) return "arity outside [0, 3]";
+    if (!op_fits(x.arity, x.op)) return "operation of the wrong arity";
+    if (top.second < x.arity) {
+      const int32_t c = x.child[top.second++];
+      if (c < 0 || c >= n_nodes) return "child index out of range";
+      if (seen[c]) return "a node is reached twice (not a tree)";
+      seen[c] = 1;
+      stack.push_back({c, 0});
+    } else {
+      order.push_back(top.first);
+      stack.pop_back();
+    }
+  }
+  return nullptr;
+}
+
+struct TmpPool {
+  uint64_t used = 0;
+  int32_t high = 0;
+  int32_t reserve() {   // the lowest free id
+    int32_t i = 0;
+    while (used >> i & 1) ++i;
+    used |= uint64_t(1) << i;
+    if (i + 1 > high) high = i + 1;
+    return i;
+  }
+  void recycle(int32_t t) {
+    if (t >= 0) used &= ~(uint64_t(1) << t);
+  }
+};
+
+void plan_node(const tpp_eq_node* nodes, int32_t r, tpp_eq_plan_node* plan, int32_t& clock,
+               TmpPool& pool) {
+  const tpp_eq_node& x = nodes[r];
+  if (x.arity == TPP_EQ_LEAF) return;
+  // children by decreasing score; among equal scores the earlier child first (stable)
+  int32_t idx[3] = {0, 1, 2};
+  for (int a = 1; a < x.arity; ++a)
+    for (int b = a; b > 0 && plan[x.child[idx[b]]].score > plan[x.child[idx[b - 1]]].score; --b) {
+      const int32_t t = idx[b];
+      idx[b] = idx[b - 1];
+      idx[b - 1] = t;
+    }
+  for (int a = 0; a < x.arity; ++a) plan_node(nodes, x.child[idx[a]], plan, clock, pool);
+  plan[r].timestamp = clock++;
+  bool all_leaves = true;
+  for (int a = 0; a < x.arity; ++a) all_leaves = all_leaves && is_leaf(nodes, x.child[a]);
+  if (all_leaves) {
+    plan[r].tmp = pool.reserve();
+    return;
+  }
+  // the temporary the node takes over: Left's, else Right's (ternary), else the other child's
+  int keep = 1;
+  if (!is_leaf(nodes, x.child[0])) keep = 0;
+  else if (x.arity == TPP_EQ_TERNARY && !is_leaf(nodes, x.child[2])) keep = 2;
+  plan[r].tmp = plan[x.child[keep]].tmp;
+  for (int a = 0; a < x.arity; ++a)
+    if (a != keep) pool.recycle(plan[x.child[a]].tmp);
+}
+
+}  // namespace
+
+const char* equation_plan(const tpp_eq_node* nodes, int32_t n_nodes, int32_t root,
+                          tpp_eq_plan_node* plan, int32_t* n_tmps) {
+  if (!nodes || !plan || !n_tmps) return "NULL nodes, plan or n_tmps";
+  if (n_nodes < 1 || n_nodes > EQ_MAX_NODES) return "n_nodes must be in [1, 64]";
+  std::vector<int32_t> order;
+  if (const char* err = post_order(nodes, n_nodes, root, order)) return err;
+  for (int32_t i = 0; i < n_nodes; ++i) plan[i] = {0, -1, -1};
+  // Alg. 3 over the post-order (children are scored before their parent)
+  for (int32_t r : order) {
+    const tpp_eq_node& x = nodes[r];
+    int32_t s = 0;
+    if (x.arity == TPP_EQ_UNARY) {
+      s = is_leaf(nodes, x.child[0]) ? 1 : plan[x.child[0]].score;
+    } else if (x.arity == TPP_EQ_BINARY) {
+      const int32_t a = plan[x.child[0]].score, b = plan[x.child[1]].score;
+      s = a == b ? a + 1 : (a > b ? a : b);
+    } else if (x.arity == TPP_EQ_TERNARY) {
+      if (is_leaf(nodes, x.child[0]) && is_leaf(nodes, x.child[1]) && is_leaf(nodes, x.child[2])) {
+        s = 1;
+      } else {
+        s = 3;
+        for (int a = 0; a < 3; ++a)
+          if (plan[x.child[a]].score > s) s = plan[x.child[a]].score;
+      }
+    }
+    plan[r].score = s;
+  }
+  // Alg. 4
+  int32_t clock = 0;
+  TmpPool pool;
+  plan_node(nodes, root, plan, clock, pool);
+  *n_tmps = pool.high;
+  return nullptr;
+}
+
+const char* equation_compile(const tpp_eq_node* nodes, int32_t n_nodes, int32_t root,
+                             EqProgram& prog, bool* too_many_tmps) {
+  *too_many_tmps = false;
+  tpp_eq_plan_node plan[EQ_MAX_NODES];
+  int32_t n_tmps = 0;
+  if (const char* err = equation_plan(nodes, n_nodes, root, plan, &n_tmps)) return err;
+  if (nodes[root].arity == TPP_EQ_LEAF) {   // the output is a copy of one leaf
+    prog.n_instr = 1;
+    prog.instr[0] = {TPP_EQ_IDENTITY, 1, 0, {EQ_LEAF_BASE + nodes[root].leaf, 0, 0}};
+    prog.result = 0;
+    return nullptr;
+  }
+  if (n_tmps > EQ_MAX_TMPS) {
+    *too_many_tmps = true;
+    return "the plan needs more than 8 temporaries";
+  }
+  int32_t n_instr = 0;
+  for (int32_t i = 0; i < n_nodes; ++i)
+    if (plan[i].timestamp >= 0) ++n_instr;
+  for (int32_t i = 0; i < n_nodes; ++i) {
+    const int32_t t = plan[i].timestamp;
+    if (t < 0) continue;
+    const tpp_eq_node& x = nodes[i];
+    EqInstr& in = prog.instr[t];
+    in.op = x.op;
+    in.arity = x.arity;
+    in.dst = plan[i].tmp;
+    for (int a = 0; a < 3; ++a) {
+      if (a >= x.arity) {
+        in.src[a] = 0;
+        continue;
+      }
+      const int32_t c = x.child[a];
+      in.src[a] = is_leaf(nodes, c) ? EQ_LEAF_BASE + nodes[c].leaf : plan[c].tmp;
+    }
+  }
+  prog.n_instr = n_instr;
+  prog.result = plan[root].tmp;
+  return nullptr;
+}
+
+// ---- executor (device) -----------------------------------------------------------------------
+namespace {
+
+using namespace dev;
+
+constexpr int EQ_T = 256;   // threads per workgroup
+
+constexpr int EPT = 8;   // output elements per thread
+
+// EPT output elements per thread, in column-major element order: element k of thread t in
+// workgroup b is e = (b * EPT + k) * EQ_T + t, so for every k a wavefront covers 64 consecutive
+// elements (contiguous runs of every full-tensor leaf and of the output, whatever the shape: a
+// 1 x n row of statistics as well as a tall tensor).  Each instruction of the plan dispatches
+// once on its operands' kind and once on its operation, then runs over the EPT elements without
+// further branches: the interpretation cost is shared by EPT elements.  The temporaries are
+// named register arrays (the plan's reuse of temporaries is register reuse).  WIDE: m * n does
+// not fit 32 bits.
+template <bool OUT_BF16, bool WIDE>
+__global__ __launch_bounds__(EQ_T) void equation_kernel(EqProgram p) {
+  const int64_t total = (int64_t)p.m * p.n;
+  const int64_t step = (int64_t)gridDim.x * EPT * EQ_T;
+  for (int64_t e0 = (int64_t)blockIdx.x * EPT * EQ_T + threadIdx.x; e0 < total; e0 += step) {
+    int32_t r[EPT], c[EPT];
+    bool ok[EPT];
+#pragma unroll
+    for (int k = 0; k < EPT; ++k) {
+      const int64_t e = e0 + (int64_t)k * EQ_T;
+      ok[k] = e < total;
+      const int64_t ee = ok[k] ? e : 0;   // element 0 stands in past the end
+      c[k] = WIDE ? (int32_t)(ee / p.m) : (int32_t)((uint32_t)ee / (uint32_t)p.m);
+      r[k] = (int32_t)(ee - (int64_t)c[k] * p.m);
+    }
+    float t0[EPT], t1[EPT], t2[EPT], t3[EPT], t4[EPT], t5[EPT], t6[EPT], t7[EPT];
+    // FETCH: operand `code` of all EPT elements into o (a temporary, or a leaf loaded for each
+    // element); PUT: v into temporary `code`.  Expanded in place (statement macros), so that
+    // every array index is a compile-time constant and the arrays stay in registers.
+#define TPP_EQ_TMP_CASE(j, o) \
+    case j: { _Pragma("unroll") for (int k = 0; k < EPT; ++k) o[k] = t##j[k]; } break;
+#define FETCH(code, o)                                                                          \
+    switch (code) {                                                                             \
+      TPP_EQ_TMP_CASE(0, o) TPP_EQ_TMP_CASE(1, o) TPP_EQ_TMP_CASE(2, o) TPP_EQ_TMP_CASE(3, o)     \
+      TPP_EQ_TMP_CASE(4, o) TPP_EQ_TMP_CASE(5, o) TPP_EQ_TMP_CASE(6, o) TPP_EQ_TMP_CASE(7, o)     \
+      default: {                                                                                \
+        const EqArg& g = p.arg[(code) - EQ_LEAF_BASE];                                          \
+        _Pragma("unroll") for (int k = 0; k < EPT; ++k) {                                       \
+          const int64_t at = g.bcast == TPP_BC_NONE ? (int64_t)r[k] + (int64_t)c[k] * g.ld      \
+                             : g.bcast == TPP_BC_COL ? r[k] : g.bcast == TPP_BC_ROW ? c[k] : 0; \
+          o[k] = g.bf16 ? bf16_bits_to_f32(gld<uint16_t>(static_cast<const uint16_t*>(g.ptr) + at)) \
+                        : gld<float>(static_cast<const float*>(g.ptr) + at);                    \
+        }                                                                                       \
+      } break;                                                                                  \
+    }
+#define TPP_EQ_PUT_CASE(j) \
+    case j: { _Pragma("unroll") for (int k = 0; k < EPT; ++k) t##j[k] = v[k]; } break;
+#define PUT(code)                                                                               \
+    switch (code) {                                                                             \
+      TPP_EQ_PUT_CASE(0) TPP_EQ_PUT_CASE(1) TPP_EQ_PUT_CASE(2) TPP_EQ_PUT_CASE(3)                \
+      TPP_EQ_PUT_CASE(4) TPP_EQ_PUT_CASE(5) TPP_EQ_PUT_CASE(6) TPP_EQ_PUT_CASE(7)                \
+      default: break;                                                                           \
+    }
+    for (int32_t i = 0; i < p.n_instr; ++i) {
+      const EqInstr& in = p.instr[i];
+      float a[EPT], b[EPT], cc[EPT], v[EPT];
+      FETCH(in.src[0], a)
+      if (in.arity > 1) { FETCH(in.src[1], b) }
+      if (in.arity > 2) { FETCH(in.src[2], cc) }
+      switch (in.op) {
+#define TPP_EQ_OP_CASE(op, expr) \
+        case op: { _Pragma("unroll") for (int k = 0; k < EPT; ++k) v[k] = (expr); } break;
+        TPP_EQ_OP_CASE(TPP_EQ_IDENTITY, a[k])
+        TPP_EQ_OP_CASE(TPP_EQ_NEG, -a[k])
+        TPP_EQ_OP_CASE(TPP_EQ_EXP, expf(a[k]))
+        TPP_EQ_OP_CASE(TPP_EQ_TANH, tanhf(a[k]))
+        TPP_EQ_OP_CASE(TPP_EQ_RELU, a[k] > 0.0f ? a[k] : 0.0f)
+        TPP_EQ_OP_CASE(TPP_EQ_GELU_TANH, gelu_tanh(a[k]))
+        TPP_EQ_OP_CASE(TPP_EQ_SQRT, sqrtf(a[k]))
+        TPP_EQ_OP_CASE(TPP_EQ_RCP, 1.0f / a[k])
+        TPP_EQ_OP_CASE(TPP_EQ_SQUARE, a[k] * a[k])
+        TPP_EQ_OP_CASE(TPP_EQ_SIGMOID, 1.0f / (1.0f + expf(-a[k])))
+        TPP_EQ_OP_CASE(TPP_EQ_ADD, a[k] + b[k])
+        TPP_EQ_OP_CASE(TPP_EQ_SUB, a[k] - b[k])
+        TPP_EQ_OP_CASE(TPP_EQ_MUL, a[k] * b[k])
+        TPP_EQ_OP_CASE(TPP_EQ_DIV, a[k] / b[k])
+        TPP_EQ_OP_CASE(TPP_EQ_MAX, a[k] > b[k] ? a[k] : b[k])
+        TPP_EQ_OP_CASE(TPP_EQ_MIN, a[k] < b[k] ? a[k] : b[k])
+        TPP_EQ_OP_CASE(TPP_EQ_MULADD, __builtin_fmaf(a[k], b[k], cc[k]))
+#undef TPP_EQ_OP_CASE
+        default: { _Pragma("unroll") for (int k = 0; k < EPT; ++k) v[k] = 0.0f; } break;
+      }
+      PUT(in.dst)
+    }
+    float res[EPT];
+    FETCH(p.result, res)
+#undef FETCH
+#undef PUT
+#undef TPP_EQ_TMP_CASE
+#undef TPP_EQ_PUT_CASE
+#pragma unroll
+    for (int k = 0; k < EPT; ++k) {
+      if (!ok[k]) continue;
+      const int64_t at = (int64_t)r[k] + (int64_t)c[k] * p.ldo;
+      if (OUT_BF16)
+        gst<uint16_t>(static_cast<uint16_t*>(p.out) + at, f32_to_bf16_bits(res[k]));
+      else
+        gst<float>(static_cast<float*>(p.out) + at, res[k]);
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_equation(const EqProgram& prog, hipStream_t stream) {
+  if (prog.m == 0 || prog.n == 0) return hipSuccess;
+  const int64_t total = (int64_t)prog.m * prog.n;
+  // enough workgroups for every element once, at most 8 per CU on the 256 CUs (grid stride
+  // beyond)
+  int64_t blocks = (total + EPT * EQ_T - 1) / (EPT * EQ_T);
+  if (blocks > 8 * 256) blocks = 8 * 256;
+  const dim3 grid((unsigned)blocks);
+  const bool wide = total > 0xffffffffLL;
+  if (prog.out_bf16) {
+    if (wide) hipLaunchKernelGGL((equation_kernel<true, true>), grid, dim3(EQ_T), 0, stream, prog);
+    else hipLaunchKernelGGL((equation_kernel<true, false>), grid, dim3(EQ_T), 0, stream, prog);
+  } else {
+    if (wide) hipLaunchKernelGGL((equation_kernel<false, true>), grid, dim3(EQ_T), 0, stream, prog);
+    else hipLaunchKernelGGL((equation_kernel<false, false>), grid, dim3(EQ_T), 0, stream, prog);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace tpp

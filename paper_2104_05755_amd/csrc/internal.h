@@ -6,6 +6,7 @@
 
 #include "tpp_brgemm.h"
 #include "tpp_embedding.h"
+#include "tpp_equation.h"
 #include "tpp_transform.h"
 
 namespace tpp {
@@ -148,5 +149,45 @@ struct EmbeddingParams {
   int64_t ldo;
 };
 hipError_t launch_embedding(const EmbeddingParams& p, hipStream_t stream);
+
+// TPP matrix equations (equation.hip).  The planner of Alg. 3 / Alg. 4 runs on the host; a
+// compiled program lists the internal nodes in timestamp order, each with its operation, the
+// temporary it writes and its operands (a temporary id below EQ_LEAF_BASE, or EQ_LEAF_BASE + the
+// leaf's argument index), and travels to the executor kernel by value.
+constexpr int EQ_MAX_NODES = 64;
+constexpr int EQ_MAX_TMPS = 8;
+constexpr int EQ_MAX_ARGS = 16;
+constexpr int EQ_LEAF_BASE = 16;
+// The kernel reads these arrays at indices known only at run time, with scalar loads from the
+// kernel-argument block; every element is a whole number of dwords, so every such address stays
+// dword aligned (scalar loads drop the low address bits).
+struct EqInstr {
+  int32_t op, arity, dst;
+  int32_t src[3];
+};
+struct EqArg {
+  const void* ptr;
+  int64_t ld;
+  int32_t bf16, bcast;
+};
+struct EqProgram {
+  int32_t n_instr;
+  int32_t result;                       // temporary holding the root's value
+  int32_t m, n;
+  int64_t ldo;
+  void* out;
+  int32_t out_bf16, n_args;
+  EqInstr instr[EQ_MAX_NODES];
+  EqArg arg[EQ_MAX_ARGS];
+};
+// nullptr on success, else what is wrong with the tree.
+const char* equation_plan(const tpp_eq_node* nodes, int32_t n_nodes, int32_t root,
+                          tpp_eq_plan_node* plan, int32_t* n_tmps);
+// The program of a planned tree (a root that is a leaf becomes one IDENTITY instruction);
+// nullptr on success, else what is wrong.  *too_many_tmps is set when the plan needs more than
+// EQ_MAX_TMPS temporaries.
+const char* equation_compile(const tpp_eq_node* nodes, int32_t n_nodes, int32_t root,
+                             EqProgram& prog, bool* too_many_tmps);
+hipError_t launch_equation(const EqProgram& prog, hipStream_t stream);
 
 }  // namespace tpp

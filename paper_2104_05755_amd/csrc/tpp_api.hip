@@ -1,8 +1,8 @@
-// tpp_api.hip -- the C ABI of include/tpp_brgemm.h, include/tpp_transform.h and
-// include/tpp_embedding.h: argument checks,
+// tpp_api.hip -- the C ABI of include/tpp_brgemm.h, include/tpp_transform.h,
+// include/tpp_embedding.h and include/tpp_equation.h: argument checks,
 // the dispatch cache, kernel selection and launches.  Host code only; the kernels live in
-// brgemm_kernels.hip, brgemm_dl_kernels.hip, reduce_kernels.hip, transform_kernels.hip and
-// embedding_kernels.hip.
+// brgemm_kernels.hip, brgemm_dl_kernels.hip, reduce_kernels.hip, transform_kernels.hip,
+// embedding_kernels.hip and equation.hip (which also holds the equation planner).
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -616,6 +616,56 @@ tpp_status tpp_embedding_bag(int64_t M, int32_t E, int32_t w_type, const void* W
   if (e == hipErrorInvalidConfiguration)
     return fail(TPP_ERR_UNSUPPORTED, "embedding needs more than 2^31 - 1 workgroups");
   if (e != hipSuccess) return fail(TPP_ERR_HIP, "embedding launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+tpp_status tpp_equation_plan(const tpp_eq_node* nodes, int32_t n_nodes, int32_t root,
+                             tpp_eq_plan_node* plan, int32_t* n_tmps) {
+  if (const char* err = tpp::equation_plan(nodes, n_nodes, root, plan, n_tmps))
+    return fail(TPP_ERR_INVALID_ARG, "equation: %s", err);
+  return ok();
+}
+
+tpp_status tpp_equation_execute(const tpp_eq_node* nodes, int32_t n_nodes, int32_t root,
+                                int32_t m, int32_t n, const tpp_eq_arg* args, int32_t n_args,
+                                void* out, int64_t ldo, int32_t out_type, void* stream) {
+  if (m < 0 || n < 0) return fail(TPP_ERR_INVALID_ARG, "m, n must be >= 0");
+  if (ldo < m) return fail(TPP_ERR_INVALID_ARG, "ldo < m");
+  if (!valid_dtype(out_type)) return fail(TPP_ERR_INVALID_ARG, "unknown output datatype");
+  if (n_args < 0 || n_args > tpp::EQ_MAX_ARGS || (n_args > 0 && !args))
+    return fail(TPP_ERR_INVALID_ARG, "n_args must be in [0, 16] with a non-NULL args");
+  tpp::EqProgram prog;
+  std::memset(&prog, 0, sizeof prog);
+  bool too_many = false;
+  if (const char* err = tpp::equation_compile(nodes, n_nodes, root, prog, &too_many))
+    return fail(too_many ? TPP_ERR_UNSUPPORTED : TPP_ERR_INVALID_ARG, "equation: %s", err);
+  // every leaf the tree reaches names a well-described argument
+  for (int32_t t = 0; t < prog.n_instr; ++t)
+    for (int a = 0; a < prog.instr[t].arity; ++a) {
+      const int32_t code = prog.instr[t].src[a];
+      if (code < tpp::EQ_LEAF_BASE) continue;
+      const int32_t k = code - tpp::EQ_LEAF_BASE;
+      if (k >= n_args) return fail(TPP_ERR_INVALID_ARG, "leaf argument %d of %d", k, n_args);
+    }
+  for (int32_t k = 0; k < n_args; ++k) {
+    const tpp_eq_arg& g = args[k];
+    if (!valid_dtype(g.dtype) || g.bcast < TPP_BC_NONE || g.bcast > TPP_BC_SCALAR)
+      return fail(TPP_ERR_INVALID_ARG, "argument %d: unknown datatype or broadcast", k);
+    if (g.bcast == TPP_BC_NONE && g.ld < m)
+      return fail(TPP_ERR_INVALID_ARG, "argument %d: ld < m", k);
+    if (!g.ptr && m > 0 && n > 0) return fail(TPP_ERR_INVALID_ARG, "argument %d: NULL", k);
+    prog.arg[k] = {g.ptr, g.ld, g.dtype == TPP_DT_BF16 ? 1 : 0, g.bcast};
+  }
+  if (m == 0 || n == 0) return ok();
+  if (!out) return fail(TPP_ERR_INVALID_ARG, "NULL out");
+  prog.n_args = n_args;
+  prog.m = m;
+  prog.n = n;
+  prog.ldo = ldo;
+  prog.out = out;
+  prog.out_bf16 = out_type == TPP_DT_BF16;
+  const hipError_t e = tpp::launch_equation(prog, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(TPP_ERR_HIP, "equation launch failed: %s", hipGetErrorString(e));
   return ok();
 }
 

@@ -119,12 +119,16 @@ def prepare_step(step, dev: dict, device="cuda"):
 
 
 def launch_step(st, dev: dict, stream: Optional[int] = None):
-    """One step of a chained workload (see ``workloads.TransformStep``, ``ReduceStep`` and
-    ``EmbeddingStep``)."""
+    """One step of a chained workload (see ``workloads.TransformStep``, ``ReduceStep``,
+    ``EmbeddingStep`` and ``EquationStep``)."""
     if stream is None:
         stream = tpp.current_stream()
     if isinstance(st, DeviceCall):
         launch(st, stream)
+    elif hasattr(st, "nodes"):      # matrix equation
+        args = [(dev[name], ld, _DT[dt], bc) for name, ld, dt, bc in st.leaves]
+        tpp.tpp_equation_execute(st.nodes, st.root, st.m, st.n, args, dev[st.out], st.ldo,
+                                 _DT[st.out_type], stream)
     elif hasattr(st, "ldw"):        # embedding gather-reduce
         begin = dev[st.begin]
         tpp.tpp_embedding_bag(st.M, st.E, _DT[st.w_type], dev[st.w], st.ldw, begin.numel() - 1,

@@ -226,3 +226,89 @@ def test_embedding_argument_checks(tpp):
         tpp.tpp_embedding_bag(10, 8, 0, fake, 8, 1, None, fake, 0, fake, 8)
     assert e.value.status == tpp.TPP_ERR_INVALID_ARG
     tpp.tpp_embedding_bag(10, 8, 0, fake, 8, 0, fake, fake, 0, fake, 8)   # no bags: a no-op
+
+
+# ---- the equation planner (Alg. 3 / Alg. 4) is host code: checked here against the oracle ---
+EXAMPLE_EQ = [("leaf", 0), ("leaf", 1), ("leaf", 2), ("leaf", 3), ("leaf", 4),
+              ("tanh", 0), ("mul", 1, 2), ("sub", 3, 4), ("div", 6, 7), ("add", 5, 8)]
+
+
+def _rand_tree(rng, k, ternary):
+    nodes = []
+
+    def build(k):
+        if k == 0:
+            nodes.append(("leaf", sum(x[0] == "leaf" for x in nodes)))
+            return len(nodes) - 1
+        kinds = ["exp", "add"] + (["muladd"] if ternary else [])
+        kind = kinds[rng.integers(len(kinds))]
+        if kind == "exp":
+            c = build(k - 1)
+            nodes.append(("exp", c))
+        elif kind == "add":
+            kl = int(rng.integers(0, k))
+            a, b = build(kl), build(k - 1 - kl)
+            nodes.append(("add", a, b))
+        else:
+            ks = rng.multinomial(k - 1, [1 / 3] * 3)
+            a, b, c = (build(int(x)) for x in ks)
+            nodes.append(("muladd", a, b, c))
+        return len(nodes) - 1
+
+    return nodes, build(k)
+
+
+def test_equation_planner_matches_oracle(tpp):
+    import numpy as np
+    import oracle
+    sc, ts, tm, n = tpp.tpp_equation_plan(EXAMPLE_EQ, 9)
+    assert sc[9] == 2 and n == 2
+    assert (ts, tm, n) == oracle.eq_plan(EXAMPLE_EQ, 9) and sc == oracle.eq_scores(EXAMPLE_EQ, 9)
+    rng = np.random.default_rng(81)
+    for trial in range(300):
+        nodes, root = _rand_tree(rng, int(rng.integers(1, 12)), ternary=trial % 2 == 1)
+        sc, ts, tm, n = tpp.tpp_equation_plan(nodes, root)
+        assert sc == oracle.eq_scores(nodes, root), nodes
+        assert (ts, tm, n) == oracle.eq_plan(nodes, root), nodes
+
+
+def test_equation_planner_rejects_malformed_trees(tpp):
+    bad = [([("add", 0, 1), ("leaf", 0)], 0),                     # cycle through the root
+           ([("leaf", 0), ("exp", 7)], 1),                         # child out of range
+           ([("leaf", 0), ("add", 0, 0)], 1),                      # a node reached twice
+           ([("leaf", 0)], 3)]                                     # root out of range
+    for nodes, root in bad:
+        with pytest.raises(tpp.TppError) as e:
+            tpp.tpp_equation_plan(nodes, root)
+        assert e.value.status == tpp.TPP_ERR_INVALID_ARG
+    arr = tpp.eq_nodes([("leaf", 0), ("exp", 0)])
+    arr[1].op = tpp.TPP_EQ_OPS["add"]                              # a binary op on one child
+    plan = (tpp.tpp_eq_plan_node * 2)()
+    import ctypes
+    st = tpp._lib.tpp_equation_plan(arr, 2, 1, plan, ctypes.byref(ctypes.c_int32()))
+    assert st == tpp.TPP_ERR_INVALID_ARG
+
+
+def test_equation_execute_host_checks(tpp):
+    fake = 1 << 40   # never dereferenced
+    nodes = [("leaf", 0), ("leaf", 1), ("add", 0, 1)]
+    with pytest.raises(tpp.TppError) as e:           # leaf 1 has no argument
+        tpp.tpp_equation_execute(nodes, 2, 4, 4, [(fake, 4, 0, "none")], fake, 4, 0)
+    assert e.value.status == tpp.TPP_ERR_INVALID_ARG
+    with pytest.raises(tpp.TppError) as e:           # ld < m
+        tpp.tpp_equation_execute(nodes, 2, 4, 4, [(fake, 3, 0, "none"), (fake, 4, 0, "none")],
+                                 fake, 4, 0)
+    assert e.value.status == tpp.TPP_ERR_INVALID_ARG
+    # a balanced binary tree of 63 nodes needs 5 temporaries (within the executor's 8; a tree of
+    # at most 64 nodes never needs more than that)
+    def grow(level):
+        if level == 0:
+            deep.append(("leaf", 0))
+            return len(deep) - 1
+        a, b = grow(level - 1), grow(level - 1)
+        deep.append(("add", a, b))
+        return len(deep) - 1
+    deep = []
+    root = grow(5)                                    # 63 nodes, score 5: fits
+    assert tpp.tpp_equation_plan(deep, root)[3] == 5
+    tpp.tpp_equation_execute(deep, root, 0, 4, [(fake, 4, 0, "none")], fake, 4, 0)   # m = 0

@@ -1,0 +1,142 @@
+"""GPU parity of the TPP matrix equations (Sec. 4), through the C ABI, against the CPU oracle's
+recursive fp64 evaluation of the tree: relative Frobenius error <= 1e-5 with fp32 leaves and
+output (the fp32 transcendentals are within a few ulp), <= 5e-3 with bf16 involved; exact where
+the arithmetic is (integer data, max / min / relu / neg, broadcast copies).  Covers every
+operation, every broadcast form, ragged shapes, padded leading dimensions, a leaf as the root,
+the paper's example at full size, and a layer norm built from a Reduce TPP and equations."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as wk
+from helpers import rel_fro, run_steps_oracle, values
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    import paper_2104_05755_amd  # noqa: F401  (fails loudly if the HIP library is missing)
+    return torch.device("cuda:0")
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def gpu_steps(steps, arrays, names):
+    from paper_2104_05755_amd import torch_io
+    dev = torch_io.upload(wk.Workload("x", arrays, []))
+    for st in steps:
+        torch_io.launch_step(torch_io.prepare_step(st, dev), dev)
+    torch.cuda.synchronize()
+    return {k: torch_io.to_host(dev[k], arrays[k]) for k in names}
+
+
+def one(nodes, root, m, n, leaf_specs, out_type="f32", ldo=None, seed=0, integer=False):
+    """Random leaves per spec (lo, hi, dtype, bcast, pad) and the GPU / oracle outputs."""
+    rng = np.random.default_rng(seed)
+    ldo = ldo or m
+    arrays, leaves = {}, []
+    for i, (lo, hi, dt, bc, pad) in enumerate(leaf_specs):
+        ld = m + pad
+        size = {"none": ld * n, "col": m, "row": n, "scalar": 1}[bc]
+        v = (rng.integers(lo, hi + 1, size) if integer else rng.uniform(lo, hi, size)).astype(np.float32)
+        arrays[f"l{i}"] = v if dt == "f32" else wk.bf16_bits(v)
+        leaves.append((f"l{i}", ld if bc == "none" else 1, dt, bc))
+    arrays["out"] = (np.full(ldo * n, np.nan, np.float32) if out_type == "f32"
+                     else np.full(ldo * n, 0x7FC0, np.uint16))
+    st = wk.EquationStep(nodes, root, m, n, leaves, "out", ldo, out_type)
+    got = gpu_steps([st], arrays, ["out"])["out"]
+    ref = np.array(arrays["out"], copy=True)
+    oracle.eq_eval(nodes, root, m, n, [(arrays[a], ld, dt, bc) for a, ld, dt, bc in leaves], ref,
+                   ldo, out_type)
+    live = lambda x: values(x, out_type).reshape(n, ldo)[:, :m]
+    return live(got), live(ref), got, arrays["out"]
+
+
+UNARY = [("identity", -2, 2), ("neg", -2, 2), ("exp", -4, 4), ("tanh", -4, 4), ("relu", -2, 2),
+         ("gelu_tanh", -5, 5), ("sqrt", 0.1, 9), ("rcp", 0.5, 3), ("square", -3, 3),
+         ("sigmoid", -6, 6)]
+BINARY = ["add", "sub", "mul", "div", "max", "min"]
+
+
+@pytest.mark.parametrize("op,lo,hi", UNARY, ids=[u[0] for u in UNARY])
+def test_every_unary_op(op, lo, hi):
+    say(f"equation unary {op}")
+    g, r, _, _ = one([("leaf", 0), (op, 0)], 1, 200, 33, [(lo, hi, "f32", "none", 0)], seed=1)
+    assert rel_fro(g, r) <= 1e-5
+    if op in ("identity", "neg", "relu", "square"):
+        assert np.array_equal(g, r)
+
+
+@pytest.mark.parametrize("op", BINARY)
+def test_every_binary_op(op):
+    say(f"equation binary {op}")
+    g, r, _, _ = one([("leaf", 0), ("leaf", 1), (op, 0, 1)], 1 + 1, 130, 17,
+                     [(-3, 3, "f32", "none", 5), (0.5, 2, "f32", "none", 0)], seed=2)
+    assert rel_fro(g, r) <= 1e-5
+    if op in ("add", "sub", "mul", "max", "min"):
+        assert np.array_equal(g, r)   # one fp32 rounding of the exact result on both sides
+
+
+def test_muladd_is_fused():
+    g, r, _, _ = one([("leaf", 0), ("leaf", 1), ("leaf", 2), ("muladd", 0, 1, 2)], 3, 64, 40,
+                     [(-2, 2, "f32", "none", 0)] * 3, seed=3)
+    # fma rounds once; the oracle rounds the fp64 value (exact product, rounded sum) to fp32
+    assert rel_fro(g, r) <= 1e-7
+
+
+@pytest.mark.parametrize("bc", ["col", "row", "scalar"])
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_broadcast_forms(bc, dt):
+    say(f"equation broadcast {bc} {dt}")
+    g, r, _, _ = one([("leaf", 0), ("leaf", 1), ("sub", 0, 1)], 2, 300, 29,
+                     [(-8, 8, dt, "none", 3), (-8, 8, dt, bc, 0)], seed=4, integer=True)
+    assert np.array_equal(g, r)
+
+
+def test_paper_example_small_bf16_out_padded():
+    g, r, got, init = one(wk.EXAMPLE_EQUATION, 9, 257, 31,
+                          [(-2, 2, "bf16", "none", 1), (-1, 1, "f32", "none", 0),
+                           (-1, 1, "f32", "none", 7), (1, 2, "f32", "none", 0),
+                           (-2, -1, "bf16", "none", 0)], out_type="bf16", ldo=260, seed=5)
+    assert rel_fro(g, r) <= 5e-3
+    gaps = lambda x: x.reshape(31, 260)[:, 257:]
+    assert np.array_equal(gaps(got), gaps(init))          # the output's gaps are untouched
+
+
+def test_leaf_root_is_a_copy():
+    g, r, _, _ = one([("leaf", 0)], 0, 100, 7, [(-9, 9, "bf16", "none", 2)], seed=6,
+                     integer=True)
+    assert np.array_equal(g, r)
+
+
+def test_paper_example_full_size():
+    wl = wk.equation_example()
+    st = wl.steps[0]
+    say(f"equation example full size {st.m} x {st.n}")
+    got = gpu_steps(wl.steps, wl.arrays, ["out"])["out"]
+    ref = np.array(wl.arrays["out"], copy=True)
+    oracle.eq_eval(st.nodes, st.root, st.m, st.n,
+                   [(wl.arrays[a], ld, dt, bc) for a, ld, dt, bc in st.leaves], ref, st.ldo,
+                   st.out_type)
+    assert not np.isnan(got).any()
+    assert rel_fro(got, ref) <= 1e-5
+
+
+def test_layernorm_chain_matches_oracle():
+    wl = wk.layernorm(seed=91, features=1024, tokens=512)
+    say("layernorm chain")
+    got = gpu_steps(wl.steps, wl.arrays, ["mu", "rs", "y"])
+    ref = run_steps_oracle(wl)
+    assert rel_fro(got["mu"], ref["mu"]) <= 1e-5
+    assert rel_fro(got["rs"], ref["rs"]) <= 1e-5
+    assert rel_fro(values(got["y"], "bf16"), values(ref["y"], "bf16")) <= 5e-3
