@@ -190,6 +190,32 @@ constexpr int EQ_T = 256;   // threads per workgroup
 
 constexpr int EPT = 8;   // output elements per thread
 
+// v[k] = op(a[k], b[k], cc[k]) for the EPT elements, one dispatch on op.
+#define TPP_EQ_OP_CASE(op, expr) \
+  case op: { _Pragma("unroll") for (int k = 0; k < EPT; ++k) v[k] = (expr); } break;
+#define TPP_EQ_APPLY(opcode)                                                                    \
+  switch (opcode) {                                                                             \
+    TPP_EQ_OP_CASE(TPP_EQ_IDENTITY, a[k])                                                       \
+    TPP_EQ_OP_CASE(TPP_EQ_NEG, -a[k])                                                           \
+    TPP_EQ_OP_CASE(TPP_EQ_EXP, expf(a[k]))                                                      \
+    TPP_EQ_OP_CASE(TPP_EQ_TANH, tanhf(a[k]))                                                    \
+    TPP_EQ_OP_CASE(TPP_EQ_RELU, a[k] > 0.0f ? a[k] : 0.0f)                                      \
+    TPP_EQ_OP_CASE(TPP_EQ_GELU_TANH, gelu_tanh(a[k]))                                           \
+    TPP_EQ_OP_CASE(TPP_EQ_SQRT, sqrtf(a[k]))                                                    \
+    TPP_EQ_OP_CASE(TPP_EQ_RCP, 1.0f / a[k])                                                     \
+    TPP_EQ_OP_CASE(TPP_EQ_SQUARE, a[k] * a[k])                                                  \
+    TPP_EQ_OP_CASE(TPP_EQ_SIGMOID, 1.0f / (1.0f + expf(-a[k])))                                 \
+    TPP_EQ_OP_CASE(TPP_EQ_ADD, a[k] + b[k])                                                     \
+    TPP_EQ_OP_CASE(TPP_EQ_SUB, a[k] - b[k])                                                     \
+    TPP_EQ_OP_CASE(TPP_EQ_MUL, a[k] * b[k])                                                     \
+    TPP_EQ_OP_CASE(TPP_EQ_DIV, a[k] / b[k])                                                     \
+    TPP_EQ_OP_CASE(TPP_EQ_MAX, a[k] > b[k] ? a[k] : b[k])                                       \
+    TPP_EQ_OP_CASE(TPP_EQ_MIN, a[k] < b[k] ? a[k] : b[k])                                       \
+    TPP_EQ_OP_CASE(TPP_EQ_MULADD, __builtin_fmaf(a[k], b[k], cc[k]))                            \
+    default: { _Pragma("unroll") for (int k = 0; k < EPT; ++k) v[k] = 0.0f; } break;            \
+  }
+
+
 // EPT output elements per thread, in column-major element order: element k of thread t in
 // workgroup b is e = (b * EPT + k) * EQ_T + t, so for every k a wavefront covers 64 consecutive
 // elements (contiguous runs of every full-tensor leaf and of the output, whatever the shape: a
@@ -247,29 +273,7 @@ __global__ __launch_bounds__(EQ_T) void equation_kernel(EqProgram p) {
       FETCH(in.src[0], a)
       if (in.arity > 1) { FETCH(in.src[1], b) }
       if (in.arity > 2) { FETCH(in.src[2], cc) }
-      switch (in.op) {
-#define TPP_EQ_OP_CASE(op, expr) \
-        case op: { _Pragma("unroll") for (int k = 0; k < EPT; ++k) v[k] = (expr); } break;
-        TPP_EQ_OP_CASE(TPP_EQ_IDENTITY, a[k])
-        TPP_EQ_OP_CASE(TPP_EQ_NEG, -a[k])
-        TPP_EQ_OP_CASE(TPP_EQ_EXP, expf(a[k]))
-        TPP_EQ_OP_CASE(TPP_EQ_TANH, tanhf(a[k]))
-        TPP_EQ_OP_CASE(TPP_EQ_RELU, a[k] > 0.0f ? a[k] : 0.0f)
-        TPP_EQ_OP_CASE(TPP_EQ_GELU_TANH, gelu_tanh(a[k]))
-        TPP_EQ_OP_CASE(TPP_EQ_SQRT, sqrtf(a[k]))
-        TPP_EQ_OP_CASE(TPP_EQ_RCP, 1.0f / a[k])
-        TPP_EQ_OP_CASE(TPP_EQ_SQUARE, a[k] * a[k])
-        TPP_EQ_OP_CASE(TPP_EQ_SIGMOID, 1.0f / (1.0f + expf(-a[k])))
-        TPP_EQ_OP_CASE(TPP_EQ_ADD, a[k] + b[k])
-        TPP_EQ_OP_CASE(TPP_EQ_SUB, a[k] - b[k])
-        TPP_EQ_OP_CASE(TPP_EQ_MUL, a[k] * b[k])
-        TPP_EQ_OP_CASE(TPP_EQ_DIV, a[k] / b[k])
-        TPP_EQ_OP_CASE(TPP_EQ_MAX, a[k] > b[k] ? a[k] : b[k])
-        TPP_EQ_OP_CASE(TPP_EQ_MIN, a[k] < b[k] ? a[k] : b[k])
-        TPP_EQ_OP_CASE(TPP_EQ_MULADD, __builtin_fmaf(a[k], b[k], cc[k]))
-#undef TPP_EQ_OP_CASE
-        default: { _Pragma("unroll") for (int k = 0; k < EPT; ++k) v[k] = 0.0f; } break;
-      }
+      TPP_EQ_APPLY(in.op)
       PUT(in.dst)
     }
     float res[EPT];
@@ -290,7 +294,99 @@ __global__ __launch_bounds__(EQ_T) void equation_kernel(EqProgram p) {
   }
 }
 
+// Vector path: m a multiple of 8, every full-tensor and column leaf and the output 16-byte
+// aligned with whole 16-byte units per column (checked on the host).  A thread takes 8 consecutive
+// rows of one column (one index split per thread), loads 8 entries of a full or column leaf with
+// 16-byte loads, one entry of a row or scalar leaf, and stores its 8 outputs with 16-byte stores.
+template <bool OUT_BF16>
+__global__ __launch_bounds__(EQ_T) void equation_vec_kernel(EqProgram p) {
+  const int64_t groups = (int64_t)p.m * p.n / EPT;
+  for (int64_t gidx = (int64_t)blockIdx.x * EQ_T + threadIdx.x; gidx < groups;
+       gidx += (int64_t)gridDim.x * EQ_T) {
+    const int64_t e0 = gidx * EPT;
+    const int32_t c = (int32_t)(e0 / p.m);
+    const int32_t r = (int32_t)(e0 - (int64_t)c * p.m);
+    float t0[EPT], t1[EPT], t2[EPT], t3[EPT], t4[EPT], t5[EPT], t6[EPT], t7[EPT];
+#define TPP_EQ_TMP_CASE(j, o) \
+    case j: { _Pragma("unroll") for (int k = 0; k < EPT; ++k) o[k] = t##j[k]; } break;
+#define FETCH(code, o)                                                                          \
+    switch (code) {                                                                             \
+      TPP_EQ_TMP_CASE(0, o) TPP_EQ_TMP_CASE(1, o) TPP_EQ_TMP_CASE(2, o) TPP_EQ_TMP_CASE(3, o)     \
+      TPP_EQ_TMP_CASE(4, o) TPP_EQ_TMP_CASE(5, o) TPP_EQ_TMP_CASE(6, o) TPP_EQ_TMP_CASE(7, o)     \
+      default: {                                                                                \
+        const EqArg& g = p.arg[(code) - EQ_LEAF_BASE];                                          \
+        if (g.bcast == TPP_BC_NONE || g.bcast == TPP_BC_COL) {                                  \
+          const int64_t at = g.bcast == TPP_BC_NONE ? (int64_t)r + (int64_t)c * g.ld : r;       \
+          if (g.bf16) {                                                                         \
+            const u32x4 w = gld<u32x4>(static_cast<const uint16_t*>(g.ptr) + at);              \
+            _Pragma("unroll") for (int q = 0; q < 4; ++q) {                                     \
+              o[2 * q] = __uint_as_float(w[q] << 16);                                           \
+              o[2 * q + 1] = __uint_as_float(w[q] & 0xffff0000u);                               \
+            }                                                                                   \
+          } else {                                                                              \
+            const f32x4 lo = gld<f32x4>(static_cast<const float*>(g.ptr) + at);                \
+            const f32x4 hi = gld<f32x4>(static_cast<const float*>(g.ptr) + at + 4);            \
+            _Pragma("unroll") for (int q = 0; q < 4; ++q) { o[q] = lo[q]; o[q + 4] = hi[q]; }   \
+          }                                                                                     \
+        } else {                                                                                \
+          const int64_t at = g.bcast == TPP_BC_ROW ? c : 0;                                     \
+          const float x = g.bf16 ? bf16_bits_to_f32(gld<uint16_t>(static_cast<const uint16_t*>(g.ptr) + at)) \
+                                 : gld<float>(static_cast<const float*>(g.ptr) + at);          \
+          _Pragma("unroll") for (int k = 0; k < EPT; ++k) o[k] = x;                             \
+        }                                                                                       \
+      } break;                                                                                  \
+    }
+#define TPP_EQ_PUT_CASE(j) \
+    case j: { _Pragma("unroll") for (int k = 0; k < EPT; ++k) t##j[k] = v[k]; } break;
+#define PUT(code)                                                                               \
+    switch (code) {                                                                             \
+      TPP_EQ_PUT_CASE(0) TPP_EQ_PUT_CASE(1) TPP_EQ_PUT_CASE(2) TPP_EQ_PUT_CASE(3)                \
+      TPP_EQ_PUT_CASE(4) TPP_EQ_PUT_CASE(5) TPP_EQ_PUT_CASE(6) TPP_EQ_PUT_CASE(7)                \
+      default: break;                                                                           \
+    }
+    for (int32_t i = 0; i < p.n_instr; ++i) {
+      const EqInstr& in = p.instr[i];
+      float a[EPT], b[EPT], cc[EPT], v[EPT];
+      FETCH(in.src[0], a)
+      if (in.arity > 1) { FETCH(in.src[1], b) }
+      if (in.arity > 2) { FETCH(in.src[2], cc) }
+      TPP_EQ_APPLY(in.op)
+      PUT(in.dst)
+    }
+    float res[EPT];
+    FETCH(p.result, res)
+#undef FETCH
+#undef PUT
+#undef TPP_EQ_TMP_CASE
+#undef TPP_EQ_PUT_CASE
+    const int64_t at = (int64_t)r + (int64_t)c * p.ldo;
+    if (OUT_BF16) {
+      gst<u32x4>(static_cast<uint16_t*>(p.out) + at,
+                 (u32x4){pack_bf16x2(res[0], res[1]), pack_bf16x2(res[2], res[3]),
+                         pack_bf16x2(res[4], res[5]), pack_bf16x2(res[6], res[7])});
+    } else {
+      float* q = static_cast<float*>(p.out) + at;
+      gst<f32x4>(q, (f32x4){res[0], res[1], res[2], res[3]});
+      gst<f32x4>(q + 4, (f32x4){res[4], res[5], res[6], res[7]});
+    }
+  }
+}
+
 }  // namespace
+
+// The vector path's conditions: m a multiple of 8; every full-tensor or column leaf and the
+// output 16-byte aligned, with column strides of whole 16-byte units.
+static bool prog_vec(const EqProgram& p) {
+  const auto al = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; };
+  if (p.m % EPT != 0 || !al(p.out) || (p.ldo * (p.out_bf16 ? 2 : 4)) % 16 != 0) return false;
+  for (int32_t k = 0; k < p.n_args; ++k) {
+    const EqArg& g = p.arg[k];
+    if (g.bcast != TPP_BC_NONE && g.bcast != TPP_BC_COL) continue;
+    if (!al(g.ptr)) return false;
+    if (g.bcast == TPP_BC_NONE && (g.ld * (g.bf16 ? 2 : 4)) % 16 != 0) return false;
+  }
+  return true;
+}
 
 hipError_t launch_equation(const EqProgram& prog, hipStream_t stream) {
   if (prog.m == 0 || prog.n == 0) return hipSuccess;
@@ -301,7 +397,14 @@ hipError_t launch_equation(const EqProgram& prog, hipStream_t stream) {
   if (blocks > 8 * 256) blocks = 8 * 256;
   const dim3 grid((unsigned)blocks);
   const bool wide = total > 0xffffffffLL;
-  if (prog.out_bf16) {
+  if (prog_vec(prog)) {
+    int64_t vblocks = (total / EPT + EQ_T - 1) / EQ_T;
+    if (vblocks > 8 * 256) vblocks = 8 * 256;
+    if (prog.out_bf16)
+      hipLaunchKernelGGL(equation_vec_kernel<true>, dim3((unsigned)vblocks), dim3(EQ_T), 0, stream, prog);
+    else
+      hipLaunchKernelGGL(equation_vec_kernel<false>, dim3((unsigned)vblocks), dim3(EQ_T), 0, stream, prog);
+  } else if (prog.out_bf16) {
     if (wide) hipLaunchKernelGGL((equation_kernel<true, true>), grid, dim3(EQ_T), 0, stream, prog);
     else hipLaunchKernelGGL((equation_kernel<true, false>), grid, dim3(EQ_T), 0, stream, prog);
   } else {

@@ -103,6 +103,28 @@ def test_broadcast_forms(bc, dt):
     assert np.array_equal(g, r)
 
 
+MIXED = [("leaf", 0), ("leaf", 1), ("sub", 0, 1), ("leaf", 2), ("leaf", 3), ("leaf", 4),
+         ("add", 4, 5), ("muladd", 2, 3, 6)]
+
+
+@pytest.mark.parametrize("out_type", ["f32", "bf16"])
+@pytest.mark.parametrize("pad", [8, 1])
+def test_all_leaf_kinds_in_one_tree(out_type, pad):
+    # m a multiple of 8: with pad 8 every column starts 16-byte aligned (16-byte loads and
+    # stores of 8 rows per thread); with pad 1 the same tree runs element by element
+    say(f"equation mixed leaves pad {pad} {out_type}")
+    g, r, got, init = one(MIXED, 7, 248, 23,
+                          [(-8, 8, "bf16", "none", pad), (-8, 8, "f32", "col", 0),
+                           (-4, 4, "bf16", "row", 0), (-4, 4, "f32", "scalar", 0),
+                           (-4, 4, "bf16", "col", 0)],
+                          out_type=out_type, ldo=248 + pad, seed=10, integer=True)
+    assert np.array_equal(g, r)   # integers below 256 in magnitude: exact in bf16 and fp32
+    # the gaps hold NaN: compare their bits
+    gaps = lambda x: x.view(np.uint32 if x.dtype == np.float32 else np.uint16) \
+        .reshape(23, 248 + pad)[:, 248:]
+    assert np.array_equal(gaps(got), gaps(init))
+
+
 def test_paper_example_small_bf16_out_padded():
     g, r, got, init = one(wk.EXAMPLE_EQUATION, 9, 257, 31,
                           [(-2, 2, "bf16", "none", 1), (-1, 1, "f32", "none", 0),
