@@ -200,24 +200,37 @@ class FenceFreeEvents:
         self.hip.hipEventDestroy(e)
 
 
-def time_in_steps(fns, steps, torch, stream):
+def time_in_steps(fns, steps, torch, stream, chunk=25, lead=3):
     """Mean duration (ms) of each fn as it runs inside the step: `steps` more steps with a
-    fence-free HIP event on the launch stream before each launch and after the last one."""
+    fence-free HIP event on the launch stream before each launch and after the last one.  The
+    steps go in chunks of `chunk`, each behind `lead` untimed steps and followed by a
+    synchronisation: the host then stays ahead of the GPU while the timed steps run, so the
+    events bracket launches and not host-side gaps (recording hundreds of events in one go can
+    stall the host for milliseconds while the GPU drains its queue)."""
     ev = FenceFreeEvents(torch)
-    evs = [[ev.create() for _ in range(len(fns) + 1)] for _ in range(steps)]
+    evs = [[ev.create() for _ in range(len(fns) + 1)] for _ in range(min(chunk, steps))]
+    sums = [0.0] * len(fns)
+    done = 0
     torch.cuda.synchronize()
-    for s in range(steps):
-        for i, f in enumerate(fns):
-            ev.record(evs[s][i], stream)
-            f()
-        ev.record(evs[s][-1], stream)
-    torch.cuda.synchronize()
-    per = [sum(ev.elapsed_ms(evs[s][i], evs[s][i + 1]) for s in range(steps)) / steps
-           for i in range(len(fns))]
+    while done < steps:
+        n = min(chunk, steps - done)
+        for _ in range(lead):
+            for f in fns:
+                f()
+        for s in range(n):
+            for i, f in enumerate(fns):
+                ev.record(evs[s][i], stream)
+                f()
+            ev.record(evs[s][-1], stream)
+        torch.cuda.synchronize()
+        for s in range(n):
+            for i in range(len(fns)):
+                sums[i] += ev.elapsed_ms(evs[s][i], evs[s][i + 1])
+        done += n
     for row in evs:
         for e in row:
             ev.destroy(e)
-    return per
+    return [x / steps for x in sums]
 
 
 def main():
@@ -258,7 +271,10 @@ def main():
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                 "traffic": traffic_from_profile(dom), "traffic_unit": "bytes per launch",
                 "kernel": f"call {dom} ({'GEMM1 1024->4096 bias+GELU' if dom == 0 else 'GEMM2 4096->1024 bias'})",
-                "launch_ms": round(per[dom], 4), "flops_per_launch": dom_flops}
+                "launch_ms": round(per[dom], 4), "flops_per_launch": dom_flops,
+                # the launches' in-step durations add up to about the step time of the
+                # event-free steps (a value well above 1 would mean the events timed gaps)
+                "launch_sum_over_step": round(sum(per) / (elapsed / args.steps * 1e3), 3)}
     result = {
         "metric": "BRGEMM TFLOP/s (bf16, fp32 acc) and % of MFMA peak per config",
         "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
