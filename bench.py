@@ -354,15 +354,17 @@ def per_config(args, torch, tpp, torch_io, wk, np, stream):
 
 
 def equation_entries(args, torch, tpp, torch_io, wk, stream):
-    """TPP matrix equations (Sec. 4): the paper's example tree on 4096 x 4096 fp32 tensors, and a
+    """TPP matrix equations (Sec. 4): the paper's example tree on 4096 x 4096 fp32 tensors, a
     layer norm over 1024 features of 8192 tokens (Reduce TPP, then equations for the statistics
-    and the normalization), each timed over max(steps, 50) back-to-back runs.  HBM bound: the
-    algorithmic bytes are every leaf tensor read once and the output written once (for the layer
-    norm: X read twice, Y written once)."""
+    and the normalization) and a softmax over 512 keys of 32768 columns (Reduce MAX, an exp
+    equation, Reduce SUM, a scaling equation), each timed over max(steps, 50) back-to-back runs.
+    HBM bound: the algorithmic bytes are every leaf tensor read once and the output written once
+    (for the layer norm: X read twice, Y written once; for the softmax: X read twice, X' written
+    once and read twice, Y written once)."""
     out = {}
     steps = max(args.steps, 50)
     for name, wl in (("equation_example", wk.equation_example()),
-                     ("layernorm", wk.layernorm())):
+                     ("layernorm", wk.layernorm()), ("softmax", wk.softmax())):
         dev = torch_io.upload(wl)
         sts = [torch_io.prepare_step(st, dev) for st in wl.steps]
         fns = [lambda st=st: torch_io.launch_step(st, dev, stream) for st in sts]
@@ -373,10 +375,16 @@ def equation_entries(args, torch, tpp, torch_io, wk, stream):
             st = wl.steps[0]
             byts = 6 * st.m * st.n * 4
             what = f"Tanh(T0) + (T1 x T2) / (T3 - T4), elementwise, {st.m} x {st.n} fp32"
-        else:
+        elif name == "layernorm":
             y = wl.steps[-1]
             byts = 2 * y.m * y.n * 2 + y.m * y.n * 2
             what = f"layer norm over {y.m} features of {y.n} tokens, bf16 (Reduce + 3 equations)"
+        else:
+            y = wl.steps[-1]
+            # X read twice (bf16), X' written once and read twice (fp32), Y written (bf16)
+            byts = y.m * y.n * (2 * 2 + 3 * 4 + 2)
+            what = (f"softmax over {y.m} keys of {y.n} columns, bf16 in and out, fp32 X' "
+                    f"(Reduce MAX, exp equation, Reduce SUM, scaling equation)")
         gbs = byts / (ms * 1e-3) / 1e9
         out[name] = {"workload": what, "launch_us": round(ms * 1e3, 2), "launches": len(fns),
                      "alg_bytes": byts, "hbm_gbs": round(gbs, 1),

@@ -298,7 +298,8 @@ __global__ __launch_bounds__(EQ_T) void equation_kernel(EqProgram p) {
 // aligned with whole 16-byte units per column (checked on the host).  A thread takes 8 consecutive
 // rows of one column (one index split per thread), loads 8 entries of a full or column leaf with
 // 16-byte loads, one entry of a row or scalar leaf, and stores its 8 outputs with 16-byte stores.
-template <bool OUT_BF16>
+// NTMP: the temporaries the plan uses are below NTMP (fewer registers, more waves in flight).
+template <bool OUT_BF16, int NTMP>
 __global__ __launch_bounds__(EQ_T) void equation_vec_kernel(EqProgram p) {
   const int64_t groups = (int64_t)p.m * p.n / EPT;
   for (int64_t gidx = (int64_t)blockIdx.x * EQ_T + threadIdx.x; gidx < groups;
@@ -308,7 +309,7 @@ __global__ __launch_bounds__(EQ_T) void equation_vec_kernel(EqProgram p) {
     const int32_t r = (int32_t)(e0 - (int64_t)c * p.m);
     float t0[EPT], t1[EPT], t2[EPT], t3[EPT], t4[EPT], t5[EPT], t6[EPT], t7[EPT];
 #define TPP_EQ_TMP_CASE(j, o) \
-    case j: { _Pragma("unroll") for (int k = 0; k < EPT; ++k) o[k] = t##j[k]; } break;
+    case j: if constexpr (j < NTMP) { _Pragma("unroll") for (int k = 0; k < EPT; ++k) o[k] = t##j[k]; } break;
 #define FETCH(code, o)                                                                          \
     switch (code) {                                                                             \
       TPP_EQ_TMP_CASE(0, o) TPP_EQ_TMP_CASE(1, o) TPP_EQ_TMP_CASE(2, o) TPP_EQ_TMP_CASE(3, o)     \
@@ -337,7 +338,7 @@ __global__ __launch_bounds__(EQ_T) void equation_vec_kernel(EqProgram p) {
       } break;                                                                                  \
     }
 #define TPP_EQ_PUT_CASE(j) \
-    case j: { _Pragma("unroll") for (int k = 0; k < EPT; ++k) t##j[k] = v[k]; } break;
+    case j: if constexpr (j < NTMP) { _Pragma("unroll") for (int k = 0; k < EPT; ++k) t##j[k] = v[k]; } break;
 #define PUT(code)                                                                               \
     switch (code) {                                                                             \
       TPP_EQ_PUT_CASE(0) TPP_EQ_PUT_CASE(1) TPP_EQ_PUT_CASE(2) TPP_EQ_PUT_CASE(3)                \
@@ -400,10 +401,21 @@ hipError_t launch_equation(const EqProgram& prog, hipStream_t stream) {
   if (prog_vec(prog)) {
     int64_t vblocks = (total / EPT + EQ_T - 1) / EQ_T;
     if (vblocks > 8 * 256) vblocks = 8 * 256;
-    if (prog.out_bf16)
-      hipLaunchKernelGGL(equation_vec_kernel<true>, dim3((unsigned)vblocks), dim3(EQ_T), 0, stream, prog);
-    else
-      hipLaunchKernelGGL(equation_vec_kernel<false>, dim3((unsigned)vblocks), dim3(EQ_T), 0, stream, prog);
+    int32_t ntmp = prog.result + 1;
+    for (int32_t i = 0; i < prog.n_instr; ++i)
+      if (prog.instr[i].dst + 1 > ntmp) ntmp = prog.instr[i].dst + 1;
+    const dim3 vgrid((unsigned)vblocks);
+#define TPP_EQ_VEC(B, N) hipLaunchKernelGGL((equation_vec_kernel<B, N>), vgrid, dim3(EQ_T), 0, stream, prog)
+    if (prog.out_bf16) {
+      if (ntmp <= 2) TPP_EQ_VEC(true, 2);
+      else if (ntmp <= 4) TPP_EQ_VEC(true, 4);
+      else TPP_EQ_VEC(true, EQ_MAX_TMPS);
+    } else {
+      if (ntmp <= 2) TPP_EQ_VEC(false, 2);
+      else if (ntmp <= 4) TPP_EQ_VEC(false, 4);
+      else TPP_EQ_VEC(false, EQ_MAX_TMPS);
+    }
+#undef TPP_EQ_VEC
   } else if (prog.out_bf16) {
     if (wide) hipLaunchKernelGGL((equation_kernel<true, true>), grid, dim3(EQ_T), 0, stream, prog);
     else hipLaunchKernelGGL((equation_kernel<true, false>), grid, dim3(EQ_T), 0, stream, prog);

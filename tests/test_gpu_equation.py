@@ -162,3 +162,18 @@ def test_layernorm_chain_matches_oracle():
     assert rel_fro(got["mu"], ref["mu"]) <= 1e-5
     assert rel_fro(got["rs"], ref["rs"]) <= 1e-5
     assert rel_fro(values(got["y"], "bf16"), values(ref["y"], "bf16")) <= 5e-3
+
+
+@pytest.mark.parametrize("keys,columns", [(512, 300), (77, 50)])
+def test_softmax_chain_matches_oracle(keys, columns):
+    # 512 keys: both equations on the vector path; 77: element path
+    wl = wk.softmax(seed=92, keys=keys, columns=columns)
+    say(f"softmax chain {keys} x {columns}")
+    got = gpu_steps(wl.steps, wl.arrays, ["mx", "xe", "s", "y"])
+    ref = run_steps_oracle(wl)
+    assert np.array_equal(got["mx"], ref["mx"])          # max is exact
+    assert rel_fro(got["xe"], ref["xe"]) <= 1e-5
+    assert rel_fro(got["s"], ref["s"]) <= 1e-5
+    assert rel_fro(values(got["y"], "bf16"), values(ref["y"], "bf16")) <= 5e-3
+    cols = values(got["y"], "bf16").astype(np.float64).reshape(columns, keys).sum(axis=1)
+    assert np.max(np.abs(cols - 1.0)) <= keys * 2.0 ** -8  # each column a distribution

@@ -217,3 +217,52 @@ def test_layernorm_chain_against_torch():
     got = wk.bf16_values(out["y"]).astype(np.float64).reshape(T, F)
     # bf16 output, fp32 statistics: agreement to bf16 rounding
     assert np.max(np.abs(got - ref.numpy())) <= 2.0 ** -7 * (np.abs(ref.numpy()).max() + 1)
+
+
+def _softmax_oracle(x_bits, keys, columns):
+    from helpers import run_steps_oracle
+    wl = wk.softmax(seed=0, keys=keys, columns=columns)
+    wl.arrays["x"] = x_bits
+    return run_steps_oracle(wl)
+
+
+def test_softmax_chain_against_torch():
+    """Reduce MAX + exp equation + Reduce SUM + scaling equation give torch's softmax over the
+    keys of each column (float64), to the bf16 rounding of the output."""
+    from helpers import run_steps_oracle
+    K, C = 96, 40
+    wl = wk.softmax(seed=75, keys=K, columns=C)
+    out = run_steps_oracle(wl)
+    x = wk.bf16_values(wl.arrays["x"]).astype(np.float64).reshape(C, K)
+    ref = torch.softmax(torch.tensor(x), dim=1).numpy()
+    got = wk.bf16_values(out["y"]).astype(np.float64).reshape(C, K)
+    assert np.max(np.abs(got - ref) / ref) <= 2.0 ** -8
+    np.testing.assert_array_equal(out["mx"], x.max(axis=1).astype(np.float32))
+    xe = out["xe"].astype(np.float64).reshape(C, K)
+    np.testing.assert_allclose(xe, np.exp(x - x.max(axis=1, keepdims=True)), rtol=6e-8)
+    np.testing.assert_allclose(out["s"], xe.sum(axis=1), rtol=1e-6)
+
+
+def test_softmax_subtracts_the_column_maximum():
+    # scores near 100: exp(x) alone overflows fp32, exp(x - max) does not; each column's largest
+    # X' entry is exactly exp(0) = 1
+    rng = np.random.default_rng(76)
+    K, C = 64, 16
+    x = 100.0 + rng.integers(-8, 1, size=K * C).astype(np.float32)
+    out = _softmax_oracle(wk.bf16_bits(x), K, C)
+    xe = out["xe"].reshape(C, K)
+    assert np.all(np.isfinite(xe)) and np.array_equal(xe.max(axis=1), np.ones(C, np.float32))
+    y = wk.bf16_values(out["y"]).astype(np.float64).reshape(C, K)
+    ref = torch.softmax(torch.tensor(x.astype(np.float64).reshape(C, K) - 100.0), dim=1).numpy()
+    assert np.max(np.abs(y - ref) / ref) <= 2.0 ** -8
+
+
+def test_softmax_shift_invariance_is_exact():
+    # integer scores shifted by an integer: X - max is the same exact value, so every output bit
+    # agrees
+    rng = np.random.default_rng(77)
+    K, C = 48, 24
+    x = rng.integers(-6, 7, size=K * C).astype(np.float32)
+    a = _softmax_oracle(wk.bf16_bits(x), K, C)
+    b = _softmax_oracle(wk.bf16_bits(x + 8.0), K, C)
+    assert np.array_equal(a["y"], b["y"]) and np.array_equal(a["xe"], b["xe"])

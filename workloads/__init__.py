@@ -449,6 +449,32 @@ def layernorm(seed: int = 9, features: int = 1024, tokens: int = 8192, eps: floa
     return Workload("layernorm", arrays, [], steps=[red, mu, rs, y])
 
 
+def softmax(seed: int = 10, keys: int = 512, columns: int = 32768) -> Workload:
+    """Softmax over the keys of each column of attention scores, from TPPs (Sec. 5.1.1 expresses
+    it as two equation trees around reduce TPPs): X (keys x columns, bf16, a column per query and
+    head) ->
+      1. Reduce by rows with MAX: per column, the largest score (fp32)
+      2. equation X' = exp(X - max), the maximum broadcast over the rows; fp32 output
+      3. Reduce by rows with SUM of X' (fp32)
+      4. equation Y = X' * rcp(sum), the sum broadcast over the rows; bf16 output.
+    The stand-in for BERT-Large attention: 512 keys, 32768 columns (16 heads x 512 queries x 4
+    sequences), scores 2 * N(0, 1)."""
+    rng = np.random.default_rng(seed)
+    x = bf16_bits((2.0 * rng.standard_normal(keys * columns)).astype(np.float32))
+    nan = lambda k: np.full(k, np.nan, np.float32)
+    arrays = dict(x=x, mx=nan(columns), xe=nan(keys * columns), s=nan(columns),
+                  y=np.full(keys * columns, 0x7FC0, np.uint16))
+    red_max = ReduceStep("x", keys, columns, keys, "bf16", "max", "rows", dst_x="mx")
+    # X' = exp(sub(x, max))
+    e = EquationStep([("leaf", 0), ("leaf", 1), ("sub", 0, 1), ("exp", 2)], 3, keys, columns,
+                     [("x", keys, "bf16", "none"), ("mx", 1, "f32", "row")], "xe", keys, "f32")
+    red_sum = ReduceStep("xe", keys, columns, keys, "f32", "sum", "rows", dst_x="s")
+    # Y = mul(x', rcp(sum))
+    y = EquationStep([("leaf", 0), ("leaf", 1), ("rcp", 1), ("mul", 0, 2)], 3, keys, columns,
+                     [("xe", keys, "f32", "none"), ("s", 1, "f32", "row")], "y", keys, "bf16")
+    return Workload("softmax", arrays, [], steps=[red_max, e, red_sum, y])
+
+
 CONFIGS = {
     1: fp32_single,
     2: mlp_fc,
