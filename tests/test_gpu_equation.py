@@ -177,3 +177,32 @@ def test_softmax_chain_matches_oracle(keys, columns):
     assert rel_fro(values(got["y"], "bf16"), values(ref["y"], "bf16")) <= 5e-3
     cols = values(got["y"], "bf16").astype(np.float64).reshape(columns, keys).sum(axis=1)
     assert np.max(np.abs(cols - 1.0)) <= keys * 2.0 ** -8  # each column a distribution
+
+
+def _balanced(depth):
+    """A balanced tree of 2^depth leaf nodes (over at most 16 arguments, reused in turn) under
+    add / sub / max / min nodes: Alg. 3 scores it depth, the temporaries its plan needs."""
+    nodes = [("leaf", i % 16) for i in range(2 ** depth)]
+    level = list(range(2 ** depth))
+    ops = ["add", "sub", "max", "min"]
+    while len(level) > 1:
+        nxt = []
+        for j in range(0, len(level), 2):
+            nodes.append((ops[len(nodes) % 4], level[j], level[j + 1]))
+            nxt.append(len(nodes) - 1)
+        level = nxt
+    return nodes, level[0]
+
+
+@pytest.mark.parametrize("depth", [3, 5])
+@pytest.mark.parametrize("m", [256, 100])
+def test_deep_trees_use_more_temporaries(depth, m):
+    # 3 and 5 temporaries: the vector kernel's 4- and 8-temporary variants (m = 256) and the
+    # element path (m = 100); small integers keep every result exact
+    nodes, root = _balanced(depth)
+    from paper_2104_05755_amd import tpp_equation_plan
+    assert tpp_equation_plan(nodes, root)[3] == depth
+    say(f"equation balanced depth {depth} m {m}")
+    g, r, _, _ = one(nodes, root, m, 19, [(-3, 3, "f32", "none", 0)] * min(2 ** depth, 16),
+                     seed=11, integer=True)
+    assert np.array_equal(g, r)
