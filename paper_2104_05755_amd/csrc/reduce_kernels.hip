@@ -136,6 +136,60 @@ __global__ __launch_bounds__(RT) void reduce_rows_kernel(ReduceParams p, int32_t
   }
 }
 
+// BY_ROWS with one segment per column and many columns: wavefront wid folds the CG columns
+// [wid*CG, min(n, wid*CG + CG)) whole, with every column's chunk of a pass loaded before any is
+// folded (CG loads in flight per lane in place of one).
+template <int OP, bool BF16, int V, int CG>
+__global__ __launch_bounds__(RT) void reduce_rows_group_kernel(ReduceParams p, int64_t per) {
+  const int lane = threadIdx.x & 63;
+  float* no_work = nullptr;
+  const int64_t lb = batch_of<BF16>(p, per, no_work, 0);
+  const int64_t wid = lb * (RT / 64) + (threadIdx.x >> 6);
+  const int64_t c0 = wid * CG;
+  if (c0 >= p.n) return;
+  const bool want_x = (p.flags & TPP_RED_X) != 0, want_x2 = (p.flags & TPP_RED_X2) != 0;
+  // columns past n repeat the last column's address: loaded, folded, never stored
+  int64_t col[CG];
+#pragma unroll
+  for (int q = 0; q < CG; ++q) col[q] = (c0 + q < p.n ? c0 + q : p.n - 1) * p.ld;
+  float ax[CG], ax2[CG];
+#pragma unroll
+  for (int q = 0; q < CG; ++q) ax[q] = ax2[q] = fold_identity<OP>();
+  const int32_t nv = p.m / V;   // full V-chunks
+  for (int32_t j = lane; j < nv; j += 64) {
+    float x[CG][V];
+#pragma unroll
+    for (int q = 0; q < CG; ++q) {
+      if (V == 1) x[q][0] = load1<BF16>(p.in, col[q] + j);
+      else loadv<BF16, V>(p.in, col[q] + (int64_t)j * V, x[q]);
+    }
+#pragma unroll
+    for (int q = 0; q < CG; ++q)
+#pragma unroll
+      for (int e = 0; e < V; ++e) {
+        ax[q] = fold<OP>(ax[q], x[q][e]);
+        ax2[q] = fold<OP>(ax2[q], x[q][e] * x[q][e]);
+      }
+  }
+  for (int32_t r = nv * V + lane; r < p.m; r += 64) {
+#pragma unroll
+    for (int q = 0; q < CG; ++q) {
+      const float x = load1<BF16>(p.in, col[q] + r);
+      ax[q] = fold<OP>(ax[q], x);
+      ax2[q] = fold<OP>(ax2[q], x * x);
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < CG; ++q) {
+    const float fx = wave_fold<OP>(ax[q]);
+    const float fx2 = wave_fold<OP>(ax2[q]);
+    if (lane == 0 && c0 + q < p.n) {
+      if (want_x) p.out_x[c0 + q] = fx;
+      if (want_x2) p.out_x2[c0 + q] = fx2;
+    }
+  }
+}
+
 // BY_COLS: workgroup (rb, s) folds columns [s*col_seg, min(n, (s+1)*col_seg)) for rows
 // [rb*TR*V, (rb+1)*TR*V).  Thread t: row vector tr = t % TR, column lane tc = t / TR.
 template <int OP, bool BF16, int V>
@@ -317,6 +371,7 @@ struct Plan {
   int32_t tr;     // BY_COLS: row vectors per workgroup
   int32_t nrb;    // BY_COLS: row blocks
   int64_t blocks; // first-pass workgroups
+  int32_t cg;     // BY_ROWS with one segment: columns per wavefront (1: the segment kernel)
 };
 
 Plan make_plan(const ReduceParams& p) {
@@ -335,6 +390,13 @@ Plan make_plan(const ReduceParams& p) {
     pl.seg = (int32_t)(((per + rows_per_pass - 1) / rows_per_pass) * rows_per_pass);
     pl.nseg = (int32_t)((p.m + pl.seg - 1) / pl.seg);
     pl.blocks = ((int64_t)p.n * pl.nseg + (RT / 64) - 1) / (RT / 64);
+    // whole columns and plenty of them: 2 or 4 columns per wavefront, still >= 4096 wavefronts
+    pl.cg = 1;
+    if (pl.nseg == 1) {
+      pl.cg = p.n >= 4 * 4096 ? 4 : (p.n >= 2 * 4096 ? 2 : 1);
+      const int64_t waves = (p.n + pl.cg - 1) / pl.cg;
+      pl.blocks = (waves + (RT / 64) - 1) / (RT / 64);
+    }
   } else {
     // Up to 64 row vectors per workgroup (at least four column lanes): a tall input gets more
     // row blocks rather than more column ranges, which keeps the partials per output few.
@@ -362,7 +424,13 @@ void launch_first(const ReduceParams& p, const Plan& pl, float* work, hipStream_
   // with one partial per output the first pass writes the outputs itself (no work buffer)
   float* w = pl.nseg > 1 ? work : nullptr;
   const dim3 grid((unsigned)(pl.blocks * p.G));
-  if (!pl.by_cols)
+  if (!pl.by_cols && pl.cg == 4)
+    hipLaunchKernelGGL((reduce_rows_group_kernel<OP, BF16, V, 4>), grid, dim3(RT), 0, stream, p,
+                       pl.blocks);
+  else if (!pl.by_cols && pl.cg == 2)
+    hipLaunchKernelGGL((reduce_rows_group_kernel<OP, BF16, V, 2>), grid, dim3(RT), 0, stream, p,
+                       pl.blocks);
+  else if (!pl.by_cols)
     hipLaunchKernelGGL((reduce_rows_kernel<OP, BF16, V>), grid, dim3(RT), 0, stream, p, pl.seg,
                        pl.nseg, w, pl.blocks);
   else

@@ -55,10 +55,13 @@ def check(got, ref, absdata, op, by, what):
 
 
 # (1024, 4096) by columns and (8192, 1024) by rows fold over 100+ and 4 partial results per
-# output in the many-outputs combine pass.
+# output in the many-outputs combine pass.  By rows, 8192 columns or more take whole columns,
+# several per wavefront: (8, 200000) and (77, 16387) four (the latter with a last group of three
+# and a row tail), (512, 8193) two, (300, 9000, ld 301) two with element loads.
 SHAPES = [(1, 1, 1), (3, 5, 3), (64, 100, 64), (64, 100, 67), (37, 513, 40), (1000, 7, 1000),
           (100000, 3, 100003), (8, 200000, 8), (257, 1031, 264), (4096, 64, 4096),
-          (1024, 4096, 1024), (8192, 1024, 8192)]
+          (1024, 4096, 1024), (8192, 1024, 8192), (77, 16387, 80), (512, 8193, 512),
+          (300, 9000, 301)]
 
 
 @pytest.mark.parametrize("m,n,ld", SHAPES)
