@@ -51,12 +51,15 @@ COPY_BYTES = 512 << 20   # calibration copy: 512 MiB read, 512 MiB written
 
 
 def kernel_source_sha() -> str:
-    """Hash of the HIP sources of the library (the counters below are valid for exactly these)."""
+    """Hash of the sources that build and choose the BRGEMM kernels (the HBM-traffic counters
+    below are valid for exactly these): the brgemm*.hip / brgemm*.h files, the shared internal
+    header and the host API that picks the instance."""
     import hashlib
     h = hashlib.sha256()
     csrc = os.path.join(HERE, "paper_2104_05755_amd", "csrc")
     for name in sorted(os.listdir(csrc)):
-        if name.endswith((".hip", ".h")):
+        if name.endswith((".hip", ".h")) and (name.startswith("brgemm") or
+                                              name in ("internal.h", "tpp_api.hip")):
             with open(os.path.join(csrc, name), "rb") as f:
                 h.update(name.encode() + b"\0" + f.read())
     return h.hexdigest()[:16]
