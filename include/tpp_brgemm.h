@@ -43,7 +43,7 @@ extern "C" {
 typedef enum {
   TPP_OK = 0,
   TPP_ERR_INVALID_ARG = -1,   /* a size, pointer, flag or handle is not acceptable            */
-  TPP_ERR_UNSUPPORTED = -2,   /* well-formed, but a type combination this build does not do  */
+  TPP_ERR_UNSUPPORTED = -2,   /* well-formed, but a type combination the library does not do */
   TPP_ERR_HIP = -4,           /* a HIP runtime call failed (launch, device query, memory)    */
   TPP_ERR_NO_MEMORY = -5      /* a host or device allocation failed                         */
 } tpp_status;

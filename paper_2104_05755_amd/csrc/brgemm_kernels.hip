@@ -11,7 +11,7 @@
 //     blocks side by side, so a tile may fuse several neighbouring instances (they share their
 //     A_i rows and B_i columns, as the ib_m / ib_n loops of Alg. 6 do); for an explicit grid the
 //     virtual C is one instance's m x n block;
-//   - Alg. 2 lines 4-7: the loop over pairs i and over k in steps of BK=64 is one flat loop over
+//   - Alg. 2's loops over the pairs i and over k become one flat loop, in steps of BK=64, over
 //     stages; each stage copies an A_i panel (BM x 64) and a B_i panel (64 x BN) from HBM into
 //     one of two LDS buffers with 16-byte loads, while the MFMAs consume the other buffer;
 //   - A is M-contiguous in memory but the MFMA wants 8 consecutive k per lane, so every thread
