@@ -203,6 +203,28 @@ class FenceFreeEvents:
         self.hip.hipEventDestroy(e)
 
 
+def time_cold(fn, reps, torch, stream):
+    """Mean duration (ms) of fn with cold caches: before each launch a 512 MiB fill (more than the
+    8 x 4 MB of L2 and the 256 MB MALL) evicts the inputs, then fence-free HIP events on the
+    launch stream bracket the launch alone."""
+    ev = FenceFreeEvents(torch)
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    evs = [(ev.create(), ev.create()) for _ in range(reps)]
+    torch.cuda.synchronize()
+    for r in range(reps):
+        flush.fill_(r & 0xFF)
+        ev.record(evs[r][0], stream)
+        fn()
+        ev.record(evs[r][1], stream)
+    torch.cuda.synchronize()
+    ms = sum(ev.elapsed_ms(a, b) for a, b in evs) / reps
+    for a, b in evs:
+        ev.destroy(a)
+        ev.destroy(b)
+    del flush
+    return ms
+
+
 def time_in_steps(fns, steps, torch, stream, chunk=25, lead=3):
     """Mean duration (ms) of each fn as it runs inside the step: `steps` more steps with a
     fence-free HIP event on the launch stream before each launch and after the last one.  The
@@ -304,7 +326,8 @@ def main():
 
 def per_config(args, torch, tpp, torch_io, wk, np, stream):
     """Each of the other workloads: one launch per call (plus the reduce for the convolution),
-    each timed over max(steps, 50) back-to-back launches after a warm-up."""
+    each timed over max(steps, 50) back-to-back launches after a warm-up (inputs warm in L2 and
+    the MALL), and for the three small workloads also with cold caches (`cold_us`)."""
     out = {}
     steps = max(args.steps, 50)
     for cfg in (1, 2, 3, 5):
@@ -339,6 +362,11 @@ def per_config(args, torch, tpp, torch_io, wk, np, stream):
                  "tflops": round(tfl, 2), "mfma_frac": round(tfl / peak, 4),
                  "alg_bytes": byts, "hbm_gbs": round(gbs, 1),
                  "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)}
+        if cfg in (1, 2, 3):
+            # the same launch with its inputs evicted from L2 and the MALL (from HBM)
+            cold = time_cold(fns[0], 20, torch, stream)
+            entry["cold_us"] = round(cold * 1e3, 2)
+            entry["cold_hbm_frac"] = round(byts / (cold * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)
         if red is not None:
             rb = wl.reduce["m"] * wl.reduce["n"] * 2 + 8 * wl.reduce["m"]
             entry["reduce"] = {"what": "per-channel sum and sum of squares of the conv output "
