@@ -403,12 +403,18 @@ Plan make_plan(const ReduceParams& p) {
     const int64_t vecs = (p.m + pl.v - 1) / pl.v;
     int32_t tr = 1;
     while (tr < vecs && tr < RT / 4) tr <<= 1;
+    // A tall input with enough rows for 512 row blocks of at least 8 row vectors takes fewer
+    // row vectors per workgroup (down to 8, up to 2048 row blocks) instead of column ranges:
+    // every workgroup then folds whole columns, no combine pass runs, and the many short
+    // workgroups keep more loads in flight per CU.
+    if (vecs >= 512LL * 8)
+      while (tr > 8 && (vecs + tr - 1) / tr < 2048) tr >>= 1;
     pl.tr = tr;
     pl.nrb = (int32_t)((p.m + (int64_t)tr * pl.v - 1) / ((int64_t)tr * pl.v));
     const int32_t tc = RT / tr;
-    // aim for ~1024 workgroups (four per CU), each walking at least 8 columns per column lane,
-    // and at most 512 partial results per output for the combine pass
-    int64_t nseg = (1024 + pl.nrb - 1) / pl.nrb;
+    // otherwise aim for ~1024 workgroups (four per CU), each walking at least 8 columns per
+    // column lane, and at most 512 partial results per output for the combine pass
+    int64_t nseg = pl.nrb >= 512 ? 1 : (1024 + pl.nrb - 1) / pl.nrb;
     const int64_t max_seg = (p.n + 8LL * tc - 1) / (8LL * tc);
     nseg = nseg < 1 ? 1 : (nseg > max_seg ? max_seg : nseg);
     if (nseg > 512) nseg = 512;
