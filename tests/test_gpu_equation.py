@@ -206,3 +206,36 @@ def test_deep_trees_use_more_temporaries(depth, m):
     g, r, _, _ = one(nodes, root, m, 19, [(-3, 3, "f32", "none", 0)] * min(2 ** depth, 16),
                      seed=11, integer=True)
     assert np.array_equal(g, r)
+
+
+@pytest.mark.parametrize("m,n", [(65537, 65537), (65544, 65536)], ids=["element", "vector"])
+def test_equation_past_2_pow_32_elements(m, n):
+    """m * n just past 2^32 (8.6 GB per bf16 tensor): 64-bit element indices on the element path
+    (odd m) and on the vector path.  X is the closed-form pattern x(e) = (e mod 251) - 125 built
+    on the device in chunks, and Y = muladd(X, 2, row[c]) with row[c] = (c mod 7) - 3 is checked
+    against the same closed form at every element (small integers: exact in bf16)."""
+    from paper_2104_05755_amd import TPP_DT_BF16, TPP_DT_F32, current_stream, tpp_equation_execute
+    total = m * n
+    assert total > 2 ** 32
+    say(f"equation past 2^32: {m} x {n}")
+    dev = torch.device("cuda:0")
+    chunk = 1 << 28
+    x = torch.empty(total, dtype=torch.bfloat16, device=dev)
+    for s in range(0, total, chunk):
+        e = torch.arange(s, min(s + chunk, total), dtype=torch.int64, device=dev)
+        x[s:s + e.numel()] = ((e % 251) - 125).to(torch.bfloat16)
+    row = ((torch.arange(n, dtype=torch.int64, device=dev) % 7) - 3).to(torch.float32)
+    two = torch.full((1,), 2.0, dtype=torch.float32, device=dev)
+    y = torch.full((total,), float("nan"), dtype=torch.bfloat16, device=dev)
+    nodes = [("leaf", 0), ("leaf", 1), ("leaf", 2), ("muladd", 0, 1, 2)]
+    tpp_equation_execute(nodes, 3, m, n, [(x, m, TPP_DT_BF16, "none"), (two, 1, TPP_DT_F32, "scalar"),
+                                          (row, 1, TPP_DT_F32, "row")],
+                         y, m, TPP_DT_BF16, current_stream())
+    torch.cuda.synchronize()
+    del x
+    bad = 0
+    for s in range(0, total, chunk):
+        e = torch.arange(s, min(s + chunk, total), dtype=torch.int64, device=dev)
+        want = (2 * ((e % 251) - 125) + ((e // m) % 7) - 3).to(torch.float32)
+        bad += int((y[s:s + e.numel()].to(torch.float32) != want).sum().item())
+    assert bad == 0, f"{bad} wrong elements"
