@@ -94,3 +94,46 @@ def test_reduce_batchnorm_statistics_shape():
     X = np.abs(values(t.reshape(-1), "bf16").reshape(n, m).T)
     check(gx, rx, X, "sum", "cols", "bn sum")
     check(gx2, rx2, X * X, "sum", "cols", "bn sumsq")
+
+
+def test_reduce_past_2_pow_32_elements():
+    """65536 x 65537 bf16 (8.6 GB, past 2^32 elements): 64-bit column offsets in the by-rows
+    (several columns per wavefront) and by-columns (whole columns per workgroup) kernels.  X is the
+    closed-form pattern x(e) = (e mod 251) - 125 built on the device, so every result has a closed
+    form: each period of 251 sums to zero, every partial sum stays below 2^24 (exact in fp32 in
+    any order), and every column holds all 251 residues (its maximum is 125)."""
+    import paper_2104_05755_amd as tpp
+    m, n = 65536, 65537
+    total = m * n
+    assert total > 2 ** 32
+    print(f"reduce past 2^32: {m} x {n}", flush=True)
+    dev = torch.device("cuda:0")
+    chunk = 1 << 28
+    x = torch.empty(total, dtype=torch.bfloat16, device=dev)
+    for s in range(0, total, chunk):
+        e = torch.arange(s, min(s + chunk, total), dtype=torch.int64, device=dev)
+        x[s:s + e.numel()] = ((e % 251) - 125).to(torch.bfloat16)
+    stream = tpp.current_stream()
+    by_rows = torch.full((n,), float("nan"), device=dev)
+    mx = torch.full((n,), float("nan"), device=dev)
+    by_cols = torch.full((m,), float("nan"), device=dev)
+    tpp.tpp_reduce(m, n, m, tpp.TPP_DT_BF16, x, tpp.TPP_RED_SUM, tpp.TPP_RED_BY_ROWS | tpp.TPP_RED_X,
+                   by_rows, None, stream)
+    tpp.tpp_reduce(m, n, m, tpp.TPP_DT_BF16, x, tpp.TPP_RED_MAX, tpp.TPP_RED_BY_ROWS | tpp.TPP_RED_X,
+                   mx, None, stream)
+    tpp.tpp_reduce(m, n, m, tpp.TPP_DT_BF16, x, tpp.TPP_RED_SUM, tpp.TPP_RED_BY_COLS | tpp.TPP_RED_X,
+                   by_cols, None, stream)
+    torch.cuda.synchronize()
+
+    def prefix(N):   # sum of x(e) for e < N
+        r = N % 251
+        return r * (r - 1) // 2 - 125 * r
+
+    c = np.arange(n, dtype=np.int64)
+    want_rows = prefix((c + 1) * m) - prefix(c * m)
+    tail = np.arange((n // 251) * 251, n, dtype=np.int64)          # the columns past whole periods
+    r = np.arange(m, dtype=np.int64)
+    want_cols = (((r[:, None] + tail[None, :] * m) % 251) - 125).sum(axis=1)
+    assert np.array_equal(by_rows.cpu().numpy(), want_rows.astype(np.float32))
+    assert np.array_equal(mx.cpu().numpy(), np.full(n, 125.0, np.float32))
+    assert np.array_equal(by_cols.cpu().numpy(), want_cols.astype(np.float32))
