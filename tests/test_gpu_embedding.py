@@ -136,3 +136,35 @@ def test_embedding_full_size_sampled():
     oracle.embedding_bag(wl.arrays["w"], st.M, st.E, st.ldw, st.w_type, sub_begin, sub_idx, out,
                          st.ldo, st.out_type)
     assert rel_fro(got[sel], out.reshape(len(sel), st.ldo)) <= 1e-5
+
+
+def test_embedding_table_past_2_pow_32_bytes():
+    """A 20,000,000 x 128 fp32 table (10.2 GB: row offsets past 2^31 elements and 2^32 bytes) with
+    W[r][e] = ((128 r + e) mod 251) - 125 built on the device; 2048 bags of 1..64 seeded lookups
+    (the last row among them).  Sums of at most 64 integers of magnitude <= 125 are exact in fp32,
+    so every output element is checked against the closed form."""
+    import paper_2104_05755_amd as tpp
+    M, E = 20_000_000, 128
+    assert M * E * 4 > 2 ** 32
+    say(f"embedding table past 2^32 bytes: {M} x {E}")
+    dev = torch.device("cuda:0")
+    total = M * E
+    chunk = 1 << 28
+    W = torch.empty(total, dtype=torch.float32, device=dev)
+    for s in range(0, total, chunk):
+        e = torch.arange(s, min(s + chunk, total), dtype=torch.int64, device=dev)
+        W[s:s + e.numel()] = ((e % 251) - 125).to(torch.float32)
+    rng = np.random.default_rng(93)
+    n_bags = 2048
+    lens = rng.integers(1, 65, n_bags)
+    begin = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    idx = rng.integers(0, M, int(begin[-1])).astype(np.int64)
+    idx[-1] = M - 1
+    out = torch.full((n_bags * E,), float("nan"), device=dev)
+    tpp.tpp_embedding_bag(M, E, tpp.TPP_DT_F32, W, E, n_bags, torch.from_numpy(begin).to(dev),
+                          torch.from_numpy(idx).to(dev), tpp.TPP_DT_F32, out, E,
+                          tpp.current_stream())
+    torch.cuda.synchronize()
+    rows = ((idx[:, None] * E + np.arange(E)[None, :]) % 251) - 125          # lookups x E
+    want = np.add.reduceat(rows, begin[:-1], axis=0).astype(np.float32)      # bags x E
+    assert np.array_equal(out.cpu().numpy().reshape(n_bags, E), want)
