@@ -119,3 +119,32 @@ def test_empty_shapes_leave_the_output_alone(kind):
 ])
 def test_full_size_tensors(kind, m, n, alpha):
     check(kind, m, n, 0, 0, "bf16", alpha, seed=9)
+
+
+@pytest.mark.parametrize("m,n", [(65537, 65537), (65536, 65544)], ids=["entry", "vector"])
+def test_transpose_past_2_pow_32_entries(m, n):
+    """Transposes of m x n bf16 past 2^32 entries (8.6 GB each way): odd leading dimensions
+    (entry loads) and whole 16-byte units (16-byte chunks).  The input is x(e) = (e mod 251) - 125
+    built on the device; output entry (i, j) must be input entry (j, i), checked everywhere."""
+    import paper_2104_05755_amd as tpp
+    total = m * n
+    assert total > 2 ** 32
+    print(f"transpose past 2^32: {m} x {n}", flush=True)
+    dev = torch.device("cuda:0")
+    chunk = 1 << 28
+    x = torch.empty(total, dtype=torch.bfloat16, device=dev)
+    for s in range(0, total, chunk):
+        e = torch.arange(s, min(s + chunk, total), dtype=torch.int64, device=dev)
+        x[s:s + e.numel()] = ((e % 251) - 125).to(torch.bfloat16)
+    out = torch.full((total,), float("nan"), dtype=torch.bfloat16, device=dev)
+    tpp.tpp_transform(tpp.TPP_TR_TRANSPOSE, m, n, m, n, tpp.TPP_DT_BF16, 1, x, out,
+                      tpp.current_stream())
+    torch.cuda.synchronize()
+    del x
+    bad = 0
+    for s in range(0, total, chunk):
+        f = torch.arange(s, min(s + chunk, total), dtype=torch.int64, device=dev)
+        src = f // n + (f % n) * m          # output (i = f % n, j = f // n) <- input (j, i)
+        want = ((src % 251) - 125).to(torch.float32)
+        bad += int((out[s:s + f.numel()].to(torch.float32) != want).sum().item())
+    assert bad == 0, f"{bad} wrong entries"
