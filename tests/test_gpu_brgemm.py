@@ -290,3 +290,57 @@ def test_every_tile_kernel_matches_oracle(kid, shape, monkeypatch):
     else:
         ref, _ = run_oracle(wl)
         check_close(got["out"], ref, wl.calls[0], f"k{kid} ragged")
+
+
+def _bf16_dev(v, dev):
+    return torch.tensor(np.asarray(v, np.float32), dtype=torch.bfloat16, device=dev)
+
+
+def test_operands_spread_past_2_pow_32_bytes():
+    """Addresses past 2^32 bytes, small-integer data (exact):
+    - stride variant, 16 pairs of 64x64x64 blocks 2^28 elements (512 MB) apart, so each operand
+      spans 8 GB: 64-bit pair bases in the direct-to-LDS kernel;
+    - a B block of 2 columns 2^30 + 64 elements (2 GB) apart: its span exceeds the 32-bit offsets
+      of the direct-to-LDS kernels, so the host takes the register-staged kernel.
+    Each is checked against the oracle on compact copies of the same blocks."""
+    import paper_2104_05755_amd as tpp
+    dev = torch.device("cuda:0")
+    stream = tpp.current_stream()
+    rng = np.random.default_rng(94)
+    m = n = k = 64
+    count, step = 16, 1 << 28
+    say("brgemm: 16 pairs 512 MB apart")
+    ablk = rng.integers(-4, 5, (count, m * k)).astype(np.float32)
+    bblk = rng.integers(-4, 5, (count, k * n)).astype(np.float32)
+    A = torch.empty(count * step, dtype=torch.bfloat16, device=dev)
+    B = torch.empty(count * step, dtype=torch.bfloat16, device=dev)
+    for i in range(count):
+        A[i * step:i * step + m * k] = _bf16_dev(ablk[i], dev)
+        B[i * step:i * step + k * n] = _bf16_dev(bblk[i], dev)
+    C = torch.full((m * n,), float("nan"), device=dev)
+    h = tpp.tpp_brgemm_dispatch(tpp.make_desc(m, n, k, m, k, m, "bf16", "f32", 0.0, "stride",
+                                              step, step))
+    tpp.tpp_brgemm_execute_stride(h, A, B, C, None, count, stream)
+    torch.cuda.synchronize()
+    del A, B
+    ref = np.full(m * n, np.nan, np.float32)
+    oracle.brgemm_batched(oracle.Desc(m, n, k, m, k, m, "bf16", "f32", 0.0, "stride", m * k, k * n),
+                          wk.bf16_bits(ablk.ravel()), wk.bf16_bits(bblk.ravel()), ref, count=count)
+    assert np.array_equal(C.cpu().numpy(), ref)
+
+    say("brgemm: B columns 2 GB apart")
+    n2, ldb = 2, (1 << 30) + 64
+    a1 = rng.integers(-4, 5, m * k).astype(np.float32)
+    b1 = rng.integers(-4, 5, (n2, k)).astype(np.float32)
+    B2 = torch.empty(ldb * (n2 - 1) + k, dtype=torch.bfloat16, device=dev)
+    for c in range(n2):
+        B2[c * ldb:c * ldb + k] = _bf16_dev(b1[c], dev)
+    C2 = torch.full((m * n2,), float("nan"), device=dev)
+    h2 = tpp.tpp_brgemm_dispatch(tpp.make_desc(m, n2, k, m, ldb, m, "bf16", "f32", 0.0, "stride"))
+    tpp.tpp_brgemm_execute_stride(h2, _bf16_dev(a1, dev), B2, C2, None, 1, stream)
+    torch.cuda.synchronize()
+    del B2
+    ref2 = np.full(m * n2, np.nan, np.float32)
+    oracle.brgemm_batched(oracle.Desc(m, n2, k, m, k, m, "bf16", "f32", 0.0, "stride"),
+                          wk.bf16_bits(a1), wk.bf16_bits(b1.ravel()), ref2, count=1)
+    assert np.array_equal(C2.cpu().numpy(), ref2)
