@@ -47,6 +47,7 @@ def parse():
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 TRAFFIC_FILE = os.path.join(HERE, "profiles", "traffic_mlp_block_8192tok.txt")
+TRAFFIC_GATHERED_FILE = os.path.join(HERE, "profiles", "traffic_gathered_4096x128.txt")
 COPY_BYTES = 512 << 20   # calibration copy: 512 MiB read, 512 MiB written
 
 
@@ -65,14 +66,15 @@ def kernel_source_sha() -> str:
     return h.hexdigest()[:16]
 
 
-def traffic_from_profile(call_index: int):
-    """HBM bytes per launch of headline call `call_index` from the committed rocprofv3 counter
-    summary: FETCH_SIZE and WRITE_SIZE of the kernel, each scaled by what the same counter read
-    for a copy of known size.  None when the summary is missing or the kernels changed since."""
-    if not os.path.exists(TRAFFIC_FILE):
+def traffic_from_profile(call_index: int, path: str = TRAFFIC_FILE):
+    """HBM bytes per launch of call `call_index` from a committed rocprofv3 counter summary (the
+    headline calls by default): FETCH_SIZE and WRITE_SIZE of the kernel, each scaled by what the
+    same counter read for a copy of known size.  None when the summary is missing or the kernels
+    changed since."""
+    if not os.path.exists(path):
         return None
     kv = {}
-    with open(TRAFFIC_FILE) as f:
+    with open(path) as f:
         for line in f:
             if "=" in line and not line.lstrip().startswith("#"):
                 k, v = line.split("=", 1)
@@ -88,7 +90,9 @@ def traffic_from_profile(call_index: int):
 
 
 def traffic_run(torch, tpp, torch_io, wk, stream):
-    """Launch sequence for the counter passes: 3 copies of COPY_BYTES, then 3 of each headline call."""
+    """Launch sequence for the counter passes: 3 copies of COPY_BYTES, then 3 of each headline
+    call, then 3 launches of the gathered workload (pointer lists into pools about the size of
+    the MALL)."""
     src = torch.empty(COPY_BYTES, dtype=torch.uint8, device="cuda")
     dst = torch.empty_like(src)
     src.fill_(1)
@@ -101,6 +105,15 @@ def traffic_run(torch, tpp, torch_io, wk, stream):
     for _ in range(3):
         for dc in dcs:
             torch_io.launch(dc, stream)
+    torch.cuda.synchronize()
+    del dev, dcs
+    torch.cuda.empty_cache()
+    gw = wk.CONFIGS[5]()
+    gdev = torch_io.upload(gw)
+    gdc = torch_io.prepare(gw.calls[0], gdev)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        torch_io.launch(gdc, stream)
     torch.cuda.synchronize()
 
 
@@ -362,6 +375,13 @@ def per_config(args, torch, tpp, torch_io, wk, np, stream):
                  "tflops": round(tfl, 2), "mfma_frac": round(tfl / peak, 4),
                  "alg_bytes": byts, "hbm_gbs": round(gbs, 1),
                  "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)}
+        if cfg == 5:
+            # bytes past L2 per launch, from the counter passes (the gathered blocks come from
+            # pools about the size of the MALL, so nearly every one misses L2)
+            traffic = traffic_from_profile(0, TRAFFIC_GATHERED_FILE)
+            entry["traffic"] = traffic
+            if traffic is not None:
+                entry["traffic_frac"] = round(traffic / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)
         if cfg in (1, 2, 3):
             # the same launch with its inputs evicted from L2 and the MALL (from HBM)
             cold = time_cold(fns[0], 20, torch, stream)
