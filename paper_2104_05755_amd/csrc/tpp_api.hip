@@ -126,7 +126,9 @@ int32_t choose_kernel(const tpp_brgemm_kernel_s& h, const tpp::BrgemmParams& p) 
 
 // Device work buffers for partial results, one per (device, stream, purpose) so that calls on
 // different streams never share one; allocated on first use, grown when a call needs more (after
-// a device synchronisation, since queued work may still use the old one), kept until exit.
+// a device synchronisation, since queued work may still use the old one), kept until exit.  The
+// caller keeps `hold` (the cache's lock) until its kernels are enqueued, so another host thread
+// cannot free the buffer between the lookup and the launch that uses it.
 enum WorkPurpose { WORK_REDUCE = 0, WORK_SPLIT = 1 };
 struct WorkBuffer {
   float* ptr = nullptr;
@@ -135,10 +137,11 @@ struct WorkBuffer {
 std::mutex g_work_mu;
 std::map<std::tuple<int, void*, int>, WorkBuffer> g_work;
 
-tpp_status work_buffer(int purpose, void* stream, int64_t floats, float** out) {
+tpp_status work_buffer(int purpose, void* stream, int64_t floats, float** out,
+                       std::unique_lock<std::mutex>& hold) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return fail(TPP_ERR_HIP, "hipGetDevice failed");
-  std::lock_guard<std::mutex> lock(g_work_mu);
+  hold = std::unique_lock<std::mutex>(g_work_mu);
   WorkBuffer& wb = g_work[std::make_tuple(dev, stream, purpose)];
   if (wb.floats < floats) {
     if (wb.ptr) {
@@ -173,6 +176,7 @@ tpp_status launch(const tpp_brgemm_kernel_s* h, tpp::BrgemmParams& p, void* stre
   const int32_t id = choose_kernel(*h, p);
   p.split = 1;
   p.ws = nullptr;
+  std::unique_lock<std::mutex> work_hold;   // held from a work-buffer lookup to the launch
   if (id == tpp::K_F32_GENERIC && p.kind != TPP_BR_ADDRESS && p.count >= 2 &&
       !(p.flags & tpp::EPI_AUX_MASK)) {
     // A grid of few 64 x 64 tiles leaves most of the GPU idle while each workgroup walks the
@@ -185,7 +189,8 @@ tpp_status launch(const tpp_brgemm_kernel_s* h, tpp::BrgemmParams& p, void* stre
       if (split > 1) {
         p.split = (int32_t)split;
         const tpp_status st =
-            work_buffer(WORK_SPLIT, stream, tpp::f32_split_ws_floats(p.split, tiles), &p.ws);
+            work_buffer(WORK_SPLIT, stream, tpp::f32_split_ws_floats(p.split, tiles), &p.ws,
+                        work_hold);
         if (st != TPP_OK) return st;
       }
     }
@@ -208,7 +213,7 @@ tpp_status launch(const tpp_brgemm_kernel_s* h, tpp::BrgemmParams& p, void* stre
     if (split > 1) {
       p.split = (int32_t)split;
       const tpp_status st =
-          work_buffer(WORK_SPLIT, stream, split * tiles * (int64_t)bm * bn, &p.ws);
+          work_buffer(WORK_SPLIT, stream, split * tiles * (int64_t)bm * bn, &p.ws, work_hold);
       if (st != TPP_OK) return st;
     }
   }
@@ -530,8 +535,9 @@ tpp_status reduce_impl(int32_t m, int32_t n, int64_t ld, int32_t in_type, const 
   const int64_t need = tpp::reduce_work_floats(p);
   if (need < 0) return fail(TPP_ERR_UNSUPPORTED, "reduce needs more than 2^31 - 1 workgroups");
   float* work = nullptr;
+  std::unique_lock<std::mutex> work_hold;   // held from the work-buffer lookup to the launch
   if (need > 0) {
-    const tpp_status st = work_buffer(WORK_REDUCE, stream, need, &work);
+    const tpp_status st = work_buffer(WORK_REDUCE, stream, need, &work, work_hold);
     if (st != TPP_OK) return st;
   }
   const hipError_t e = tpp::launch_reduce(p, work, static_cast<hipStream_t>(stream));
