@@ -137,3 +137,46 @@ def test_reduce_past_2_pow_32_elements():
     assert np.array_equal(by_rows.cpu().numpy(), want_rows.astype(np.float32))
     assert np.array_equal(mx.cpu().numpy(), np.full(n, 125.0, np.float32))
     assert np.array_equal(by_cols.cpu().numpy(), want_cols.astype(np.float32))
+
+
+def test_concurrent_calls_on_two_streams():
+    """Two host threads, each on its own stream, make Reduce calls that need a work buffer
+    (several partials per output), with growing sizes so that the buffers are regrown while the
+    other thread's work is queued; every result matches the oracle."""
+    import threading
+    import paper_2104_05755_amd as tpp
+    dev = torch.device("cuda:0")
+    rng = np.random.default_rng(95)
+    cases = []
+    for i in range(6):
+        m, n = 64 * (i + 1), 20000 + 7000 * i          # by columns: many partials per output
+        x = wk.bf16_bits(rng.uniform(-2, 2, m * n).astype(np.float32))
+        rx, _ = oracle.reduce(x, m, n, m, "bf16", "sum", "cols", ("x",))
+        cases.append((m, n, x, rx))
+    errors = []
+
+    def worker(order):
+        try:
+            s = torch.cuda.Stream(device=dev)
+            with torch.cuda.stream(s):
+                for _ in range(3):
+                    for i in order:
+                        m, n, x, rx = cases[i]
+                        xd = torch.from_numpy(x.view(np.int16)).to(dev).view(torch.bfloat16)
+                        out = torch.full((m,), float("nan"), device=dev)
+                        tpp.tpp_reduce(m, n, m, tpp.TPP_DT_BF16, xd, tpp.TPP_RED_SUM,
+                                       tpp.TPP_RED_BY_COLS | tpp.TPP_RED_X, out, None,
+                                       s.cuda_stream)
+                        s.synchronize()
+                        X = np.abs(values(x, "bf16").reshape(n, m).T)
+                        if not np.all(np.abs(out.cpu().numpy() - rx) <= 1e-5 * X.sum(axis=1)):
+                            errors.append((order, i))
+        except Exception as e:   # reported below, on the test's thread
+            errors.append(repr(e))
+
+    threads = [threading.Thread(target=worker, args=(o,)) for o in (range(6), range(5, -1, -1))]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
