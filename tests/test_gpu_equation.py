@@ -239,3 +239,15 @@ def test_equation_past_2_pow_32_elements(m, n):
         want = (2 * ((e % 251) - 125) + ((e // m) % 7) - 3).to(torch.float32)
         bad += int((y[s:s + e.numel()].to(torch.float32) != want).sum().item())
     assert bad == 0, f"{bad} wrong elements"
+
+
+@pytest.mark.parametrize("n,pad", [(4096, 0), (1001, 0), (4096, 2)], ids=["n4096", "n1001", "ld3"])
+def test_single_row_equations(n, pad):
+    # single-row equations (the shape of a norm's statistics), every leaf kind, contiguous and
+    # padded leading dimensions
+    say(f"equation 1 x {n} pad {pad}")
+    g, r, _, _ = one(MIXED, 7, 1, n,
+                     [(-8, 8, "bf16", "none", pad), (-8, 8, "f32", "col", 0),
+                      (-4, 4, "bf16", "row", 0), (-4, 4, "f32", "scalar", 0),
+                      (-4, 4, "bf16", "col", 0)], seed=12, integer=True)
+    assert np.array_equal(g, r)
