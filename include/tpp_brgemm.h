@@ -75,7 +75,13 @@ enum {
   TPP_EPI_GELU_TANH = 1u << 2, /* 0.5 x (1 + tanh(sqrt(2/pi) (x + 0.044715 x^3)))                */
   TPP_EPI_RELU_INV = 1u << 3,
   TPP_EPI_GELU_TANH_INV = 1u << 4,
-  TPP_EPI_SAVE_PREACT = 1u << 5
+  TPP_EPI_SAVE_PREACT = 1u << 5,
+  /* Operand layout, not an epilogue step: every A_i is stored transposed, element (r, p) at
+   * A_i + r * lda + p (k contiguous per row, lda >= k), as the Transform TPP's transpose leaves
+   * a column-major block (Sec. 3.1; the MFMA reads 8 consecutive k per lane).  Supported for
+   * bf16 with k % 64 == 0 and m, lda and every element step a multiple of 8 (direct-to-LDS
+   * kernels); any other call returns TPP_ERR_UNSUPPORTED at execute. */
+  TPP_LAYOUT_A_TRANS = 1u << 8
 };
 
 /* Problem description: the dispatch-time fields of the TPP (Sec. 2.2: rows, columns, leading

@@ -240,6 +240,18 @@ __device__ __forceinline__ bool row_in_a(const BrgemmParams& p, int32_t R, int64
   return R < p.m;
 }
 
+// The same for a transposed A (row r's k-run starts at r * lda).
+__device__ __forceinline__ bool row_in_at(const BrgemmParams& p, int32_t R, int64_t& off) {
+  if (p.fused) {
+    if (R >= p.vrows) return false;
+    const int32_t gi = R / p.m, r = R - gi * p.m;
+    off = (int64_t)gi * p.a_step_m + (int64_t)r * p.lda;
+    return true;
+  }
+  off = (int64_t)R * p.lda;
+  return R < p.m;
+}
+
 // Virtual column C -> element offset of that column inside B (relative to the instance base).
 __device__ __forceinline__ bool col_in_b(const BrgemmParams& p, int32_t C, int64_t& off) {
   if (p.fused) {

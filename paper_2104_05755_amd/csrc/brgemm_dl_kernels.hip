@@ -93,7 +93,7 @@ __device__ __forceinline__ int swz_a(int k) {
 // BKT: k per stage, 32 or 64.  At 64 every stage reads whole 128-byte lines of the K-contiguous B
 // blocks (a column of a 64-k block is 128 bytes); at 32 each B column load covers half a line.
 template <int BM, int BN, int WAVES_M, int WAVES_N, bool FULL, int KIND, bool ALIGNED, int SCHED,
-          int BKT, int SLOTS_T>
+          int BKT, int SLOTS_T, bool AT>
 // Four-wave instances run two workgroups per CU, i.e. two waves per SIMD: at most 256 registers.
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, (WAVES_M * WAVES_N == 4) ? 2 : 1)
 void brgemm_bf16_dl_kernel(BrgemmParams p) {
@@ -150,10 +150,22 @@ void brgemm_bf16_dl_kernel(BrgemmParams p) {
   // Per-lane load assignments.  A wave-load r covers bytes [q*1024, q*1024 + 1024) of the A
   // panel (q = wave * A_PER_W + r); lane j fills the 16-byte chunk at q*1024 + 16 j, i.e. k-row
   // kr and swizzled chunk position sc, which holds the 8 rows m = 8 * (sc ^ swz(kr)).
+  // AT (A_i stored transposed): the A panel is laid out and loaded like the B panel, BM rows of
+  // COLB bytes (row m's k-run of the stage), swizzled by row as B is by column.
   int64_t a_off[A_PER_W];
   int a_kr[A_PER_W];
 #pragma unroll
   for (int r = 0; r < A_PER_W; ++r) {
+    if constexpr (AT) {
+      const int byte = (wave * A_PER_W + r) * 1024 + lane * 16;
+      const int row = byte / COLB, sc = (byte % COLB) / 16;
+      const int kc = sc ^ swz_b<BKT>(row);
+      int64_t off = 0;
+      const bool ok = row_in_at(p, tc.row0 + row, off);
+      a_kr[r] = 0;
+      a_off[r] = (ok ? off : base_a) + kc * 8;
+      continue;
+    }
     const int byte = (wave * A_PER_W + r) * 1024 + lane * 16;
     const int kr = byte / A_ROW, sc = (byte % A_ROW) / 16;
     const int m_local = (sc ^ swz_a<A_ROW>(kr)) * 8;
@@ -180,7 +192,8 @@ void brgemm_bf16_dl_kernel(BrgemmParams p) {
   // descriptor) plus this per-lane offset.
   uint32_t la[A_PER_W], lb[B_PER_W];
 #pragma unroll
-  for (int r = 0; r < A_PER_W; ++r) la[r] = (uint32_t)((a_off[r] - base_a + (int64_t)a_kr[r] * p.lda) * 2);
+  for (int r = 0; r < A_PER_W; ++r)
+    la[r] = (uint32_t)((a_off[r] - base_a + (AT ? 0 : (int64_t)a_kr[r] * p.lda)) * 2);
 #pragma unroll
   for (int r = 0; r < B_PER_W; ++r) lb[r] = (uint32_t)((b_off[r] - base_b) * 2);
 
@@ -227,7 +240,7 @@ void brgemm_bf16_dl_kernel(BrgemmParams p) {
     } else {
       pair_bases_k<KIND, uint16_t>(p, in, iss_i, pa, pb);
     }
-    ua = reinterpret_cast<const char*>(pa + base_a) + (int64_t)iss_kk * p.lda * 2;
+    ua = reinterpret_cast<const char*>(pa + base_a) + (int64_t)iss_kk * (AT ? 1 : p.lda) * 2;
     ub = reinterpret_cast<const char*>(pb + base_b) + (int64_t)iss_kk * 2;
     ra = raw_buffer(ua);
     rb = raw_buffer(ub);
@@ -286,6 +299,11 @@ void brgemm_bf16_dl_kernel(BrgemmParams p) {
   // reads), B fragment tn (one 16-byte read).
   auto read_a = [&](int slot_idx, int kq, int tm) {
     const char* As = lds + slot_idx * SLOT;
+    if constexpr (AT) {   // one plain 16-byte read, as for B: row lane%32, k-chunk 2 kq + lane/32
+      const int row = wm * WTM + tm * 32 + (lane & 31);
+      const int kc = 2 * kq + (lane >> 5);
+      return *reinterpret_cast<const bf16x8*>(As + row * COLB + ((kc ^ b_swz) << 4));
+    }
     const int hi = (wm * WTM + tm * 32) >> 3;     // first chunk of the 32-row group
     v4i16 half[2];
 #pragma unroll
@@ -431,34 +449,34 @@ void brgemm_bf16_dl_kernel(BrgemmParams p) {
                                             reinterpret_cast<float*>(lds), acc);
 }
 
-template <int BM, int BN, int WM, int WN, bool FULL, int KIND, int PP, int BKT, int SL>
+template <int BM, int BN, int WM, int WN, bool FULL, int KIND, int PP, int BKT, int SL, bool AT>
 void launch_dl_k(const BrgemmParams& p, dim3 grid, hipStream_t stream) {
   const dim3 block(64 * WM * WN);
   if constexpr (KIND == TPP_BR_STRIDE) {
     if (p.aligned) {
-      hipLaunchKernelGGL((brgemm_bf16_dl_kernel<BM, BN, WM, WN, FULL, KIND, true, PP, BKT, SL>), grid, block,
-                         0, stream, p);
+      hipLaunchKernelGGL((brgemm_bf16_dl_kernel<BM, BN, WM, WN, FULL, KIND, true, PP, BKT, SL, AT>),
+                         grid, block, 0, stream, p);
       return;
     }
   }
-  hipLaunchKernelGGL((brgemm_bf16_dl_kernel<BM, BN, WM, WN, FULL, KIND, false, PP, BKT, SL>), grid, block, 0,
-                     stream, p);
+  hipLaunchKernelGGL((brgemm_bf16_dl_kernel<BM, BN, WM, WN, FULL, KIND, false, PP, BKT, SL, AT>),
+                     grid, block, 0, stream, p);
 }
 
-template <int BM, int BN, int WM, int WN, int PP = 0, int BKT = 32, int SL = 0>
+template <int BM, int BN, int WM, int WN, int PP = 0, int BKT = 32, int SL = 0, bool AT = false>
 void launch_dl(const BrgemmParams& p, bool full, dim3 grid, hipStream_t stream) {
   switch (p.kind) {
     case TPP_BR_STRIDE:
-      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_STRIDE, PP, BKT, SL>(p, grid, stream)
-           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_STRIDE, PP, BKT, SL>(p, grid, stream);
+      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_STRIDE, PP, BKT, SL, AT>(p, grid, stream)
+           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_STRIDE, PP, BKT, SL, AT>(p, grid, stream);
       break;
     case TPP_BR_OFFSET:
-      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_OFFSET, PP, BKT, SL>(p, grid, stream)
-           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_OFFSET, PP, BKT, SL>(p, grid, stream);
+      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_OFFSET, PP, BKT, SL, AT>(p, grid, stream)
+           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_OFFSET, PP, BKT, SL, AT>(p, grid, stream);
       break;
     default:
-      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_ADDRESS, PP, BKT, SL>(p, grid, stream)
-           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_ADDRESS, PP, BKT, SL>(p, grid, stream);
+      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_ADDRESS, PP, BKT, SL, AT>(p, grid, stream)
+           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_ADDRESS, PP, BKT, SL, AT>(p, grid, stream);
       break;
   }
 }
@@ -480,14 +498,27 @@ bool dl_wave_grid(int32_t id, int& waves_m, int& waves_n) {
 
 hipError_t launch_brgemm_dl(const BrgemmParams& p, int32_t id, bool full, dim3 grid,
                             hipStream_t stream) {
+  // a transposed A only on the 64-k instances (the host never picks another for it)
+  if (p.a_trans && id != K_BF16_DL64K_256x256 && id != K_BF16_DL64K_128x128 &&
+      id != K_BF16_DL64K_64x64)
+    return hipErrorInvalidValue;
   switch (id) {
     case K_BF16_DL_256x256: launch_dl<256, 256, 2, 4>(p, full, grid, stream); break;
     case K_BF16_DL_128x128: launch_dl<128, 128, 2, 2>(p, full, grid, stream); break;
     case K_BF16_DL_64x64: launch_dl<64, 64, 2, 2>(p, full, grid, stream); break;
     case K_BF16_PP_256x256: launch_dl<256, 256, 4, 2, 1>(p, full, grid, stream); break;
-    case K_BF16_DL64K_256x256: launch_dl<256, 256, 4, 2, 0, 64>(p, full, grid, stream); break;
-    case K_BF16_DL64K_128x128: launch_dl<128, 128, 2, 2, 0, 64>(p, full, grid, stream); break;
-    case K_BF16_DL64K_64x64: launch_dl<64, 64, 2, 2, 0, 64>(p, full, grid, stream); break;
+    case K_BF16_DL64K_256x256:
+      p.a_trans ? launch_dl<256, 256, 4, 2, 0, 64, 0, true>(p, full, grid, stream)
+                : launch_dl<256, 256, 4, 2, 0, 64>(p, full, grid, stream);
+      break;
+    case K_BF16_DL64K_128x128:
+      p.a_trans ? launch_dl<128, 128, 2, 2, 0, 64, 0, true>(p, full, grid, stream)
+                : launch_dl<128, 128, 2, 2, 0, 64>(p, full, grid, stream);
+      break;
+    case K_BF16_DL64K_64x64:
+      p.a_trans ? launch_dl<64, 64, 2, 2, 0, 64, 0, true>(p, full, grid, stream)
+                : launch_dl<64, 64, 2, 2, 0, 64>(p, full, grid, stream);
+      break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -68,12 +68,13 @@ bool valid_dtype(int32_t t) { return t == TPP_DT_F32 || t == TPP_DT_BF16; }
 bool dl_offsets_fit(const tpp_brgemm_kernel_s& h, const tpp::BrgemmParams& p, int bm, int bn) {
   const int64_t m = h.desc.m, n = h.desc.n, k = h.desc.k, lda = h.desc.lda, ldb = h.desc.ldb;
   int64_t span_a, span_b;   // elements
+  const int64_t block_a = p.a_trans ? m * lda + k : m + k * lda;   // one A_i block
   if (p.fused) {
     if (p.a_step_m < 0 || p.b_step_n < 0) return false;
-    span_a = (bm / m + 2) * p.a_step_m + m + k * lda;
+    span_a = (bm / m + 2) * p.a_step_m + block_a;
     span_b = (bn / n + 2) * p.b_step_n + n * ldb + k;
   } else {
-    span_a = m + k * lda;
+    span_a = block_a;
     span_b = n * ldb + k;
   }
   return span_a < (int64_t(1) << 30) && span_b < (int64_t(1) << 30);   // bf16: 2 bytes each
@@ -84,9 +85,32 @@ bool dl_offsets_fit(const tpp_brgemm_kernel_s& h, const tpp::BrgemmParams& p, in
 // steps multiples of 8); the tile shape is the largest that still gives two tiles per compute
 // unit (512 tiles on the 256 CUs).  Anything else takes the element-load instance.
 int32_t choose_kernel(const tpp_brgemm_kernel_s& h, const tpp::BrgemmParams& p) {
-  if (!h.bf16) return tpp::K_F32_GENERIC;
+  if (!h.bf16) return p.a_trans ? -1 : tpp::K_F32_GENERIC;
   bool vec = h.vec_ok;
   if (p.fused) vec = vec && (p.a_step_m % 8 == 0) && (p.b_step_n % 8 == 0);
+  if (p.a_trans) {
+    // transposed A: the 64-k direct-to-LDS instances only (-1: unsupported)
+    if (!vec || h.desc.k % 64 != 0) return -1;
+    const int32_t ids[] = {tpp::K_BF16_DL64K_256x256, tpp::K_BF16_DL64K_128x128,
+                           tpp::K_BF16_DL64K_64x64};
+    if (const char* env = std::getenv("TPP_FORCE_KERNEL")) {
+      const int id = std::atoi(env);
+      for (int32_t c : ids)
+        if (c == id && dl_offsets_fit(h, p, tpp::kernel_tile_m(c), tpp::kernel_tile_n(c)))
+          return id;
+    }
+    for (int32_t c : ids) {
+      const int bm = tpp::kernel_tile_m(c), bn = tpp::kernel_tile_n(c);
+      const bool last = bm == 64;
+      if (!last && (bm > p.vrows || bn > p.vcols)) continue;
+      if (!dl_offsets_fit(h, p, bm, bn)) continue;
+      const int64_t tiles = p.groups * ((p.vrows + bm - 1) / bm) * ((p.vcols + bn - 1) / bn);
+      const int64_t ktot = h.desc.kind == TPP_BR_ADDRESS ? 0 : p.count * (int64_t)h.desc.k;
+      if (tiles >= 512 || last) return c;
+      if (bm == 256 && ktot >= 8192 && tiles * 8 >= 256) return c;
+    }
+    return -1;
+  }
   if (!vec) return tpp::K_BF16_GENERIC;
   // Direct buffer->LDS instances when k is a multiple of 32, with 64-k stages when it is a
   // multiple of 64 (whole 128-byte lines of B per load); pointer lists only with 64-k stages
@@ -174,6 +198,10 @@ tpp_status launch(const tpp_brgemm_kernel_s* h, tpp::BrgemmParams& p, void* stre
                 (p.fused || p.grid_form || (!p.a_off && !p.b_off));
   }
   const int32_t id = choose_kernel(*h, p);
+  if (id < 0)
+    return fail(TPP_ERR_UNSUPPORTED,
+                "A_TRANS needs bf16, k %% 64 == 0, m, lda and element steps multiples of 8 and "
+                "operand spans below 2^30 elements");
   p.split = 1;
   p.ws = nullptr;
   std::unique_lock<std::mutex> work_hold;   // held from a work-buffer lookup to the launch
@@ -232,7 +260,8 @@ void fill_common(const tpp_brgemm_kernel_s* h, tpp::BrgemmParams& p) {
   p.m = d.m; p.n = d.n; p.k = d.k;
   p.lda = d.lda; p.ldb = d.ldb; p.ldc = d.ldc;
   p.beta = d.beta;
-  p.flags = d.flags;
+  p.flags = d.flags & ~(uint32_t)TPP_LAYOUT_A_TRANS;   // the layout bit travels as a_trans
+  p.a_trans = (d.flags & TPP_LAYOUT_A_TRANS) != 0;
   p.c_bf16 = d.c_type == TPP_DT_BF16;
   p.kind = d.kind;
   p.stride_a = d.stride_a;
@@ -291,8 +320,9 @@ tpp_status tpp_brgemm_dispatch(const tpp_brgemm_desc* desc, tpp_brgemm_handle* o
   const tpp_brgemm_desc& d = *desc;
   if (d.m <= 0 || d.n <= 0 || d.k <= 0)
     return fail(TPP_ERR_INVALID_ARG, "m, n, k must be > 0 (got %d, %d, %d)", d.m, d.n, d.k);
-  if (d.lda < d.m || d.ldb < d.k || d.ldc < d.m)
-    return fail(TPP_ERR_INVALID_ARG, "leading dimension too small (lda %lld < m, ldb %lld < k or ldc %lld < m)",
+  const bool a_trans = (d.flags & TPP_LAYOUT_A_TRANS) != 0;
+  if (d.lda < (a_trans ? d.k : d.m) || d.ldb < d.k || d.ldc < d.m)
+    return fail(TPP_ERR_INVALID_ARG, "leading dimension too small (lda %lld < m (k with A_TRANS), ldb %lld < k or ldc %lld < m)",
                 (long long)d.lda, (long long)d.ldb, (long long)d.ldc);
   if (!valid_dtype(d.a_type) || !valid_dtype(d.b_type) || !valid_dtype(d.c_type) ||
       !valid_dtype(d.comp_type))
@@ -303,8 +333,9 @@ tpp_status tpp_brgemm_dispatch(const tpp_brgemm_desc* desc, tpp_brgemm_handle* o
     return fail(TPP_ERR_UNSUPPORTED, "accumulation is fp32 only");
   if (d.kind != TPP_BR_STRIDE && d.kind != TPP_BR_OFFSET && d.kind != TPP_BR_ADDRESS)
     return fail(TPP_ERR_INVALID_ARG, "unknown batch kind %d", d.kind);
-  if (d.flags & ~(uint32_t)(TPP_EPI_BIAS | TPP_EPI_RELU | TPP_EPI_GELU_TANH | tpp::EPI_AUX_MASK))
-    return fail(TPP_ERR_INVALID_ARG, "unknown epilogue flag bits 0x%x", d.flags);
+  if (d.flags & ~(uint32_t)(TPP_EPI_BIAS | TPP_EPI_RELU | TPP_EPI_GELU_TANH | tpp::EPI_AUX_MASK |
+                            TPP_LAYOUT_A_TRANS))
+    return fail(TPP_ERR_INVALID_ARG, "unknown flag bits 0x%x", d.flags);
   if ((d.flags & TPP_EPI_RELU) && (d.flags & TPP_EPI_GELU_TANH))
     return fail(TPP_ERR_INVALID_ARG, "RELU and GELU_TANH exclude each other");
   const uint32_t inv = TPP_EPI_RELU_INV | TPP_EPI_GELU_TANH_INV;
@@ -330,9 +361,9 @@ tpp_status tpp_brgemm_dispatch(const tpp_brgemm_desc* desc, tpp_brgemm_handle* o
   h->vec_ok = h->bf16 && d.m % 8 == 0 && d.k % 8 == 0 && d.lda % 8 == 0 && d.ldb % 8 == 0 &&
               (d.kind != TPP_BR_STRIDE || (d.stride_a % 8 == 0 && d.stride_b % 8 == 0));
   static const char* kinds[] = {"stride", "offset", "address"};
-  std::snprintf(h->name, sizeof h->name, "brgemm_%s_%s_m%d_n%d_k%d_%s%s", h->bf16 ? "bf16" : "f32",
+  std::snprintf(h->name, sizeof h->name, "brgemm_%s_%s_m%d_n%d_k%d_%s%s%s", h->bf16 ? "bf16" : "f32",
                 d.c_type == TPP_DT_BF16 ? "bf16out" : "f32out", d.m, d.n, d.k, kinds[d.kind],
-                h->vec_ok ? "_vec" : "_generic");
+                h->vec_ok ? "_vec" : "_generic", a_trans ? "_atrans" : "");
   *out = h.get();
   cache().push_back(std::move(h));
   return ok();

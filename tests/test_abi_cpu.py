@@ -312,3 +312,17 @@ def test_equation_execute_host_checks(tpp):
     root = grow(5)                                    # 63 nodes, score 5: fits
     assert tpp.tpp_equation_plan(deep, root)[3] == 5
     tpp.tpp_equation_execute(deep, root, 0, 4, [(fake, 4, 0, "none")], fake, 4, 0)   # m = 0
+
+
+def test_a_trans_dispatch_checks(tpp):
+    # with A_TRANS the rows of A_i hold k entries: lda >= k is required and suffices (lda < m)
+    ok = tpp.make_desc(128, 64, 64, 64, 64, 128, "bf16", "f32", 0.0, "stride", 128 * 64, 64 * 64,
+                       flags=("a_trans",))
+    assert tpp.tpp_brgemm_dispatch(ok)
+    assert "_atrans" in tpp.tpp_brgemm_describe(tpp.tpp_brgemm_dispatch(ok))
+    for bad in (tpp.make_desc(128, 64, 64, 32, 64, 128, "bf16", "f32", 0.0, "stride", 128 * 64,
+                              64 * 64, flags=("a_trans",)),
+                tpp.make_desc(128, 64, 64, 64, 64, 128, "bf16", "f32", 0.0, "stride", 128 * 64,
+                              64 * 64)):
+        with pytest.raises(tpp.TppError):
+            tpp.tpp_brgemm_dispatch(bad)

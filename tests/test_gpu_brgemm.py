@@ -292,6 +292,52 @@ def test_every_tile_kernel_matches_oracle(kid, shape, monkeypatch):
         check_close(got["out"], ref, wl.calls[0], f"k{kid} ragged")
 
 
+# A_i stored transposed (TPP_LAYOUT_A_TRANS): the 64-k direct-to-LDS instances, every batch
+# variant.  Each workload's A blocks are read as transposed blocks with lda = k (the block extent
+# m * k never exceeds the column-major one), by the GPU and by the oracle alike.
+AT_KERNEL_IDS = [9, 10, 11]
+AT_CASES = {
+    "full": lambda: wk.mlp_block(seed=13, tokens=512, hidden=512, inter=512),
+    "ragged": lambda: wk.mlp_fc(seed=14, minibatch=7 * 64, c_in=192, k_out=5 * 64),
+    "offset": lambda: wk.conv3x3(seed=15, images=2, h=9, w=56, c=64, k=64),
+    "address": lambda: wk.gathered(seed=16, n_out=24, pool=64, min_len=0, max_len=12),
+}
+
+
+@pytest.mark.parametrize("kid", AT_KERNEL_IDS)
+@pytest.mark.parametrize("case", sorted(AT_CASES))
+def test_a_trans_matches_oracle(kid, case, monkeypatch):
+    monkeypatch.setenv("TPP_FORCE_KERNEL", str(kid))
+    wl = AT_CASES[case]()
+    for c in wl.calls:
+        c.flags = set(c.flags) | {"a_trans"}
+        c.lda = c.k
+    say(f"a_trans kernel {kid} {case} {wl.name}")
+    got = run_gpu(wl)
+    if wl.name == "mlp_block":
+        h_ref, _ = run_oracle(wl, 0)
+        check_close(got["h"], h_ref, wl.calls[0], f"k{kid} at h")
+        y_ref, _ = run_oracle(wk.Workload(wl.name, dict(wl.arrays, h=h_ref), wl.calls), 1)
+        check_close(got["y"], y_ref, wl.calls[1], f"k{kid} at y")
+    else:
+        ref, _ = run_oracle(wl)
+        out = wl.calls[0].c
+        check_close(got[out], ref, wl.calls[0], f"k{kid} at {case}")
+
+
+def test_a_trans_unsupported_shapes_are_refused():
+    # k not a multiple of 64: no instance takes a transposed A
+    import paper_2104_05755_amd as tpp
+    dev = torch.device("cuda:0")
+    a = torch.zeros(64 * 40, dtype=torch.bfloat16, device=dev)
+    b = torch.zeros(40 * 64, dtype=torch.bfloat16, device=dev)
+    c = torch.zeros(64 * 64, device=dev)
+    h = tpp.tpp_brgemm_dispatch(tpp.make_desc(64, 64, 40, 40, 40, 64, "bf16", "f32", 0.0, "stride",
+                                              64 * 40, 40 * 64, flags=("a_trans",)))
+    with pytest.raises(RuntimeError):
+        tpp.tpp_brgemm_execute_stride(h, a, b, c, None, 1, tpp.current_stream())
+
+
 def _bf16_dev(v, dev):
     return torch.tensor(np.asarray(v, np.float32), dtype=torch.bfloat16, device=dev)
 

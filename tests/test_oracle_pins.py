@@ -383,3 +383,36 @@ def test_oracle_rejects_bad_descriptors():
         kw.update(bad)
         with pytest.raises(ValueError):
             oracle.brgemm(oracle.Desc(**kw), x, x, x.copy(), count=1)
+
+
+@pytest.mark.parametrize("kind", ["stride", "offset", "address"])
+def test_a_trans_layout_is_the_transposed_block(kind):
+    """The transposed-A layout (element (r, p) of A_i at r * lda + p) gives the bit-identical
+    result of the column-major layout holding the numpy transpose of each block, for every batch
+    variant, with a padded lda; a lda below k is rejected."""
+    rng = np.random.default_rng(61)
+    m, n, k, count = 24, 20, 32, 5
+    lda_t = k + 3
+    blocks = rng.uniform(-1, 1, (count, k, m)).astype(np.float32)        # block i: A_i[r, p] = blocks[i, p, r]
+    plain = wk.bf16_bits(blocks.reshape(-1))                              # column-major, lda = m
+    tr = np.zeros((count, m, lda_t), np.float32)
+    tr[:, :, :k] = np.swapaxes(blocks, 1, 2)                              # row r holds A_i[r, :]
+    trans = wk.bf16_bits(tr.reshape(-1))
+    b = wk.bf16_bits(rng.uniform(-1, 1, count * k * n).astype(np.float32))
+    outs = []
+    for a, lda, flags, step in ((plain, m, set(), m * k), (trans, lda_t, {"a_trans"}, m * lda_t)):
+        c = np.full(m * n, np.nan, np.float32)
+        d = oracle.Desc(m, n, k, lda, k, m, "bf16", "f32", 0.0, kind,
+                        step if kind == "stride" else 0, k * n if kind == "stride" else 0, flags)
+        if kind == "stride":
+            oracle.brgemm(d, a, b, c, count=count)
+        elif kind == "offset":
+            oracle.brgemm(d, a, b, c, count=count, offs_a=np.arange(count) * step,
+                          offs_b=np.arange(count) * k * n)
+        else:
+            oracle.brgemm(d, a, b, c, idx_a=np.arange(count) * step, idx_b=np.arange(count) * k * n)
+        outs.append(c)
+    assert np.array_equal(outs[0], outs[1]) and not np.isnan(outs[0]).any()
+    with pytest.raises(ValueError):
+        oracle.brgemm(oracle.Desc(m, n, k, k - 1, k, m, "bf16", "f32", 0.0, "stride", m * k, k * n,
+                                  {"a_trans"}), trans, b, np.zeros(m * n, np.float32), count=1)
