@@ -472,7 +472,8 @@ def embedding_entry(args, torch, tpp, torch_io, wk, stream):
 
 def backward_entry(args, torch, tpp, torch_io, wk, stream):
     """The transformer MLP's backward pass at the headline size (see workloads.mlp_backward): the
-    four weight / activation transposes, the four gradient BRGEMMs (GELU_inv fused into dZ) and
+    two activation transposes, the four gradient BRGEMMs (the weights read transposed by dZ and
+    dX, GELU_inv fused into dZ) and
     the bias-gradient reduces, timed as one step over K steps (nothing between the launches), and
     each launch's mean duration inside the step from fence-free events.  The forward call that
     keeps the pre-activation (GEMM1 + SAVE_PREACT) runs once before and is timed on its own."""
@@ -488,14 +489,17 @@ def backward_entry(args, torch, tpp, torch_io, wk, stream):
     bw_calls = wl.calls[1:]
     bw_flops = sum(c.flops for c in bw_calls)
     launches = []
-    names = {1: "transpose W2 blocks", 2: "transpose W1 blocks", 3: "transpose H blocks",
-             4: "transpose X blocks", 5: "dZ = (W2^T dY) * gelu'(Z)  [GELU_inv fused]",
-             6: "dW2 = sum_tokens dY H^T", 7: "db2 (sum over token blocks)",
-             8: "db2 (sum within a block)", 9: "dX = W1^T dZ", 10: "dW1 = sum_tokens dZ X^T",
-             11: "db1 (sum over token blocks)", 12: "db1 (sum within a block)"}
+    names = {"ht": "transpose H blocks", "xt": "transpose X blocks",
+             "dz": "dZ = (W2^T dY) * gelu'(Z)  [W2 read transposed, GELU_inv fused]",
+             "dw2": "dW2 = sum_tokens dY H^T", "p2": "db2 (sum over token blocks)",
+             "db2": "db2 (sum within a block)", "dx": "dX = W1^T dZ  [W1 read transposed]",
+             "dw1": "dW1 = sum_tokens dZ X^T", "p1": "db1 (sum over token blocks)",
+             "db1": "db1 (sum within a block)"}
+    out_name = lambda st: (st.c if isinstance(st, wk.Call) else
+                           st.dst if isinstance(st, wk.TransformStep) else st.dst_x)
     brgemm_ms = 0.0
     for i, (st, ms) in enumerate(zip(wl.steps[1:], per), start=1):
-        e = {"what": names[i], "launch_us": round(ms * 1e3, 2)}
+        e = {"what": names[out_name(st)], "launch_us": round(ms * 1e3, 2)}
         if isinstance(st, wk.Call):
             tfl = st.flops / (ms * 1e-3) / 1e12
             brgemm_ms += ms

@@ -299,14 +299,15 @@ def mlp_backward(seed: int = 6, tokens: int = 8192, hidden: int = 1024,
 
     Forward (kept for back-propagation): Z = W1 X + b1 saved in ``z`` (bf16, H's layout), H =
     gelu(Z) in ``h``.  The incoming gradient dY (N(0,1), Y's layout [Nb][Hb][64n][64h]) then gives
-      dZ  = (W2^T dY) * gelu'(Z)      B1: A = W2 blocks transposed, GELU_inv fused, bf16
+      dZ  = (W2^T dY) * gelu'(Z)      B1: A = W2 blocks read transposed (A_TRANS), GELU_inv, bf16
       dW2 = sum over tokens dY H^T    B2: A = dY, B = H blocks transposed, fp32
       db2 = sum over tokens dY        two Reduce TPP calls (over token blocks, then within one)
-      dX  = W1^T dZ                   B3: A = W1 blocks transposed, bf16
+      dX  = W1^T dZ                   B3: A = W1 blocks read transposed (A_TRANS), bf16
       dW1 = sum over tokens dZ X^T    B4: A = dZ, B = X blocks transposed, fp32
       db1 = sum over tokens dZ        two Reduce TPP calls
-    Every transposed operand is a batched Transform TPP (transpose of each 64 x 64 block in place
-    of the block).  The weight gradients keep W's blocked layout, dX keeps X's.
+    A weight block read with A_TRANS is its own transpose (k contiguous per row).  The transposed
+    B operands are batched Transform TPP calls (each 64 x 64 block transposed in place of the
+    block).  The weight gradients keep W's blocked layout, dX keeps X's.
     """
     rng = np.random.default_rng(seed)
     nb, hb, ib = tokens // BLK, hidden // BLK, inter // BLK
@@ -320,7 +321,6 @@ def mlp_backward(seed: int = 6, tokens: int = 8192, hidden: int = 1024,
     nan32 = lambda shape: np.full(shape, np.nan, dtype=np.float32)
     arrays = dict(x=x, w1=w1, b1=b1, w2=w2, dy=dy,
                   z=nan16((nb, ib, BLK, BLK)), h=nan16((nb, ib, BLK, BLK)),
-                  w1t=nan16((ib, hb, BLK, BLK)), w2t=nan16((hb, ib, BLK, BLK)),
                   ht=nan16((nb, ib, BLK, BLK)), xt=nan16((nb, hb, BLK, BLK)),
                   dz=nan16((nb, ib, BLK, BLK)), dx=nan16((nb, hb, BLK, BLK)),
                   dw1=nan32((ib, hb, BLK, BLK)), dw2=nan32((hb, ib, BLK, BLK)),
@@ -337,10 +337,10 @@ def mlp_backward(seed: int = 6, tokens: int = 8192, hidden: int = 1024,
                                            G=g, in_stride=blk, out_stride=blk)
     # dZ[nb][ib] (i x n) = gelu'(Z) * sum_hb W2[hb][ib]^T (i x h) dY[nb][hb] (h x n)
     b1c = Call(BLK, BLK, BLK, BLK, BLK, BLK, "bf16", "bf16", 0.0, "stride", ib * blk, blk,
-               {"gelu_tanh_inv"}, G=ib * nb,
+               {"gelu_tanh_inv", "a_trans"}, G=ib * nb,
                grid=sq(gm=ib, gn=nb, a_step_m=blk, b_step_n=hb * blk, c_step_m=blk,
                        c_step_n=ib * blk),
-               count=hb, a="w2t", b="dy", c="dz", aux="z")
+               count=hb, a="w2", b="dy", c="dz", aux="z")
     # dW2[hb][ib] (h x i) = sum_nb dY[nb][hb] (h x n) H[nb][ib]^T (n x i)
     b2c = Call(BLK, BLK, BLK, BLK, BLK, BLK, "bf16", "f32", 0.0, "stride", hb * blk, ib * blk,
                set(), G=hb * ib,
@@ -349,10 +349,10 @@ def mlp_backward(seed: int = 6, tokens: int = 8192, hidden: int = 1024,
                count=nb, a="dy", b="ht", c="dw2")
     # dX[nb][hb] (h x n) = sum_ib W1[ib][hb]^T (h x i) dZ[nb][ib] (i x n)
     b3c = Call(BLK, BLK, BLK, BLK, BLK, BLK, "bf16", "bf16", 0.0, "stride", hb * blk, blk,
-               set(), G=hb * nb,
+               {"a_trans"}, G=hb * nb,
                grid=sq(gm=hb, gn=nb, a_step_m=blk, b_step_n=ib * blk, c_step_m=blk,
                        c_step_n=hb * blk),
-               count=ib, a="w1t", b="dz", c="dx")
+               count=ib, a="w1", b="dz", c="dx")
     # dW1[ib][hb] (i x h) = sum_nb dZ[nb][ib] (i x n) X[nb][hb]^T (n x h)
     b4c = Call(BLK, BLK, BLK, BLK, BLK, BLK, "bf16", "f32", 0.0, "stride", ib * blk, hb * blk,
                set(), G=ib * hb,
@@ -365,8 +365,7 @@ def mlp_backward(seed: int = 6, tokens: int = 8192, hidden: int = 1024,
         ReduceStep(src, fb * blk, nb, fb * blk, "bf16", "sum", "cols", dst_x=p),
         ReduceStep(p, BLK, BLK, BLK, "f32", "sum", "cols", dst_x=db, G=fb, in_stride=blk,
                    out_stride=BLK)]
-    steps = [fwd, tr("w2", "w2t", hb * ib), tr("w1", "w1t", ib * hb), tr("h", "ht", nb * ib),
-             tr("x", "xt", nb * hb), b1c, b2c, *red("dy", hb, "p2", "db2"), b3c, b4c,
+    steps = [fwd, tr("h", "ht", nb * ib), tr("x", "xt", nb * hb), b1c, b2c, *red("dy", hb, "p2", "db2"), b3c, b4c,
              *red("dz", ib, "p1", "db1")]
     return Workload("mlp_backward", arrays, [fwd, b1c, b2c, b3c, b4c], steps=steps)
 
