@@ -81,7 +81,11 @@ enum {
    * a column-major block (Sec. 3.1; the MFMA reads 8 consecutive k per lane).  Supported for
    * bf16 with k % 64 == 0 and m, lda and every element step a multiple of 8 (direct-to-LDS
    * kernels); any other call returns TPP_ERR_UNSUPPORTED at execute. */
-  TPP_LAYOUT_A_TRANS = 1u << 8
+  TPP_LAYOUT_A_TRANS = 1u << 8,
+  /* Operand layout: every B_i is stored transposed, element (p, c) at B_i + p * ldb + c (n
+   * contiguous per k-row, ldb >= n), the block of Y^T as a column-major Y stores it.  Same
+   * support as TPP_LAYOUT_A_TRANS, with n a multiple of 8 as well. */
+  TPP_LAYOUT_B_TRANS = 1u << 9
 };
 
 /* Problem description: the dispatch-time fields of the TPP (Sec. 2.2: rows, columns, leading

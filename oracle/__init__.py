@@ -29,7 +29,7 @@ EPI_BIAS, EPI_RELU, EPI_GELU_TANH = 1, 2, 4
 EPI_RELU_INV, EPI_GELU_TANH_INV, EPI_SAVE_PREACT = 8, 16, 32
 _EPI_BITS = {"bias": EPI_BIAS, "relu": EPI_RELU, "gelu_tanh": EPI_GELU_TANH,
              "relu_inv": EPI_RELU_INV, "gelu_tanh_inv": EPI_GELU_TANH_INV,
-             "save_preact": EPI_SAVE_PREACT, "a_trans": 256}
+             "save_preact": EPI_SAVE_PREACT, "a_trans": 256, "b_trans": 512}
 RED_SUM, RED_MUL, RED_MIN, RED_MAX = 0, 1, 2, 3
 RED_BY_COLS, RED_BY_ROWS, RED_X, RED_X2 = 1, 2, 4, 8
 TR_TRANSPOSE, TR_VNNI, TR_VNNI_TO_VNNI_T = 0, 1, 2

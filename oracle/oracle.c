@@ -115,13 +115,15 @@ static void pair_addresses(const oracle_desc* d, const void* a, const void* b, i
 static int check_desc(const oracle_desc* d) {
   if (!d || d->m <= 0 || d->n <= 0 || d->k <= 0) return -1;
   const int a_trans = (d->flags & ORACLE_A_TRANS) != 0;
-  if (d->lda < (a_trans ? d->k : d->m) || d->ldb < d->k || d->ldc < d->m) return -1;
+  const int b_trans = (d->flags & ORACLE_B_TRANS) != 0;
+  if (d->lda < (a_trans ? d->k : d->m) || d->ldb < (b_trans ? d->n : d->k) || d->ldc < d->m)
+    return -1;
   if (d->ab_type != ORACLE_F32 && d->ab_type != ORACLE_BF16) return -1;
   if (d->c_type != ORACLE_F32 && d->c_type != ORACLE_BF16) return -1;
   const uint32_t f = d->flags;
   const uint32_t known = ORACLE_EPI_BIAS | ORACLE_EPI_RELU | ORACLE_EPI_GELU_TANH |
                          ORACLE_EPI_RELU_INV | ORACLE_EPI_GELU_TANH_INV | ORACLE_EPI_SAVE_PREACT |
-                         ORACLE_A_TRANS;
+                         ORACLE_A_TRANS | ORACLE_B_TRANS;
   if (f & ~known) return -1;
   if ((f & ORACLE_EPI_RELU) && (f & ORACLE_EPI_GELU_TANH)) return -1;
   if ((f & ORACLE_EPI_RELU_INV) && (f & ORACLE_EPI_GELU_TANH_INV)) return -1;
@@ -151,6 +153,7 @@ static int check_desc(const oracle_desc* d) {
 static void brgemm_resolved(const oracle_desc* d, const char* const* pa, const char* const* pb,
                             int64_t count, void* c, const float* bias, void* aux, double* ref64) {
   const int a_trans = (d->flags & ORACLE_A_TRANS) != 0;
+  const int b_trans = (d->flags & ORACLE_B_TRANS) != 0;
   for (int32_t col = 0; col < d->n; ++col) {
     for (int32_t row = 0; row < d->m; ++row) {
       double s = 0.0;
@@ -159,7 +162,9 @@ static void brgemm_resolved(const oracle_desc* d, const char* const* pa, const c
           /* A_i(row, p): column-major, or transposed (Sec. 3.1's transpose of the block) */
           const int64_t at = a_trans ? (int64_t)row * d->lda + p : (int64_t)row + (int64_t)p * d->lda;
           double x = oracle_widen(pa[i], at, d->ab_type);
-          double y = oracle_widen(pb[i], (int64_t)p + (int64_t)col * d->ldb, d->ab_type);
+          /* B_i(p, col): column-major, or transposed */
+          const int64_t bt = b_trans ? (int64_t)p * d->ldb + col : (int64_t)p + (int64_t)col * d->ldb;
+          double y = oracle_widen(pb[i], bt, d->ab_type);
           s += x * y;
         }
       }

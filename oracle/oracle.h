@@ -40,7 +40,9 @@ enum { ORACLE_STRIDE = 0, ORACLE_OFFSET = 1, ORACLE_ADDRESS = 2 };
 enum { ORACLE_EPI_BIAS = 1u, ORACLE_EPI_RELU = 2u, ORACLE_EPI_GELU_TANH = 4u,
        ORACLE_EPI_RELU_INV = 8u, ORACLE_EPI_GELU_TANH_INV = 16u, ORACLE_EPI_SAVE_PREACT = 32u,
        /* layout: A_i stored transposed, element (row, p) at row * lda + p (lda >= k) */
-       ORACLE_A_TRANS = 256u };
+       ORACLE_A_TRANS = 256u,
+       /* layout: B_i stored transposed, element (p, col) at p * ldb + col (ldb >= n) */
+       ORACLE_B_TRANS = 512u };
 enum { ORACLE_RED_SUM = 0, ORACLE_RED_MUL = 1, ORACLE_RED_MIN = 2, ORACLE_RED_MAX = 3 };
 enum { ORACLE_RED_BY_COLS = 1u, ORACLE_RED_BY_ROWS = 2u, ORACLE_RED_X = 4u, ORACLE_RED_X2 = 8u };
 enum { ORACLE_TR_TRANSPOSE = 0, ORACLE_TR_VNNI = 1, ORACLE_TR_VNNI_TO_VNNI_T = 2 };

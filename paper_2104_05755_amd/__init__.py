@@ -29,7 +29,7 @@ TPP_DT_F32, TPP_DT_BF16 = 0, 1
 TPP_BR_STRIDE, TPP_BR_OFFSET, TPP_BR_ADDRESS = 0, 1, 2
 TPP_EPI_BIAS, TPP_EPI_RELU, TPP_EPI_GELU_TANH = 1, 2, 4
 TPP_EPI_RELU_INV, TPP_EPI_GELU_TANH_INV, TPP_EPI_SAVE_PREACT = 8, 16, 32
-TPP_LAYOUT_A_TRANS = 256
+TPP_LAYOUT_A_TRANS, TPP_LAYOUT_B_TRANS = 256, 512
 TPP_RED_SUM, TPP_RED_MUL, TPP_RED_MIN, TPP_RED_MAX = 0, 1, 2, 3
 TPP_RED_BY_COLS, TPP_RED_BY_ROWS, TPP_RED_X, TPP_RED_X2 = 1, 2, 4, 8
 TPP_TR_TRANSPOSE, TPP_TR_VNNI, TPP_TR_VNNI_TO_VNNI_T = 0, 1, 2
@@ -266,12 +266,13 @@ def make_desc(m, n, k, lda, ldb, ldc, ab_type="bf16", c_type="f32", beta=0.0, ki
               stride_a=0, stride_b=0, flags=()) -> tpp_brgemm_desc:
     """Convenience: a descriptor from readable names (dtype "f32"/"bf16", kind
     "stride"/"offset"/"address", flags from {"bias", "relu", "gelu_tanh", "relu_inv",
-    "gelu_tanh_inv", "save_preact"} and the layout flag "a_trans")."""
+    "gelu_tanh_inv", "save_preact"} and the layout flags "a_trans", "b_trans")."""
     dt = {"f32": TPP_DT_F32, "bf16": TPP_DT_BF16}
     kd = {"stride": TPP_BR_STRIDE, "offset": TPP_BR_OFFSET, "address": TPP_BR_ADDRESS}
     fl = {"bias": TPP_EPI_BIAS, "relu": TPP_EPI_RELU, "gelu_tanh": TPP_EPI_GELU_TANH,
           "relu_inv": TPP_EPI_RELU_INV, "gelu_tanh_inv": TPP_EPI_GELU_TANH_INV,
-          "save_preact": TPP_EPI_SAVE_PREACT, "a_trans": TPP_LAYOUT_A_TRANS}
+          "save_preact": TPP_EPI_SAVE_PREACT, "a_trans": TPP_LAYOUT_A_TRANS,
+          "b_trans": TPP_LAYOUT_B_TRANS}
     bits = 0
     for f in flags:
         bits |= fl[f]

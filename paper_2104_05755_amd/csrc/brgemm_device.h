@@ -252,6 +252,18 @@ __device__ __forceinline__ bool row_in_at(const BrgemmParams& p, int32_t R, int6
   return R < p.m;
 }
 
+// The same for a transposed B: element offset of column C in k-row 0 (columns are contiguous).
+__device__ __forceinline__ bool col_in_bt(const BrgemmParams& p, int32_t C, int64_t& off) {
+  if (p.fused) {
+    if (C >= p.vcols) return false;
+    const int32_t gi = C / p.n, c = C - gi * p.n;
+    off = (int64_t)gi * p.b_step_n + c;
+    return true;
+  }
+  off = C;
+  return C < p.n;
+}
+
 // Virtual column C -> element offset of that column inside B (relative to the instance base).
 __device__ __forceinline__ bool col_in_b(const BrgemmParams& p, int32_t C, int64_t& off) {
   if (p.fused) {

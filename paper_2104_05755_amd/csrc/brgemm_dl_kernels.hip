@@ -93,7 +93,7 @@ __device__ __forceinline__ int swz_a(int k) {
 // BKT: k per stage, 32 or 64.  At 64 every stage reads whole 128-byte lines of the K-contiguous B
 // blocks (a column of a 64-k block is 128 bytes); at 32 each B column load covers half a line.
 template <int BM, int BN, int WAVES_M, int WAVES_N, bool FULL, int KIND, bool ALIGNED, int SCHED,
-          int BKT, int SLOTS_T, bool AT>
+          int BKT, int SLOTS_T, bool AT, bool BT>
 // Four-wave instances run two workgroups per CU, i.e. two waves per SIMD: at most 256 registers.
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N, (WAVES_M * WAVES_N == 4) ? 2 : 1)
 void brgemm_bf16_dl_kernel(BrgemmParams p) {
@@ -105,6 +105,7 @@ void brgemm_bf16_dl_kernel(BrgemmParams p) {
   constexpr int A_ROW = BM * 2;                 // bytes per k-row of the A panel
   constexpr int A_BYTES = DL_BK * A_ROW;        // A panel of one slot
   constexpr int COLB = DL_BK * 2;               // bytes of one B column in a slot
+  constexpr int B_ROW = BN * 2;                 // bytes per k-row of a transposed B panel (BT)
   constexpr int B_BYTES = BN * COLB;            // B panel of one slot
   constexpr int SLOT = A_BYTES + B_BYTES;
   constexpr int A_PER_W = A_BYTES / 1024 / NW;  // 1 KB wave-loads per wave and stage
@@ -176,9 +177,23 @@ void brgemm_bf16_dl_kernel(BrgemmParams p) {
   }
   // B wave-load r: 16 columns of 64 bytes; lane j fills column 4*q + j/4 (q-th group of 16
   // columns), chunk position j%4, which holds k-chunk (j%4) ^ ((column >> 2) & 3).
+  // BT (B_i stored transposed): the B panel is laid out and loaded like the A panel, DL_BK
+  // k-rows of B_ROW bytes holding 8 consecutive columns per 16-byte chunk, swizzled by k-row.
   int64_t b_off[B_PER_W];
+  int b_kr[B_PER_W];
 #pragma unroll
   for (int r = 0; r < B_PER_W; ++r) {
+    if constexpr (BT) {
+      const int byte = (wave * B_PER_W + r) * 1024 + lane * 16;
+      const int kr = byte / B_ROW, sc = (byte % B_ROW) / 16;
+      const int n_local = (sc ^ swz_a<B_ROW>(kr)) * 8;
+      b_kr[r] = kr;
+      int64_t off = 0;
+      const bool ok = col_in_bt(p, tc.col0 + n_local, off);
+      b_off[r] = ok ? off : base_b;   // out-of-range columns read a valid one (discarded)
+      continue;
+    }
+    b_kr[r] = 0;
     const int byte = (wave * B_PER_W + r) * 1024 + lane * 16;
     const int col = byte / COLB, sc = (byte % COLB) / 16;
     const int kc = sc ^ swz_b<BKT>(col);
@@ -195,7 +210,8 @@ void brgemm_bf16_dl_kernel(BrgemmParams p) {
   for (int r = 0; r < A_PER_W; ++r)
     la[r] = (uint32_t)((a_off[r] - base_a + (AT ? 0 : (int64_t)a_kr[r] * p.lda)) * 2);
 #pragma unroll
-  for (int r = 0; r < B_PER_W; ++r) lb[r] = (uint32_t)((b_off[r] - base_b) * 2);
+  for (int r = 0; r < B_PER_W; ++r)
+    lb[r] = (uint32_t)((b_off[r] - base_b + (BT ? (int64_t)b_kr[r] * p.ldb : 0)) * 2);
 
   // Stages are issued in order; (iss_i, iss_kk) is the pair and k offset of the next one, so no
   // stage index is ever divided.  A stage's wave-loads can be spread over other work:
@@ -241,7 +257,7 @@ void brgemm_bf16_dl_kernel(BrgemmParams p) {
       pair_bases_k<KIND, uint16_t>(p, in, iss_i, pa, pb);
     }
     ua = reinterpret_cast<const char*>(pa + base_a) + (int64_t)iss_kk * (AT ? 1 : p.lda) * 2;
-    ub = reinterpret_cast<const char*>(pb + base_b) + (int64_t)iss_kk * 2;
+    ub = reinterpret_cast<const char*>(pb + base_b) + (int64_t)iss_kk * (BT ? p.ldb : 1) * 2;
     ra = raw_buffer(ua);
     rb = raw_buffer(ub);
     slot = lds + (iss_s % SLOTS) * SLOT;
@@ -320,6 +336,21 @@ void brgemm_bf16_dl_kernel(BrgemmParams p) {
   };
   auto read_b = [&](int slot_idx, int kq, int tn) {
     const char* Bs = lds + slot_idx * SLOT + A_BYTES;
+    if constexpr (BT) {   // two transposing reads, as for a column-major A: column lane%32
+      const int hi = (wn * WTN + tn * 32) >> 3;
+      v4i16 half[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int k = kq * 16 + 8 * (g >> 1) + 4 * h + (j >> 2);
+        const int byte = k * B_ROW + (((hi ^ swz_a<B_ROW>(k)) + a_lo) << 4) + a_sub;
+        half[h] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((LDS_AS v4i16*)(Bs + byte));
+      }
+      const u32x4 w = {(uint32_t)(uint16_t)half[0][0] | ((uint32_t)(uint16_t)half[0][1] << 16),
+                       (uint32_t)(uint16_t)half[0][2] | ((uint32_t)(uint16_t)half[0][3] << 16),
+                       (uint32_t)(uint16_t)half[1][0] | ((uint32_t)(uint16_t)half[1][1] << 16),
+                       (uint32_t)(uint16_t)half[1][2] | ((uint32_t)(uint16_t)half[1][3] << 16)};
+      return __builtin_bit_cast(bf16x8, w);
+    }
     const int col = wn * WTN + tn * 32 + (lane & 31);
     const int kc = 2 * kq + (lane >> 5);
     return *reinterpret_cast<const bf16x8*>(Bs + col * COLB + ((kc ^ b_swz) << 4));
@@ -449,36 +480,47 @@ void brgemm_bf16_dl_kernel(BrgemmParams p) {
                                             reinterpret_cast<float*>(lds), acc);
 }
 
-template <int BM, int BN, int WM, int WN, bool FULL, int KIND, int PP, int BKT, int SL, bool AT>
+template <int BM, int BN, int WM, int WN, bool FULL, int KIND, int PP, int BKT, int SL, bool AT,
+          bool BT>
 void launch_dl_k(const BrgemmParams& p, dim3 grid, hipStream_t stream) {
   const dim3 block(64 * WM * WN);
   if constexpr (KIND == TPP_BR_STRIDE) {
     if (p.aligned) {
-      hipLaunchKernelGGL((brgemm_bf16_dl_kernel<BM, BN, WM, WN, FULL, KIND, true, PP, BKT, SL, AT>),
+      hipLaunchKernelGGL((brgemm_bf16_dl_kernel<BM, BN, WM, WN, FULL, KIND, true, PP, BKT, SL, AT, BT>),
                          grid, block, 0, stream, p);
       return;
     }
   }
-  hipLaunchKernelGGL((brgemm_bf16_dl_kernel<BM, BN, WM, WN, FULL, KIND, false, PP, BKT, SL, AT>),
+  hipLaunchKernelGGL((brgemm_bf16_dl_kernel<BM, BN, WM, WN, FULL, KIND, false, PP, BKT, SL, AT, BT>),
                      grid, block, 0, stream, p);
 }
 
-template <int BM, int BN, int WM, int WN, int PP = 0, int BKT = 32, int SL = 0, bool AT = false>
+template <int BM, int BN, int WM, int WN, int PP = 0, int BKT = 32, int SL = 0, bool AT = false,
+          bool BT = false>
 void launch_dl(const BrgemmParams& p, bool full, dim3 grid, hipStream_t stream) {
   switch (p.kind) {
     case TPP_BR_STRIDE:
-      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_STRIDE, PP, BKT, SL, AT>(p, grid, stream)
-           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_STRIDE, PP, BKT, SL, AT>(p, grid, stream);
+      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_STRIDE, PP, BKT, SL, AT, BT>(p, grid, stream)
+           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_STRIDE, PP, BKT, SL, AT, BT>(p, grid, stream);
       break;
     case TPP_BR_OFFSET:
-      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_OFFSET, PP, BKT, SL, AT>(p, grid, stream)
-           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_OFFSET, PP, BKT, SL, AT>(p, grid, stream);
+      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_OFFSET, PP, BKT, SL, AT, BT>(p, grid, stream)
+           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_OFFSET, PP, BKT, SL, AT, BT>(p, grid, stream);
       break;
     default:
-      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_ADDRESS, PP, BKT, SL, AT>(p, grid, stream)
-           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_ADDRESS, PP, BKT, SL, AT>(p, grid, stream);
+      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_ADDRESS, PP, BKT, SL, AT, BT>(p, grid, stream)
+           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_ADDRESS, PP, BKT, SL, AT, BT>(p, grid, stream);
       break;
   }
+}
+
+// The 64-k instances with each combination of transposed operands.
+template <int BM, int BN, int WM, int WN>
+void launch_dl64(const BrgemmParams& p, bool full, dim3 grid, hipStream_t stream) {
+  if (p.a_trans && p.b_trans) launch_dl<BM, BN, WM, WN, 0, 64, 0, true, true>(p, full, grid, stream);
+  else if (p.a_trans) launch_dl<BM, BN, WM, WN, 0, 64, 0, true, false>(p, full, grid, stream);
+  else if (p.b_trans) launch_dl<BM, BN, WM, WN, 0, 64, 0, false, true>(p, full, grid, stream);
+  else launch_dl<BM, BN, WM, WN, 0, 64>(p, full, grid, stream);
 }
 
 }  // namespace
@@ -498,8 +540,8 @@ bool dl_wave_grid(int32_t id, int& waves_m, int& waves_n) {
 
 hipError_t launch_brgemm_dl(const BrgemmParams& p, int32_t id, bool full, dim3 grid,
                             hipStream_t stream) {
-  // a transposed A only on the 64-k instances (the host never picks another for it)
-  if (p.a_trans && id != K_BF16_DL64K_256x256 && id != K_BF16_DL64K_128x128 &&
+  // transposed operands only on the 64-k instances (the host never picks another for them)
+  if ((p.a_trans || p.b_trans) && id != K_BF16_DL64K_256x256 && id != K_BF16_DL64K_128x128 &&
       id != K_BF16_DL64K_64x64)
     return hipErrorInvalidValue;
   switch (id) {
@@ -507,18 +549,9 @@ hipError_t launch_brgemm_dl(const BrgemmParams& p, int32_t id, bool full, dim3 g
     case K_BF16_DL_128x128: launch_dl<128, 128, 2, 2>(p, full, grid, stream); break;
     case K_BF16_DL_64x64: launch_dl<64, 64, 2, 2>(p, full, grid, stream); break;
     case K_BF16_PP_256x256: launch_dl<256, 256, 4, 2, 1>(p, full, grid, stream); break;
-    case K_BF16_DL64K_256x256:
-      p.a_trans ? launch_dl<256, 256, 4, 2, 0, 64, 0, true>(p, full, grid, stream)
-                : launch_dl<256, 256, 4, 2, 0, 64>(p, full, grid, stream);
-      break;
-    case K_BF16_DL64K_128x128:
-      p.a_trans ? launch_dl<128, 128, 2, 2, 0, 64, 0, true>(p, full, grid, stream)
-                : launch_dl<128, 128, 2, 2, 0, 64>(p, full, grid, stream);
-      break;
-    case K_BF16_DL64K_64x64:
-      p.a_trans ? launch_dl<64, 64, 2, 2, 0, 64, 0, true>(p, full, grid, stream)
-                : launch_dl<64, 64, 2, 2, 0, 64>(p, full, grid, stream);
-      break;
+    case K_BF16_DL64K_256x256: launch_dl64<256, 256, 4, 2>(p, full, grid, stream); break;
+    case K_BF16_DL64K_128x128: launch_dl64<128, 128, 2, 2>(p, full, grid, stream); break;
+    case K_BF16_DL64K_64x64: launch_dl64<64, 64, 2, 2>(p, full, grid, stream); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -822,8 +822,8 @@ void launch_vec(const BrgemmParams& p, bool full, dim3 grid, hipStream_t stream)
 
 hipError_t launch_brgemm(BrgemmParams& p, int32_t id, hipStream_t stream) {
   if (id < 0 || id >= K_COUNT) return hipErrorInvalidValue;
-  // a transposed A only on the 64-k direct-to-LDS instances
-  if (p.a_trans && id != K_BF16_DL64K_256x256 && id != K_BF16_DL64K_128x128 &&
+  // transposed operands only on the 64-k direct-to-LDS instances
+  if ((p.a_trans || p.b_trans) && id != K_BF16_DL64K_256x256 && id != K_BF16_DL64K_128x128 &&
       id != K_BF16_DL64K_64x64)
     return hipErrorInvalidValue;
   const int bm = kInfo[id].bm, bn = kInfo[id].bn;

@@ -24,6 +24,7 @@ struct BrgemmParams {
   int32_t c_bf16;  // 1: C is bf16, 0: C is fp32
   int32_t aligned; // host-verified: every A_i / B_i base is 16-byte aligned (stride kind)
   int32_t a_trans; // 1: A_i stored transposed (k contiguous per row, lda >= k)
+  int32_t b_trans; // 1: B_i stored transposed (n contiguous per k-row, ldb >= n)
   int32_t kind;    // tpp_br_kind
   int64_t count;
   int64_t stride_a, stride_b;

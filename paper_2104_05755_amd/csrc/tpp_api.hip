@@ -69,13 +69,14 @@ bool dl_offsets_fit(const tpp_brgemm_kernel_s& h, const tpp::BrgemmParams& p, in
   const int64_t m = h.desc.m, n = h.desc.n, k = h.desc.k, lda = h.desc.lda, ldb = h.desc.ldb;
   int64_t span_a, span_b;   // elements
   const int64_t block_a = p.a_trans ? m * lda + k : m + k * lda;   // one A_i block
+  const int64_t block_b = p.b_trans ? k * ldb + n : n * ldb + k;   // one B_i block
   if (p.fused) {
     if (p.a_step_m < 0 || p.b_step_n < 0) return false;
     span_a = (bm / m + 2) * p.a_step_m + block_a;
-    span_b = (bn / n + 2) * p.b_step_n + n * ldb + k;
+    span_b = (bn / n + 2) * p.b_step_n + block_b;
   } else {
     span_a = block_a;
-    span_b = n * ldb + k;
+    span_b = block_b;
   }
   return span_a < (int64_t(1) << 30) && span_b < (int64_t(1) << 30);   // bf16: 2 bytes each
 }
@@ -85,12 +86,13 @@ bool dl_offsets_fit(const tpp_brgemm_kernel_s& h, const tpp::BrgemmParams& p, in
 // steps multiples of 8); the tile shape is the largest that still gives two tiles per compute
 // unit (512 tiles on the 256 CUs).  Anything else takes the element-load instance.
 int32_t choose_kernel(const tpp_brgemm_kernel_s& h, const tpp::BrgemmParams& p) {
-  if (!h.bf16) return p.a_trans ? -1 : tpp::K_F32_GENERIC;
+  if (!h.bf16) return (p.a_trans || p.b_trans) ? -1 : tpp::K_F32_GENERIC;
   bool vec = h.vec_ok;
   if (p.fused) vec = vec && (p.a_step_m % 8 == 0) && (p.b_step_n % 8 == 0);
-  if (p.a_trans) {
-    // transposed A: the 64-k direct-to-LDS instances only (-1: unsupported)
-    if (!vec || h.desc.k % 64 != 0) return -1;
+  if (p.a_trans || p.b_trans) {
+    // transposed operands: the 64-k direct-to-LDS instances only (-1: unsupported); a
+    // transposed B moves 8 consecutive columns per 16-byte chunk
+    if (!vec || h.desc.k % 64 != 0 || (p.b_trans && h.desc.n % 8 != 0)) return -1;
     const int32_t ids[] = {tpp::K_BF16_DL64K_256x256, tpp::K_BF16_DL64K_128x128,
                            tpp::K_BF16_DL64K_64x64};
     if (const char* env = std::getenv("TPP_FORCE_KERNEL")) {
@@ -200,8 +202,8 @@ tpp_status launch(const tpp_brgemm_kernel_s* h, tpp::BrgemmParams& p, void* stre
   const int32_t id = choose_kernel(*h, p);
   if (id < 0)
     return fail(TPP_ERR_UNSUPPORTED,
-                "A_TRANS needs bf16, k %% 64 == 0, m, lda and element steps multiples of 8 and "
-                "operand spans below 2^30 elements");
+                "A_TRANS / B_TRANS need bf16, k %% 64 == 0, m, n, lda, ldb and element steps "
+                "multiples of 8 and operand spans below 2^30 elements");
   p.split = 1;
   p.ws = nullptr;
   std::unique_lock<std::mutex> work_hold;   // held from a work-buffer lookup to the launch
@@ -260,8 +262,10 @@ void fill_common(const tpp_brgemm_kernel_s* h, tpp::BrgemmParams& p) {
   p.m = d.m; p.n = d.n; p.k = d.k;
   p.lda = d.lda; p.ldb = d.ldb; p.ldc = d.ldc;
   p.beta = d.beta;
-  p.flags = d.flags & ~(uint32_t)TPP_LAYOUT_A_TRANS;   // the layout bit travels as a_trans
+  // the layout bits travel as a_trans / b_trans
+  p.flags = d.flags & ~(uint32_t)(TPP_LAYOUT_A_TRANS | TPP_LAYOUT_B_TRANS);
   p.a_trans = (d.flags & TPP_LAYOUT_A_TRANS) != 0;
+  p.b_trans = (d.flags & TPP_LAYOUT_B_TRANS) != 0;
   p.c_bf16 = d.c_type == TPP_DT_BF16;
   p.kind = d.kind;
   p.stride_a = d.stride_a;
@@ -321,8 +325,10 @@ tpp_status tpp_brgemm_dispatch(const tpp_brgemm_desc* desc, tpp_brgemm_handle* o
   if (d.m <= 0 || d.n <= 0 || d.k <= 0)
     return fail(TPP_ERR_INVALID_ARG, "m, n, k must be > 0 (got %d, %d, %d)", d.m, d.n, d.k);
   const bool a_trans = (d.flags & TPP_LAYOUT_A_TRANS) != 0;
-  if (d.lda < (a_trans ? d.k : d.m) || d.ldb < d.k || d.ldc < d.m)
-    return fail(TPP_ERR_INVALID_ARG, "leading dimension too small (lda %lld < m (k with A_TRANS), ldb %lld < k or ldc %lld < m)",
+  const bool b_trans = (d.flags & TPP_LAYOUT_B_TRANS) != 0;
+  if (d.lda < (a_trans ? d.k : d.m) || d.ldb < (b_trans ? d.n : d.k) || d.ldc < d.m)
+    return fail(TPP_ERR_INVALID_ARG, "leading dimension too small (lda %lld < m (k with A_TRANS), ldb %lld < k (n with "
+                "B_TRANS) or ldc %lld < m)",
                 (long long)d.lda, (long long)d.ldb, (long long)d.ldc);
   if (!valid_dtype(d.a_type) || !valid_dtype(d.b_type) || !valid_dtype(d.c_type) ||
       !valid_dtype(d.comp_type))
@@ -334,7 +340,7 @@ tpp_status tpp_brgemm_dispatch(const tpp_brgemm_desc* desc, tpp_brgemm_handle* o
   if (d.kind != TPP_BR_STRIDE && d.kind != TPP_BR_OFFSET && d.kind != TPP_BR_ADDRESS)
     return fail(TPP_ERR_INVALID_ARG, "unknown batch kind %d", d.kind);
   if (d.flags & ~(uint32_t)(TPP_EPI_BIAS | TPP_EPI_RELU | TPP_EPI_GELU_TANH | tpp::EPI_AUX_MASK |
-                            TPP_LAYOUT_A_TRANS))
+                            TPP_LAYOUT_A_TRANS | TPP_LAYOUT_B_TRANS))
     return fail(TPP_ERR_INVALID_ARG, "unknown flag bits 0x%x", d.flags);
   if ((d.flags & TPP_EPI_RELU) && (d.flags & TPP_EPI_GELU_TANH))
     return fail(TPP_ERR_INVALID_ARG, "RELU and GELU_TANH exclude each other");
@@ -363,7 +369,8 @@ tpp_status tpp_brgemm_dispatch(const tpp_brgemm_desc* desc, tpp_brgemm_handle* o
   static const char* kinds[] = {"stride", "offset", "address"};
   std::snprintf(h->name, sizeof h->name, "brgemm_%s_%s_m%d_n%d_k%d_%s%s%s", h->bf16 ? "bf16" : "f32",
                 d.c_type == TPP_DT_BF16 ? "bf16out" : "f32out", d.m, d.n, d.k, kinds[d.kind],
-                h->vec_ok ? "_vec" : "_generic", a_trans ? "_atrans" : "");
+                h->vec_ok ? "_vec" : "_generic", a_trans ? (b_trans ? "_atrans_btrans" : "_atrans")
+                                                 : (b_trans ? "_btrans" : ""));
   *out = h.get();
   cache().push_back(std::move(h));
   return ok();

@@ -326,3 +326,13 @@ def test_a_trans_dispatch_checks(tpp):
                               64 * 64)):
         with pytest.raises(tpp.TppError):
             tpp.tpp_brgemm_dispatch(bad)
+
+
+def test_b_trans_dispatch_checks(tpp):
+    # with B_TRANS the k-rows of B_i hold n entries: ldb >= n is required and suffices (ldb < k)
+    ok = tpp.make_desc(64, 64, 128, 64, 64, 64, "bf16", "f32", 0.0, "stride", 64 * 128, 128 * 64,
+                       flags=("b_trans",))
+    assert "_btrans" in tpp.tpp_brgemm_describe(tpp.tpp_brgemm_dispatch(ok))
+    with pytest.raises(tpp.TppError):
+        tpp.tpp_brgemm_dispatch(tpp.make_desc(64, 64, 128, 64, 32, 64, "bf16", "f32", 0.0,
+                                              "stride", 64 * 128, 128 * 64, flags=("b_trans",)))

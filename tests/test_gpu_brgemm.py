@@ -304,15 +304,21 @@ AT_CASES = {
 }
 
 
+@pytest.mark.parametrize("layout", ["a_trans", "b_trans", "both"])
 @pytest.mark.parametrize("kid", AT_KERNEL_IDS)
 @pytest.mark.parametrize("case", sorted(AT_CASES))
-def test_a_trans_matches_oracle(kid, case, monkeypatch):
+def test_a_trans_matches_oracle(kid, case, layout, monkeypatch):
+    # B blocks are read as transposed blocks with ldb = n in the same way (extent k * n)
     monkeypatch.setenv("TPP_FORCE_KERNEL", str(kid))
     wl = AT_CASES[case]()
     for c in wl.calls:
-        c.flags = set(c.flags) | {"a_trans"}
-        c.lda = c.k
-    say(f"a_trans kernel {kid} {case} {wl.name}")
+        if layout in ("a_trans", "both"):
+            c.flags = set(c.flags) | {"a_trans"}
+            c.lda = c.k
+        if layout in ("b_trans", "both"):
+            c.flags = set(c.flags) | {"b_trans"}
+            c.ldb = c.n
+    say(f"{layout} kernel {kid} {case} {wl.name}")
     got = run_gpu(wl)
     if wl.name == "mlp_block":
         h_ref, _ = run_oracle(wl, 0)

@@ -16,6 +16,7 @@ MUTANTS = {
     "transposed_a": ("(int64_t)row + (int64_t)p * d->lda", "(int64_t)p + (int64_t)row * d->lda"),
     "transposed_b": ("(int64_t)p + (int64_t)col * d->ldb", "(int64_t)col + (int64_t)p * d->ldb"),
     "a_trans_read_plain": ("(int64_t)row * d->lda + p", "(int64_t)row + (int64_t)p * d->lda"),
+    "b_trans_read_plain": ("(int64_t)p * d->ldb + col", "(int64_t)p + (int64_t)col * d->ldb"),
     "dropped_k_term": ("for (int32_t p = 0; p < d->k; ++p)", "for (int32_t p = 1; p < d->k; ++p)"),
     "dropped_pair": ("for (int64_t i = 0; i < count; ++i) {\n        for (int32_t p",
                      "for (int64_t i = 1; i < count; ++i) {\n        for (int32_t p"),

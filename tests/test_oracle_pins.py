@@ -416,3 +416,36 @@ def test_a_trans_layout_is_the_transposed_block(kind):
     with pytest.raises(ValueError):
         oracle.brgemm(oracle.Desc(m, n, k, k - 1, k, m, "bf16", "f32", 0.0, "stride", m * k, k * n,
                                   {"a_trans"}), trans, b, np.zeros(m * n, np.float32), count=1)
+
+
+@pytest.mark.parametrize("kind", ["stride", "offset", "address"])
+def test_b_trans_layout_is_the_transposed_block(kind):
+    """The transposed-B layout (element (p, c) of B_i at p * ldb + c) gives the bit-identical
+    result of the column-major layout holding numpy's transpose of each block; ldb below n is
+    rejected."""
+    rng = np.random.default_rng(62)
+    m, n, k, count = 24, 16, 32, 5
+    ldb_t = n + 5
+    blocks = rng.uniform(-1, 1, (count, n, k)).astype(np.float32)        # block i: B_i[p, c] = blocks[i, c, p]
+    plain = wk.bf16_bits(blocks.reshape(-1))                              # column-major, ldb = k
+    tr = np.zeros((count, k, ldb_t), np.float32)
+    tr[:, :, :n] = np.swapaxes(blocks, 1, 2)                              # k-row p holds B_i[p, :]
+    trans = wk.bf16_bits(tr.reshape(-1))
+    a = wk.bf16_bits(rng.uniform(-1, 1, count * m * k).astype(np.float32))
+    outs = []
+    for b, ldb, flags, step in ((plain, k, set(), k * n), (trans, ldb_t, {"b_trans"}, k * ldb_t)):
+        c = np.full(m * n, np.nan, np.float32)
+        d = oracle.Desc(m, n, k, m, ldb, m, "bf16", "f32", 0.0, kind,
+                        m * k if kind == "stride" else 0, step if kind == "stride" else 0, flags)
+        if kind == "stride":
+            oracle.brgemm(d, a, b, c, count=count)
+        elif kind == "offset":
+            oracle.brgemm(d, a, b, c, count=count, offs_a=np.arange(count) * m * k,
+                          offs_b=np.arange(count) * step)
+        else:
+            oracle.brgemm(d, a, b, c, idx_a=np.arange(count) * m * k, idx_b=np.arange(count) * step)
+        outs.append(c)
+    assert np.array_equal(outs[0], outs[1]) and not np.isnan(outs[0]).any()
+    with pytest.raises(ValueError):
+        oracle.brgemm(oracle.Desc(m, n, k, m, n - 1, m, "bf16", "f32", 0.0, "stride", m * k, k * n,
+                                  {"b_trans"}), a, trans, np.zeros(m * n, np.float32), count=1)
