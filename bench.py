@@ -472,8 +472,8 @@ def embedding_entry(args, torch, tpp, torch_io, wk, stream):
 
 def backward_entry(args, torch, tpp, torch_io, wk, stream):
     """The transformer MLP's backward pass at the headline size (see workloads.mlp_backward): the
-    two activation transposes, the four gradient BRGEMMs (the weights read transposed by dZ and
-    dX, GELU_inv fused into dZ) and
+    four gradient BRGEMMs (the weights read transposed by dZ and dX, the activations by dW2 and
+    dW1, GELU_inv fused into dZ) and
     the bias-gradient reduces, timed as one step over K steps (nothing between the launches), and
     each launch's mean duration inside the step from fence-free events.  The forward call that
     keeps the pre-activation (GEMM1 + SAVE_PREACT) runs once before and is timed on its own."""
@@ -489,11 +489,10 @@ def backward_entry(args, torch, tpp, torch_io, wk, stream):
     bw_calls = wl.calls[1:]
     bw_flops = sum(c.flops for c in bw_calls)
     launches = []
-    names = {"ht": "transpose H blocks", "xt": "transpose X blocks",
-             "dz": "dZ = (W2^T dY) * gelu'(Z)  [W2 read transposed, GELU_inv fused]",
-             "dw2": "dW2 = sum_tokens dY H^T", "p2": "db2 (sum over token blocks)",
+    names = {"dz": "dZ = (W2^T dY) * gelu'(Z)  [W2 read transposed, GELU_inv fused]",
+             "dw2": "dW2 = sum_tokens dY H^T  [H read transposed]", "p2": "db2 (sum over token blocks)",
              "db2": "db2 (sum within a block)", "dx": "dX = W1^T dZ  [W1 read transposed]",
-             "dw1": "dW1 = sum_tokens dZ X^T", "p1": "db1 (sum over token blocks)",
+             "dw1": "dW1 = sum_tokens dZ X^T  [X read transposed]", "p1": "db1 (sum over token blocks)",
              "db1": "db1 (sum within a block)"}
     out_name = lambda st: (st.c if isinstance(st, wk.Call) else
                            st.dst if isinstance(st, wk.TransformStep) else st.dst_x)

@@ -300,14 +300,14 @@ def mlp_backward(seed: int = 6, tokens: int = 8192, hidden: int = 1024,
     Forward (kept for back-propagation): Z = W1 X + b1 saved in ``z`` (bf16, H's layout), H =
     gelu(Z) in ``h``.  The incoming gradient dY (N(0,1), Y's layout [Nb][Hb][64n][64h]) then gives
       dZ  = (W2^T dY) * gelu'(Z)      B1: A = W2 blocks read transposed (A_TRANS), GELU_inv, bf16
-      dW2 = sum over tokens dY H^T    B2: A = dY, B = H blocks transposed, fp32
+      dW2 = sum over tokens dY H^T    B2: A = dY, B = H blocks read transposed (B_TRANS), fp32
       db2 = sum over tokens dY        two Reduce TPP calls (over token blocks, then within one)
       dX  = W1^T dZ                   B3: A = W1 blocks read transposed (A_TRANS), bf16
-      dW1 = sum over tokens dZ X^T    B4: A = dZ, B = X blocks transposed, fp32
+      dW1 = sum over tokens dZ X^T    B4: A = dZ, B = X blocks read transposed (B_TRANS), fp32
       db1 = sum over tokens dZ        two Reduce TPP calls
-    A weight block read with A_TRANS is its own transpose (k contiguous per row).  The transposed
-    B operands are batched Transform TPP calls (each 64 x 64 block transposed in place of the
-    block).  The weight gradients keep W's blocked layout, dX keeps X's.
+    A block read with A_TRANS or B_TRANS is its own transpose as stored (k contiguous per row of
+    W^T, n contiguous per k-row of H^T and X^T), so no transposed copy is made.  The weight
+    gradients keep W's blocked layout, dX keeps X's.
     """
     rng = np.random.default_rng(seed)
     nb, hb, ib = tokens // BLK, hidden // BLK, inter // BLK
@@ -321,7 +321,6 @@ def mlp_backward(seed: int = 6, tokens: int = 8192, hidden: int = 1024,
     nan32 = lambda shape: np.full(shape, np.nan, dtype=np.float32)
     arrays = dict(x=x, w1=w1, b1=b1, w2=w2, dy=dy,
                   z=nan16((nb, ib, BLK, BLK)), h=nan16((nb, ib, BLK, BLK)),
-                  ht=nan16((nb, ib, BLK, BLK)), xt=nan16((nb, hb, BLK, BLK)),
                   dz=nan16((nb, ib, BLK, BLK)), dx=nan16((nb, hb, BLK, BLK)),
                   dw1=nan32((ib, hb, BLK, BLK)), dw2=nan32((hb, ib, BLK, BLK)),
                   p1=nan32((ib * blk,)), p2=nan32((hb * blk,)),
@@ -333,8 +332,6 @@ def mlp_backward(seed: int = 6, tokens: int = 8192, hidden: int = 1024,
                grid=sq(gm=ib, gn=nb, a_step_m=hb * blk, b_step_n=hb * blk, c_step_m=blk,
                        c_step_n=ib * blk, bias_step_m=BLK),
                count=hb, a="w1", b="x", c="h", bias="b1", aux="z")
-    tr = lambda src, dst, g: TransformStep("transpose", BLK, BLK, BLK, BLK, "bf16", src, dst,
-                                           G=g, in_stride=blk, out_stride=blk)
     # dZ[nb][ib] (i x n) = gelu'(Z) * sum_hb W2[hb][ib]^T (i x h) dY[nb][hb] (h x n)
     b1c = Call(BLK, BLK, BLK, BLK, BLK, BLK, "bf16", "bf16", 0.0, "stride", ib * blk, blk,
                {"gelu_tanh_inv", "a_trans"}, G=ib * nb,
@@ -343,10 +340,10 @@ def mlp_backward(seed: int = 6, tokens: int = 8192, hidden: int = 1024,
                count=hb, a="w2", b="dy", c="dz", aux="z")
     # dW2[hb][ib] (h x i) = sum_nb dY[nb][hb] (h x n) H[nb][ib]^T (n x i)
     b2c = Call(BLK, BLK, BLK, BLK, BLK, BLK, "bf16", "f32", 0.0, "stride", hb * blk, ib * blk,
-               set(), G=hb * ib,
+               {"b_trans"}, G=hb * ib,
                grid=sq(gm=hb, gn=ib, a_step_m=blk, b_step_n=blk, c_step_m=ib * blk,
                        c_step_n=blk),
-               count=nb, a="dy", b="ht", c="dw2")
+               count=nb, a="dy", b="h", c="dw2")
     # dX[nb][hb] (h x n) = sum_ib W1[ib][hb]^T (h x i) dZ[nb][ib] (i x n)
     b3c = Call(BLK, BLK, BLK, BLK, BLK, BLK, "bf16", "bf16", 0.0, "stride", hb * blk, blk,
                {"a_trans"}, G=hb * nb,
@@ -355,17 +352,17 @@ def mlp_backward(seed: int = 6, tokens: int = 8192, hidden: int = 1024,
                count=ib, a="w1", b="dz", c="dx")
     # dW1[ib][hb] (i x h) = sum_nb dZ[nb][ib] (i x n) X[nb][hb]^T (n x h)
     b4c = Call(BLK, BLK, BLK, BLK, BLK, BLK, "bf16", "f32", 0.0, "stride", ib * blk, hb * blk,
-               set(), G=ib * hb,
+               {"b_trans"}, G=ib * hb,
                grid=sq(gm=ib, gn=hb, a_step_m=blk, b_step_n=blk, c_step_m=hb * blk,
                        c_step_n=blk),
-               count=nb, a="dz", b="xt", c="dw1")
+               count=nb, a="dz", b="x", c="dw1")
     # bias gradients: rows (feature within block, token within block, feature block) of the
     # gradient summed over the token blocks, then each 64 x 64 block's columns summed
     red = lambda src, fb, p, db: [
         ReduceStep(src, fb * blk, nb, fb * blk, "bf16", "sum", "cols", dst_x=p),
         ReduceStep(p, BLK, BLK, BLK, "f32", "sum", "cols", dst_x=db, G=fb, in_stride=blk,
                    out_stride=BLK)]
-    steps = [fwd, tr("h", "ht", nb * ib), tr("x", "xt", nb * hb), b1c, b2c, *red("dy", hb, "p2", "db2"), b3c, b4c,
+    steps = [fwd, b1c, b2c, *red("dy", hb, "p2", "db2"), b3c, b4c,
              *red("dz", ib, "p1", "db1")]
     return Workload("mlp_backward", arrays, [fwd, b1c, b2c, b3c, b4c], steps=steps)
 
