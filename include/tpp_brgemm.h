@@ -59,7 +59,7 @@ typedef enum {
 
 /* Epilogue bits.  RELU and GELU_TANH exclude each other.
  * The last three serve back-propagation (Table 1 pairs RELU and GELU with the inverses that the
- * backward pass uses; Sec. 5.2.2 builds the backward pass of the fully-connected layer from the
+ * backward pass uses; Sec. 5.1.6 builds the backward pass of the fully-connected layer from the
  * same TPPs).  They use an AUX tensor of C's type, shaped and laid out exactly as C (same ldc,
  * same per-instance offsets), and need tpp_brgemm_execute_batched_aux:
  *   SAVE_PREACT    with RELU or GELU_TANH: aux = the pre-activation beta C + sum + bias, rounded

@@ -14,7 +14,7 @@
  *   - Unary Reduce TPP, Table 1 and Sec. 3.1 (reduction-by-columns turns M x N into M x 1).
  *   - Unary Transform TPP, Table 1 and Sec. 3.1: Transpose, VNNI formatting and VNNI to
  *     VNNI-transpose (entry permutations; no arithmetic).
- *   - For back-propagation through the fused layers (Sec. 5.2.2 implements the backward pass of
+ *   - For back-propagation through the fused layers (Sec. 5.1.6 implements the backward pass of
  *     the fully-connected layer with TPPs as well): the RELU_inv / GELU_inv TPPs of Table 1 fused
  *     after the BRGEMM, the pre-activation kept by the forward call, and the loops of Alg. 6 around
  *     the Reduce and Transform TPPs.

@@ -182,6 +182,20 @@ struct EqProgram {
   EqInstr instr[EQ_MAX_NODES];
   EqArg arg[EQ_MAX_ARGS];
 };
+// Layout guards for the scalar-load reads above: every record, and every field the kernel reads
+// from a record, sits at a whole-dword offset, and the arrays start on dword boundaries.
+static_assert(sizeof(EqInstr) == 24 && sizeof(EqInstr) % 4 == 0, "EqInstr is 6 dwords");
+static_assert(offsetof(EqInstr, op) == 0 && offsetof(EqInstr, arity) == 4 &&
+                  offsetof(EqInstr, dst) == 8 && offsetof(EqInstr, src) == 12,
+              "EqInstr fields on dword boundaries");
+static_assert(sizeof(EqArg) == 24 && sizeof(EqArg) % 8 == 0, "EqArg is 3 qwords");
+static_assert(offsetof(EqArg, ptr) == 0 && offsetof(EqArg, ld) == 8 &&
+                  offsetof(EqArg, bf16) == 16 && offsetof(EqArg, bcast) == 20,
+              "EqArg fields on dword boundaries");
+static_assert(offsetof(EqProgram, instr) % 8 == 0 && offsetof(EqProgram, arg) % 8 == 0 &&
+                  offsetof(EqProgram, ldo) % 8 == 0 && offsetof(EqProgram, out) % 8 == 0,
+              "EqProgram arrays and 64-bit fields 8-byte aligned");
+static_assert(sizeof(EqProgram) % 8 == 0, "EqProgram a whole number of qwords");
 // nullptr on success, else what is wrong with the tree.
 const char* equation_plan(const tpp_eq_node* nodes, int32_t n_nodes, int32_t root,
                           tpp_eq_plan_node* plan, int32_t* n_tmps);

@@ -2,7 +2,7 @@
 // ([D1][D0] -> [D1/alpha][D0][alpha], the layout of Sec. 3.2.2) and VNNI to VNNI-transpose.
 //
 // All three only move entries, so they are bound by HBM traffic: each entry is read once and
-// written once.  The paper builds its transposes from register shuffle networks (Sec. 3.4.1);
+// written once.  The paper builds its transposes from register shuffle networks (Sec. 3.3.1);
 // here a workgroup stages a 64 x 64 tile in LDS, reading it along the input's contiguous
 // direction and writing it along the output's, so both sides are coalesced.
 //   - Transpose: 16-byte loads and stores when the operands allow (aligned bases, leading

@@ -3,7 +3,7 @@
 - The aux epilogue bits (SAVE_PREACT in the forward call, RELU_INV and GELU_TANH_INV after the
   data-gradient BRGEMM; Table 1's inverse activations) on every kernel instance.
 - The batched Transform and Reduce TPPs (the loops of Alg. 6 around a TPP).
-- The transformer MLP's backward pass (Sec. 5.2.2 builds the backward pass of the fully-connected
+- The transformer MLP's backward pass (Sec. 5.1.6 builds the backward pass of the fully-connected
   layer from the same TPPs): step by step on the oracle's own inputs, end to end, and at full size
   on sampled output blocks.
 Bars as for the forward path: bit-exact on small-integer data and for data movement, relative

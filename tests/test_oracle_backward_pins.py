@@ -2,7 +2,7 @@
 
 The inverse activations of Table 1 (RELU_inv, GELU_inv) fused after the BRGEMM, the
 pre-activation kept by a forward call, the loops of Alg. 6 around the Reduce and Transform TPPs,
-and the whole backward pass of the transformer MLP (Sec. 5.2.2 builds the back-propagation of the
+and the whole backward pass of the transformer MLP (Sec. 5.1.6 builds the back-propagation of the
 fully-connected layer from the same TPPs) are checked against what does not come from the
 oracle: torch autograd in float64, numpy, central differences, and exact integer arithmetic.
 """
