@@ -35,19 +35,26 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--settle", type=float, default=3.0,
+                    help="seconds of untimed headline steps before the counted warm-up, so that "
+                         "the clock has settled under load when the timed steps start")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target wall time of the oracle CPU baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-per-config", action="store_true")
     ap.add_argument("--traffic-run", action="store_true",
-                    help="only launch the calibration copy and the headline kernels a few times "
-                         "(for rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE passes), print nothing")
+                    help="only launch the calibration copy and the calls of --workloads three "
+                         "times each (for rocprofv3 --pmc counter passes), print nothing")
+    ap.add_argument("--workloads", default="mlp_block,gathered",
+                    help="comma-separated workloads of --traffic-run, in launch order (mlp_block, "
+                         "gathered, mlp_fc, conv3x3, fp32_single)")
     return ap.parse_args()
 
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 TRAFFIC_FILE = os.path.join(HERE, "profiles", "traffic_mlp_block_8192tok.txt")
 TRAFFIC_GATHERED_FILE = os.path.join(HERE, "profiles", "traffic_gathered_4096x128.txt")
+MFMA_FILE = os.path.join(HERE, "profiles", "mfma_mlp_block_8192tok.txt")
 COPY_BYTES = 512 << 20   # calibration copy: 512 MiB read, 512 MiB written
 
 
@@ -66,11 +73,9 @@ def kernel_source_sha() -> str:
     return h.hexdigest()[:16]
 
 
-def traffic_from_profile(call_index: int, path: str = TRAFFIC_FILE):
-    """HBM bytes per launch of call `call_index` from a committed rocprofv3 counter summary (the
-    headline calls by default): FETCH_SIZE and WRITE_SIZE of the kernel, each scaled by what the
-    same counter read for a copy of known size.  None when the summary is missing or the kernels
-    changed since."""
+def _profile_kv(path: str):
+    """key = value lines of a committed counter summary, or None when it is missing or was taken
+    on kernels other than the current sources."""
     if not os.path.exists(path):
         return None
     kv = {}
@@ -79,7 +84,55 @@ def traffic_from_profile(call_index: int, path: str = TRAFFIC_FILE):
             if "=" in line and not line.lstrip().startswith("#"):
                 k, v = line.split("=", 1)
                 kv[k.strip()] = v.strip()
-    if kv.get("kernel_source_sha") != kernel_source_sha():
+    return kv if kv.get("kernel_source_sha") == kernel_source_sha() else None
+
+
+def mfma_counters_from_profile(call_index: int, flops_per_launch: int):
+    """The MFMA counters of call `call_index` from the committed counter summary: bf16 MFMA work
+    (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512, which must equal the algorithmic FLOP), the MFMA busy
+    share (SQ_VALU_MFMA_BUSY_CYCLES over GRBM_GUI_ACTIVE x 1024 SIMDs) and the shader clock during
+    the launch (GRBM_GUI_ACTIVE over the launch's duration in the same run).  None when the
+    summary is missing or the kernels changed since."""
+    kv = _profile_kv(MFMA_FILE)
+    if kv is None:
+        return None
+    try:
+        mops = float(kv[f"call{call_index}_mfma_mops_bf16"])
+        busy = float(kv[f"call{call_index}_mfma_busy_cycles"])
+        gui = float(kv[f"call{call_index}_grbm_gui_active"])
+        dur_ns = float(kv[f"call{call_index}_duration_ns"])
+    except KeyError:
+        return None
+    out = {"mfma_flop": int(mops * 512), "mfma_flop_over_algorithmic": round(mops * 512 / flops_per_launch, 4),
+           "mfma_busy": round(busy / (gui * 1024), 4), "sclk_mhz": round(gui / dur_ns * 1e3, 0),
+           "source": os.path.relpath(MFMA_FILE, HERE)}
+    for extra in ("tcc_hit", "tcc_miss"):
+        if f"call{call_index}_{extra}" in kv:
+            out[extra] = int(float(kv[f"call{call_index}_{extra}"]))
+    if "tcc_hit" in out and "tcc_miss" in out:
+        out["tcc_hit_rate"] = round(out["tcc_hit"] / max(1, out["tcc_hit"] + out["tcc_miss"]), 4)
+    return out
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def traffic_from_profile(call_index: int, path: str = TRAFFIC_FILE):
+    """HBM bytes per launch of call `call_index` from a committed rocprofv3 counter summary (the
+    headline calls by default): FETCH_SIZE and WRITE_SIZE of the kernel, each scaled by what the
+    same counter read for a copy of known size.  None when the summary is missing or the kernels
+    changed since."""
+    kv = _profile_kv(path)
+    if kv is None:
         return None
     try:
         fetch = float(kv[f"call{call_index}_fetch_kib"]) * float(kv["fetch_scale"])
@@ -89,32 +142,31 @@ def traffic_from_profile(call_index: int, path: str = TRAFFIC_FILE):
     return int(round((fetch + write) * 1024))
 
 
-def traffic_run(torch, tpp, torch_io, wk, stream):
-    """Launch sequence for the counter passes: 3 copies of COPY_BYTES, then 3 of each headline
-    call, then 3 launches of the gathered workload (pointer lists into pools about the size of
-    the MALL)."""
+def traffic_run(torch, tpp, torch_io, wk, stream, workloads):
+    """Launch sequence for the counter passes: 3 copies of COPY_BYTES, then for each workload in
+    order 3 launches of each of its calls (the gathered workload's pointer lists reach into pools
+    about the size of the MALL)."""
     src = torch.empty(COPY_BYTES, dtype=torch.uint8, device="cuda")
     dst = torch.empty_like(src)
     src.fill_(1)
-    wl = wk.mlp_block()
-    dev = torch_io.upload(wl)
-    dcs = [torch_io.prepare(c, dev) for c in wl.calls]
     torch.cuda.synchronize()
     for _ in range(3):
         dst.copy_(src)
-    for _ in range(3):
-        for dc in dcs:
-            torch_io.launch(dc, stream)
     torch.cuda.synchronize()
-    del dev, dcs
-    torch.cuda.empty_cache()
-    gw = wk.CONFIGS[5]()
-    gdev = torch_io.upload(gw)
-    gdc = torch_io.prepare(gw.calls[0], gdev)
-    torch.cuda.synchronize()
-    for _ in range(3):
-        torch_io.launch(gdc, stream)
-    torch.cuda.synchronize()
+    del src, dst
+    make = {"mlp_block": wk.mlp_block, "gathered": wk.CONFIGS[5], "mlp_fc": wk.CONFIGS[2],
+            "conv3x3": wk.CONFIGS[3], "fp32_single": wk.CONFIGS[1]}
+    for name in workloads:
+        wl = make[name]()
+        dev = torch_io.upload(wl)
+        dcs = [torch_io.prepare(c, dev) for c in wl.calls]
+        torch.cuda.synchronize()
+        for _ in range(3):
+            for dc in dcs:
+                torch_io.launch(dc, stream)
+        torch.cuda.synchronize()
+        del dev, dcs
+        torch.cuda.empty_cache()
 
 
 def array_bytes(a) -> int:
@@ -148,6 +200,20 @@ def time_steps(fns, steps, warmup, torch):
         for f in fns:
             f()
     torch.cuda.synchronize()
+    return time.perf_counter() - t0
+
+
+def settle(fns, seconds, torch):
+    """Run whole steps, untimed, for about `seconds` (the clock ramps down under sustained MFMA
+    load over the first second or so); returns the time spent."""
+    if seconds <= 0:
+        return 0.0
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(20):
+            for f in fns:
+                f()
+        torch.cuda.synchronize()
     return time.perf_counter() - t0
 
 
@@ -288,7 +354,7 @@ def main():
     dev_name = torch.cuda.get_device_name(0)
     stream = tpp.current_stream()
     if args.traffic_run:
-        traffic_run(torch, tpp, torch_io, wk, stream)
+        traffic_run(torch, tpp, torch_io, wk, stream, [w for w in args.workloads.split(",") if w])
         return
 
     # ---------------- headline: transformer MLP block ----------------
@@ -296,11 +362,12 @@ def main():
     dev = torch_io.upload(wl)
     dcs = [torch_io.prepare(c, dev) for c in wl.calls]
     fns = [lambda dc=dc: torch_io.launch(dc, stream) for dc in dcs]
+    settle_s = settle(fns, args.settle, torch)
     elapsed = time_steps(fns, args.steps, args.warmup, torch)
     per = time_in_steps(fns, args.steps, torch, stream)
     flops_step = wl.flops
     value = flops_step * args.steps / elapsed / 1e12
-    kernel_names = [tpp.tpp_brgemm_describe(dc.handle) for dc in dcs]
+    kernel_names = [torch_io.describe(dc) for dc in dcs]
     # dominant kernel = the launch with the largest mean duration
     dom = int(np.argmax(per))
     dom_flops = wl.calls[dom].flops
@@ -310,6 +377,8 @@ def main():
                 "traffic": traffic_from_profile(dom), "traffic_unit": "bytes per launch",
                 "kernel": f"call {dom} ({'GEMM1 1024->4096 bias+GELU' if dom == 0 else 'GEMM2 4096->1024 bias'})",
                 "launch_ms": round(per[dom], 4), "flops_per_launch": dom_flops,
+                "kernel_instance": kernel_names[dom],
+                "counters": mfma_counters_from_profile(dom, dom_flops),
                 # the launches' in-step durations add up to about the step time of the
                 # event-free steps (a value well above 1 would mean the events timed gaps)
                 "launch_sum_over_step": round(sum(per) / (elapsed / args.steps * 1e3), 3)}
@@ -318,6 +387,7 @@ def main():
         "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(elapsed / args.steps * 1e3, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "settle_s": round(settle_s, 2),
         "data": "synthetic (seeded numpy draws, bf16-rounded; no dataset, random-init weights)",
         "config": {"workload": "transformer MLP block as blocked BRGEMM: 8192 tokens, "
                                "1024->4096 (bias+GELU-tanh) -> 1024 (bias), bf16 64x64 blocks",
@@ -578,7 +648,7 @@ def run_cpu_baseline(seconds: float, wl):
         n = min(call.G, max(2 * n, int(n * seconds / max(dt, 1e-3))))
     flops = 2 * call.m * call.n * call.k * call.count * len(sel)
     return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": oracle.max_threads(),
-            "kind": "oracle",
+            "cpu_model": cpu_model(), "kind": "oracle",
             "sample": f"{len(sel)} of {call.G} GEMM1 instances (64x64 output block, 16 pairs of "
                       f"64x64x64) of the headline workload, fp64 loops, {dt:.1f} s"}
 

@@ -187,9 +187,28 @@ tpp_status tpp_brgemm_execute_batched_aux(tpp_brgemm_handle h, const tpp_grid_st
  * dispatch, and is safe on NULL. */
 void tpp_brgemm_release(tpp_brgemm_handle h);
 
-/* Human-readable description of the kernel instance a handle selected (tile shape, load path).
- * Writes at most len bytes including the terminating NUL.  Host-only. */
+/* Human-readable description of a handle's descriptor (types, m / n / k, batch kind, whether
+ * the 16-byte load path is open to it).  The kernel instance is chosen per launch, from the grid
+ * as well: tpp_brgemm_describe_launch names it.  Writes at most len bytes including the
+ * terminating NUL.  Host-only. */
 tpp_status tpp_brgemm_describe(tpp_brgemm_handle h, char* buf, size_t len);
+
+/* The kernels one tpp_brgemm_execute_batched call with these arguments would launch, named as
+ * the profiler names them without namespace and parameter list, e.g.
+ * "brgemm_bf16_dl_kernel<256, 256, 4, 2, true, 0, true, 0, 64, 0, false, false>"; a reduction
+ * split over several workgroups adds " + " and its finishing kernel.  The choice is the launch
+ * path's own (same grid, counts, alignment of a and b); nothing is launched, allocated or read
+ * through the pointers, so it is host-only.  G == 0 gives "".  Writes at most len bytes
+ * including the terminating NUL.  Errors: those of tpp_brgemm_execute_batched's argument checks,
+ * INVALID_ARG for a NULL buf or len == 0. */
+tpp_status tpp_brgemm_describe_launch(tpp_brgemm_handle h, const tpp_grid_strided* grid,
+                                      int64_t G, const int64_t* d_a_off, const int64_t* d_b_off,
+                                      const int64_t* d_c_off, const int64_t* d_bias_off,
+                                      const void* a, const void* b, void* c, const float* bias,
+                                      int64_t count, const int64_t* d_offs_a,
+                                      const int64_t* d_offs_b, const int64_t* d_begin,
+                                      const void* const* d_ptrs_a, const void* const* d_ptrs_b,
+                                      char* buf, size_t len);
 
 /* Reduce TPP (Table 1; Sec. 3.1: reduction-by-columns turns an M x N input into M x 1).
  *   in: device, m x n column-major with leading dimension ld >= m, type in_type (F32 or BF16).

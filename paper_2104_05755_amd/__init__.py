@@ -81,6 +81,10 @@ _sig("tpp_brgemm_execute_batched_aux", _i32, _c_void_p, ctypes.POINTER(tpp_grid_
      _c_void_p, _i64, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p)
 _sig("tpp_brgemm_release", None, _c_void_p)
 _sig("tpp_brgemm_describe", _i32, _c_void_p, ctypes.c_char_p, ctypes.c_size_t)
+_sig("tpp_brgemm_describe_launch", _i32, _c_void_p, ctypes.POINTER(tpp_grid_strided), _i64,
+     _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p,
+     _i64, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, ctypes.c_char_p,
+     ctypes.c_size_t)
 _sig("tpp_reduce", _i32, _i32, _i32, _i64, _i32, _c_void_p, _i32, ctypes.c_uint32, _c_void_p,
      _c_void_p, _c_void_p)
 _sig("tpp_transform", _i32, _i32, _i32, _i32, _i64, _i64, _i32, _i32, _c_void_p, _c_void_p,
@@ -181,6 +185,19 @@ def tpp_brgemm_execute_batched_aux(h, grid, G, a_off, b_off, c_off, bias_off, a,
         h, ctypes.byref(g) if g is not None else None, G, _p(a_off), _p(b_off), _p(c_off),
         _p(bias_off), _p(a), _p(b), _p(c), _p(aux), _p(bias), count, _p(offs_a), _p(offs_b),
         _p(begin), _p(ptrs_a), _p(ptrs_b), stream), "tpp_brgemm_execute_batched_aux")
+
+
+def tpp_brgemm_describe_launch(h, grid, G, a_off, b_off, c_off, bias_off, a, b, c, bias, count,
+                               offs_a, offs_b, begin, ptrs_a, ptrs_b) -> str:
+    """Names of the kernels tpp_brgemm_execute_batched would launch with these arguments (as the
+    profiler names them).  Only the pointers' values are looked at: plain ints will do."""
+    g = _grid(grid)
+    buf = ctypes.create_string_buffer(512)
+    _check(_lib.tpp_brgemm_describe_launch(
+        h, ctypes.byref(g) if g is not None else None, G, _p(a_off), _p(b_off), _p(c_off),
+        _p(bias_off), _p(a), _p(b), _p(c), _p(bias), count, _p(offs_a), _p(offs_b), _p(begin),
+        _p(ptrs_a), _p(ptrs_b), buf, 512), "tpp_brgemm_describe_launch")
+    return buf.value.decode()
 
 
 def tpp_brgemm_release(h):

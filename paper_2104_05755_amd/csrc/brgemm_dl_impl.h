@@ -15,6 +15,9 @@
 #pragma once
 #include <hip/hip_runtime.h>
 
+#include <cstdio>
+#include <string>
+
 #include "brgemm_device.h"
 #include "internal.h"
 
@@ -481,36 +484,59 @@ void brgemm_bf16_dl_kernel(BrgemmParams p) {
                                             reinterpret_cast<float*>(lds), acc);
 }
 
+// The kernel's name as the profiler prints it (template arguments in declaration order).
+template <int BM, int BN, int WM, int WN, bool FULL, int KIND, bool ALIGNED, int PP, int BKT,
+          int SL, bool AT, bool BT>
+std::string dl_kernel_name() {
+  const auto tf = [](bool v) { return v ? "true" : "false"; };
+  char buf[160];
+  std::snprintf(buf, sizeof buf,
+                "brgemm_bf16_dl_kernel<%d, %d, %d, %d, %s, %d, %s, %d, %d, %d, %s, %s>", BM, BN, WM,
+                WN, tf(FULL), KIND, tf(ALIGNED), PP, BKT, SL, tf(AT), tf(BT));
+  return buf;
+}
+
+template <int BM, int BN, int WM, int WN, bool FULL, int KIND, bool ALIGNED, int PP, int BKT,
+          int SL, bool AT, bool BT>
+void launch_dl_kk(const BrgemmParams& p, dim3 grid, hipStream_t stream, std::string* name_out) {
+  if (name_out) {
+    *name_out = dl_kernel_name<BM, BN, WM, WN, FULL, KIND, ALIGNED, PP, BKT, SL, AT, BT>();
+    return;
+  }
+  hipLaunchKernelGGL(
+      (brgemm_bf16_dl_kernel<BM, BN, WM, WN, FULL, KIND, ALIGNED, PP, BKT, SL, AT, BT>), grid,
+      dim3(64 * WM * WN), 0, stream, p);
+}
+
 template <int BM, int BN, int WM, int WN, bool FULL, int KIND, int PP, int BKT, int SL, bool AT,
           bool BT>
-void launch_dl_k(const BrgemmParams& p, dim3 grid, hipStream_t stream) {
-  const dim3 block(64 * WM * WN);
+void launch_dl_k(const BrgemmParams& p, dim3 grid, hipStream_t stream, std::string* name_out) {
   if constexpr (KIND == TPP_BR_STRIDE) {
     if (p.aligned) {
-      hipLaunchKernelGGL((brgemm_bf16_dl_kernel<BM, BN, WM, WN, FULL, KIND, true, PP, BKT, SL, AT, BT>),
-                         grid, block, 0, stream, p);
+      launch_dl_kk<BM, BN, WM, WN, FULL, KIND, true, PP, BKT, SL, AT, BT>(p, grid, stream,
+                                                                         name_out);
       return;
     }
   }
-  hipLaunchKernelGGL((brgemm_bf16_dl_kernel<BM, BN, WM, WN, FULL, KIND, false, PP, BKT, SL, AT, BT>),
-                     grid, block, 0, stream, p);
+  launch_dl_kk<BM, BN, WM, WN, FULL, KIND, false, PP, BKT, SL, AT, BT>(p, grid, stream, name_out);
 }
 
 template <int BM, int BN, int WM, int WN, int PP = 0, int BKT = 32, int SL = 0, bool AT = false,
           bool BT = false>
-void launch_dl(const BrgemmParams& p, bool full, dim3 grid, hipStream_t stream) {
+void launch_dl(const BrgemmParams& p, bool full, dim3 grid, hipStream_t stream,
+               std::string* name_out) {
   switch (p.kind) {
     case TPP_BR_STRIDE:
-      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_STRIDE, PP, BKT, SL, AT, BT>(p, grid, stream)
-           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_STRIDE, PP, BKT, SL, AT, BT>(p, grid, stream);
+      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_STRIDE, PP, BKT, SL, AT, BT>(p, grid, stream, name_out)
+           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_STRIDE, PP, BKT, SL, AT, BT>(p, grid, stream, name_out);
       break;
     case TPP_BR_OFFSET:
-      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_OFFSET, PP, BKT, SL, AT, BT>(p, grid, stream)
-           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_OFFSET, PP, BKT, SL, AT, BT>(p, grid, stream);
+      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_OFFSET, PP, BKT, SL, AT, BT>(p, grid, stream, name_out)
+           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_OFFSET, PP, BKT, SL, AT, BT>(p, grid, stream, name_out);
       break;
     default:
-      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_ADDRESS, PP, BKT, SL, AT, BT>(p, grid, stream)
-           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_ADDRESS, PP, BKT, SL, AT, BT>(p, grid, stream);
+      full ? launch_dl_k<BM, BN, WM, WN, true, TPP_BR_ADDRESS, PP, BKT, SL, AT, BT>(p, grid, stream, name_out)
+           : launch_dl_k<BM, BN, WM, WN, false, TPP_BR_ADDRESS, PP, BKT, SL, AT, BT>(p, grid, stream, name_out);
       break;
   }
 }

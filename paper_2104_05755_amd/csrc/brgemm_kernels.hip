@@ -22,6 +22,9 @@
 //     each output element is stored once.
 #include <hip/hip_runtime.h>
 
+#include <cstdio>
+#include <string>
+
 #include "brgemm_device.h"
 #include "internal.h"
 
@@ -788,39 +791,61 @@ int kernel_tile_m(int32_t id) { return (id >= 0 && id < K_COUNT) ? kInfo[id].bm 
 int kernel_tile_n(int32_t id) { return (id >= 0 && id < K_COUNT) ? kInfo[id].bn : 64; }
 int kernel_k_step(int32_t id) { return (id >= 0 && id < K_COUNT) ? kInfo[id].kstep : 1; }
 
+bool kernel_full(int32_t id, const BrgemmParams& p) {
+  const int bm = kernel_tile_m(id), bn = kernel_tile_n(id);
+  return (p.k % BK == 0) && (p.vrows % bm == 0) && (p.vcols % bn == 0);
+}
+
+namespace {
+
+const char* tf(bool v) { return v ? "true" : "false"; }
+
+template <int BM, int BN, int WM, int WN, bool FULL, int KIND, bool ALIGNED>
+void launch_vec_kk(const BrgemmParams& p, dim3 grid, hipStream_t stream, std::string* name_out) {
+  if (name_out) {
+    char buf[128];
+    std::snprintf(buf, sizeof buf, "brgemm_bf16_vec_kernel<%d, %d, %d, %d, %s, %d, %s>", BM, BN,
+                  WM, WN, tf(FULL), KIND, tf(ALIGNED));
+    *name_out = buf;
+    return;
+  }
+  hipLaunchKernelGGL((brgemm_bf16_vec_kernel<BM, BN, WM, WN, FULL, KIND, ALIGNED>), grid,
+                     dim3(64 * WM * WN), 0, stream, p);
+}
+
 template <int BM, int BN, int WM, int WN, bool FULL, int KIND>
-void launch_vec_k(const BrgemmParams& p, dim3 grid, hipStream_t stream) {
-  const dim3 block(64 * WM * WN);
+void launch_vec_k(const BrgemmParams& p, dim3 grid, hipStream_t stream, std::string* name_out) {
   if constexpr (KIND == TPP_BR_STRIDE) {
     if (p.aligned) {
-      hipLaunchKernelGGL((brgemm_bf16_vec_kernel<BM, BN, WM, WN, FULL, KIND, true>), grid, block,
-                         0, stream, p);
+      launch_vec_kk<BM, BN, WM, WN, FULL, KIND, true>(p, grid, stream, name_out);
       return;
     }
   }
-  hipLaunchKernelGGL((brgemm_bf16_vec_kernel<BM, BN, WM, WN, FULL, KIND, false>), grid, block, 0,
-                     stream, p);
+  launch_vec_kk<BM, BN, WM, WN, FULL, KIND, false>(p, grid, stream, name_out);
 }
 
 template <int BM, int BN, int WM, int WN>
-void launch_vec(const BrgemmParams& p, bool full, dim3 grid, hipStream_t stream) {
+void launch_vec(const BrgemmParams& p, bool full, dim3 grid, hipStream_t stream,
+                std::string* name_out) {
   switch (p.kind) {
     case TPP_BR_STRIDE:
-      full ? launch_vec_k<BM, BN, WM, WN, true, TPP_BR_STRIDE>(p, grid, stream)
-           : launch_vec_k<BM, BN, WM, WN, false, TPP_BR_STRIDE>(p, grid, stream);
+      full ? launch_vec_k<BM, BN, WM, WN, true, TPP_BR_STRIDE>(p, grid, stream, name_out)
+           : launch_vec_k<BM, BN, WM, WN, false, TPP_BR_STRIDE>(p, grid, stream, name_out);
       break;
     case TPP_BR_OFFSET:
-      full ? launch_vec_k<BM, BN, WM, WN, true, TPP_BR_OFFSET>(p, grid, stream)
-           : launch_vec_k<BM, BN, WM, WN, false, TPP_BR_OFFSET>(p, grid, stream);
+      full ? launch_vec_k<BM, BN, WM, WN, true, TPP_BR_OFFSET>(p, grid, stream, name_out)
+           : launch_vec_k<BM, BN, WM, WN, false, TPP_BR_OFFSET>(p, grid, stream, name_out);
       break;
     default:
-      full ? launch_vec_k<BM, BN, WM, WN, true, TPP_BR_ADDRESS>(p, grid, stream)
-           : launch_vec_k<BM, BN, WM, WN, false, TPP_BR_ADDRESS>(p, grid, stream);
+      full ? launch_vec_k<BM, BN, WM, WN, true, TPP_BR_ADDRESS>(p, grid, stream, name_out)
+           : launch_vec_k<BM, BN, WM, WN, false, TPP_BR_ADDRESS>(p, grid, stream, name_out);
       break;
   }
 }
 
-hipError_t launch_brgemm(BrgemmParams& p, int32_t id, hipStream_t stream) {
+}  // namespace
+
+hipError_t launch_brgemm(BrgemmParams& p, int32_t id, hipStream_t stream, std::string* name_out) {
   if (id < 0 || id >= K_COUNT) return hipErrorInvalidValue;
   // transposed operands only on the 64-k direct-to-LDS instances
   if ((p.a_trans || p.b_trans) && id != K_BF16_DL64K_256x256 && id != K_BF16_DL64K_128x128 &&
@@ -830,13 +855,16 @@ hipError_t launch_brgemm(BrgemmParams& p, int32_t id, hipStream_t stream) {
   p.tiles_m = (p.vrows + bm - 1) / bm;
   p.tiles_n = (p.vcols + bn - 1) / bn;
   p.total_tiles = p.groups * p.tiles_m * p.tiles_n;
-  if (p.total_tiles <= 0) return hipSuccess;
+  if (p.total_tiles <= 0) {
+    if (name_out) *name_out = "";
+    return hipSuccess;
+  }
   const dim3 grid((unsigned)p.total_tiles), block(NT);
-  const bool full = (p.k % BK == 0) && (p.vrows % bm == 0) && (p.vcols % bn == 0);
+  const bool full = kernel_full(id, p);
   switch (id) {
-    case K_BF16_256x256: launch_vec<256, 256, 2, 4>(p, full, grid, stream); break;
-    case K_BF16_128x128: launch_vec<128, 128, 2, 2>(p, full, grid, stream); break;
-    case K_BF16_64x64: launch_vec<64, 64, 2, 2>(p, full, grid, stream); break;
+    case K_BF16_256x256: launch_vec<256, 256, 2, 4>(p, full, grid, stream, name_out); break;
+    case K_BF16_128x128: launch_vec<128, 128, 2, 2>(p, full, grid, stream, name_out); break;
+    case K_BF16_64x64: launch_vec<64, 64, 2, 2>(p, full, grid, stream, name_out); break;
     case K_BF16_DL_256x256:
     case K_BF16_DL_128x128:
     case K_BF16_DL_64x64:
@@ -844,22 +872,35 @@ hipError_t launch_brgemm(BrgemmParams& p, int32_t id, hipStream_t stream) {
     case K_BF16_DL64K_256x256:
     case K_BF16_DL64K_128x128:
     case K_BF16_DL64K_64x64: {
-      if (p.split <= 1) return launch_brgemm_dl(p, id, full, grid, stream);
+      if (p.split <= 1) return launch_brgemm_dl(p, id, full, grid, stream, name_out);
       // split over the stage list: chunk partials, then the finishing sum and epilogue
-      const hipError_t e =
-          launch_brgemm_dl(p, id, full, dim3((unsigned)(p.total_tiles * p.split)), stream);
+      const hipError_t e = launch_brgemm_dl(p, id, full, dim3((unsigned)(p.total_tiles * p.split)),
+                                            stream, name_out);
       if (e != hipSuccess) return e;
       int wm = 0, wn = 0;
       if (!dl_wave_grid(id, wm, wn)) return hipErrorInvalidValue;
+      if (name_out) {
+        *name_out += " + brgemm_dl_split_finish";
+        return hipSuccess;
+      }
       const int32_t per_tile = bm * bn / 4 / NT;
       hipLaunchKernelGGL(brgemm_dl_split_finish, dim3((unsigned)(p.total_tiles * per_tile)),
                          block, 0, stream, p, bm, bn, wm, wn, per_tile);
       break;
     }
     case K_BF16_GENERIC:
+      if (name_out) {
+        *name_out = "brgemm_bf16_kernel<64, 64, 2, 2, true>";
+        return hipSuccess;
+      }
       hipLaunchKernelGGL((brgemm_bf16_kernel<64, 64, 2, 2, true>), grid, block, 0, stream, p);
       break;
     default:
+      if (name_out) {
+        *name_out = p.split > 1 ? "brgemm_f32_kernel + brgemm_f32_split_finish"
+                                : "brgemm_f32_kernel";
+        return hipSuccess;
+      }
       if (p.split > 1) {
         hipLaunchKernelGGL(brgemm_f32_kernel, dim3((unsigned)(p.total_tiles * p.split)), block, 0,
                            stream, p);
@@ -870,7 +911,7 @@ hipError_t launch_brgemm(BrgemmParams& p, int32_t id, hipStream_t stream) {
       }
       break;
   }
-  return hipGetLastError();
+  return name_out ? hipSuccess : hipGetLastError();
 }
 
 int64_t f32_split_ws_floats(int32_t split, int64_t total_tiles) {

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <string>
+
 #include "tpp_brgemm.h"
 #include "tpp_embedding.h"
 #include "tpp_equation.h"
@@ -87,12 +89,19 @@ int64_t f32_split_ws_floats(int32_t split, int64_t total_tiles);
 int kernel_tile_n(int32_t id);   // tile columns
 int kernel_k_step(int32_t id);   // k granularity the instance needs (1 = any k)
 
-// Fill the tiling fields of p for kernel `id` and launch on `stream`.
-hipError_t launch_brgemm(BrgemmParams& p, int32_t id, hipStream_t stream);
+// Whether kernel `id` runs every tile of p complete (no row, column or k tail: the FULL
+// instances); p.vrows / p.vcols / p.k filled.
+bool kernel_full(int32_t id, const BrgemmParams& p);
+// Fill the tiling fields of p for kernel `id` and launch on `stream`.  With name_out set nothing
+// is launched: the same dispatch writes the names of the kernels it would launch, as the
+// profiler names them ("brgemm_bf16_dl_kernel<256, 256, 4, 2, true, 0, true, ...>", and
+// " + <finishing kernel>" for a split).
+hipError_t launch_brgemm(BrgemmParams& p, int32_t id, hipStream_t stream,
+                         std::string* name_out = nullptr);
 // The direct-to-LDS instances (brgemm_dl_kernels.hip); p's tiling fields already filled.
 // With p.split > 1, grid covers total_tiles * split workgroups writing partial tiles to p.ws.
 hipError_t launch_brgemm_dl(const BrgemmParams& p, int32_t id, bool full, dim3 grid,
-                            hipStream_t stream);
+                            hipStream_t stream, std::string* name_out = nullptr);
 // Wave layout (waves along m, along n) of a direct-to-LDS instance; false for other ids.
 bool dl_wave_grid(int32_t id, int& waves_m, int& waves_n);
 

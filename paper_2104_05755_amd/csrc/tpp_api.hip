@@ -186,7 +186,16 @@ tpp_status work_buffer(int purpose, void* stream, int64_t floats, float** out,
   return TPP_OK;
 }
 
-tpp_status launch(const tpp_brgemm_kernel_s* h, tpp::BrgemmParams& p, void* stream) {
+// What one launch runs: the kernel instance, the split of its stage (or pair) list and the
+// floats of work space the split's partial tiles need (0 without a split).  Host-only; no device
+// work and no allocation.
+struct LaunchPlan {
+  int32_t id = -1;
+  int32_t split = 1;
+  int64_t ws_floats = 0;
+};
+
+tpp_status plan_launch(const tpp_brgemm_kernel_s* h, tpp::BrgemmParams& p, LaunchPlan& lp) {
   // the kernels count stages (pairs x k-steps of 32 or 64) and tiles in 32 bits
   const int64_t ksteps = (h->desc.k + 31) / 32;
   if (p.kind != TPP_BR_ADDRESS && p.count * ksteps >= (1LL << 31))
@@ -204,9 +213,9 @@ tpp_status launch(const tpp_brgemm_kernel_s* h, tpp::BrgemmParams& p, void* stre
     return fail(TPP_ERR_UNSUPPORTED,
                 "A_TRANS / B_TRANS need bf16, k %% 64 == 0, m, n, lda, ldb and element steps "
                 "multiples of 8 and operand spans below 2^30 elements");
-  p.split = 1;
-  p.ws = nullptr;
-  std::unique_lock<std::mutex> work_hold;   // held from a work-buffer lookup to the launch
+  lp = LaunchPlan();
+  lp.id = id;
+  const int bm = tpp::kernel_tile_m(id), bn = tpp::kernel_tile_n(id);
   if (id == tpp::K_F32_GENERIC && p.kind != TPP_BR_ADDRESS && p.count >= 2 &&
       !(p.flags & tpp::EPI_AUX_MASK)) {
     // A grid of few 64 x 64 tiles leaves most of the GPU idle while each workgroup walks the
@@ -217,19 +226,15 @@ tpp_status launch(const tpp_brgemm_kernel_s* h, tpp::BrgemmParams& p, void* stre
       int64_t split = 256 / tiles;
       if (split > p.count) split = p.count;
       if (split > 1) {
-        p.split = (int32_t)split;
-        const tpp_status st =
-            work_buffer(WORK_SPLIT, stream, tpp::f32_split_ws_floats(p.split, tiles), &p.ws,
-                        work_hold);
-        if (st != TPP_OK) return st;
+        lp.split = (int32_t)split;
+        lp.ws_floats = tpp::f32_split_ws_floats(lp.split, tiles);
       }
     }
   }
-  if (p.split == 1 && tpp::kernel_k_step(id) > 1 && p.kind != TPP_BR_ADDRESS && p.count > 0) {
+  if (lp.split == 1 && tpp::kernel_k_step(id) > 1 && p.kind != TPP_BR_ADDRESS && p.count > 0) {
     // Direct-to-LDS kernel on a grid of fewer tiles than compute units: split every tile's
     // stage list into chunks reduced by separate workgroups (about 256 in all, at least 8 stages
     // each) and add the chunks in a finishing kernel.  TPP_SPLIT overrides the count.
-    const int bm = tpp::kernel_tile_m(id), bn = tpp::kernel_tile_n(id);
     const int64_t tiles = p.groups * ((p.vrows + bm - 1) / bm) * ((p.vcols + bn - 1) / bn);
     const int64_t stages = p.count * (h->desc.k / tpp::kernel_k_step(id));
     int64_t split = 1;
@@ -241,16 +246,51 @@ tpp_status launch(const tpp_brgemm_kernel_s* h, tpp::BrgemmParams& p, void* stre
     if (const char* env = std::getenv("TPP_SPLIT")) split = std::atoi(env);
     if (split > stages) split = stages;
     if (split > 1) {
-      p.split = (int32_t)split;
-      const tpp_status st =
-          work_buffer(WORK_SPLIT, stream, split * tiles * (int64_t)bm * bn, &p.ws, work_hold);
+      lp.split = (int32_t)split;
+      lp.ws_floats = split * tiles * (int64_t)bm * bn;
+    }
+  }
+  return TPP_OK;
+}
+
+// Work space given by the caller of launch(): `floats` floats at `ptr` (ptr may be null when
+// floats is 0).
+struct FixedWorkspace {
+  float* ptr;
+  int64_t floats;
+};
+
+// Plan and launch.  fixed == nullptr: a split's work space comes from the per-stream work buffer
+// (allocated or grown here); otherwise only from *fixed, and a plan that needs more is refused
+// without launching anything.
+tpp_status launch(const tpp_brgemm_kernel_s* h, tpp::BrgemmParams& p, void* stream,
+                  const FixedWorkspace* fixed = nullptr) {
+  LaunchPlan lp;
+  if (tpp_status s = plan_launch(h, p, lp)) return s;
+  p.split = lp.split;
+  p.ws = nullptr;
+  std::unique_lock<std::mutex> work_hold;   // held from a work-buffer lookup to the launch
+  if (lp.split > 1) {
+    if (fixed) {
+      if (lp.ws_floats > fixed->floats || !fixed->ptr)
+        return fail(TPP_ERR_UNSUPPORTED,
+                    "this launch splits its reduction %d ways and needs %lld floats of work "
+                    "space; the caller's holds %lld",
+                    lp.split, (long long)lp.ws_floats, (long long)fixed->floats);
+      p.ws = fixed->ptr;
+    } else {
+      const tpp_status st = work_buffer(WORK_SPLIT, stream, lp.ws_floats, &p.ws, work_hold);
       if (st != TPP_OK) return st;
     }
   }
-  if (std::getenv("TPP_LOG"))
+  if (std::getenv("TPP_LOG")) {
+    std::string name;
+    tpp::BrgemmParams q = p;
+    (void)tpp::launch_brgemm(q, lp.id, nullptr, &name);
     std::fprintf(stderr, "[tpp] %s: G=%lld vrows=%d vcols=%d fused=%d split=%d -> %s\n", h->name,
-                 (long long)p.groups, p.vrows, p.vcols, p.fused, p.split, tpp::kernel_name(id));
-  const hipError_t e = tpp::launch_brgemm(p, id, static_cast<hipStream_t>(stream));
+                 (long long)p.groups, p.vrows, p.vcols, p.fused, p.split, name.c_str());
+  }
+  const hipError_t e = tpp::launch_brgemm(p, lp.id, static_cast<hipStream_t>(stream));
   if (e != hipSuccess)
     return fail(TPP_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
@@ -449,13 +489,16 @@ tpp_status tpp_brgemm_execute_address(tpp_brgemm_handle h, const void* const* pt
 
 namespace {
 
-tpp_status execute_batched(tpp_brgemm_handle h, const tpp_grid_strided* grid, int64_t G,
+// The arguments of a batched call checked and resolved into p.  *empty is set (and p left
+// unfilled) for G == 0, which is a no-op.
+tpp_status prepare_batched(tpp_brgemm_handle h, const tpp_grid_strided* grid, int64_t G,
                            const int64_t* d_a_off, const int64_t* d_b_off, const int64_t* d_c_off,
                            const int64_t* d_bias_off, const void* a, const void* b, void* c,
                            void* aux, const float* bias, int64_t count, const int64_t* d_offs_a,
                            const int64_t* d_offs_b, const int64_t* d_begin,
                            const void* const* d_ptrs_a, const void* const* d_ptrs_b,
-                           void* stream) {
+                           tpp::BrgemmParams& p, bool* empty) {
+  *empty = false;
   const tpp_brgemm_desc& d = h->desc;
   if (G < 0) return fail(TPP_ERR_INVALID_ARG, "G < 0");
   if (grid) {
@@ -466,7 +509,10 @@ tpp_status execute_batched(tpp_brgemm_handle h, const tpp_grid_strided* grid, in
     if (d_a_off || d_b_off || d_c_off || d_bias_off)
       return fail(TPP_ERR_INVALID_ARG, "offset arrays given together with a strided grid");
   }
-  if (G == 0) return ok();
+  if (G == 0) {
+    *empty = true;
+    return ok();
+  }
   if (!c) return fail(TPP_ERR_INVALID_ARG, "NULL c");
   if (tpp_status s = check_bias(h, bias)) return s;
   if ((d.flags & tpp::EPI_AUX_MASK) && !aux)
@@ -480,7 +526,6 @@ tpp_status execute_batched(tpp_brgemm_handle h, const tpp_grid_strided* grid, in
     if (d.kind == TPP_BR_OFFSET && count > 0 && (!d_offs_a || !d_offs_b))
       return fail(TPP_ERR_INVALID_ARG, "NULL offset array");
   }
-  tpp::BrgemmParams p;
   fill_common(h, p);
   p.a = a; p.b = b; p.c = c; p.bias = bias;
   p.count = count;
@@ -511,7 +556,24 @@ tpp_status execute_batched(tpp_brgemm_handle h, const tpp_grid_strided* grid, in
     p.vrows = d.m;
     p.vcols = d.n;
   }
-  return launch(h, p, stream);
+  return TPP_OK;
+}
+
+tpp_status execute_batched(tpp_brgemm_handle h, const tpp_grid_strided* grid, int64_t G,
+                           const int64_t* d_a_off, const int64_t* d_b_off, const int64_t* d_c_off,
+                           const int64_t* d_bias_off, const void* a, const void* b, void* c,
+                           void* aux, const float* bias, int64_t count, const int64_t* d_offs_a,
+                           const int64_t* d_offs_b, const int64_t* d_begin,
+                           const void* const* d_ptrs_a, const void* const* d_ptrs_b,
+                           void* stream, const FixedWorkspace* fixed = nullptr) {
+  tpp::BrgemmParams p;
+  bool empty = false;
+  if (tpp_status s = prepare_batched(h, grid, G, d_a_off, d_b_off, d_c_off, d_bias_off, a, b, c,
+                                     aux, bias, count, d_offs_a, d_offs_b, d_begin, d_ptrs_a,
+                                     d_ptrs_b, p, &empty))
+    return s;
+  if (empty) return ok();
+  return launch(h, p, stream, fixed);
 }
 
 }  // namespace
@@ -544,6 +606,35 @@ tpp_status tpp_brgemm_execute_batched_aux(tpp_brgemm_handle h, const tpp_grid_st
   if (tpp_status s = check_handle(h)) return s;
   return execute_batched(h, grid, G, d_a_off, d_b_off, d_c_off, d_bias_off, a, b, c, aux, bias,
                          count, d_offs_a, d_offs_b, d_begin, d_ptrs_a, d_ptrs_b, stream);
+}
+
+tpp_status tpp_brgemm_describe_launch(
+    tpp_brgemm_handle h, const tpp_grid_strided* grid, int64_t G, const int64_t* d_a_off,
+    const int64_t* d_b_off, const int64_t* d_c_off, const int64_t* d_bias_off, const void* a,
+    const void* b, void* c, const float* bias, int64_t count, const int64_t* d_offs_a,
+    const int64_t* d_offs_b, const int64_t* d_begin, const void* const* d_ptrs_a,
+    const void* const* d_ptrs_b, char* buf, size_t len) {
+  if (tpp_status s = check_handle(h)) return s;
+  if (!buf || len == 0) return fail(TPP_ERR_INVALID_ARG, "NULL buffer");
+  buf[0] = 0;
+  // a stand-in for the aux tensor: only its presence is checked, nothing is launched
+  void* aux = (h->desc.flags & tpp::EPI_AUX_MASK) ? c : nullptr;
+  tpp::BrgemmParams p;
+  bool empty = false;
+  if (tpp_status s = prepare_batched(h, grid, G, d_a_off, d_b_off, d_c_off, d_bias_off, a, b, c,
+                                     aux, bias, count, d_offs_a, d_offs_b, d_begin, d_ptrs_a,
+                                     d_ptrs_b, p, &empty))
+    return s;
+  std::string name;
+  if (!empty) {
+    LaunchPlan lp;
+    if (tpp_status s = plan_launch(h, p, lp)) return s;
+    p.split = lp.split;
+    if (tpp::launch_brgemm(p, lp.id, nullptr, &name) != hipSuccess)
+      return fail(TPP_ERR_UNSUPPORTED, "no kernel instance for this launch");
+  }
+  std::snprintf(buf, len, "%s", name.c_str());
+  return ok();
 }
 
 }  // extern "C"

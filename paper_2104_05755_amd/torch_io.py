@@ -85,6 +85,16 @@ def prepare(call, dev: dict, device="cuda") -> DeviceCall:
     return dc
 
 
+def describe(dc: DeviceCall) -> str:
+    """The kernels launch(dc) runs, as the profiler names them."""
+    call = dc.call
+    a = dc.a if call.kind != "address" else None
+    b = dc.b if call.kind != "address" else None
+    return tpp.tpp_brgemm_describe_launch(
+        dc.handle, call.grid, call.G, dc.a_off, dc.b_off, dc.c_off, dc.bias_off, a, b, dc.c,
+        dc.bias, call.count, dc.offs_a, dc.offs_b, dc.begin, dc.ptrs_a, dc.ptrs_b)
+
+
 def launch(dc: DeviceCall, stream: Optional[int] = None):
     """One batched BRGEMM launch for the whole call (all G instances)."""
     call = dc.call

@@ -336,3 +336,68 @@ def test_b_trans_dispatch_checks(tpp):
     with pytest.raises(tpp.TppError):
         tpp.tpp_brgemm_dispatch(tpp.make_desc(64, 64, 128, 64, 32, 64, "bf16", "f32", 0.0,
                                               "stride", 64 * 128, 128 * 64, flags=("b_trans",)))
+
+
+# ----------------------------------------------------------------------------------------------
+# tpp_brgemm_describe_launch: the launch path's own kernel choice, named as the profiler names
+# the kernels, without launching (fake device addresses are never dereferenced)
+# ----------------------------------------------------------------------------------------------
+def _describe(tpp, call, a=1 << 40, b=1 << 41, c=1 << 42, bias=1 << 43):
+    h = tpp.tpp_brgemm_dispatch(
+        tpp.make_desc(call.m, call.n, call.k, call.lda, call.ldb, call.ldc, call.ab_type,
+                      call.c_type, call.beta, call.kind, call.stride_a, call.stride_b,
+                      sorted(call.flags)))
+    fake = 1 << 44
+    offs = fake if call.kind == "offset" else None
+    lists = fake if call.kind == "address" else None
+    explicit = fake if call.grid is None and call.kind != "address" else None
+    return tpp.tpp_brgemm_describe_launch(
+        h, call.grid, call.G, explicit, explicit, fake if call.grid is None else None, None,
+        a if call.kind != "address" else None, b if call.kind != "address" else None, c,
+        bias if call.bias else None, call.count, offs, offs, lists, lists, lists)
+
+
+def test_describe_launch_names_the_headline_instances(tpp):
+    import workloads as wk
+    g1, g2 = wk.mlp_block().calls
+    assert _describe(tpp, g1) == ("brgemm_bf16_dl_kernel<256, 256, 4, 2, true, 0, true, 0, 64, 0, "
+                                  "false, false>")
+    assert _describe(tpp, g2) == ("brgemm_bf16_dl_kernel<128, 128, 2, 2, true, 0, true, 0, 64, 0, "
+                                  "false, false>")
+    # a base off 16-byte alignment takes the unaligned instance of the same tile
+    assert _describe(tpp, g1, a=(1 << 40) + 2) == ("brgemm_bf16_dl_kernel<256, 256, 4, 2, true, 0, "
+                                                   "false, 0, 64, 0, false, false>")
+
+
+def test_describe_launch_other_workloads(tpp):
+    import workloads as wk
+    assert _describe(tpp, wk.fp32_single().calls[0]) == ("brgemm_f32_kernel + "
+                                                         "brgemm_f32_split_finish")
+    conv = _describe(tpp, wk.conv3x3().calls[0])
+    assert conv.startswith("brgemm_bf16_dl_kernel<64, 64, 2, 2, false, 1, false, 0, 64"), conv
+    gath = _describe(tpp, wk.gathered().calls[0])
+    assert gath.startswith("brgemm_bf16_dl_kernel<128, 128, 2, 2, true, 2, false, 0, 64"), gath
+    # the weight gradient of the MLP backward pass splits its stage list
+    bw = wk.mlp_backward()
+    dw = [c for c in bw.calls if c.c == "dw1"][0]
+    assert _describe(tpp, dw).endswith(" + brgemm_dl_split_finish")
+
+
+def test_describe_launch_empty_grid_and_errors(tpp):
+    import workloads as wk
+    call = wk.mlp_fc().calls[0]
+    h = tpp.tpp_brgemm_dispatch(
+        tpp.make_desc(call.m, call.n, call.k, call.lda, call.ldb, call.ldc, call.ab_type,
+                      call.c_type, call.beta, call.kind, call.stride_a, call.stride_b,
+                      sorted(call.flags)))
+    fake = 1 << 40
+    g0 = dict(call.grid, gm=0, gn=0)
+    assert tpp.tpp_brgemm_describe_launch(h, None, 0, None, None, None, None, fake, fake, fake,
+                                          fake, call.count, None, None, None, None, None) == ""
+    with pytest.raises(tpp.TppError):   # gm * gn != G
+        tpp.tpp_brgemm_describe_launch(h, call.grid, call.G + 1, None, None, None, None, fake,
+                                       fake, fake, fake, call.count, None, None, None, None, None)
+    with pytest.raises(tpp.TppError):   # bias missing
+        tpp.tpp_brgemm_describe_launch(h, call.grid, call.G, None, None, None, None, fake, fake,
+                                       fake, None, call.count, None, None, None, None, None)
+    del g0
