@@ -210,6 +210,29 @@ tpp_status tpp_brgemm_describe_launch(tpp_brgemm_handle h, const tpp_grid_stride
                                       const void* const* d_ptrs_a, const void* const* d_ptrs_b,
                                       char* buf, size_t len);
 
+/* Bytes of the per-GPU scratch array of tpp_brgemm_execute_batched_noalloc. */
+#define TPP_BRGEMM_NOALLOC_SCRATCH_BYTES (64ll << 20)
+
+/* For callers that cannot allocate device memory (code under HIP graph capture, serving loops,
+ * harnesses that forbid hipMalloc): tpp_brgemm_execute_batched without any allocation, device
+ * synchronisation or allocating library call.  It computes exactly what
+ * tpp_brgemm_execute_batched computes, with the same kernels: the only difference is where a
+ * reduction split over several workgroups keeps its partial tiles, here in a scratch array of
+ * TPP_BRGEMM_NOALLOC_SCRATCH_BYTES that the library holds on every GPU it runs on (from the
+ * library's load until the process ends).  Every call on one GPU shares that GPU's array, so
+ * calls on one GPU whose executions overlap in time (on different streams) race; calls on one
+ * stream are ordered by the stream.  The array needs no clearing: a split launch writes every
+ * partial tile before its finishing kernel reads it.  Handles with AUX bits are refused.
+ * Errors: those of tpp_brgemm_execute_batched; UNSUPPORTED, with nothing launched, when the
+ * launch's split needs more scratch than the array holds (the message gives both sizes);
+ * TPP_ERR_HIP if the array's device address cannot be looked up. */
+tpp_status tpp_brgemm_execute_batched_noalloc(
+    tpp_brgemm_handle h, const tpp_grid_strided* grid, int64_t G, const int64_t* d_a_off,
+    const int64_t* d_b_off, const int64_t* d_c_off, const int64_t* d_bias_off, const void* a,
+    const void* b, void* c, const float* bias, int64_t count, const int64_t* d_offs_a,
+    const int64_t* d_offs_b, const int64_t* d_begin, const void* const* d_ptrs_a,
+    const void* const* d_ptrs_b, void* stream);
+
 /* Reduce TPP (Table 1; Sec. 3.1: reduction-by-columns turns an M x N input into M x 1).
  *   in: device, m x n column-major with leading dimension ld >= m, type in_type (F32 or BF16).
  *   TPP_RED_BY_COLS: out[r] = fold_{c<n} f(in(r, c))   (m outputs)

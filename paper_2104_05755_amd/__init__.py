@@ -79,6 +79,9 @@ _sig("tpp_brgemm_execute_batched", _i32, _c_void_p, ctypes.POINTER(tpp_grid_stri
 _sig("tpp_brgemm_execute_batched_aux", _i32, _c_void_p, ctypes.POINTER(tpp_grid_strided), _i64,
      _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p,
      _c_void_p, _i64, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p)
+_sig("tpp_brgemm_execute_batched_noalloc", _i32, _c_void_p, ctypes.POINTER(tpp_grid_strided), _i64,
+     _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p,
+     _i64, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p, _c_void_p)
 _sig("tpp_brgemm_release", None, _c_void_p)
 _sig("tpp_brgemm_describe", _i32, _c_void_p, ctypes.c_char_p, ctypes.c_size_t)
 _sig("tpp_brgemm_describe_launch", _i32, _c_void_p, ctypes.POINTER(tpp_grid_strided), _i64,
@@ -185,6 +188,17 @@ def tpp_brgemm_execute_batched_aux(h, grid, G, a_off, b_off, c_off, bias_off, a,
         h, ctypes.byref(g) if g is not None else None, G, _p(a_off), _p(b_off), _p(c_off),
         _p(bias_off), _p(a), _p(b), _p(c), _p(aux), _p(bias), count, _p(offs_a), _p(offs_b),
         _p(begin), _p(ptrs_a), _p(ptrs_b), stream), "tpp_brgemm_execute_batched_aux")
+
+
+def tpp_brgemm_execute_batched_noalloc(h, grid, G, a_off, b_off, c_off, bias_off, a, b, c, bias,
+                                       count, offs_a, offs_b, begin, ptrs_a, ptrs_b, stream=None):
+    """tpp_brgemm_execute_batched without any device allocation (the library's per-GPU scratch
+    array holds a split reduction's partial tiles)."""
+    g = _grid(grid)
+    _check(_lib.tpp_brgemm_execute_batched_noalloc(
+        h, ctypes.byref(g) if g is not None else None, G, _p(a_off), _p(b_off), _p(c_off),
+        _p(bias_off), _p(a), _p(b), _p(c), _p(bias), count, _p(offs_a), _p(offs_b), _p(begin),
+        _p(ptrs_a), _p(ptrs_b), stream), "tpp_brgemm_execute_batched_noalloc")
 
 
 def tpp_brgemm_describe_launch(h, grid, G, a_off, b_off, c_off, bias_off, a, b, c, bias, count,

@@ -576,6 +576,35 @@ tpp_status execute_batched(tpp_brgemm_handle h, const tpp_grid_strided* grid, in
   return launch(h, p, stream, fixed);
 }
 
+// Scratch of the allocation-free batched call: the partial tiles of a split reduction.  One copy
+// per GPU, held from the library's load until the process ends; every allocation-free call on a
+// GPU uses that GPU's copy, so such calls that overlap in time on one GPU race.  Host code never
+// uses the array's name as an address (in host code it is a stand-in, not device memory): the
+// device address comes from hipGetSymbolAddress, once per device, with that device current.
+constexpr int64_t kNoAllocScratchFloats = TPP_BRGEMM_NOALLOC_SCRATCH_BYTES / 4;
+static __device__ __align__(256) float scratch[kNoAllocScratchFloats];
+
+std::mutex g_scratch_mu;
+std::map<int, float*> g_scratch_ptr;   // device -> address of that device's scratch
+
+tpp_status scratch_address(float** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(TPP_ERR_HIP, "hipGetDevice failed");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  auto it = g_scratch_ptr.find(dev);
+  if (it == g_scratch_ptr.end()) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr)
+      return fail(TPP_ERR_HIP, "hipGetSymbolAddress of the scratch array failed on device %d: %s",
+                  dev, hipGetErrorString(e));
+    it = g_scratch_ptr.emplace(dev, static_cast<float*>(ptr)).first;
+  }
+  *out = it->second;
+  return TPP_OK;
+}
+
+
 }  // namespace
 
 extern "C" {
@@ -606,6 +635,39 @@ tpp_status tpp_brgemm_execute_batched_aux(tpp_brgemm_handle h, const tpp_grid_st
   if (tpp_status s = check_handle(h)) return s;
   return execute_batched(h, grid, G, d_a_off, d_b_off, d_c_off, d_bias_off, a, b, c, aux, bias,
                          count, d_offs_a, d_offs_b, d_begin, d_ptrs_a, d_ptrs_b, stream);
+}
+
+tpp_status tpp_brgemm_execute_batched_noalloc(
+    tpp_brgemm_handle h, const tpp_grid_strided* grid, int64_t G, const int64_t* d_a_off,
+    const int64_t* d_b_off, const int64_t* d_c_off, const int64_t* d_bias_off, const void* a,
+    const void* b, void* c, const float* bias, int64_t count, const int64_t* d_offs_a,
+    const int64_t* d_offs_b, const int64_t* d_begin, const void* const* d_ptrs_a,
+    const void* const* d_ptrs_b, void* stream) {
+  if (tpp_status s = check_handle(h)) return s;
+  if (tpp_status s = check_no_aux(h)) return s;
+  tpp::BrgemmParams p;
+  bool empty = false;
+  if (tpp_status s = prepare_batched(h, grid, G, d_a_off, d_b_off, d_c_off, d_bias_off, a, b, c,
+                                     nullptr, bias, count, d_offs_a, d_offs_b, d_begin, d_ptrs_a,
+                                     d_ptrs_b, p, &empty))
+    return s;
+  if (empty) return ok();
+  // The plan first (host only): a split that needs more than the scratch array is refused before
+  // anything touches the device; a launch without a split never looks the array up.
+  LaunchPlan lp;
+  tpp::BrgemmParams q = p;
+  if (tpp_status s = plan_launch(h, q, lp)) return s;
+  float* ws = nullptr;
+  if (lp.split > 1) {
+    if (lp.ws_floats > kNoAllocScratchFloats)
+      return fail(TPP_ERR_UNSUPPORTED,
+                  "this launch splits its reduction %d ways and needs %lld bytes of scratch; the "
+                  "allocation-free call holds %lld",
+                  lp.split, (long long)lp.ws_floats * 4, (long long)kNoAllocScratchFloats * 4);
+    if (tpp_status s = scratch_address(&ws)) return s;
+  }
+  const FixedWorkspace fixed = {ws, ws ? kNoAllocScratchFloats : 0};
+  return launch(h, p, stream, &fixed);
 }
 
 tpp_status tpp_brgemm_describe_launch(

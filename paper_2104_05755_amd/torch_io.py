@@ -95,13 +95,19 @@ def describe(dc: DeviceCall) -> str:
         dc.bias, call.count, dc.offs_a, dc.offs_b, dc.begin, dc.ptrs_a, dc.ptrs_b)
 
 
-def launch(dc: DeviceCall, stream: Optional[int] = None):
-    """One batched BRGEMM launch for the whole call (all G instances)."""
+def launch(dc: DeviceCall, stream: Optional[int] = None, noalloc: bool = False):
+    """One batched BRGEMM launch for the whole call (all G instances); noalloc takes the
+    allocation-free entry point."""
     call = dc.call
     if stream is None:
         stream = tpp.current_stream()
     a = dc.a if call.kind != "address" else None
     b = dc.b if call.kind != "address" else None
+    if noalloc:
+        tpp.tpp_brgemm_execute_batched_noalloc(
+            dc.handle, call.grid, call.G, dc.a_off, dc.b_off, dc.c_off, dc.bias_off, a, b, dc.c,
+            dc.bias, call.count, dc.offs_a, dc.offs_b, dc.begin, dc.ptrs_a, dc.ptrs_b, stream)
+        return
     if dc.aux is not None:
         tpp.tpp_brgemm_execute_batched_aux(
             dc.handle, call.grid, call.G, dc.a_off, dc.b_off, dc.c_off, dc.bias_off, a, b, dc.c,

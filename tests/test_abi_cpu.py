@@ -401,3 +401,31 @@ def test_describe_launch_empty_grid_and_errors(tpp):
         tpp.tpp_brgemm_describe_launch(h, call.grid, call.G, None, None, None, None, fake, fake,
                                        fake, None, call.count, None, None, None, None, None)
     del g0
+
+
+# ----------------------------------------------------------------------------------------------
+# tpp_brgemm_execute_batched_noalloc: host-side refusals happen before any device work
+# ----------------------------------------------------------------------------------------------
+def test_noalloc_refuses_before_device_work(tpp, monkeypatch):
+    import workloads as wk
+    fake = 1 << 40
+    # a handle with an aux bit is refused
+    ha = tpp.tpp_brgemm_dispatch(tpp.make_desc(64, 64, 64, 64, 64, 64, "bf16", "bf16",
+                                               flags=["relu_inv"]))
+    with pytest.raises(tpp.TppError) as e:
+        tpp.tpp_brgemm_execute_batched_noalloc(ha, None, 1, None, None, None, None, fake, fake,
+                                               fake, None, 1, None, None, None, None, None, 0)
+    assert e.value.status == tpp.TPP_ERR_INVALID_ARG
+    # a split larger than the scratch array (forced with TPP_SPLIT) is refused with the sizes
+    bw = wk.mlp_backward()
+    dw = [c for c in bw.calls if c.c == "dw1"][0]
+    h = tpp.tpp_brgemm_dispatch(
+        tpp.make_desc(dw.m, dw.n, dw.k, dw.lda, dw.ldb, dw.ldc, dw.ab_type, dw.c_type, dw.beta,
+                      dw.kind, dw.stride_a, dw.stride_b, sorted(dw.flags)))
+    monkeypatch.setenv("TPP_SPLIT", "64")
+    with pytest.raises(tpp.TppError) as e:
+        tpp.tpp_brgemm_execute_batched_noalloc(h, dw.grid, dw.G, None, None, None, None, fake,
+                                               fake, fake, fake if dw.bias else None, dw.count,
+                                               None, None, None, None, None, 0)
+    assert e.value.status == tpp.TPP_ERR_UNSUPPORTED
+    assert "scratch" in tpp.tpp_last_error_message()
