@@ -44,8 +44,9 @@ def _jobs() -> int:
     return max(1, min(n, 16))
 
 
-def build(verbose: bool = False, extra: list | None = None) -> str:
-    """Compile every HIP source of the library for gfx950 and link the shared library."""
+def build(verbose: bool = False, extra: list | None = None, out: str = LIB) -> str:
+    """Compile every HIP source of the library for gfx950 and link the shared library at `out`
+    (`extra`: more hipcc options for every source, e.g. -D settings of the kernels' tunables)."""
     os.makedirs(OBJDIR, exist_ok=True)
     inc = ["-I", os.path.join(ROOT, "include"), "-I", os.path.join(PKG, "csrc")]
     tag = f".{os.getpid()}"
@@ -72,19 +73,19 @@ def build(verbose: bool = False, extra: list | None = None) -> str:
             if verbose and r.stderr.strip():
                 print(r.stderr[-4000:])
             objs.append(obj)
-        tmp = LIB + f".tmp{os.getpid()}"
+        tmp = out + f".tmp{os.getpid()}"
         cmd = [hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp]
         if verbose:
             print(" ".join(cmd), flush=True)
         r = subprocess.run(cmd, capture_output=True, text=True)
         if r.returncode != 0:
             raise RuntimeError(f"hipcc link failed ({r.returncode}):\n{r.stderr[-6000:]}")
-        os.replace(tmp, LIB)
+        os.replace(tmp, out)
     finally:
         for _, obj, _ in results:
             if os.path.exists(obj):
                 os.remove(obj)
-    return LIB
+    return out
 
 
 if __name__ == "__main__":

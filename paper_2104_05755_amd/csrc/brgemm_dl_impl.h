@@ -72,6 +72,62 @@ __device__ __forceinline__ void buffer_load_lds16(i32x4 rsrc, uint32_t voff, cha
       : "memory");
 }
 
+// N consecutive 16-byte buffer -> LDS wave-loads: load r reads rsrc base + voff[r] and lands at
+// lds_addr + 1024 r.  One asm block sets M0 once and steps it by 1 KB between the loads, so a
+// wave-load costs two scalar instructions instead of the nine of a separate buffer_load_lds16
+// (M0 save, set, wait state, restore, and the null check of the LDS pointer's address-space
+// conversion).  The scalar unit is shared by the compute unit's waves, and every wave copies its
+// share of a stage right after the same barrier: measured per wave and stage, issuing the copies
+// of the 256 x 256 tile took ~980 cycles one by one and ~845 in blocks, of the 128 x 128 tile 758
+// and 587.  (The rest is the copies themselves: each direct-to-LDS load takes ~100 cycles to
+// issue while all waves copy.)  One wait state after each M0 write, as the ISA requires before an
+// LDS-DMA load.
+#define TPP_LDS16_FIRST "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %[lds]\n\ts_nop 0\n\t"
+#define TPP_LDS16_LOAD(i) "buffer_load_dwordx4 %[v" #i "], %[rsrc], 0 offen lds\n\t"
+#define TPP_LDS16_STEP "s_add_u32 m0, m0, 0x400\n\ts_nop 0\n\t"
+#define TPP_LDS16_LAST "s_nop 0\n\ts_mov_b32 m0, %0"
+template <int N>
+__device__ __forceinline__ void buffer_load_lds16_block(i32x4 rsrc, const uint32_t* voff,
+                                                        uint32_t lds_addr) {
+  uint32_t saved;
+  if constexpr (N == 1) {
+    asm volatile(TPP_LDS16_FIRST TPP_LDS16_LOAD(0) TPP_LDS16_LAST
+                 : "=&s"(saved)
+                 : [v0] "v"(voff[0]), [rsrc] "s"(rsrc), [lds] "s"(lds_addr)
+                 : "memory", "scc");
+  } else if constexpr (N == 2) {
+    asm volatile(TPP_LDS16_FIRST TPP_LDS16_LOAD(0) TPP_LDS16_STEP TPP_LDS16_LOAD(1) TPP_LDS16_LAST
+                 : "=&s"(saved)
+                 : [v0] "v"(voff[0]), [v1] "v"(voff[1]), [rsrc] "s"(rsrc), [lds] "s"(lds_addr)
+                 : "memory", "scc");
+  } else if constexpr (N == 4) {
+    asm volatile(TPP_LDS16_FIRST TPP_LDS16_LOAD(0) TPP_LDS16_STEP TPP_LDS16_LOAD(1)
+                     TPP_LDS16_STEP TPP_LDS16_LOAD(2) TPP_LDS16_STEP TPP_LDS16_LOAD(3)
+                         TPP_LDS16_LAST
+                 : "=&s"(saved)
+                 : [v0] "v"(voff[0]), [v1] "v"(voff[1]), [v2] "v"(voff[2]), [v3] "v"(voff[3]),
+                   [rsrc] "s"(rsrc), [lds] "s"(lds_addr)
+                 : "memory", "scc");
+  } else if constexpr (N == 8) {
+    asm volatile(TPP_LDS16_FIRST TPP_LDS16_LOAD(0) TPP_LDS16_STEP TPP_LDS16_LOAD(1)
+                     TPP_LDS16_STEP TPP_LDS16_LOAD(2) TPP_LDS16_STEP TPP_LDS16_LOAD(3)
+                         TPP_LDS16_STEP TPP_LDS16_LOAD(4) TPP_LDS16_STEP TPP_LDS16_LOAD(5)
+                             TPP_LDS16_STEP TPP_LDS16_LOAD(6) TPP_LDS16_STEP TPP_LDS16_LOAD(7)
+                                 TPP_LDS16_LAST
+                 : "=&s"(saved)
+                 : [v0] "v"(voff[0]), [v1] "v"(voff[1]), [v2] "v"(voff[2]), [v3] "v"(voff[3]),
+                   [v4] "v"(voff[4]), [v5] "v"(voff[5]), [v6] "v"(voff[6]), [v7] "v"(voff[7]),
+                   [rsrc] "s"(rsrc), [lds] "s"(lds_addr)
+                 : "memory", "scc");
+  } else {
+    static_assert(N == 1 || N == 2 || N == 4 || N == 8, "block sizes 1, 2, 4, 8");
+  }
+}
+#undef TPP_LDS16_FIRST
+#undef TPP_LDS16_LOAD
+#undef TPP_LDS16_STEP
+#undef TPP_LDS16_LAST
+
 // XOR swizzle of the 16-byte k-chunks of a B-panel column (COLB = 2 BK bytes): the 16 columns a
 // ds_read_b128 serves per cycle land in 16 distinct 16-byte bank groups of a 256-byte row.
 template <int BK>
@@ -296,6 +352,58 @@ void brgemm_bf16_dl_kernel(BrgemmParams p) {
     for (int r = 0; r < LPS; ++r) issue_load(r);
     stage_end();
   };
+  // The same issue with each operand's wave-loads in one block (buffer_load_lds16_block), and for
+  // the stride kind the stage's byte addresses advanced by additions: a pair's A / B base moves
+  // by the stride, a stage within the pair by the k-step (no 64-bit multiplies per stage).
+  const uint32_t lds_u32 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(LDS_AS char*)lds);
+  auto uni64 = [](uint64_t v) {
+    return ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(v >> 32)) << 32) |
+           (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)v);
+  };
+  const uint64_t a_kstep = (uint64_t)DL_BK * (AT ? 1 : p.lda) * 2;
+  const uint64_t b_kstep = (uint64_t)DL_BK * (BT ? p.ldb : 1) * 2;
+  uint64_t sa_pair = 0, sb_pair = 0, sa = 0, sb = 0;
+  if constexpr (KIND == TPP_BR_STRIDE) {
+    sa_pair = uni64(reinterpret_cast<uint64_t>(static_cast<const uint16_t*>(p.a) + in.a + base_a +
+                                               (int64_t)iss_i * p.stride_a));
+    sb_pair = uni64(reinterpret_cast<uint64_t>(static_cast<const uint16_t*>(p.b) + in.b + base_b +
+                                               (int64_t)iss_i * p.stride_b));
+    sa = sa_pair + (uint64_t)(iss_kk / DL_BK) * a_kstep;
+    sb = sb_pair + (uint64_t)(iss_kk / DL_BK) * b_kstep;
+  }
+  auto issue_block = [&]() {
+    if constexpr (KIND == TPP_BR_STRIDE && ALIGNED) {
+      const uint32_t slot_u32 = lds_u32 + (uint32_t)(iss_s % SLOTS) * SLOT;
+      buffer_load_lds16_block<A_PER_W>(raw_buffer(reinterpret_cast<const void*>(sa)), la,
+                                       slot_u32 + wave * A_PER_W * 1024);
+      buffer_load_lds16_block<B_PER_W>(raw_buffer(reinterpret_cast<const void*>(sb)), lb,
+                                       slot_u32 + A_BYTES + wave * B_PER_W * 1024);
+      ++iss_s;
+      iss_kk += DL_BK;
+      if (iss_kk == p.k) {
+        iss_kk = 0;
+        ++iss_i;
+        sa_pair += (uint64_t)p.stride_a * 2;
+        sb_pair += (uint64_t)p.stride_b * 2;
+        sa = sa_pair;
+        sb = sb_pair;
+      } else {
+        sa += a_kstep;
+        sb += b_kstep;
+      }
+    } else {
+      stage_begin();
+      if (ALIGNED || aligned) {
+        const uint32_t slot_u32 = lds_u32 + (uint32_t)(iss_s % SLOTS) * SLOT;
+        buffer_load_lds16_block<A_PER_W>(ra, la, slot_u32 + wave * A_PER_W * 1024);
+        buffer_load_lds16_block<B_PER_W>(rb, lb, slot_u32 + A_BYTES + wave * B_PER_W * 1024);
+      } else {
+#pragma unroll
+        for (int r = 0; r < LPS; ++r) issue_load(r);
+      }
+      stage_end();
+    }
+  };
 
   f32x16 acc[TM][TN];
 #pragma unroll
@@ -401,14 +509,16 @@ void brgemm_bf16_dl_kernel(BrgemmParams p) {
   auto lmin = [](int32_t a, int32_t b) { return a < b ? a : b; };
 
   const int32_t pre = stages < SLOTS - 1 ? stages : SLOTS - 1;
-  for (int32_t s = 0; s < pre; ++s) issue();
+  for (int32_t s = 0; s < pre; ++s) {
+    if constexpr (SCHED == 0) issue_block(); else issue();
+  }
   if constexpr (SCHED == 0) {
     for (int32_t s = 0; s < stages; ++s) {
       // This wave's loads of stage s are done once at most the later stages' loads are pending;
       // the barrier then publishes every wave's stage s and retires everyone's reads of s - 1.
       wait_loads(lmin(stages - 1 - s, SLOTS - 2));
       lds_barrier();
-      if (s + SLOTS - 1 < stages) issue();   // stage s + SLOTS - 1 refills the slot of s - 1
+      if (s + SLOTS - 1 < stages) issue_block();   // stage s + SLOTS - 1 refills the slot of s - 1
       compute(s % SLOTS);
     }
   } else if constexpr (SCHED == 1) {
