@@ -53,7 +53,8 @@ __device__ __forceinline__ void store_group(const BrgemmParams& p, const Instanc
   const float* bias = p.bias;
   const bool has_bias = (p.flags & TPP_EPI_BIAS) != 0;
   if (!GENERIC) {
-    // m % 8 == 0: the four rows R0..R0+3 are valid together and belong to one instance.
+    // m % 4 == 0 and R0 % 4 == 0: the four rows R0..R0+3 are valid together and belong to one
+    // instance.
     int64_t row_off, bias_idx;
     if (p.fused) {
       if (R0 >= p.vrows) return;
@@ -606,16 +607,41 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void brgemm_bf16_vec_kernel
 }
 
 // ---------------------------------------------------------------------------------------------
-// fp32 kernel: 64x64 tile, 4 waves of 32x32, v_mfma_f32_32x32x2f32, element loads with full
-// bounds checks (any shape, leading dimension or alignment).
+// fp32 kernel: 64x64 tile, 4 waves of 32x32, v_mfma_f32_32x32x2f32, stages of 32 k.
+//   - VEC (stride kind; m, k, lda, ldb and the grid steps multiples of 4, every pair base 16-byte
+//     aligned and every block within 2 GB of its base, all checked on the host per launch): each
+//     thread moves two 16-byte vectors of A (4 rows of one k-column) and two of B (4 k of one
+//     column) per stage with buffer loads; otherwise element loads.  Out-of-range rows, columns
+//     and k read as zero (any shape).
+//   - Two LDS buffers (both panels k-major, rows padded against bank conflicts) fed from a ring
+//     of four register sets: the global loads of the next four stages are in flight while the
+//     MFMAs run on the current buffer; one barrier per stage.
+//   - Split launches (few tiles, long pair lists): workgroup b reduces chunk b % split of tile
+//     b / split's pair list into a partial tile of the work space, and brgemm_f32_split_finish
+//     adds the chunks and applies the epilogue.  (Finishing in the same launch, by the last
+//     workgroup of a tile to arrive at a per-tile counter, measured 3.4 us slower per call on
+//     the single 64 x 64 instance: the returning device-scope atomic and one workgroup loading
+//     every chunk cost more than a second launch queued behind the first.)
 // ---------------------------------------------------------------------------------------------
 constexpr int F_BM = 64, F_BN = 64, F_BK = 32;
-constexpr int F_AROW = F_BM + 4;   // A panel stored k-major: As[k][m]
-constexpr int F_BROW = F_BK + 1;   // B panel stored n-major: Bs[n][k], odd stride
+constexpr int F_ROW = F_BM + 4;   // padded k-row of a panel (floats)
+constexpr int F_RING = 4;         // stages of global loads in flight (register sets)
+// Buffer descriptors of the vector path: F_RANGE bytes addressable from a pair base (the host
+// checks that every block fits), offsets at F_OUT_OF_RANGE and beyond read as zero.
+constexpr int32_t F_RANGE = 0x7fff0000;
+constexpr int32_t F_OUT_OF_RANGE = F_RANGE;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t f32_rsrc(const float* base) {
+  // pair bases are uniform over the workgroup: keep the descriptor in scalar registers
+  const uint64_t b = reinterpret_cast<uint64_t>(base);
+  const uint64_t u = (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)b) |
+                     ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(b >> 32)) << 32);
+  return __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void*>(u), 0, F_RANGE, 0x00020000);
+}
 
+template <bool VEC>
 __global__ __launch_bounds__(NT) void brgemm_f32_kernel(BrgemmParams p) {
-  __shared__ float As[F_BK * F_AROW];
-  __shared__ float Bs[F_BN * F_BROW];
+  __shared__ __attribute__((aligned(16))) float As[2][F_BK * F_ROW];
+  __shared__ __attribute__((aligned(16))) float Bs[2][F_BK * F_ROW];
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int wm = wave & 1, wn = wave >> 1;
   // With a split, workgroup bid takes chunk bid % split of tile bid / split's pair list.
@@ -629,101 +655,198 @@ __global__ __launch_bounds__(NT) void brgemm_f32_kernel(BrgemmParams p) {
   const int32_t ksteps = (p.k + F_BK - 1) / F_BK;
   const int64_t stages = (pair_hi - pair_lo) * ksteps;
 
-  // A element e = t + 256*j: row t%64 (fixed), k = t/64 + 4*j.
-  const int a_r = t & 63, a_k0 = t >> 6;
-  int64_t a_off = 0;
-  const bool a_ok = row_in_a(p, tc.row0 + a_r, a_off);
-  // B element e = t + 256*j: k = t%32 (fixed), column t/32 + 8*j.
-  const int b_k = t & 31, b_c0 = t >> 5;
-  int64_t b_off[8];
-  bool b_ok[8];
+  // Thread t moves A vectors q = t + 256 j (j < 2): k-column kq = q / 16, rows 4 (q % 16) .. +3;
+  // and B vectors q = t + 256 j: column q / 8, k 4 (q % 8) .. +3.
+  int64_t a_off[2][4], b_off[2];
+  bool a_ok[2][4], b_ok[2];
+  int a_k[2], a_r[2], b_c[2], b_k[2];
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
+  for (int j = 0; j < 2; ++j) {
+    const int q = t + NT * j;
+    a_k[j] = q >> 4;
+    a_r[j] = (q & 15) * 4;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      a_off[j][e] = 0;
+      a_ok[j][e] = row_in_a(p, tc.row0 + a_r[j] + e, a_off[j][e]);
+    }
+    b_c[j] = q >> 3;
+    b_k[j] = (q & 7) * 4;
     b_off[j] = 0;
-    b_ok[j] = col_in_b(p, tc.col0 + b_c0 + 8 * j, b_off[j]);
+    b_ok[j] = col_in_b(p, tc.col0 + b_c[j], b_off[j]);
   }
 
   f32x16 acc;
 #pragma unroll
   for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
-  float ar[8], br[8];
-  auto load = [&](int64_t s) {
-    const int64_t i = s / ksteps;
-    const int32_t kk = (int32_t)(s - i * ksteps) * F_BK;
-    const float* pa;
-    const float* pb;
-    pair_bases<float>(p, in, pair_lo + i, pa, pb);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int32_t ka = kk + a_k0 + 4 * j;
-      ar[j] = (a_ok && ka < p.k) ? pa[a_off + (int64_t)ka * p.lda] : 0.0f;
-      const int32_t kb = kk + b_k;
-      br[j] = (b_ok[j] && kb < p.k) ? pb[b_off[j] + kb] : 0.0f;
+  // Ring of F_RING register sets: stage s is loaded into set s % F_RING about F_RING stages
+  // before it is written to LDS, so that many stages' global loads are in flight behind the MFMAs
+  // (a stage's MFMAs take far less time than a load's round trip to memory).
+  f32x4 ra[F_RING][2], rb[F_RING][2];
+  // Stages are loaded strictly in order, so a cursor walks them: pair ld_i (pair bases ld_pa /
+  // ld_pb), k offset ld_kk; no division per stage.
+  int64_t ld_s = 0, ld_i = pair_lo;
+  int32_t ld_kk = 0;
+  const float* ld_pa = nullptr;
+  const float* ld_pb = nullptr;
+  if (stages > 0) pair_bases<float>(p, in, ld_i, ld_pa, ld_pb);
+  auto advance = [&]() {
+    ++ld_s;
+    ld_kk += F_BK;
+    if (ld_kk >= p.k) {
+      ld_kk = 0;
+      ++ld_i;
+      if constexpr (VEC) {   // stride kind
+        ld_pa += p.stride_a;
+        ld_pb += p.stride_b;
+      } else if (ld_s < stages) {
+        pair_bases<float>(p, in, ld_i, ld_pa, ld_pb);
+      }
     }
   };
-  if (stages > 0) load(0);
-  for (int64_t s = 0; s < stages; ++s) {
+  auto load = [&](auto slot) {
+    constexpr int R = decltype(slot)::value;
+    if constexpr (VEC) {
+      // Exactly four 16-byte buffer loads per call, no branches, so the compiler can count the
+      // loads in flight: a vector outside the block (rows past the tile group, k past the end;
+      // whole vectors, since m and k are multiples of 4) or of a stage past the chunk's last gets
+      // an offset past the descriptor's range and reads as zero.
+      const bool live = ld_s < stages;
+      const __amdgpu_buffer_rsrc_t sa = f32_rsrc(ld_pa), sb = f32_rsrc(ld_pb);
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      As[(a_k0 + 4 * j) * F_AROW + a_r] = ar[j];
-      Bs[(b_c0 + 8 * j) * F_BROW + b_k] = br[j];
+      for (int j = 0; j < 2; ++j) {
+        const int32_t ka = ld_kk + a_k[j];
+        const int32_t oa = live && a_ok[j][0] && ka < p.k
+                               ? (int32_t)((a_off[j][0] + (int64_t)ka * p.lda) * 4)
+                               : F_OUT_OF_RANGE;
+        ra[R][j] = __builtin_amdgcn_raw_buffer_load_b128(sa, oa, 0, 0);
+        const int32_t kb = ld_kk + b_k[j];
+        const int32_t ob =
+            live && b_ok[j] && kb < p.k ? (int32_t)((b_off[j] + kb) * 4) : F_OUT_OF_RANGE;
+        rb[R][j] = __builtin_amdgcn_raw_buffer_load_b128(sb, ob, 0, 0);
+      }
+    } else {
+      const float* const pa = ld_pa;
+      const float* const pb = ld_pb;
+      const int32_t kk = ld_kk;
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int32_t ka = kk + a_k[j];
+        const int32_t kb = kk + b_k[j];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          ra[R][j][e] = (a_ok[j][e] && ka < p.k)
+                            ? gld<float>(pa + a_off[j][e] + (int64_t)ka * p.lda)
+                            : 0.0f;
+          rb[R][j][e] = (b_ok[j] && kb + e < p.k) ? gld<float>(pb + b_off[j] + kb + e) : 0.0f;
+        }
+      }
     }
-    __syncthreads();
-    if (s + 1 < stages) load(s + 1);
+    advance();
+  };
+  auto store = [&](int buf, auto slot) {
+    constexpr int R = decltype(slot)::value;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      *reinterpret_cast<f32x4*>(&As[buf][a_k[j] * F_ROW + a_r[j]]) = ra[R][j];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) Bs[buf][(b_k[j] + e) * F_ROW + b_c[j]] = rb[R][j][e];
+    }
+  };
+  // Prologue: stages 0 .. F_RING - 1 in flight, stage 0 in LDS buffer 0, stage F_RING loading.
+  // (The vector path always issues its loads; past the last stage they read zeros.)
+  if (stages > 0) {
+    load(IntC<0>());
+    if (VEC || 1 < stages) load(IntC<1>());
+    if (VEC || 2 < stages) load(IntC<2>());
+    if (VEC || 3 < stages) load(IntC<3>());
+    store(0, IntC<0>());
+    if (VEC || F_RING < stages) load(IntC<0>());
+    lds_barrier();
+  }
+  // Iteration s: MFMAs on LDS buffer s & 1 (stage s); stage s + 1 from its register set into the
+  // other buffer (free: every wave passed the barrier after stage s - 1's MFMAs); that set then
+  // takes stage s + 1 + F_RING.  One barrier per stage.  The slot index (s + 1) % F_RING and the
+  // buffer parity are compile-time constants of the unrolled steps.
+  int64_t s = 0;
+  auto step = [&](auto nslot) {
+    constexpr int NS = decltype(nslot)::value;   // (s + 1) % F_RING
+    const int buf = (int)(s & 1);
 #pragma unroll
     for (int kq = 0; kq < F_BK / 2; ++kq) {
-      const float a = As[(kq * 2 + (lane >> 5)) * F_AROW + wm * 32 + (lane & 31)];
-      const float b = Bs[(wn * 32 + (lane & 31)) * F_BROW + kq * 2 + (lane >> 5)];
+      const int kr = kq * 2 + (lane >> 5);
+      const float a = As[buf][kr * F_ROW + wm * 32 + (lane & 31)];
+      const float b = Bs[buf][kr * F_ROW + wn * 32 + (lane & 31)];
       acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, acc, 0, 0, 0);
     }
-    __syncthreads();
+    if (s + 1 < stages) store(buf ^ 1, IntC<NS>());
+    if (VEC || s + 1 + F_RING < stages) load(IntC<NS>());
+    lds_barrier();   // LDS traffic only: the ring's global loads stay in flight
+    ++s;
+  };
+  while (s < stages) {
+    step(IntC<1>());
+    if (s >= stages) break;
+    step(IntC<2>());
+    if (s >= stages) break;
+    step(IntC<3>());
+    if (s >= stages) break;
+    step(IntC<0>());
   }
+
   if (split > 1) {
-    // raw partial sums: tile-local column-major 64 x 64 block of this (tile, chunk)
-    float* w = p.ws + ((size_t)tile_bid * split + chunk) * (F_BM * F_BN);
-    const int c_local = wn * 32 + (lane & 31);
+    // This chunk's partial tile, the accumulators in register order: thread t's group q at float
+    // ((wave * 4 + q) * 64 + lane) * 4 of the chunk's 64 x 64 block, so each wave-wide 16-byte
+    // store covers 1 KB of consecutive bytes.
+    float* const w = p.ws + ((size_t)tile_bid * split + chunk) * (F_BM * F_BN) +
+                     ((wave * 4) * 64 + lane) * 4;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int r_local = wm * 32 + q * 8 + (lane >> 5) * 4;
-      gst<f32x4>(w + c_local * F_BM + r_local,
+    for (int q = 0; q < 4; ++q)
+      gst<f32x4>(w + q * 256,
                  (f32x4){acc[q * 4 + 0], acc[q * 4 + 1], acc[q * 4 + 2], acc[q * 4 + 3]});
-    }
     return;
   }
+  // Four consecutive rows per group: with m a multiple of 4 (the vector instance) they are valid
+  // together and lie in one instance, and the group is one 16-byte store when aligned.
   const int32_t C = tc.col0 + wn * 32 + (lane & 31);
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const int32_t R0 = tc.row0 + wm * 32 + q * 8 + (lane >> 5) * 4;
     const float v[4] = {acc[q * 4 + 0], acc[q * 4 + 1], acc[q * 4 + 2], acc[q * 4 + 3]};
-    store_group<true>(p, in, R0, C, v);
+    store_group<!VEC>(p, in, R0, C, v);
   }
 }
 
-// Finishing step of a split fp32 launch: four workgroups per tile, each thread four consecutive
-// rows of one column (16 rows x 64 columns per workgroup).  It sums the split partial tiles in
-// chunk order (so the result does not depend on timing), eight chunk loads in flight at a time,
-// and applies beta * C, bias, activation and the store exactly as the unsplit kernel's epilogue.
+// Finishing step of a split fp32 launch: four workgroups per tile, thread f of a tile's 1024
+// taking the partial tiles' 16-byte group f (wave f / 256, register group (f / 64) % 4, lane
+// f % 64 of the main kernel: four consecutive rows of one column).  It sums the chunks in chunk
+// order (the result does not depend on timing), eight loads in flight at a time, and applies
+// beta * C, bias, activation and the store exactly as the unsplit kernel's epilogue.
 __global__ __launch_bounds__(NT) void brgemm_f32_split_finish(BrgemmParams p) {
-  const int t = threadIdx.x;
   const int64_t tile_bid = blockIdx.x / 4;
-  const int quarter = (int)(blockIdx.x - tile_bid * 4);
+  const int f = (int)(blockIdx.x - tile_bid * 4) * NT + threadIdx.x;
+  const int wave = f >> 8, q = (f >> 6) & 3, lane = f & 63;
+  const int wm = wave & 1, wn = wave >> 1;
   const TileCoord tc = decode_tile_at(p, F_BM, F_BN, tile_bid);
   const Instance in = instance_of(p, tc.g);
-  const int c_local = t & 63, r0 = quarter * 16 + (t >> 6) * 4;
-  const float* w = p.ws + (size_t)tile_bid * p.split * (F_BM * F_BN) + c_local * F_BM + r0;
-  const size_t step = F_BM * F_BN;
+  const float* w = p.ws + (size_t)tile_bid * p.split * (F_BM * F_BN) + f * 4;
   f32x4 sum = {0.0f, 0.0f, 0.0f, 0.0f};
   int32_t ch = 0;
   for (; ch + 8 <= p.split; ch += 8) {
     f32x4 v[8];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = gld<f32x4>(w + (size_t)(ch + u) * step);
+    for (int u = 0; u < 8; ++u) v[u] = gld<f32x4>(w + (size_t)(ch + u) * (F_BM * F_BN));
 #pragma unroll
     for (int u = 0; u < 8; ++u) sum += v[u];
   }
-  for (; ch < p.split; ++ch) sum += gld<f32x4>(w + (size_t)ch * step);
-  const float v4[4] = {sum[0], sum[1], sum[2], sum[3]};
-  store_group<true>(p, in, tc.row0 + r0, tc.col0 + c_local, v4);
+  for (; ch < p.split; ++ch) sum += gld<f32x4>(w + (size_t)ch * (F_BM * F_BN));
+  const int32_t C = tc.col0 + wn * 32 + (lane & 31);
+  const int32_t R0 = tc.row0 + wm * 32 + q * 8 + (lane >> 5) * 4;
+  const float v[4] = {sum[0], sum[1], sum[2], sum[3]};
+  if (p.m % 4 == 0)
+    store_group<false>(p, in, R0, C, v);
+  else
+    store_group<true>(p, in, R0, C, v);
 }
 
 // Finishing step of a split direct-LDS launch.  A partial tile holds, for each wave (waves_m x
@@ -895,21 +1018,35 @@ hipError_t launch_brgemm(BrgemmParams& p, int32_t id, hipStream_t stream, std::s
       }
       hipLaunchKernelGGL((brgemm_bf16_kernel<64, 64, 2, 2, true>), grid, block, 0, stream, p);
       break;
-    default:
+    default: {
+      // 16-byte buffer loads when every k-column of A and every k-run of B splits into whole
+      // aligned vectors (stride kind: all pair bases follow from the bases and the steps) and every
+      // block lies within the descriptor's range of its pair base
+      const auto fits = [](int64_t last) { return last >= 0 && (last + 4) * 4 <= F_RANGE; };
+      const int64_t a_last = (p.fused ? (p.gm - 1) * p.a_step_m : 0) + p.m - 4 +
+                             (int64_t)(p.k - 1) * p.lda;
+      const int64_t b_last = (p.fused ? (p.gn - 1) * p.b_step_n : 0) +
+                             (int64_t)(p.n - 1) * p.ldb + p.k - 4;
+      const bool vec = p.kind == TPP_BR_STRIDE && p.aligned && p.m % 4 == 0 && p.k % 4 == 0 &&
+                       p.lda % 4 == 0 && p.ldb % 4 == 0 &&
+                       (!p.fused || (p.a_step_m % 4 == 0 && p.b_step_n % 4 == 0 &&
+                                     p.a_step_m >= 0 && p.b_step_n >= 0)) &&
+                       fits(a_last) && fits(b_last);
       if (name_out) {
-        *name_out = p.split > 1 ? "brgemm_f32_kernel + brgemm_f32_split_finish"
-                                : "brgemm_f32_kernel";
+        *name_out = vec ? "brgemm_f32_kernel<true>" : "brgemm_f32_kernel<false>";
+        if (p.split > 1) *name_out += " + brgemm_f32_split_finish";
         return hipSuccess;
       }
-      if (p.split > 1) {
-        hipLaunchKernelGGL(brgemm_f32_kernel, dim3((unsigned)(p.total_tiles * p.split)), block, 0,
-                           stream, p);
+      const dim3 g = p.split > 1 ? dim3((unsigned)(p.total_tiles * p.split)) : grid;
+      if (vec)
+        hipLaunchKernelGGL(brgemm_f32_kernel<true>, g, block, 0, stream, p);
+      else
+        hipLaunchKernelGGL(brgemm_f32_kernel<false>, g, block, 0, stream, p);
+      if (p.split > 1)
         hipLaunchKernelGGL(brgemm_f32_split_finish, dim3((unsigned)(p.total_tiles * 4)), block, 0,
                            stream, p);
-      } else {
-        hipLaunchKernelGGL(brgemm_f32_kernel, grid, block, 0, stream, p);
-      }
       break;
+    }
   }
   return name_out ? hipSuccess : hipGetLastError();
 }

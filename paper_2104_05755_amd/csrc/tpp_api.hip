@@ -224,6 +224,7 @@ tpp_status plan_launch(const tpp_brgemm_kernel_s* h, tpp::BrgemmParams& p, Launc
     const int64_t tiles = p.groups * ((p.vrows + 63) / 64) * ((p.vcols + 63) / 64);
     if (tiles < 128) {
       int64_t split = 256 / tiles;
+      if (const char* env = std::getenv("TPP_SPLIT")) split = std::atoi(env);   // override
       if (split > p.count) split = p.count;
       if (split > 1) {
         lp.split = (int32_t)split;

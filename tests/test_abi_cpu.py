@@ -371,7 +371,7 @@ def test_describe_launch_names_the_headline_instances(tpp):
 
 def test_describe_launch_other_workloads(tpp):
     import workloads as wk
-    assert _describe(tpp, wk.fp32_single().calls[0]) == ("brgemm_f32_kernel + "
+    assert _describe(tpp, wk.fp32_single().calls[0]) == ("brgemm_f32_kernel<true> + "
                                                          "brgemm_f32_split_finish")
     conv = _describe(tpp, wk.conv3x3().calls[0])
     assert conv.startswith("brgemm_bf16_dl_kernel<64, 64, 2, 2, false, 1, false, 0, 64"), conv
