@@ -47,7 +47,7 @@ def parse():
                          "times each (for rocprofv3 --pmc counter passes), print nothing")
     ap.add_argument("--workloads", default="mlp_block,gathered",
                     help="comma-separated workloads of --traffic-run, in launch order (mlp_block, "
-                         "gathered, mlp_fc, conv3x3, fp32_single)")
+                         "gathered, mlp_fc, conv3x3, fp32_single, mlp_backward)")
     return ap.parse_args()
 
 
@@ -157,6 +157,18 @@ def traffic_run(torch, tpp, torch_io, wk, stream, workloads):
     make = {"mlp_block": wk.mlp_block, "gathered": wk.CONFIGS[5], "mlp_fc": wk.CONFIGS[2],
             "conv3x3": wk.CONFIGS[3], "fp32_single": wk.CONFIGS[1]}
     for name in workloads:
+        if name == "mlp_backward":   # every step of the backward pass (forward with SAVE_PREACT first)
+            wl = wk.mlp_backward()
+            dev = torch_io.upload(wl)
+            sts = [torch_io.prepare_step(st, dev) for st in wl.steps]
+            torch.cuda.synchronize()
+            for _ in range(3):
+                for st in sts:
+                    torch_io.launch_step(st, dev, stream)
+            torch.cuda.synchronize()
+            del dev, sts
+            torch.cuda.empty_cache()
+            continue
         wl = make[name]()
         dev = torch_io.upload(wl)
         dcs = [torch_io.prepare(c, dev) for c in wl.calls]
@@ -201,6 +213,48 @@ def time_steps(fns, steps, warmup, torch):
             f()
     torch.cuda.synchronize()
     return time.perf_counter() - t0
+
+
+class ClockSampler:
+    """Samples the GPU's current GFX clock with `amd-smi metric -c` (a child process) from a thread
+    while the headline steps run; `result()` gives the median over samples of the mean over the
+    XCDs, in MHz, or None when the tool is missing or prints no clock."""
+
+    def __init__(self):
+        import threading
+        self.samples, self.stop = [], threading.Event()
+        self.thread = threading.Thread(target=self._run, daemon=True)
+
+    def _run(self):
+        import re
+        import subprocess
+        while not self.stop.is_set():
+            try:
+                out = subprocess.run(["amd-smi", "metric", "-c", "-g", "0"], capture_output=True,
+                                     text=True, timeout=10).stdout
+            except (OSError, subprocess.SubprocessError):
+                return
+            # the GFX_i blocks' current clocks ("CLK: 2100 MHz" right after each "GFX_i:")
+            clks = [int(m) for m in re.findall(r"GFX_\d+:\s*\n\s*CLK:\s*(\d+)\s*MHz", out)]
+            if not clks:
+                return
+            self.samples.append(sum(clks) / len(clks))
+
+    def __enter__(self):
+        self.thread.start()
+        return self
+
+    def __exit__(self, *exc):
+        self.stop.set()
+        self.thread.join(timeout=15)
+
+    def result(self):
+        if not self.samples:
+            return None
+        s = sorted(self.samples)
+        return {"sclk_mhz_median": round(s[len(s) // 2], 0), "samples": len(s),
+                "min": round(s[0], 0), "max": round(s[-1], 0),
+                "how": "amd-smi metric -c during the untimed settle steps (mean of the XCDs' GFX clocks)"}
 
 
 def settle(fns, seconds, torch):
@@ -362,7 +416,8 @@ def main():
     dev = torch_io.upload(wl)
     dcs = [torch_io.prepare(c, dev) for c in wl.calls]
     fns = [lambda dc=dc: torch_io.launch(dc, stream) for dc in dcs]
-    settle_s = settle(fns, args.settle, torch)
+    with ClockSampler() as clock:
+        settle_s = settle(fns, args.settle, torch)
     elapsed = time_steps(fns, args.steps, args.warmup, torch)
     per = time_in_steps(fns, args.steps, torch, stream)
     flops_step = wl.flops
@@ -388,6 +443,7 @@ def main():
         "warmup": args.warmup, "ms_per_step": round(elapsed / args.steps * 1e3, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "settle_s": round(settle_s, 2),
+        "clock_under_load": clock.result(),
         "data": "synthetic (seeded numpy draws, bf16-rounded; no dataset, random-init weights)",
         "config": {"workload": "transformer MLP block as blocked BRGEMM: 8192 tokens, "
                                "1024->4096 (bias+GELU-tanh) -> 1024 (bias), bf16 64x64 blocks",
@@ -440,7 +496,8 @@ def per_config(args, torch, tpp, torch_io, wk, np, stream):
         byts = alg_bytes(wl, call)
         gbs = byts / (ms * 1e-3) / 1e9
         peak = PEAK_F32_TFLOPS if call.ab_type == "f32" else PEAK_BF16_TFLOPS
-        entry = {"workload": wl.name, "kernel": tpp.tpp_brgemm_describe(dcs[0].handle),
+        entry = {"workload": wl.name, "kernel": torch_io.describe(dcs[0]),
+                 "descriptor": tpp.tpp_brgemm_describe(dcs[0].handle),
                  "instances": call.G, "pairs": call.pairs, "launch_us": round(ms * 1e3, 2),
                  "tflops": round(tfl, 2), "mfma_frac": round(tfl / peak, 4),
                  "alg_bytes": byts, "hbm_gbs": round(gbs, 1),
@@ -572,7 +629,7 @@ def backward_entry(args, torch, tpp, torch_io, wk, stream):
         if isinstance(st, wk.Call):
             tfl = st.flops / (ms * 1e-3) / 1e12
             brgemm_ms += ms
-            e.update(kernel=tpp.tpp_brgemm_describe(sts[i].handle), instances=st.G,
+            e.update(kernel=torch_io.describe(sts[i]), instances=st.G,
                      pairs=st.pairs, tflops=round(tfl, 1), mfma_frac=round(tfl / PEAK_BF16_TFLOPS, 4))
         elif isinstance(st, wk.TransformStep):
             byts = 2 * st.G * st.m * st.n * 2
@@ -591,7 +648,7 @@ def backward_entry(args, torch, tpp, torch_io, wk, stream):
            "launches": launches,
            "forward_save_preact": {
                "what": "GEMM1 1024->4096 bias+GELU keeping the pre-activation Z (aux store)",
-               "kernel": tpp.tpp_brgemm_describe(sts[0].handle),
+               "kernel": torch_io.describe(sts[0]),
                "launch_us": round(ms_fwd * 1e3, 2),
                "tflops": round(wl.calls[0].flops / (ms_fwd * 1e-3) / 1e12, 1)}}
     del dev, sts, fns
