@@ -109,7 +109,7 @@ int32_t choose_kernel(const tpp_brgemm_kernel_s& h, const tpp::BrgemmParams& p) 
       const int64_t tiles = p.groups * ((p.vrows + bm - 1) / bm) * ((p.vcols + bn - 1) / bn);
       const int64_t ktot = h.desc.kind == TPP_BR_ADDRESS ? 0 : p.count * (int64_t)h.desc.k;
       if (tiles >= 512 || last) return c;
-      if (bm == 256 && ktot >= 8192 && tiles * 8 >= 256) return c;
+      if (bm == 128 && ktot >= 8192 && tiles * 8 >= 512) return c;   // split (see below)
     }
     return -1;
   }
@@ -144,8 +144,10 @@ int32_t choose_kernel(const tpp_brgemm_kernel_s& h, const tpp::BrgemmParams& p) 
     // two tiles per compute unit: one workgroup's barriers and epilogue overlap the other's MFMAs
     if (tiles >= 512 || last) return dl ? c.dl_id : c.vec_id;
     // a long batch reduction (weight gradients: all token blocks) makes up the parallelism by
-    // splitting its stage list instead (see launch), keeping the large tile's operand reuse
-    if (dl && bk64 && c.bm == 256 && ktot >= 8192 && tiles * 8 >= 256) return c.dl_id;
+    // splitting its stage list instead (see plan_launch): 128x128 tiles, two workgroups per
+    // compute unit (measured on the MLP weight gradients, 1024 x 4096 outputs of 128 pairs: 87 us
+    // against 94 unsplit and 96-101 for 256x256 tiles split 4)
+    if (dl && bk64 && c.bm == 128 && ktot >= 8192 && tiles * 8 >= 512) return c.dl_id;
   }
   return tpp::K_BF16_64x64;
 }
@@ -233,14 +235,16 @@ tpp_status plan_launch(const tpp_brgemm_kernel_s* h, tpp::BrgemmParams& p, Launc
     }
   }
   if (lp.split == 1 && tpp::kernel_k_step(id) > 1 && p.kind != TPP_BR_ADDRESS && p.count > 0) {
-    // Direct-to-LDS kernel on a grid of fewer tiles than compute units: split every tile's
-    // stage list into chunks reduced by separate workgroups (about 256 in all, at least 8 stages
-    // each) and add the chunks in a finishing kernel.  TPP_SPLIT overrides the count.
+    // Direct-to-LDS kernel on a grid of too few tiles: split every tile's stage list into chunks
+    // reduced by separate workgroups (about 512 in all for 128x128 tiles, two per compute unit,
+    // else about 256; at least 8 stages each) and add the chunks in a finishing kernel.
+    // TPP_SPLIT overrides the count.
     const int64_t tiles = p.groups * ((p.vrows + bm - 1) / bm) * ((p.vcols + bn - 1) / bn);
     const int64_t stages = p.count * (h->desc.k / tpp::kernel_k_step(id));
+    const int64_t target = bm == 128 ? 512 : 256;
     int64_t split = 1;
-    if (tiles < 256 && stages >= 16) {
-      split = 256 / tiles;
+    if (tiles < target && stages >= 16) {
+      split = target / tiles;
       if (split > 8) split = 8;
       if (split > stages / 8) split = stages / 8;
     }

@@ -65,9 +65,9 @@ def _blocks(flat, call, sel):
 
 
 CASES = {
-    # 36 tiles of 256 x 256, 256 stages: split 7 ways, 252 partial tiles (63 MiB of scratch);
+    # 144 tiles of 128 x 128, 256 stages: split 3 ways, 432 partial tiles (27 MiB of scratch);
     # then half the stages, the same split
-    "split_256": (lambda: wk.mlp_fc(seed=41, minibatch=1536, c_in=16384, k_out=1536),
+    "split_128": (lambda: wk.mlp_fc(seed=41, minibatch=1536, c_in=16384, k_out=1536),
                   lambda: wk.mlp_fc(seed=42, minibatch=1536, c_in=8192, k_out=1536)),
     # 16 tiles of 64 x 64, 64 stages: split 8 ways; then 6 tiles, 32 stages: split 4 ways
     "split_64": (lambda: wk.mlp_fc(seed=43, minibatch=256, c_in=4096, k_out=256),
