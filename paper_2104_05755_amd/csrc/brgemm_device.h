@@ -351,6 +351,107 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_sched_barrier(0);
 }
 
+// Direct global -> LDS copies (used by the direct-to-LDS main loops and by the epilogue's aux
+// loads).
+#define LDS_AS __attribute__((address_space(3)))
+
+// s_waitcnt immediate waiting until at most n vector-memory operations are outstanding (gfx9
+// encoding: vmcnt in bits 3:0 and 15:14, expcnt 6:4 and lgkmcnt 11:8 left at their maxima).
+constexpr int vmcnt_imm(int n) {
+  return (n & 0xF) | (((n >> 4) & 3) << 14) | (0x7 << 4) | (0xF << 8);
+}
+
+// Buffer descriptor of a raw (unswizzled, stride 0) buffer at `base`: 2^31 bytes addressable,
+// out-of-range offsets read as zero.  Built from wave-uniform values, so it lives in SGPRs.
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ i32x4 raw_buffer(const void* base) {
+  const uint64_t b = reinterpret_cast<uint64_t>(base);
+  return (i32x4){__builtin_amdgcn_readfirstlane((int)(uint32_t)b),
+                 __builtin_amdgcn_readfirstlane((int)((uint32_t)(b >> 32) & 0xffffu)), 0x7fffffff,
+                 0x00020000};
+}
+
+// 16-byte buffer -> LDS copy of a whole wave (buffer_load_dwordx4 ... offen lds): lane j's 16
+// bytes from rsrc base + voff land at l + 16 j.  The buffer form takes one 32-bit offset per lane
+// where the global form takes a 64-bit address, and unlike the global form it runs alongside the
+// MFMAs of the same compute unit instead of stalling them (measured on gfx950: a stream of 32x32x16
+// MFMAs beside 8 KB of loads per iteration took the MFMA time with buffer loads, the sum of both
+// times with global loads).  It is issued through inline asm so that the compiler does not see a
+// pending LDS write: the compiler would otherwise wait for every outstanding load (vmcnt 0)
+// before the next LDS read and so drain the stages kept in flight.  Callers order these loads
+// themselves with s_waitcnt vmcnt and lds_barrier().  M0 is saved and restored around it.
+__device__ __forceinline__ void buffer_load_lds16(i32x4 rsrc, uint32_t voff, char* l) {
+  const uint32_t lds_addr =
+      __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(LDS_AS char*)l);
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %3\n\t"
+      "s_nop 0\n\t"
+      "buffer_load_dwordx4 %1, %2, 0 offen lds\n\t"
+      "s_nop 0\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(voff), "s"(rsrc), "s"(lds_addr)
+      : "memory");
+}
+
+// N consecutive 16-byte buffer -> LDS wave-loads: load r reads rsrc base + voff[r] and lands at
+// lds_addr + 1024 r.  One asm block sets M0 once and steps it by 1 KB between the loads, so a
+// wave-load costs two scalar instructions instead of the nine of a separate buffer_load_lds16
+// (M0 save, set, wait state, restore, and the null check of the LDS pointer's address-space
+// conversion).  The scalar unit is shared by the compute unit's waves, and every wave copies its
+// share of a stage right after the same barrier: measured per wave and stage, issuing the copies
+// of the 256 x 256 tile took ~980 cycles one by one and ~845 in blocks, of the 128 x 128 tile 758
+// and 587.  (The rest is the copies themselves: each direct-to-LDS load takes ~100 cycles to
+// issue while all waves copy.)  One wait state after each M0 write, as the ISA requires before an
+// LDS-DMA load.
+#define TPP_LDS16_FIRST "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %[lds]\n\ts_nop 0\n\t"
+#define TPP_LDS16_LOAD(i) "buffer_load_dwordx4 %[v" #i "], %[rsrc], 0 offen lds\n\t"
+#define TPP_LDS16_STEP "s_add_u32 m0, m0, 0x400\n\ts_nop 0\n\t"
+#define TPP_LDS16_LAST "s_nop 0\n\ts_mov_b32 m0, %0"
+template <int N>
+__device__ __forceinline__ void buffer_load_lds16_block(i32x4 rsrc, const uint32_t* voff,
+                                                        uint32_t lds_addr) {
+  uint32_t saved;
+  if constexpr (N == 1) {
+    asm volatile(TPP_LDS16_FIRST TPP_LDS16_LOAD(0) TPP_LDS16_LAST
+                 : "=&s"(saved)
+                 : [v0] "v"(voff[0]), [rsrc] "s"(rsrc), [lds] "s"(lds_addr)
+                 : "memory", "scc");
+  } else if constexpr (N == 2) {
+    asm volatile(TPP_LDS16_FIRST TPP_LDS16_LOAD(0) TPP_LDS16_STEP TPP_LDS16_LOAD(1) TPP_LDS16_LAST
+                 : "=&s"(saved)
+                 : [v0] "v"(voff[0]), [v1] "v"(voff[1]), [rsrc] "s"(rsrc), [lds] "s"(lds_addr)
+                 : "memory", "scc");
+  } else if constexpr (N == 4) {
+    asm volatile(TPP_LDS16_FIRST TPP_LDS16_LOAD(0) TPP_LDS16_STEP TPP_LDS16_LOAD(1)
+                     TPP_LDS16_STEP TPP_LDS16_LOAD(2) TPP_LDS16_STEP TPP_LDS16_LOAD(3)
+                         TPP_LDS16_LAST
+                 : "=&s"(saved)
+                 : [v0] "v"(voff[0]), [v1] "v"(voff[1]), [v2] "v"(voff[2]), [v3] "v"(voff[3]),
+                   [rsrc] "s"(rsrc), [lds] "s"(lds_addr)
+                 : "memory", "scc");
+  } else if constexpr (N == 8) {
+    asm volatile(TPP_LDS16_FIRST TPP_LDS16_LOAD(0) TPP_LDS16_STEP TPP_LDS16_LOAD(1)
+                     TPP_LDS16_STEP TPP_LDS16_LOAD(2) TPP_LDS16_STEP TPP_LDS16_LOAD(3)
+                         TPP_LDS16_STEP TPP_LDS16_LOAD(4) TPP_LDS16_STEP TPP_LDS16_LOAD(5)
+                             TPP_LDS16_STEP TPP_LDS16_LOAD(6) TPP_LDS16_STEP TPP_LDS16_LOAD(7)
+                                 TPP_LDS16_LAST
+                 : "=&s"(saved)
+                 : [v0] "v"(voff[0]), [v1] "v"(voff[1]), [v2] "v"(voff[2]), [v3] "v"(voff[3]),
+                   [v4] "v"(voff[4]), [v5] "v"(voff[5]), [v6] "v"(voff[6]), [v7] "v"(voff[7]),
+                   [rsrc] "s"(rsrc), [lds] "s"(lds_addr)
+                 : "memory", "scc");
+  } else {
+    static_assert(N == 1 || N == 2 || N == 4 || N == 8, "block sizes 1, 2, 4, 8");
+  }
+}
+#undef TPP_LDS16_FIRST
+#undef TPP_LDS16_LOAD
+#undef TPP_LDS16_STEP
+#undef TPP_LDS16_LAST
+
 // 16 bytes of bf16 from global memory, aligned or not; zeroing without branches.
 __device__ __forceinline__ u32x4 ld16(const uint16_t* ptr) { return gld<u32x4>(ptr); }
 
@@ -655,15 +756,69 @@ __device__ __forceinline__ void epilogue_bf16_act(const BrgemmParams& p, const I
         }
   };
   if constexpr (ACT == 3 || ACT == 4) {
-    // aux -> slab with the store's 16-byte runs (out-of-range rows / columns are never read back
-    // into a stored value, so they are left as they are)
-    const uint16_t* const a16 = static_cast<const uint16_t*>(p.aux);
-    walk([&](char* sp, int64_t off, bool ok) {
-      if (!ok) return;
-      const uint16_t* ap = a16 + off;
-      *reinterpret_cast<u32x4*>(sp) =
-          (reinterpret_cast<uintptr_t>(ap) & 15) == 0 ? ld16(ap) : ld16_unaligned(ap);
-    });
+    // aux -> slab.  Direct global -> LDS copies: copy r fills slab bytes [1 KB r, 1 KB (r + 1)),
+    // lane j's 16 bytes at 16 j, which is slot j % CPC of column r COLS_PER_IT + j / CPC; the
+    // lane reads the 8-row chunk that the slab's swizzle puts there, (j % CPC) ^ (column %
+    // CPC), the same chunk for every r since COLS_PER_IT is a multiple of CPC.  All of the
+    // wave's copies are in flight before the one wait (16 KB per wave of a 256 x 256 tile), where
+    // register loads would hold 64 more registers.  Rows and columns outside C read as zero (an
+    // offset past the descriptor's range) and are never read back into a stored value.  When
+    // some element lies outside the 2^31 bytes a buffer offset reaches from the wave's first
+    // one, the wave takes the walk's 16-byte register loads instead.
+    constexpr int NR = WTN / COLS_PER_IT;
+    constexpr int BLK = NR >= 8 ? 8 : NR;   // copies per asm block
+    constexpr bool DIRECT = COLS_PER_IT % CPC == 0 && NR % BLK == 0;
+    const int32_t C0 = tc.col0 + wn * WTN;
+    auto row_offset = [&](int32_t R, bool& ok) -> int64_t {
+      if (p.fused) {
+        const int32_t gi = R / p.m, r = R - gi * p.m;
+        ok = FULL || R < p.vrows;
+        return (int64_t)gi * p.c_step_m + r;
+      }
+      ok = FULL || R < p.m;
+      return R;
+    };
+    auto col_offset = [&](int32_t C) -> int64_t {
+      if (p.fused) {
+        const int32_t gi = C / p.n;
+        return (int64_t)gi * p.c_step_n + (int64_t)(C - gi * p.n) * p.ldc;
+      }
+      return (int64_t)C * p.ldc;
+    };
+    bool base_ok;
+    const int64_t base = in.c + row_offset(row_base, base_ok) + col_offset(C0);   // wave-uniform
+    const int csub = lane / CPC;
+    const int ch = (lane % CPC) ^ (csub & (CPC - 1));
+    bool row_ok;
+    const int64_t row_off = row_offset(row_base + ch * 8, row_ok);
+    const int32_t c_lim = p.fused ? p.vcols : p.n;
+    uint32_t voff[NR];
+    bool bad = false;
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+      const int32_t C = C0 + r * COLS_PER_IT + csub;
+      const bool ok = row_ok && (FULL || C < c_lim);
+      const int64_t rel = in.c + row_off + col_offset(C) - base;   // elements
+      const bool fits = rel >= 0 && rel < (int64_t)0x3fff0000;
+      bad |= ok && !fits;
+      voff[r] = ok && fits ? (uint32_t)(rel * 2) : 0x80000000u;
+    }
+    if (DIRECT && !__any(bad)) {
+      const i32x4 rsrc = raw_buffer(static_cast<const uint16_t*>(p.aux) + base);
+      const uint32_t l0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(LDS_AS char*)slab);
+#pragma unroll
+      for (int r = 0; r < NR; r += BLK)
+        buffer_load_lds16_block<BLK>(rsrc, voff + r, l0 + r * 1024);
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    } else {
+      const uint16_t* const a16 = static_cast<const uint16_t*>(p.aux);
+      walk([&](char* sp, int64_t off, bool ok) {
+        if (!ok) return;
+        const uint16_t* ap = a16 + off;
+        *reinterpret_cast<u32x4*>(sp) =
+            (reinterpret_cast<uintptr_t>(ap) & 15) == 0 ? ld16(ap) : ld16_unaligned(ap);
+      });
+    }
   }
   park(IntC<ACT>());
   store_slab(p.c);

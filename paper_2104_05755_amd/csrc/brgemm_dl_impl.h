@@ -27,106 +27,7 @@ namespace {
 using namespace dev;
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
-#define LDS_AS __attribute__((address_space(3)))
-
 constexpr int LDS_MAX = 160 * 1024;   // bytes of LDS per workgroup on gfx950
-
-// s_waitcnt immediate waiting until at most n vector-memory operations are outstanding (gfx9
-// encoding: vmcnt in bits 3:0 and 15:14, expcnt 6:4 and lgkmcnt 11:8 left at their maxima).
-constexpr int vmcnt_imm(int n) {
-  return (n & 0xF) | (((n >> 4) & 3) << 14) | (0x7 << 4) | (0xF << 8);
-}
-
-// Buffer descriptor of a raw (unswizzled, stride 0) buffer at `base`: 2^31 bytes addressable,
-// out-of-range offsets read as zero.  Built from wave-uniform values, so it lives in SGPRs.
-typedef int i32x4 __attribute__((ext_vector_type(4)));
-__device__ __forceinline__ i32x4 raw_buffer(const void* base) {
-  const uint64_t b = reinterpret_cast<uint64_t>(base);
-  return (i32x4){__builtin_amdgcn_readfirstlane((int)(uint32_t)b),
-                 __builtin_amdgcn_readfirstlane((int)((uint32_t)(b >> 32) & 0xffffu)), 0x7fffffff,
-                 0x00020000};
-}
-
-// 16-byte buffer -> LDS copy of a whole wave (buffer_load_dwordx4 ... offen lds): lane j's 16
-// bytes from rsrc base + voff land at l + 16 j.  The buffer form takes one 32-bit offset per lane
-// where the global form takes a 64-bit address, and unlike the global form it runs alongside the
-// MFMAs of the same compute unit instead of stalling them (measured on gfx950: a stream of 32x32x16
-// MFMAs beside 8 KB of loads per iteration took the MFMA time with buffer loads, the sum of both
-// times with global loads).  It is issued through inline asm so that the compiler does not see a
-// pending LDS write: the compiler would otherwise wait for every outstanding load (vmcnt 0)
-// before the next LDS read and so drain the stages kept in flight.  Callers order these loads
-// themselves with s_waitcnt vmcnt and lds_barrier().  M0 is saved and restored around it.
-__device__ __forceinline__ void buffer_load_lds16(i32x4 rsrc, uint32_t voff, char* l) {
-  const uint32_t lds_addr =
-      __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(LDS_AS char*)l);
-  uint32_t saved;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\t"
-      "s_mov_b32 m0, %3\n\t"
-      "s_nop 0\n\t"
-      "buffer_load_dwordx4 %1, %2, 0 offen lds\n\t"
-      "s_nop 0\n\t"
-      "s_mov_b32 m0, %0"
-      : "=&s"(saved)
-      : "v"(voff), "s"(rsrc), "s"(lds_addr)
-      : "memory");
-}
-
-// N consecutive 16-byte buffer -> LDS wave-loads: load r reads rsrc base + voff[r] and lands at
-// lds_addr + 1024 r.  One asm block sets M0 once and steps it by 1 KB between the loads, so a
-// wave-load costs two scalar instructions instead of the nine of a separate buffer_load_lds16
-// (M0 save, set, wait state, restore, and the null check of the LDS pointer's address-space
-// conversion).  The scalar unit is shared by the compute unit's waves, and every wave copies its
-// share of a stage right after the same barrier: measured per wave and stage, issuing the copies
-// of the 256 x 256 tile took ~980 cycles one by one and ~845 in blocks, of the 128 x 128 tile 758
-// and 587.  (The rest is the copies themselves: each direct-to-LDS load takes ~100 cycles to
-// issue while all waves copy.)  One wait state after each M0 write, as the ISA requires before an
-// LDS-DMA load.
-#define TPP_LDS16_FIRST "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %[lds]\n\ts_nop 0\n\t"
-#define TPP_LDS16_LOAD(i) "buffer_load_dwordx4 %[v" #i "], %[rsrc], 0 offen lds\n\t"
-#define TPP_LDS16_STEP "s_add_u32 m0, m0, 0x400\n\ts_nop 0\n\t"
-#define TPP_LDS16_LAST "s_nop 0\n\ts_mov_b32 m0, %0"
-template <int N>
-__device__ __forceinline__ void buffer_load_lds16_block(i32x4 rsrc, const uint32_t* voff,
-                                                        uint32_t lds_addr) {
-  uint32_t saved;
-  if constexpr (N == 1) {
-    asm volatile(TPP_LDS16_FIRST TPP_LDS16_LOAD(0) TPP_LDS16_LAST
-                 : "=&s"(saved)
-                 : [v0] "v"(voff[0]), [rsrc] "s"(rsrc), [lds] "s"(lds_addr)
-                 : "memory", "scc");
-  } else if constexpr (N == 2) {
-    asm volatile(TPP_LDS16_FIRST TPP_LDS16_LOAD(0) TPP_LDS16_STEP TPP_LDS16_LOAD(1) TPP_LDS16_LAST
-                 : "=&s"(saved)
-                 : [v0] "v"(voff[0]), [v1] "v"(voff[1]), [rsrc] "s"(rsrc), [lds] "s"(lds_addr)
-                 : "memory", "scc");
-  } else if constexpr (N == 4) {
-    asm volatile(TPP_LDS16_FIRST TPP_LDS16_LOAD(0) TPP_LDS16_STEP TPP_LDS16_LOAD(1)
-                     TPP_LDS16_STEP TPP_LDS16_LOAD(2) TPP_LDS16_STEP TPP_LDS16_LOAD(3)
-                         TPP_LDS16_LAST
-                 : "=&s"(saved)
-                 : [v0] "v"(voff[0]), [v1] "v"(voff[1]), [v2] "v"(voff[2]), [v3] "v"(voff[3]),
-                   [rsrc] "s"(rsrc), [lds] "s"(lds_addr)
-                 : "memory", "scc");
-  } else if constexpr (N == 8) {
-    asm volatile(TPP_LDS16_FIRST TPP_LDS16_LOAD(0) TPP_LDS16_STEP TPP_LDS16_LOAD(1)
-                     TPP_LDS16_STEP TPP_LDS16_LOAD(2) TPP_LDS16_STEP TPP_LDS16_LOAD(3)
-                         TPP_LDS16_STEP TPP_LDS16_LOAD(4) TPP_LDS16_STEP TPP_LDS16_LOAD(5)
-                             TPP_LDS16_STEP TPP_LDS16_LOAD(6) TPP_LDS16_STEP TPP_LDS16_LOAD(7)
-                                 TPP_LDS16_LAST
-                 : "=&s"(saved)
-                 : [v0] "v"(voff[0]), [v1] "v"(voff[1]), [v2] "v"(voff[2]), [v3] "v"(voff[3]),
-                   [v4] "v"(voff[4]), [v5] "v"(voff[5]), [v6] "v"(voff[6]), [v7] "v"(voff[7]),
-                   [rsrc] "s"(rsrc), [lds] "s"(lds_addr)
-                 : "memory", "scc");
-  } else {
-    static_assert(N == 1 || N == 2 || N == 4 || N == 8, "block sizes 1, 2, 4, 8");
-  }
-}
-#undef TPP_LDS16_FIRST
-#undef TPP_LDS16_LOAD
-#undef TPP_LDS16_STEP
-#undef TPP_LDS16_LAST
 
 // XOR swizzle of the 16-byte k-chunks of a B-panel column (COLB = 2 BK bytes): the 16 columns a
 // ds_read_b128 serves per cycle land in 16 distinct 16-byte bank groups of a 256-byte row.
