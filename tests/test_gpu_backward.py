@@ -341,3 +341,40 @@ def test_split_mlp_block_matches_oracle(kid, split, monkeypatch):
     _compare("y", got["y"], ref["y"], wl.calls[1])
     again = gpu_steps(wl.calls, wl.arrays, ["y"])   # chunk-order sums: the same bits every run
     assert np.array_equal(again["y"], got["y"])
+
+
+@pytest.mark.parametrize("ldc", [(1 << 29) + 64, (1 << 30) + 64], ids=["1GB", "2GB"])
+def test_inverse_epilogue_aux_columns_far_apart(ldc):
+    """RELU_inv through the bf16 register epilogue on an output whose two columns lie ldc
+    elements apart (small-integer data, exact).  A wave copies its aux tile into LDS with 32-bit
+    buffer offsets from its first element: at 1 GB apart the second column still fits them, at
+    2 GB it does not and the wave loads the tile through registers instead.  Both against the
+    oracle on compact copies."""
+    import paper_2104_05755_amd as tpp
+    dev = torch.device("cuda:0")
+    stream = tpp.current_stream()
+    rng = np.random.default_rng(ldc % 1000003)
+    m, n, k, count = 64, 2, 64, 2
+    say(f"relu_inv with C columns {ldc} elements apart")
+    a = wk.bf16_bits(rng.integers(-4, 5, count * m * k).astype(np.float32))
+    b = wk.bf16_bits(rng.integers(-4, 5, count * k * n).astype(np.float32))
+    z = wk.bf16_bits(rng.integers(-3, 4, (n, m)).astype(np.float32))
+    A = torch.from_numpy(a.view(np.int16)).to(dev)
+    B = torch.from_numpy(b.view(np.int16)).to(dev)
+    C = torch.empty(ldc * (n - 1) + m, dtype=torch.int16, device=dev)
+    Z = torch.zeros(ldc * (n - 1) + m, dtype=torch.int16, device=dev)
+    for c in range(n):
+        Z[c * ldc:c * ldc + m] = torch.from_numpy(z[c].view(np.int16)).to(dev)
+    h = tpp.tpp_brgemm_dispatch(tpp.make_desc(m, n, k, m, k, ldc, "bf16", "bf16", 0.0, "stride",
+                                              m * k, k * n, flags=("relu_inv",)))
+    grid = dict(gm=1, gn=1, a_step_m=0, b_step_n=0, c_step_m=0, c_step_n=0, bias_step_m=0)
+    tpp.tpp_brgemm_execute_batched_aux(h, grid, 1, None, None, None, None, A, B, C, Z, None,
+                                       count, None, None, None, None, None, stream)
+    torch.cuda.synchronize()
+    got = np.stack([C[c * ldc:c * ldc + m].cpu().numpy().view(np.uint16) for c in range(n)])
+    del C, Z
+    ref = np.full((n, m), 0x7FC0, dtype=np.uint16)
+    oracle.brgemm_batched(oracle.Desc(m, n, k, m, k, m, "bf16", "bf16", 0.0, "stride", m * k,
+                                      k * n, flags={"relu_inv"}),
+                          a, b, ref, aux=np.ascontiguousarray(z), count=count)
+    assert np.array_equal(got, ref)
