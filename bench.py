@@ -556,7 +556,8 @@ def equation_entries(args, torch, tpp, torch_io, wk, stream):
         elif name == "layernorm":
             y = wl.steps[-1]
             byts = 2 * y.m * y.n * 2 + y.m * y.n * 2
-            what = f"layer norm over {y.m} features of {y.n} tokens, bf16 (Reduce + 3 equations)"
+            what = (f"layer norm over {y.m} features of {y.n} tokens, bf16 (Reduce, the rs "
+                    f"equation, the normalize equation; mu a subtree of both)")
         else:
             y = wl.steps[-1]
             # X read twice (bf16), X' written once and read twice (fp32), Y written (bf16)
