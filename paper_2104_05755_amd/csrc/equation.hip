@@ -294,6 +294,94 @@ __global__ __launch_bounds__(EQ_T) void equation_kernel(EqProgram p) {
   }
 }
 
+// Small outputs (at most EQ_SMALL elements, e.g. a 1 x n row of statistics): one element per
+// thread, so that the grid has as many workgroups as the elements allow, and every leaf of the
+// element loaded before the first instruction runs, so that one memory latency replaces the
+// chain of leaf loads the interpreter would otherwise wait for one instruction at a time.  The
+// leaves and temporaries are named registers (indices dispatched by switch, never computed).
+constexpr int64_t EQ_SMALL = 1 << 16;
+
+__device__ __forceinline__ float eq_apply1(int32_t op, float a, float b, float c) {
+  switch (op) {
+    case TPP_EQ_IDENTITY: return a;
+    case TPP_EQ_NEG: return -a;
+    case TPP_EQ_EXP: return expf(a);
+    case TPP_EQ_TANH: return tanhf(a);
+    case TPP_EQ_RELU: return a > 0.0f ? a : 0.0f;
+    case TPP_EQ_GELU_TANH: return gelu_tanh(a);
+    case TPP_EQ_SQRT: return sqrtf(a);
+    case TPP_EQ_RCP: return 1.0f / a;
+    case TPP_EQ_SQUARE: return a * a;
+    case TPP_EQ_SIGMOID: return 1.0f / (1.0f + expf(-a));
+    case TPP_EQ_ADD: return a + b;
+    case TPP_EQ_SUB: return a - b;
+    case TPP_EQ_MUL: return a * b;
+    case TPP_EQ_DIV: return a / b;
+    case TPP_EQ_MAX: return a > b ? a : b;
+    case TPP_EQ_MIN: return a < b ? a : b;
+    case TPP_EQ_MULADD: return __builtin_fmaf(a, b, c);
+    default: return 0.0f;
+  }
+}
+
+template <bool OUT_BF16>
+__global__ __launch_bounds__(EQ_T) void equation_small_kernel(EqProgram p) {
+  const int32_t total = p.m * p.n;   // at most EQ_SMALL
+  const int32_t e = (int32_t)blockIdx.x * EQ_T + (int32_t)threadIdx.x;
+  if (e >= total) return;
+  const int32_t c = e / p.m, r = e - c * p.m;
+  // every leaf of this element, all loads issued before any is used
+  float l0 = 0.0f, l1 = 0.0f, l2 = 0.0f, l3 = 0.0f, l4 = 0.0f, l5 = 0.0f, l6 = 0.0f, l7 = 0.0f;
+  float l8 = 0.0f, l9 = 0.0f, l10 = 0.0f, l11 = 0.0f, l12 = 0.0f, l13 = 0.0f, l14 = 0.0f,
+        l15 = 0.0f;
+  auto leaf = [&](int j) -> float {
+    const EqArg& g = p.arg[j];
+    const int64_t at = g.bcast == TPP_BC_NONE ? (int64_t)r + (int64_t)c * g.ld
+                       : g.bcast == TPP_BC_COL ? r : g.bcast == TPP_BC_ROW ? c : 0;
+    return g.bf16 ? bf16_bits_to_f32(gld<uint16_t>(static_cast<const uint16_t*>(g.ptr) + at))
+                  : gld<float>(static_cast<const float*>(g.ptr) + at);
+  };
+#define TPP_EQ_LEAF_LOAD(j) \
+  if (j < p.n_args) l##j = leaf(j);
+  TPP_EQ_LEAF_LOAD(0) TPP_EQ_LEAF_LOAD(1) TPP_EQ_LEAF_LOAD(2) TPP_EQ_LEAF_LOAD(3)
+  TPP_EQ_LEAF_LOAD(4) TPP_EQ_LEAF_LOAD(5) TPP_EQ_LEAF_LOAD(6) TPP_EQ_LEAF_LOAD(7)
+  TPP_EQ_LEAF_LOAD(8) TPP_EQ_LEAF_LOAD(9) TPP_EQ_LEAF_LOAD(10) TPP_EQ_LEAF_LOAD(11)
+  TPP_EQ_LEAF_LOAD(12) TPP_EQ_LEAF_LOAD(13) TPP_EQ_LEAF_LOAD(14) TPP_EQ_LEAF_LOAD(15)
+#undef TPP_EQ_LEAF_LOAD
+  static_assert(EQ_MAX_ARGS == 16 && EQ_MAX_TMPS == 8 && EQ_LEAF_BASE == 16,
+                "one named register per leaf and temporary");
+  float t0 = 0.0f, t1 = 0.0f, t2 = 0.0f, t3 = 0.0f, t4 = 0.0f, t5 = 0.0f, t6 = 0.0f, t7 = 0.0f;
+  auto get = [&](int32_t code) -> float {
+    switch (code) {
+      case 0: return t0; case 1: return t1; case 2: return t2; case 3: return t3;
+      case 4: return t4; case 5: return t5; case 6: return t6; case 7: return t7;
+      case 16: return l0; case 17: return l1; case 18: return l2; case 19: return l3;
+      case 20: return l4; case 21: return l5; case 22: return l6; case 23: return l7;
+      case 24: return l8; case 25: return l9; case 26: return l10; case 27: return l11;
+      case 28: return l12; case 29: return l13; case 30: return l14; case 31: return l15;
+      default: return 0.0f;
+    }
+  };
+  for (int32_t i = 0; i < p.n_instr; ++i) {
+    const EqInstr& in = p.instr[i];
+    const float a = get(in.src[0]);
+    const float b = in.arity > 1 ? get(in.src[1]) : 0.0f;
+    const float cc = in.arity > 2 ? get(in.src[2]) : 0.0f;
+    const float v = eq_apply1(in.op, a, b, cc);
+    switch (in.dst) {
+      case 0: t0 = v; break; case 1: t1 = v; break; case 2: t2 = v; break; case 3: t3 = v; break;
+      case 4: t4 = v; break; case 5: t5 = v; break; case 6: t6 = v; break; case 7: t7 = v; break;
+      default: break;
+    }
+  }
+  const float res = get(p.result);
+  const int64_t at = (int64_t)r + (int64_t)c * p.ldo;
+  if (OUT_BF16)
+    gst<uint16_t>(static_cast<uint16_t*>(p.out) + at, f32_to_bf16_bits(res));
+  else
+    gst<float>(static_cast<float*>(p.out) + at, res);
+}
+
 // Vector path: m a multiple of 8, every full-tensor and column leaf and the output 16-byte
 // aligned with whole 16-byte units per column (checked on the host).  A thread takes 8 consecutive
 // rows of one column (one index split per thread), loads 8 entries of a full or column leaf with
@@ -416,6 +504,12 @@ hipError_t launch_equation(const EqProgram& prog, hipStream_t stream) {
       else TPP_EQ_VEC(false, EQ_MAX_TMPS);
     }
 #undef TPP_EQ_VEC
+  } else if (total <= EQ_SMALL) {
+    const dim3 sgrid((unsigned)((total + EQ_T - 1) / EQ_T));
+    if (prog.out_bf16)
+      hipLaunchKernelGGL((equation_small_kernel<true>), sgrid, dim3(EQ_T), 0, stream, prog);
+    else
+      hipLaunchKernelGGL((equation_small_kernel<false>), sgrid, dim3(EQ_T), 0, stream, prog);
   } else if (prog.out_bf16) {
     if (wide) hipLaunchKernelGGL((equation_kernel<true, true>), grid, dim3(EQ_T), 0, stream, prog);
     else hipLaunchKernelGGL((equation_kernel<true, false>), grid, dim3(EQ_T), 0, stream, prog);

@@ -251,3 +251,30 @@ def test_single_row_equations(n, pad):
                       (-4, 4, "bf16", "row", 0), (-4, 4, "f32", "scalar", 0),
                       (-4, 4, "bf16", "col", 0)], seed=12, integer=True)
     assert np.array_equal(g, r)
+
+
+# Outputs of at most 2^16 elements that the vector path does not take run one element per
+# thread with every leaf loaded up front; the cases above (a few thousand elements) exercise that
+# kernel.  Larger outputs off the vector path run the element kernel: the same trees past the
+# small-output limit (m odd, so never the vector path).
+@pytest.mark.parametrize("out_type", ["f32", "bf16"])
+def test_element_path_past_small_outputs(out_type):
+    say(f"equation element path, mixed leaves, {out_type}")
+    m, n = 251, 300   # 75,300 elements
+    g, r, got, init = one(MIXED, 7, m, n,
+                          [(-8, 8, "bf16", "none", 1), (-8, 8, "f32", "col", 0),
+                           (-4, 4, "bf16", "row", 0), (-4, 4, "f32", "scalar", 0),
+                           (-4, 4, "bf16", "col", 0)],
+                          out_type=out_type, ldo=m + 3, seed=11, integer=True)
+    assert np.array_equal(g, r)
+    gaps = lambda x: x.view(np.uint32 if x.dtype == np.float32 else np.uint16) \
+        .reshape(n, m + 3)[:, m:]
+    assert np.array_equal(gaps(got), gaps(init))
+
+
+@pytest.mark.parametrize("op,lo,hi", UNARY, ids=[u[0] for u in UNARY])
+def test_every_unary_op_element_path(op, lo, hi):
+    g, r, _, _ = one([("leaf", 0), (op, 0)], 1, 201, 400, [(lo, hi, "f32", "none", 0)], seed=12)
+    assert rel_fro(g, r) <= 1e-5
+    if op in ("identity", "neg", "relu", "square"):
+        assert np.array_equal(g, r)
