@@ -245,10 +245,12 @@ class ClockSampler:
         return self
 
     def __exit__(self, *exc):
+        # stop sampling without waiting for the last amd-smi call: a join here would leave the
+        # GPU idle (and its clock dropping) right before the timed steps
         self.stop.set()
-        self.thread.join(timeout=15)
 
     def result(self):
+        self.thread.join(timeout=15)
         if not self.samples:
             return None
         s = sorted(self.samples)
