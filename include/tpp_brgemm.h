@@ -193,6 +193,13 @@ void tpp_brgemm_release(tpp_brgemm_handle h);
  * terminating NUL.  Host-only. */
 tpp_status tpp_brgemm_describe(tpp_brgemm_handle h, char* buf, size_t len);
 
+/* Environment variables read at each launch, for diagnostics and tests (never needed for
+ * correct use): TPP_FORCE_KERNEL=<instance id> takes that kernel instance wherever the shape,
+ * alignment and layout allow it; TPP_SPLIT=<n> splits the reduction of every direct-to-LDS
+ * launch of the stride or offset kind, and of every fp32 launch of fewer than 128 tiles, into n
+ * chunks (capped by the stage or pair count); TPP_LOG prints each launch's instance and split to
+ * stderr. */
+
 /* The kernels one tpp_brgemm_execute_batched call with these arguments would launch, named as
  * the profiler names them without namespace and parameter list, e.g.
  * "brgemm_bf16_dl_kernel<256, 256, 4, 2, true, 0, true, 0, 64, 0, false, false>"; a reduction
