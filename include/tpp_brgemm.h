@@ -202,7 +202,7 @@ tpp_status tpp_brgemm_describe(tpp_brgemm_handle h, char* buf, size_t len);
 
 /* The kernels one tpp_brgemm_execute_batched call with these arguments would launch, named as
  * the profiler names them without namespace and parameter list, e.g.
- * "brgemm_bf16_dl_kernel<256, 256, 4, 2, true, 0, true, 0, 64, 0, false, false>"; a reduction
+ * "brgemm_bf16_dl_kernel<256, 256, 4, 4, true, 0, true, 0, 64, 0, false, false>"; a reduction
  * split over several workgroups adds " + " and its finishing kernel.  The choice is the launch
  * path's own (same grid, counts, alignment of a and b); nothing is launched, allocated or read
  * through the pointers, so it is host-only.  G == 0 gives "".  Writes at most len bytes

@@ -27,7 +27,7 @@ hipError_t launch_dl_part_bk32(const BrgemmParams& p, int32_t id, bool full, dim
 hipError_t DL_CAT(DL_TILE, DL_AT, DL_BT)(const BrgemmParams& p, bool full, dim3 grid,
                                          hipStream_t stream, std::string* name_out) {
 #if DL_TILE == 256
-  launch_dl<256, 256, 4, 2, 0, 64, 0, DL_AT != 0, DL_BT != 0>(p, full, grid, stream, name_out);
+  launch_dl<256, 256, 4, 4, 0, 64, 0, DL_AT != 0, DL_BT != 0>(p, full, grid, stream, name_out);
 #elif DL_TILE == 128
   launch_dl<128, 128, 2, 2, 0, 64, 0, DL_AT != 0, DL_BT != 0>(p, full, grid, stream, name_out);
 #elif DL_TILE == 64

@@ -30,8 +30,8 @@ DL_PART_DECL_ALL(64)
 bool dl_wave_grid(int32_t id, int& waves_m, int& waves_n) {
   switch (id) {
     case K_BF16_DL_256x256: waves_m = 2; waves_n = 4; return true;
-    case K_BF16_PP_256x256:
-    case K_BF16_DL64K_256x256: waves_m = 4; waves_n = 2; return true;
+    case K_BF16_PP_256x256: waves_m = 4; waves_n = 2; return true;
+    case K_BF16_DL64K_256x256: waves_m = 4; waves_n = 4; return true;
     case K_BF16_DL_128x128:
     case K_BF16_DL_64x64:
     case K_BF16_DL64K_128x128:

@@ -76,7 +76,7 @@ enum KernelId : int32_t {
   K_BF16_DL_128x128 = 6,  // direct global->LDS staging, 4 waves
   K_BF16_DL_64x64 = 7,    // direct global->LDS staging, 4 waves
   K_BF16_PP_256x256 = 8,  // direct global->LDS staging, 8 waves in two alternating groups
-  K_BF16_DL64K_256x256 = 9,  // direct global->LDS staging, 8 waves, 64-k stages (k % 64 == 0)
+  K_BF16_DL64K_256x256 = 9,  // direct global->LDS staging, 16 waves, 64-k stages (k % 64 == 0)
   K_BF16_DL64K_128x128 = 10, // as 9, 128x128 tiles, 4 waves (two workgroups per CU)
   K_BF16_DL64K_64x64 = 11,   // as 9, 64x64 tiles, 4 waves
   K_COUNT = 12
@@ -94,7 +94,7 @@ int kernel_k_step(int32_t id);   // k granularity the instance needs (1 = any k)
 bool kernel_full(int32_t id, const BrgemmParams& p);
 // Fill the tiling fields of p for kernel `id` and launch on `stream`.  With name_out set nothing
 // is launched: the same dispatch writes the names of the kernels it would launch, as the
-// profiler names them ("brgemm_bf16_dl_kernel<256, 256, 4, 2, true, 0, true, ...>", and
+// profiler names them ("brgemm_bf16_dl_kernel<256, 256, 4, 4, true, 0, true, ...>", and
 // " + <finishing kernel>" for a split).
 hipError_t launch_brgemm(BrgemmParams& p, int32_t id, hipStream_t stream,
                          std::string* name_out = nullptr);

@@ -360,12 +360,12 @@ def _describe(tpp, call, a=1 << 40, b=1 << 41, c=1 << 42, bias=1 << 43):
 def test_describe_launch_names_the_headline_instances(tpp):
     import workloads as wk
     g1, g2 = wk.mlp_block().calls
-    assert _describe(tpp, g1) == ("brgemm_bf16_dl_kernel<256, 256, 4, 2, true, 0, true, 0, 64, 0, "
+    assert _describe(tpp, g1) == ("brgemm_bf16_dl_kernel<256, 256, 4, 4, true, 0, true, 0, 64, 0, "
                                   "false, false>")
     assert _describe(tpp, g2) == ("brgemm_bf16_dl_kernel<128, 128, 2, 2, true, 0, true, 0, 64, 0, "
                                   "false, false>")
     # a base off 16-byte alignment takes the unaligned instance of the same tile
-    assert _describe(tpp, g1, a=(1 << 40) + 2) == ("brgemm_bf16_dl_kernel<256, 256, 4, 2, true, 0, "
+    assert _describe(tpp, g1, a=(1 << 40) + 2) == ("brgemm_bf16_dl_kernel<256, 256, 4, 4, true, 0, "
                                                    "false, 0, 64, 0, false, false>")
 
 

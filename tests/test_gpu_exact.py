@@ -98,7 +98,7 @@ def assert_bits_equal(got, ref, what):
 
 
 # ----------------------------------------------------------------------------------------------
-# The benchmarked launches: the 256 x 256 (8 waves) and 128 x 128 (4 waves) 64-k instances on
+# The benchmarked launches: the 256 x 256 (16 waves) and 128 x 128 (4 waves) 64-k instances on
 # complete tiles of a fused strided grid (the FULL instances), beta = 0, bf16 out through the
 # register epilogue, bias only and bias + ReLU; and the fp32-out epilogue on the same tiles.
 # Transformer-MLP shape: 1024 tokens, 256 -> 2560 -> 256, so GEMM1's virtual C is 2560 x 1024 (40
@@ -117,7 +117,7 @@ def _bench_shape(seed, epi, out_type="bf16"):
     return integerize(wk.Workload("mlp_block", arrs, [g1, g2]), seed, ranges={"w2": 1})
 
 
-@pytest.mark.parametrize("kid,tile", [(9, "256, 256, 4, 2"), (10, "128, 128, 2, 2")])
+@pytest.mark.parametrize("kid,tile", [(9, "256, 256, 4, 4"), (10, "128, 128, 2, 2")])
 @pytest.mark.parametrize("epi", [("bias",), ("bias", "relu")])
 def test_benchmarked_launch_bit_exact(kid, tile, epi, monkeypatch):
     monkeypatch.setenv("TPP_FORCE_KERNEL", str(kid))
