@@ -601,8 +601,10 @@ __device__ __forceinline__ void epilogue_via_lds(const BrgemmParams& p, const In
 // store's 16-byte runs, and each lane reads its saved pre-activations from the very 8 bytes
 // where it then parks its result.  LDS operations of one wave complete in order, so every read
 // sees the wave's earlier writes and every write lands after the wave's earlier reads.
-// (Keeping the pre-activation, SAVE_PREACT, takes the fp32-slab epilogue: a second slab pass
-// here ran the 256x256 kernels out of registers.)
+// Keeping the pre-activation (SAVE_PREACT; ACT 5 = RELU, 6 = GELU_TANH): one pass parks each
+// value + bias as the pre-activation and narrows its activation into registers (half the
+// accumulators' count); the slab goes to aux, then the activated values are parked and stored
+// to C.
 // ---------------------------------------------------------------------------------------------
 template <int WTM, int WTN, int TM, int TN, bool FULL, int ACT>
 __device__ __forceinline__ void epilogue_bf16_act(const BrgemmParams& p, const Instance& in,
@@ -725,9 +727,33 @@ __device__ __forceinline__ void epilogue_bf16_act(const BrgemmParams& p, const I
     const int ch = tm * 4 + q;                 // 16-byte chunk of this lane's 8-row group
     return slab + col * COL_BYTES + ((ch ^ (col & (CPC - 1))) << 4) + half * 8;
   };
-  // The accumulators + bias, through activation A, narrowed into the slab.
-  auto park = [&](auto act_now) {
+  // The lane's four values of (tm, tn, q): the accumulators + bias (ADD_BIAS; otherwise the bias
+  // is already in them) through activation A, narrowed.  A 3 / 4 read the saved pre-activations
+  // at sp, the slab bytes the result then goes to.
+  auto narrow = [&](auto act_now, auto add_bias, int tm, int tn, int q, const char* sp) {
     constexpr int A = decltype(act_now)::value;
+    constexpr bool ADD_BIAS = decltype(add_bias)::value != 0;
+    float v[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      v[e] = ADD_BIAS ? acc[tm][tn][4 * q + e] + bias4[tm][q][e] : acc[tm][tn][4 * q + e];
+    if constexpr (A == 3 || A == 4) {
+      const uint2 zb = *reinterpret_cast<const uint2*>(sp);   // saved pre-activations
+      const float z[4] = {bf16_bits_to_f32(zb.x & 0xffffu), bf16_bits_to_f32(zb.x >> 16),
+                          bf16_bits_to_f32(zb.y & 0xffffu), bf16_bits_to_f32(zb.y >> 16)};
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        v[e] = A == 3 ? (z[e] > 0.0f ? v[e] : 0.0f) : v[e] * gelu_tanh_grad(z[e]);
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if constexpr (A == 1) v[e] = v[e] > 0.0f ? v[e] : 0.0f;
+      if constexpr (A == 2) v[e] = gelu_tanh(v[e]);
+    }
+    return make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
+  };
+  // All of the lane's values, through activation A, narrowed into the slab.
+  auto park = [&](auto act_now, auto add_bias) {
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
@@ -735,24 +761,7 @@ __device__ __forceinline__ void epilogue_bf16_act(const BrgemmParams& p, const I
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           char* sp = slab_at(tm, tn, q);
-          float v[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = acc[tm][tn][4 * q + e] + bias4[tm][q][e];
-          if constexpr (A == 3 || A == 4) {
-            const uint2 zb = *reinterpret_cast<const uint2*>(sp);   // saved pre-activations
-            const float z[4] = {bf16_bits_to_f32(zb.x & 0xffffu), bf16_bits_to_f32(zb.x >> 16),
-                                bf16_bits_to_f32(zb.y & 0xffffu), bf16_bits_to_f32(zb.y >> 16)};
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-              v[e] = A == 3 ? (z[e] > 0.0f ? v[e] : 0.0f) : v[e] * gelu_tanh_grad(z[e]);
-          }
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            if constexpr (A == 1) v[e] = v[e] > 0.0f ? v[e] : 0.0f;
-            if constexpr (A == 2) v[e] = gelu_tanh(v[e]);
-          }
-          *reinterpret_cast<uint2*>(sp) = make_uint2(pack_bf16x2(v[0], v[1]),
-                                                     pack_bf16x2(v[2], v[3]));
+          *reinterpret_cast<uint2*>(sp) = narrow(act_now, add_bias, tm, tn, q, sp);
         }
   };
   if constexpr (ACT == 3 || ACT == 4) {
@@ -820,7 +829,41 @@ __device__ __forceinline__ void epilogue_bf16_act(const BrgemmParams& p, const I
       });
     }
   }
-  park(IntC<ACT>());
+  if constexpr (ACT == 5 || ACT == 6) {
+    // One pass over the accumulators: each value + bias goes to the slab as the pre-activation
+    // and, through the activation, into registers (half the accumulators' count), so that the
+    // accumulators die as the pass goes and are dead during the aux store.
+    uint2 h[TM][TN][4];
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          float v[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = acc[tm][tn][4 * q + e] + bias4[tm][q][e];
+          *reinterpret_cast<uint2*>(slab_at(tm, tn, q)) =
+              make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = ACT == 5 ? (v[e] > 0.0f ? v[e] : 0.0f) : gelu_tanh(v[e]);
+          h[tm][tn][q] = make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
+          // pinned here: the compiler would otherwise sink the activation to its use after the
+          // aux store and hold the accumulators (in scratch) across it
+          asm volatile("" : "+v"(h[tm][tn][q].x), "+v"(h[tm][tn][q].y));
+        }
+    __builtin_amdgcn_sched_barrier(0);
+    store_slab(p.aux);   // the slab's reads complete before the writes below (in order)
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) *reinterpret_cast<uint2*>(slab_at(tm, tn, q)) = h[tm][tn][q];
+  } else {
+    park(IntC<ACT>(), IntC<1>());
+  }
   store_slab(p.c);
 }
 
@@ -836,9 +879,9 @@ __device__ __forceinline__ void epilogue_bf16(const BrgemmParams& p, const Insta
   } else if (f & TPP_EPI_RELU_INV) {
     TPP_EPI_BF16(3);
   } else if (f & TPP_EPI_GELU_TANH) {
-    TPP_EPI_BF16(2);
+    if (f & TPP_EPI_SAVE_PREACT) TPP_EPI_BF16(6); else TPP_EPI_BF16(2);
   } else if (f & TPP_EPI_RELU) {
-    TPP_EPI_BF16(1);
+    if (f & TPP_EPI_SAVE_PREACT) TPP_EPI_BF16(5); else TPP_EPI_BF16(1);
   } else {
     TPP_EPI_BF16(0);
   }

@@ -488,7 +488,7 @@ void brgemm_bf16_dl_kernel(BrgemmParams p) {
                              acc[tm][tn][4 * q + 3]});
     return;
   }
-  if (p.c_bf16 && p.beta == 0.0f && !(p.flags & TPP_EPI_SAVE_PREACT))
+  if (p.c_bf16 && p.beta == 0.0f)
     epilogue_bf16<WTM, WTN, TM, TN, FULL>(p, in, tc, wm, wn, lane, wave, lds, acc);
   else
     epilogue_via_lds<WTM, WTN, TM, TN, FULL>(p, in, tc, wm, wn, lane, wave,

@@ -152,6 +152,30 @@ def test_benchmarked_tiles_fp32_out_bit_exact(kid, monkeypatch):
     assert_bits_equal(got["h"], h_ref, f"k{kid} fp32 H")
 
 
+@pytest.mark.parametrize("kid", [9, 10, 11])
+def test_benchmarked_tiles_save_preact_bit_exact(kid, monkeypatch):
+    """The forward call that keeps the pre-activation (bias + ReLU + SAVE_PREACT) on complete
+    tiles: the register epilogue parks the pre-activation, stores it to aux, then parks and
+    stores the activation.  Both outputs bit for bit against the oracle."""
+    from helpers import run_call_oracle
+    monkeypatch.setenv("TPP_FORCE_KERNEL", str(kid))
+    monkeypatch.setenv("TPP_SPLIT", "1")
+    base = _bench_shape(41 + kid, ("bias", "relu", "save_preact"))
+    g1 = wk.Call(**dict(base.calls[0].__dict__, aux="z"))
+    arrs = dict(base.arrays, z=np.full(base.arrays["h"].shape, 0x7FC0, np.uint16))
+    wl = wk.Workload("mlp_block", arrs, [g1])
+    in_max = {k: float(np.max(np.abs(wk.bf16_values(v) if v.dtype == np.uint16 else v)))
+              for k, v in arrs.items() if k not in ("h", "y", "z")}
+    assert max_partial(g1, arrs, in_max) < EXACT_LIMIT
+    say(f"benchmarked tiles, SAVE_PREACT, kernel {kid}")
+    got, names = run_gpu(wl)
+    assert ", true, 0, true, 0, 64, 0, false, false>" in names[0], names[0]
+    ref = {k: np.array(v, copy=True) for k, v in arrs.items()}
+    run_call_oracle(g1, ref)
+    assert_bits_equal(got["z"], ref["z"], f"k{kid} Z")
+    assert_bits_equal(got["h"], ref["h"], f"k{kid} H")
+
+
 # ----------------------------------------------------------------------------------------------
 # Operands stored transposed (A_TRANS, B_TRANS, both) on every 64-k instance and every batch
 # variant: a virtual C that is a multiple of 256 on both sides (FULL tiles, bf16 register
