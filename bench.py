@@ -613,6 +613,7 @@ def backward_entry(args, torch, tpp, torch_io, wk, stream):
     fns = [lambda st=st: torch_io.launch_step(st, dev, stream) for st in sts]
     fwd, bwd = fns[0], fns[1:]
     steps = max(10, args.steps // 4)
+    settle([fwd], 0.5, torch)
     ms_fwd = time_bursts([fwd], steps, torch)[0]
     elapsed = time_steps(bwd, steps, max(3, args.warmup // 10), torch)
     per = time_in_steps(bwd, steps, torch, stream)
