@@ -327,6 +327,38 @@ def test_split_stage_list_integer_bit_exact(kid, split, monkeypatch):
         assert np.array_equal(got, ref["c"])
 
 
+@pytest.mark.parametrize("case", ["bias_relu", "beta1", "m68"])
+@pytest.mark.parametrize("split", [2, 3])
+@pytest.mark.parametrize("kid", [6, 9, 10, 11])
+def test_split_finish_epilogue_bit_exact(kid, split, case, monkeypatch):
+    """The finishing kernel's epilogue on small-integer data without an aux step: bias + ReLU,
+    beta = 1 reading C, and m = 68 (four-row groups that are not eight-row aligned), over a
+    ragged strided grid."""
+    monkeypatch.setenv("TPP_FORCE_KERNEL", str(kid))
+    monkeypatch.setenv("TPP_SPLIT", str(split))
+    rng = np.random.default_rng(kid * 100 + split * 10 + len(case))
+    m = 68 if case == "m68" else 72
+    n, k, count, gm, gn = 64, 64, 7, 3, 2
+    draw = lambda s: rng.integers(-3, 4, size=s).astype(np.float32)
+    beta = 1.0 if case == "beta1" else 0.0
+    flags = {"bias", "relu"} if case != "beta1" else {"bias"}
+    a = wk.bf16_bits(draw((gm * count * k * m,)))
+    b = wk.bf16_bits(draw((gn * count * n * k,)))
+    c0 = wk.bf16_bits(draw((gm * gn * m * n,))) if beta else \
+        np.full(gm * gn * m * n, 0x7FC0, np.uint16)
+    arrays = dict(a=a, b=b, c=c0, bias=draw((gm * m,)))
+    call = wk.Call(m, n, k, m, k, m, "bf16", "bf16", beta, "stride", k * m, n * k, flags,
+                   G=gm * gn, grid=dict(gm=gm, gn=gn, a_step_m=count * k * m,
+                                        b_step_n=count * n * k, c_step_m=m * n,
+                                        c_step_n=gm * m * n, bias_step_m=m),
+                   count=count, a="a", b="b", c="c", bias="bias")
+    say(f"split finish {case} split {split} kernel {kid}")
+    ref = {k2: np.array(v, copy=True) for k2, v in arrays.items()}
+    run_call_oracle(call, ref)
+    got = gpu_steps([call], arrays, ["c"])["c"]
+    assert np.array_equal(got, ref["c"])
+
+
 @pytest.mark.parametrize("split", [2, 4])
 @pytest.mark.parametrize("kid", [9, 10])
 def test_split_mlp_block_matches_oracle(kid, split, monkeypatch):
