@@ -413,7 +413,36 @@ void brgemm_bf16_dl_kernel(BrgemmParams p) {
   for (int32_t s = 0; s < pre; ++s) {
     if constexpr (SCHED == 0) issue_block(); else issue();
   }
-  if constexpr (SCHED == 0) {
+  // The 16-wave instance with A stored transposed (one 16-byte fragment read per A fragment), on
+  // complete tiles of an aligned strided grid, defers each stage's last k-step past the next
+  // barrier: its fragments are read into registers
+  // before the barrier, and its MFMAs are issued right after it, ahead of the wave's copies of the
+  // stage it refills and of the next stage's fragment reads, so every SIMD has MFMAs to run while
+  // the compute unit accepts the copies.  The k-steps still accumulate in order (stage s - 1's
+  // last k-step before stage s's first).  With A in its own layout (two transposing reads per
+  // fragment), on other batch kinds and on partial tiles, the held fragments push the kernel
+  // past its 128 registers into scratch; the 128x128 tile measured slower with it.
+  constexpr bool SKEW =
+      SCHED == 0 && NW == 16 && AT && !BT && FULL && KIND == TPP_BR_STRIDE && ALIGNED;
+  if constexpr (SKEW) {
+    bf16x8 af[2][TM], bfr[2][TN];
+    for (int32_t s = 0; s < stages; ++s) {
+      wait_loads(lmin(stages - 1 - s, SLOTS - 2));
+      lds_barrier();
+      if (s > 0) mfmas(af[(KQ - 1) & 1], bfr[(KQ - 1) & 1]);   // stage s - 1, last k-step
+      __builtin_amdgcn_sched_barrier(0);
+      if (s + SLOTS - 1 < stages) issue_block();   // stage s + SLOTS - 1 refills the slot of s - 1
+      const int slot = s % SLOTS;
+      read_frags(slot, 0, af[0], bfr[0]);
+#pragma unroll
+      for (int kq = 0; kq + 1 < KQ; ++kq) {
+        read_frags(slot, kq + 1, af[(kq + 1) & 1], bfr[(kq + 1) & 1]);
+        __builtin_amdgcn_sched_barrier(0);   // keep the reads ahead of the MFMAs
+        mfmas(af[kq & 1], bfr[kq & 1]);
+      }
+    }
+    if (stages > 0) mfmas(af[(KQ - 1) & 1], bfr[(KQ - 1) & 1]);
+  } else if constexpr (SCHED == 0) {
     for (int32_t s = 0; s < stages; ++s) {
       // This wave's loads of stage s are done once at most the later stages' loads are pending;
       // the barrier then publishes every wave's stage s and retires everyone's reads of s - 1.
