@@ -589,9 +589,55 @@ __device__ __forceinline__ void epilogue_via_lds(const BrgemmParams& p, const In
   }
 }
 
+// Bias of a lane's rows in the 32x32 MFMA accumulator layout, all issued before any is used: for
+// group tm and q, the four rows row_base + 32 tm + 8 q + 4 (lane / 32) + e (an 8-row chunk never
+// straddles an instance: m % 8 == 0).  The chunks are 8 rows apart, so the instance row and bias
+// index advance by additions.  Rows outside C, and every row without TPP_EPI_BIAS, get zeros.
+template <int TM, bool FULL>
+__device__ __forceinline__ void load_bias4(const BrgemmParams& p, const Instance& in,
+                                           int32_t row_base, int lane, f32x4 (&bias4)[TM][4]) {
+  const bool has_bias = (p.flags & TPP_EPI_BIAS) != 0;
+  const int half = lane >> 5;
+  const int32_t R0 = row_base + 4 * half;
+  int32_t gi = 0, r = R0;
+  if (p.fused) {
+    gi = R0 / p.m;
+    r = R0 - gi * p.m;
+  }
+  int64_t idx = p.fused ? (int64_t)gi * p.bias_step_m + r : in.bias + R0;
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int32_t R = R0 + tm * 32 + 8 * q;
+      const bool ok = FULL || R < (p.fused ? p.vrows : p.m);
+      f32x4 b = {0.0f, 0.0f, 0.0f, 0.0f};
+      if (has_bias && ok) {
+        const float* bp = p.bias + idx;
+        if ((reinterpret_cast<uintptr_t>(bp) & 15) == 0) {
+          b = gld<f32x4>(bp);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) b[e] = gld<float>(bp + e);
+        }
+      }
+      bias4[tm][q] = b;
+      // next chunk, 8 rows on
+      idx += 8;
+      if (p.fused) {
+        r += 8;
+        while (r >= p.m) {
+          r -= p.m;
+          idx += p.bias_step_m - p.m;
+        }
+      }
+    }
+}
+
 // ---------------------------------------------------------------------------------------------
-// Epilogue for a bf16 C that is not read (beta = 0).  Bias and activation are applied to the
-// accumulators where they are, each lane narrows its four consecutive rows of a column to bf16
+// Epilogue for a bf16 C that is not read (beta = 0).  The kernel starts the accumulators at the
+// bias (load_bias4), so they hold sum + bias here; the activation is applied to them where they
+// are, each lane narrows its four consecutive rows of a column to bf16
 // and parks them in its own wave's LDS slab (column-major, WTM rows per column, 16-byte row
 // chunks XOR-swizzled by the column), and the wave then stores the slab as 16-byte runs of 8
 // rows, so every global store instruction writes whole 128-byte lines.  A wave touches only its
@@ -602,7 +648,7 @@ __device__ __forceinline__ void epilogue_via_lds(const BrgemmParams& p, const In
 // where it then parks its result.  LDS operations of one wave complete in order, so every read
 // sees the wave's earlier writes and every write lands after the wave's earlier reads.
 // Keeping the pre-activation (SAVE_PREACT; ACT 5 = RELU, 6 = GELU_TANH): one pass parks each
-// value + bias as the pre-activation and narrows its activation into registers (half the
+// value (bias included) as the pre-activation and narrows its activation into registers (half the
 // accumulators' count); the slab goes to aux, then the activated values are parked and stored
 // to C.
 // ---------------------------------------------------------------------------------------------
@@ -615,48 +661,7 @@ __device__ __forceinline__ void epilogue_bf16_act(const BrgemmParams& p, const I
   static_assert((CPC & (CPC - 1)) == 0 && CPC <= 64, "power-of-two chunks per column");
   char* slab = lds + wave * WTN * COL_BYTES;
   const int32_t row_base = tc.row0 + wm * WTM;
-  const bool has_bias = (p.flags & TPP_EPI_BIAS) != 0;
   const int half = lane >> 5;                  // rows 4*half.. of each 8-row group
-  // Bias of the lane's rows, all issued before any is used: for group tm and q, the four rows
-  // 32 tm + 8 q + 4 half + e (an 8-row chunk never straddles an instance: m % 8 == 0).  The
-  // chunks are 8 rows apart, so the instance row and bias index advance by additions.
-  f32x4 bias4[TM][4];
-  {
-    const int32_t R0 = row_base + 4 * half;
-    int32_t gi = 0, r = R0;
-    if (p.fused) {
-      gi = R0 / p.m;
-      r = R0 - gi * p.m;
-    }
-    int64_t idx = p.fused ? (int64_t)gi * p.bias_step_m + r : in.bias + R0;
-#pragma unroll
-    for (int tm = 0; tm < TM; ++tm)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int32_t R = R0 + tm * 32 + 8 * q;
-        const bool ok = FULL || R < (p.fused ? p.vrows : p.m);
-        f32x4 b = {0.0f, 0.0f, 0.0f, 0.0f};
-        if (has_bias && ok) {
-          const float* bp = p.bias + idx;
-          if ((reinterpret_cast<uintptr_t>(bp) & 15) == 0) {
-            b = gld<f32x4>(bp);
-          } else {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) b[e] = gld<float>(bp + e);
-          }
-        }
-        bias4[tm][q] = b;
-        // next chunk, 8 rows on
-        idx += 8;
-        if (p.fused) {
-          r += 8;
-          while (r >= p.m) {
-            r -= p.m;
-            idx += p.bias_step_m - p.m;
-          }
-        }
-      }
-  }
   // The slab <-> global walk: 64 lanes = 64 / CPC columns x CPC chunks per instruction, columns
   // advancing by COLS_PER_IT (instance column and offset tracked by additions, one division per
   // lane).  fn(slab chunk, global element offset relative to the instance's C base, valid).
@@ -727,16 +732,14 @@ __device__ __forceinline__ void epilogue_bf16_act(const BrgemmParams& p, const I
     const int ch = tm * 4 + q;                 // 16-byte chunk of this lane's 8-row group
     return slab + col * COL_BYTES + ((ch ^ (col & (CPC - 1))) << 4) + half * 8;
   };
-  // The lane's four values of (tm, tn, q): the accumulators + bias (ADD_BIAS; otherwise the bias
-  // is already in them) through activation A, narrowed.  A 3 / 4 read the saved pre-activations
-  // at sp, the slab bytes the result then goes to.
-  auto narrow = [&](auto act_now, auto add_bias, int tm, int tn, int q, const char* sp) {
+  // The lane's four values of (tm, tn, q) (the accumulators, which already hold the bias) through
+  // activation A, narrowed.  A 3 / 4 read the saved pre-activations at sp, the slab bytes the
+  // result then goes to.
+  auto narrow = [&](auto act_now, int tm, int tn, int q, const char* sp) {
     constexpr int A = decltype(act_now)::value;
-    constexpr bool ADD_BIAS = decltype(add_bias)::value != 0;
     float v[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e)
-      v[e] = ADD_BIAS ? acc[tm][tn][4 * q + e] + bias4[tm][q][e] : acc[tm][tn][4 * q + e];
+    for (int e = 0; e < 4; ++e) v[e] = acc[tm][tn][4 * q + e];
     if constexpr (A == 3 || A == 4) {
       const uint2 zb = *reinterpret_cast<const uint2*>(sp);   // saved pre-activations
       const float z[4] = {bf16_bits_to_f32(zb.x & 0xffffu), bf16_bits_to_f32(zb.x >> 16),
@@ -753,7 +756,7 @@ __device__ __forceinline__ void epilogue_bf16_act(const BrgemmParams& p, const I
     return make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
   };
   // All of the lane's values, through activation A, narrowed into the slab.
-  auto park = [&](auto act_now, auto add_bias) {
+  auto park = [&](auto act_now) {
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
@@ -761,7 +764,7 @@ __device__ __forceinline__ void epilogue_bf16_act(const BrgemmParams& p, const I
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           char* sp = slab_at(tm, tn, q);
-          *reinterpret_cast<uint2*>(sp) = narrow(act_now, add_bias, tm, tn, q, sp);
+          *reinterpret_cast<uint2*>(sp) = narrow(act_now, tm, tn, q, sp);
         }
   };
   if constexpr (ACT == 3 || ACT == 4) {
@@ -830,7 +833,7 @@ __device__ __forceinline__ void epilogue_bf16_act(const BrgemmParams& p, const I
     }
   }
   if constexpr (ACT == 5 || ACT == 6) {
-    // One pass over the accumulators: each value + bias goes to the slab as the pre-activation
+    // One pass over the accumulators: each value goes to the slab as the pre-activation
     // and, through the activation, into registers (half the accumulators' count), so that the
     // accumulators die as the pass goes and are dead during the aux store.
     uint2 h[TM][TN][4];
@@ -842,7 +845,7 @@ __device__ __forceinline__ void epilogue_bf16_act(const BrgemmParams& p, const I
         for (int q = 0; q < 4; ++q) {
           float v[4];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = acc[tm][tn][4 * q + e] + bias4[tm][q][e];
+          for (int e = 0; e < 4; ++e) v[e] = acc[tm][tn][4 * q + e];
           *reinterpret_cast<uint2*>(slab_at(tm, tn, q)) =
               make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
 #pragma unroll
@@ -862,7 +865,7 @@ __device__ __forceinline__ void epilogue_bf16_act(const BrgemmParams& p, const I
 #pragma unroll
         for (int q = 0; q < 4; ++q) *reinterpret_cast<uint2*>(slab_at(tm, tn, q)) = h[tm][tn][q];
   } else {
-    park(IntC<ACT>(), IntC<1>());
+    park(IntC<ACT>());
   }
   store_slab(p.c);
 }

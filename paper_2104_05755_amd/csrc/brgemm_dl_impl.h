@@ -413,6 +413,19 @@ void brgemm_bf16_dl_kernel(BrgemmParams p) {
   for (int32_t s = 0; s < pre; ++s) {
     if constexpr (SCHED == 0) issue_block(); else issue();
   }
+  // The register epilogue (bf16 C, beta = 0, whole stage lists) takes accumulators that start at
+  // the bias: the products accumulate onto it, the epilogue spends no addition per element on it,
+  // and the bias loads overlap the first stage's copies instead of opening the epilogue.
+  if (p.c_bf16 && p.beta == 0.0f && p.split <= 1 && (p.flags & TPP_EPI_BIAS)) {
+    f32x4 b4[TM][4];
+    load_bias4<TM, FULL>(p, in, tc.row0 + wm * WTM, lane, b4);
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[tm][tn][v] = b4[tm][v >> 2][v & 3];
+  }
   // The 16-wave instance with A stored transposed (one 16-byte fragment read per A fragment), on
   // complete tiles of an aligned strided grid, defers each stage's last k-step past the next
   // barrier: its fragments are read into registers
