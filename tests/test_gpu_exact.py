@@ -192,6 +192,25 @@ EXACT_AT_CASES = {
 }
 
 
+@pytest.mark.parametrize("pairs", [1, 2, 3])
+def test_a_trans_full_tiles_short_stage_lists(pairs, monkeypatch):
+    """The 16-wave instance with A stored transposed on complete tiles defers each stage's last
+    k-step past the next barrier; stage lists of one, two and three stages (the first and last
+    stages of that schedule) bit for bit against the oracle, with bias + ReLU."""
+    monkeypatch.setenv("TPP_FORCE_KERNEL", "9")
+    monkeypatch.setenv("TPP_SPLIT", "1")
+    base = wk.mlp_block(seed=60 + pairs, tokens=512, hidden=64 * pairs, inter=512)
+    g1 = wk.Call(**dict(base.calls[0].__dict__, flags={"bias", "relu", "a_trans"},
+                        lda=base.calls[0].k))
+    wl = integerize(wk.Workload("mlp_block", dict(base.arrays), [g1]), 60 + pairs)
+    say(f"a_trans full tiles, {pairs} pairs")
+    got, names = run_gpu(wl)
+    assert names[0].endswith("true, false>") and "<256, 256, 4, 4, true, 0, true," in names[0], \
+        names[0]
+    h_ref, _ = run_oracle(wl, 0)
+    assert_bits_equal(got["h"], h_ref, f"a_trans {pairs} pairs H")
+
+
 @pytest.mark.parametrize("layout", ["a_trans", "b_trans", "both"])
 @pytest.mark.parametrize("kid", [9, 10, 11])
 @pytest.mark.parametrize("case", sorted(EXACT_AT_CASES))
