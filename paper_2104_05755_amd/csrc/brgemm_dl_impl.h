@@ -272,7 +272,44 @@ void brgemm_bf16_dl_kernel(BrgemmParams p) {
     sa = sa_pair + (uint64_t)(iss_kk / DL_BK) * a_kstep;
     sb = sb_pair + (uint64_t)(iss_kk / DL_BK) * b_kstep;
   }
+  // Offset and pointer lists with one stage per pair (k equal to the stage depth), at most 64
+  // pairs and every listed block 16-byte aligned (four-wave instances): lane j holds pair j's
+  // byte addresses, so a stage's copies take two readlanes per operand instead of the pair's
+  // address arithmetic and alignment test on the scalar unit, which the compute unit's waves
+  // share (the 3x3 convolution runs six workgroups per CU).
+  uint64_t fa = 0, fb = 0;
+  bool fast_list = false;
+  if constexpr (KIND != TPP_BR_STRIDE && NW == 4) {
+    if (p.k == DL_BK && in.npairs <= 64) {
+      bool ok = true;
+      if (lane < in.npairs) {
+        const uint16_t* pa;
+        const uint16_t* pb;
+        if constexpr (KIND == TPP_BR_OFFSET) {
+          pa = static_cast<const uint16_t*>(p.a) + in.a + (int64_t)pair_a;
+          pb = static_cast<const uint16_t*>(p.b) + in.b + (int64_t)pair_b;
+        } else {
+          pa = reinterpret_cast<const uint16_t*>(pair_a);
+          pb = reinterpret_cast<const uint16_t*>(pair_b);
+        }
+        ok = ((reinterpret_cast<uintptr_t>(pa) | reinterpret_cast<uintptr_t>(pb)) & 15) == 0;
+        fa = reinterpret_cast<uint64_t>(pa + base_a);
+        fb = reinterpret_cast<uint64_t>(pb + base_b);
+      }
+      fast_list = __all(ok);
+    }
+  }
   auto issue_block = [&]() {
+    if (KIND != TPP_BR_STRIDE && NW == 4 && fast_list) {
+      const uint32_t slot_u32 = lds_u32 + (uint32_t)(iss_s % SLOTS) * SLOT;
+      buffer_load_lds16_block<A_PER_W>(raw_buffer(reinterpret_cast<const void*>(lane_u64(fa, iss_i))),
+                                       la, slot_u32 + wave * A_PER_W * 1024);
+      buffer_load_lds16_block<B_PER_W>(raw_buffer(reinterpret_cast<const void*>(lane_u64(fb, iss_i))),
+                                       lb, slot_u32 + A_BYTES + wave * B_PER_W * 1024);
+      ++iss_s;
+      ++iss_i;
+      return;
+    }
     if constexpr (KIND == TPP_BR_STRIDE && ALIGNED) {
       const uint32_t slot_u32 = lds_u32 + (uint32_t)(iss_s % SLOTS) * SLOT;
       buffer_load_lds16_block<A_PER_W>(raw_buffer(reinterpret_cast<const void*>(sa)), la,
