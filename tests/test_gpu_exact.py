@@ -239,3 +239,54 @@ def test_transposed_layouts_bit_exact(kid, case, layout, monkeypatch):
         ref, _ = run_oracle(wl)
         out = wl.calls[0].c
         assert_bits_equal(got[out], ref, f"k{kid} {layout} {case}")
+
+
+# ----------------------------------------------------------------------------------------------
+# Offset and pointer lists (Sec. 2.3's offset and address variants) with one 64-k stage per pair
+# on every 64-k instance: every listed block 16-byte aligned (on the four-wave instances each lane
+# then holds one pair's byte addresses), one block or every block off that alignment (the copies
+# go element by element through registers), lists longer than the 64 lanes, and stage lists
+# split over workgroups (a chunk starts mid-list).  192 x 136 leaves ragged tiles on every
+# instance.
+# ----------------------------------------------------------------------------------------------
+def _list_case(seed, kind, count, shift):
+    rng = np.random.default_rng(seed)
+    wl = wk.small_case(rng, 192, 136, 64, count, kind, "bf16", "bf16", 0.0, {"bias", "relu"},
+                       integer=True)
+    call = wl.calls[0]
+    arrs = dict(wl.arrays)
+    tail = wk.bf16_bits(np.zeros(8, np.float32))       # room for blocks moved up to 7 elements
+    arrs["a"] = np.concatenate([arrs["a"], tail])
+    arrs["b"] = np.concatenate([arrs["b"], tail])
+    la, lb = ("offs_a", "offs_b") if kind == "offset" else ("idx_a", "idx_b")
+    ea = np.array(getattr(call, la), dtype=np.int64)
+    eb = np.array(getattr(call, lb), dtype=np.int64)
+    if shift == "one":
+        ea[count // 2] += 3
+    elif shift == "all":
+        ea += 1
+        eb += 5
+    kw = dict(call.__dict__)
+    kw[la], kw[lb] = ea, eb
+    return wk.Workload(wl.name, arrs, [wk.Call(**kw)])
+
+
+@pytest.mark.parametrize("split", ["1", "3"])
+@pytest.mark.parametrize("count", [9, 70])
+@pytest.mark.parametrize("shift", ["none", "one", "all"])
+@pytest.mark.parametrize("kind", ["offset", "address"])
+@pytest.mark.parametrize("kid,tile", [(9, "<256, 256, 4, 4,"), (10, "<128, 128, 2, 2,"),
+                                      (11, "<64, 64, 2, 2,")])
+def test_pair_lists_one_stage_per_pair(kid, tile, kind, shift, count, split, monkeypatch):
+    monkeypatch.setenv("TPP_FORCE_KERNEL", str(kid))
+    monkeypatch.setenv("TPP_SPLIT", split)
+    wl = _list_case(1000 + 7 * kid + count, kind, count, shift)
+    call = wl.calls[0]
+    in_max = {k: float(np.max(np.abs(wk.bf16_values(v) if v.dtype == np.uint16 else v)))
+              for k, v in wl.arrays.items() if k != "c"}
+    assert max_partial(call, wl.arrays, in_max) < EXACT_LIMIT
+    say(f"pair lists: kernel {kid} {kind} shift={shift} count={count} split={split}")
+    got, names = run_gpu(wl)
+    assert tile in names[0], names[0]
+    ref, _ = run_oracle(wl)
+    assert_bits_equal(got["c"], ref, f"k{kid} {kind} {shift} {count} pairs split {split}")
