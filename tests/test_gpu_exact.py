@@ -290,3 +290,33 @@ def test_pair_lists_one_stage_per_pair(kid, tile, kind, shift, count, split, mon
     assert tile in names[0], names[0]
     ref, _ = run_oracle(wl)
     assert_bits_equal(got["c"], ref, f"k{kid} {kind} {shift} {count} pairs split {split}")
+
+
+# ----------------------------------------------------------------------------------------------
+# Empty pair lists (count 0, Table 3: C = epilogue(beta C)) on every 16-byte-load instance, forced
+# one at a time, on complete tiles with beta = 0 and bf16 out: the output is the activated bias,
+# bit for bit (the register epilogue's accumulators start at the bias and no stage runs).  The
+# 64-k instances also with SAVE_PREACT (the pre-activation is the bias itself).
+# ----------------------------------------------------------------------------------------------
+@pytest.mark.parametrize("kid,save", [(k, False) for k in (0, 1, 2, 5, 6, 7, 8)] +
+                         [(k, s) for k in (9, 10, 11) for s in (False, True)])
+def test_empty_pair_lists_give_the_activated_bias(kid, save, monkeypatch):
+    from helpers import run_call_oracle
+    monkeypatch.setenv("TPP_FORCE_KERNEL", str(kid))
+    base = wk.mlp_block(seed=70 + kid, tokens=512, hidden=512, inter=512)
+    flags = {"bias", "relu"} | ({"save_preact"} if save else set())
+    g1 = wk.Call(**dict(base.calls[0].__dict__, count=0, flags=flags,
+                        aux="z" if save else None))
+    arrs = dict(base.arrays)
+    if save:
+        arrs["z"] = np.full(arrs["h"].shape, 0x7FC0, np.uint16)
+    wl = integerize(wk.Workload("mlp_block", arrs, [g1]), 70 + kid)
+    say(f"empty pair lists, kernel {kid}, save_preact={save}")
+    got, names = run_gpu(wl)
+    tile = {0: 256, 1: 128, 2: 64, 5: 256, 6: 128, 7: 64, 8: 256, 9: 256, 10: 128, 11: 64}[kid]
+    assert f"<{tile}, {tile}," in names[0], names[0]
+    ref = {k: np.array(v, copy=True) for k, v in wl.arrays.items()}
+    run_call_oracle(g1, ref)
+    assert_bits_equal(got["h"], ref["h"], f"k{kid} H")
+    if save:
+        assert_bits_equal(got["z"], ref["z"], f"k{kid} Z")
