@@ -320,3 +320,31 @@ def test_empty_pair_lists_give_the_activated_bias(kid, save, monkeypatch):
     assert_bits_equal(got["h"], ref["h"], f"k{kid} H")
     if save:
         assert_bits_equal(got["z"], ref["z"], f"k{kid} Z")
+
+
+# ----------------------------------------------------------------------------------------------
+# beta != 0 (Alg. 2: C loaded into the accumulators; the fp32-slab epilogue reads C) on every
+# 16-byte-load instance, forced one at a time and unsplit, on complete tiles of a fused strided
+# grid, bf16 and fp32 C, bias + ReLU: bit for bit (beta * C is a multiple of 0.5 below 2^24).
+# ----------------------------------------------------------------------------------------------
+@pytest.mark.parametrize("beta", [1.0, -0.5])
+@pytest.mark.parametrize("ct", ["bf16", "f32"])
+@pytest.mark.parametrize("kid", [0, 1, 2, 5, 6, 7, 8, 9, 10, 11])
+def test_beta_reads_c_on_every_instance(kid, ct, beta, monkeypatch):
+    monkeypatch.setenv("TPP_FORCE_KERNEL", str(kid))
+    monkeypatch.setenv("TPP_SPLIT", "1")
+    base = wk.mlp_block(seed=80 + kid, tokens=512, hidden=512, inter=512)
+    g1 = wk.Call(**dict(base.calls[0].__dict__, beta=beta, c_type=ct, flags={"bias", "relu"}))
+    arrs = dict(base.arrays)
+    if ct == "f32":
+        arrs["h"] = np.zeros(arrs["h"].shape, np.float32)
+    wl = integerize(wk.Workload("mlp_block", arrs, [g1]), 80 + kid)
+    in_max = {k: float(np.max(np.abs(wk.bf16_values(v) if v.dtype == np.uint16 else v)))
+              for k, v in wl.arrays.items()}
+    assert max_partial(g1, wl.arrays, in_max) < EXACT_LIMIT
+    say(f"beta {beta} {ct} C, kernel {kid}")
+    got, names = run_gpu(wl)
+    tile = {0: 256, 1: 128, 2: 64, 5: 256, 6: 128, 7: 64, 8: 256, 9: 256, 10: 128, 11: 64}[kid]
+    assert f"<{tile}, {tile}," in names[0], names[0]
+    h_ref, _ = run_oracle(wl, 0)
+    assert_bits_equal(got["h"], h_ref, f"k{kid} beta {beta} {ct} H")
